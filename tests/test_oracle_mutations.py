@@ -1,0 +1,104 @@
+"""Planted mistakes in the oracle must be caught by its pins (CPU only).
+
+Each test swaps one oracle function for a plausible wrong version (a sign, a
+dropped term, an inverted ratio, a missing scale, a wrong transform) and
+asserts that the corresponding pin rejects it.
+"""
+import numpy as np
+import pytest
+
+from oracle import forward, forward_loops, noise, philox, posterior, sampler
+from tests.test_oracle_posterior import check_against_bayes
+from tests.test_oracle_forward import CFG, _P, _z
+from tests.test_oracle_sampler import chi2_pvalue, _peaked_probs
+
+
+def _mdm_sign(x, z_t, at, as_):
+    p = posterior.mdm_posterior(x, z_t, at, as_)
+    if int(z_t) == x.shape[0]:
+        p[:-1] = (at - as_) / (1 - at) * x
+    return p
+
+
+def _usdm_drop_uniform_term(x, z_t, at, as_):
+    K = x.shape[0]
+    a_ts = at / as_
+    z = np.zeros(K)
+    z[int(z_t)] = 1
+    num = K * at * z * x + (a_ts - at) * z + (as_ - at) * x
+    return num / (K * at * x[int(z_t)] + 1 - at)
+
+
+def _usdm_inverted_ratio(x, z_t, at, as_):
+    return posterior.usdm_posterior(x, z_t, at, as_) if as_ == 0 else \
+        _usdm_with_ats(x, z_t, at, as_, as_ / max(at, 1e-300))
+
+
+def _usdm_with_ats(x, z_t, at, as_, a_ts):
+    K = x.shape[0]
+    z = np.zeros(K)
+    z[int(z_t)] = 1
+    num = (K * at * z * x + (a_ts - at) * z + (as_ - at) * x + (1 - a_ts) * (1 - as_) / K)
+    return num / (K * at * x[int(z_t)] + 1 - at)
+
+
+@pytest.mark.parametrize("bad,prior", [(_mdm_sign, "mask"), (_usdm_drop_uniform_term, "uniform"),
+                                       (_usdm_inverted_ratio, "uniform")])
+def test_bayes_pin_catches_posterior_mistakes(bad, prior):
+    with np.errstate(all="ignore"):
+        try:
+            worst = check_against_bayes(bad, prior, 4)
+        except AssertionError:
+            return                   # non-finite or inconsistent output: caught
+    assert worst > 1e-6
+
+
+def _forward_mismatch():
+    P = _P(scale=20.0)
+    z = _z()
+    a = forward.forward(CFG, P, z, 0.37)
+    b = np.array(forward_loops.forward_loops(CFG, P, z, 0.37))
+    return np.abs(a - b).max()
+
+
+def test_loop_pin_catches_missing_attention_scale(monkeypatch):
+    def att(q, k, v):
+        s = q @ k.T
+        p = np.exp(s - s.max(-1, keepdims=True))
+        return (p / p.sum(-1, keepdims=True)) @ v
+    monkeypatch.setattr(forward, "attention", att)
+    assert _forward_mismatch() > 1e-6
+
+
+def test_loop_pin_catches_wrong_gelu(monkeypatch):
+    monkeypatch.setattr(forward, "gelu_tanh", lambda x: 0.5 * x * (1 + np.tanh(0.8 * (x + 0.044715 * x ** 3))))
+    assert _forward_mismatch() > 1e-6
+
+
+def test_loop_pin_catches_swapped_time_embedding(monkeypatch):
+    orig = forward.time_embedding
+    monkeypatch.setattr(forward, "time_embedding", lambda a, d: orig(a, d)[::-1].copy())
+    assert _forward_mismatch() > 1e-6
+
+
+def test_loop_pin_catches_unbiased_variance(monkeypatch):
+    def ln(x, g, b, eps):
+        mu = x.mean(-1, keepdims=True)
+        return (x - mu) / np.sqrt(x.var(-1, ddof=1, keepdims=True) + eps) * g + b
+    monkeypatch.setattr(forward, "layer_norm", ln)
+    assert _forward_mismatch() > 1e-6
+
+
+def test_chi2_pin_catches_gumbel_sign(monkeypatch):
+    monkeypatch.setattr(noise, "gumbel", lambda w: np.log(noise.exponential(w)))
+    V = 40
+    p = _peaked_probs("uniform", V, 2)
+    n = 20000
+    w = philox.counter_words(5, 9, 0, np.arange(n)[:, None], np.arange(V)[None, :])
+    z = np.array([sampler.sample_flat(p, w[i]) for i in range(n)])
+    assert chi2_pvalue(np.bincount(z, minlength=V), p) < 1e-6
+
+
+def test_kat_pin_catches_wrong_multiplier(monkeypatch):
+    monkeypatch.setattr(philox, "_M0", 0xD2511F55)
+    assert philox.philox_scalar((0, 0, 0, 0), (0, 0))[0] != 0x6627e8d5
