@@ -1,0 +1,230 @@
+/*
+ * dd.h - C ABI of the MI355X (gfx950) reverse-step library for discrete-diffusion
+ * language models (arXiv 2609.04010, "Unlocking Lossless Speedups in LLMs via
+ * Discrete Diffusion").
+ *
+ * The hot path is one reverse denoising step, run T times:
+ *   denoiser   x_theta(z_t, t): a bidirectional pre-LN transformer (Background,
+ *              "Discrete Diffusion Language Models": a denoising model maps the
+ *              noisy sequence and the time to per-position distributions);
+ *   posterior  p_{s|t}(z_s | z_t) = q_{s|t}(z_s | z_t, x = x_theta(z_t, t)),
+ *              masked prior (App. A.1, eq. mdm-posterior) with carry-over of
+ *              unmasked tokens, or uniform prior (App. A.2,
+ *              eq. uniform_true_reverse_posterior);
+ *   sample     one categorical draw per position (two-level Gumbel-max).
+ *
+ * Conventions shared by every entry point
+ *   - Pointers documented "device" must be device memory of the current HIP
+ *     device; "host" pointers are read during the call only.  The library never
+ *     allocates device memory: the caller owns parameters, workspace, logits,
+ *     token buffers, noise and traces.
+ *   - `stream` is a hipStream_t passed as void* (NULL = the null stream).  Every
+ *     compute call is asynchronous and ordered on that stream; nothing
+ *     synchronises the host except dd_read_device_error and dd_profile_read.
+ *   - Token ids are int32.  V is the number of real tokens (logit width).  For the
+ *     masked prior the [MASK] token is id V (the K-th category of the paper's
+ *     notation, K = V + 1 classes); for the uniform prior K = V.
+ *   - Host-side validation runs before any launch; on failure the call returns
+ *     DD_E_ARG / DD_E_SHAPE / DD_E_DTYPE / DD_E_WORKSPACE / DD_E_UNSUPPORTED,
+ *     launches nothing and writes no output.  A failed launch returns DD_E_HIP.
+ *     dd_last_error() gives a human-readable reason (thread-local).
+ *   - Out-of-range token ids met on the device set bit DD_DEVERR_TOKEN in a
+ *     device error word (the id is clamped so memory stays in bounds); read it
+ *     with dd_read_device_error.  No call aborts and no exception crosses the ABI.
+ */
+#ifndef DD_H
+#define DD_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    DD_OK = 0,
+    DD_E_ARG = 1,         /* null pointer, non-positive size, bad schedule value */
+    DD_E_SHAPE = 2,       /* inconsistent shapes (e.g. L > max_len, ld < V)      */
+    DD_E_DTYPE = 3,       /* unknown dtype                                       */
+    DD_E_WORKSPACE = 4,   /* workspace or parameter buffer too small             */
+    DD_E_HIP = 5,         /* a HIP runtime call or launch failed                 */
+    DD_E_UNSUPPORTED = 6, /* valid but not implemented (e.g. bf16 with dh != 64) */
+    DD_E_DEVICE = 7       /* the device error word is non-zero                   */
+} dd_status;
+
+typedef enum { DD_BF16 = 0, DD_FP32 = 1 } dd_dtype;
+typedef enum { DD_PRIOR_MASK = 0, DD_PRIOR_UNIFORM = 1 } dd_prior;
+
+/* Classes per level-1 group of the two-level Gumbel-max draw. */
+#define DD_GUMBEL_GROUP 256
+/* Device error word bits. */
+#define DD_DEVERR_TOKEN 1
+
+/*
+ * Denoiser architecture.  Pre-LN transformer, non-causal attention:
+ *   h = tok_emb[z] + pos_emb[l] + temb(alpha_t)       (temb only if time_cond)
+ *   temb_j = sin(tau w_j) (j < d/2), cos(tau w_{j-d/2}) (j >= d/2),
+ *   w_i = 10000^(-i/(d/2)), tau = 1000 (1 - alpha_t)
+ *   per layer: h += W_o attn(LN1(h)) + b_o ; h += W_2 gelu_tanh(W_1 LN2(h) + b_1) + b_2
+ *   logits = W_out LN_f(h)                              (V columns, no bias)
+ * d_model even, d_model % n_heads == 0.  dtype DD_BF16: bf16 weights and
+ * activations, fp32 accumulation, fp32 residual stream, LayerNorm and softmax;
+ * DD_FP32: everything fp32 (validation build).
+ */
+typedef struct {
+    int32_t n_layers;
+    int32_t d_model;
+    int32_t n_heads;
+    int32_t d_mlp;
+    int32_t vocab;      /* V */
+    int32_t max_len;    /* rows of the position embedding; L <= max_len */
+    int32_t prior;      /* dd_prior: selects tok_emb rows (V + 1 or V) */
+    int32_t dtype;      /* dd_dtype of weights, activations and logits */
+    int32_t time_cond;  /* 1: add the sinusoidal time embedding */
+    float norm_eps;     /* LayerNorm epsilon (biased variance) */
+} dd_config;
+
+/* ---------------------------------------------------------------- layout */
+
+/*
+ * Parameter blob layout.  Tensor ids in order (every matrix is [out][in],
+ * row-major; each tensor starts at a 256-byte aligned offset; element type is
+ * cfg->dtype):
+ *   0 tok_emb [V+1 or V][d]   1 pos_emb [max_len][d]
+ *   per layer l, ids 2 + 12 l + :
+ *     0 ln1_g [d]  1 ln1_b [d]  2 w_qkv [3d][d]  3 b_qkv [3d]  4 w_o [d][d]  5 b_o [d]
+ *     6 ln2_g [d]  7 ln2_b [d]  8 w_1 [F][d]     9 b_1 [F]    10 w_2 [d][F] 11 b_2 [d]
+ *   then lnf_g [d], lnf_b [d], w_out [V][d].
+ * A vector reports rows = 1, cols = length.
+ */
+int32_t dd_param_count(const dd_config* cfg);
+dd_status dd_param_tensor(const dd_config* cfg, int32_t id, size_t* offset_bytes,
+                          int64_t* rows, int64_t* cols);
+size_t dd_param_bytes(const dd_config* cfg);
+
+/* Workspace for dd_denoise_forward (activations; the device error word is its
+ * first int32).  0 if the configuration is invalid. */
+size_t dd_workspace_bytes(const dd_config* cfg, int32_t B, int32_t L);
+/* Workspace for dd_sample_loop: the forward workspace plus one logit matrix. */
+size_t dd_loop_workspace_bytes(const dd_config* cfg, int32_t B, int32_t L);
+/* Recommended logit row stride (elements): V rounded up to a multiple of 64. */
+int64_t dd_logits_ld(int32_t V);
+/* Explicit-noise words per row: level-1 words (one per group, plus one for the
+ * mask class under the masked prior) followed by one word per real class. */
+int32_t dd_noise_width(int32_t prior, int32_t V);
+
+const char* dd_status_str(dd_status s);
+const char* dd_last_error(void);
+
+/* Zero the device error word at the start of a workspace (stream-ordered). */
+dd_status dd_workspace_reset(void* ws, void* stream);
+/* Synchronise `stream`, then copy *err_word (device) to *code_out (host). */
+dd_status dd_read_device_error(const int32_t* err_word, int32_t* code_out, void* stream);
+
+/* ---------------------------------------------------------------- compute */
+
+/*
+ * dd_init_params - fill the parameter blob (device, `params_bytes` >=
+ * dd_param_bytes(cfg)).
+ *   host_src == NULL: element e of tensor `id` is a normal drawn by Box-Muller
+ *     from Philox4x32-10 block (e>>1 low word, e>>1 high word, id, 3) under key
+ *     (seed low, seed high), words 0 and 1 (cosine for even e, sine for odd e);
+ *     value 0.02 z (gains: 1 + 0.02 z), computed in float64 and rounded to
+ *     nearest-even bf16 / fp32.  (The workloads ask for weights ~ N(0, 0.02).)
+ *   host_src != NULL: host blob of dd_param_bytes(cfg) bytes in the layout
+ *     above, copied as is.
+ */
+dd_status dd_init_params(const dd_config* cfg, void* params, size_t params_bytes,
+                         uint64_t seed, const void* host_src, void* stream);
+
+/*
+ * dd_denoise_forward - logits of x_theta(z_t, t) for B sequences of length L.
+ *   z_t     device int32 [B*L], ids in [0, n_tok)
+ *   alpha_t schedule value at t (conditions the time embedding), in [0, 1]
+ *   logits  device [B*L][ld] of cfg->dtype; columns >= V are left untouched
+ *   ld      row stride in elements, ld >= V, ld % 8 == 0
+ *   ws      device workspace of >= dd_workspace_bytes(cfg, B, L) bytes
+ */
+dd_status dd_denoise_forward(const dd_config* cfg, const void* params,
+                             const int32_t* z_t, int32_t B, int32_t L, double alpha_t,
+                             void* logits, int64_t ld, void* ws, size_t ws_bytes,
+                             void* stream);
+
+/*
+ * dd_posterior_sample - one reverse-posterior draw per row (App. A.1 / A.2 with
+ * x = softmax(logits); App. A.4 eq. psi-sampler at kappa_t = 1).
+ *   prior        dd_prior
+ *   logits       device [rows][ld] of logits_dtype (bf16 or fp32), finite or -inf;
+ *                ld >= V, ld % 8 == 0.  Under the masked prior only rows whose
+ *                z_t is the mask id are read.
+ *   z_t          device int32 [rows]; z_s device int32 [rows], may alias z_t
+ *   alpha_t, alpha_s  schedule values with 0 <= alpha_t < alpha_s <= 1 (s < t)
+ *   noise_words  NULL: Philox4x32-10 noise under key `seed`, counters
+ *                (index >> 2, row0 + row, step, 0) for level-1 word `index`
+ *                and (class >> 2, row0 + row, step, 1) for the level-2 word of
+ *                a class.  Otherwise device uint32 [rows][dd_noise_width] words.
+ *                A word w stands for the uniform u = (w + 1/2) 2^-32.
+ *   probs        NULL, or device fp32 [rows][K] that receives the posterior
+ *                probabilities (debug; slow).
+ *   dev_err      NULL or device int32 error word (DD_DEVERR_TOKEN is or-ed in).
+ * Draw: level 1 picks group g by argmax of log M_g + Gumbel (M_g = posterior
+ * mass of the group of DD_GUMBEL_GROUP consecutive classes; the mask class is a
+ * group of its own), level 2 picks the class in g by argmax of log p_j + Gumbel;
+ * the lowest index wins ties.  Masked prior: rows with z_t != mask are copied.
+ */
+dd_status dd_posterior_sample(int32_t prior, const void* logits, int32_t logits_dtype,
+                              int64_t ld, int32_t rows, int32_t V, const int32_t* z_t,
+                              double alpha_t, double alpha_s, const uint32_t* noise_words,
+                              uint64_t seed, uint32_t step, uint32_t row0, int32_t* z_s,
+                              float* probs, int32_t* dev_err, void* stream);
+
+/*
+ * dd_sample_loop - T ancestral steps z_1 -> z_0 on the grid t_k = k/T.
+ *   alphas       host double [T + 1], alphas[k] = alpha(k / T): alphas[0] = 1,
+ *                alphas[T] = 0 is not required but the values must strictly
+ *                decrease in k.
+ *   z            device int32 [B*L]; in: z_1, out: z_0
+ *   step k = T..1 runs dd_denoise_forward at alphas[k] and dd_posterior_sample
+ *   with (alpha_t, alpha_s) = (alphas[k], alphas[k-1]), step = k, row0 = 0 and
+ *   noise words noise_words + (k-1) * B*L * dd_noise_width (if non-NULL,
+ *   device uint32 [T][B*L][width]) or Philox under `noise_seed`.
+ *   z_trace      NULL or device int32 [T + 1][B*L]: z_1 then the state after
+ *                each step.
+ *   ws           device workspace >= dd_loop_workspace_bytes(cfg, B, L).
+ */
+dd_status dd_sample_loop(const dd_config* cfg, const void* params, int32_t B, int32_t L,
+                         int32_t T, const double* alphas, int32_t* z,
+                         const uint32_t* noise_words, uint64_t noise_seed,
+                         int32_t* z_trace, void* ws, size_t ws_bytes, void* stream);
+
+/*
+ * dd_gaussian_latent_argmax - z = argmax_v (alpha_tilde [v == x] + sigma eps_v)
+ * per row (App. A.5: uniform-state diffusion is the argmax projection of a
+ * Gaussian diffusion on one-hot vectors).  eps_v = Phi^-1(u) of the Philox word
+ * (v >> 2, row0 + row, step, 2) under `seed`; lowest index wins ties.
+ *   x      device int32 [rows], ids in [0, V);  z_out device int32 [rows] (may alias x)
+ *   alpha_tilde >= 0, sigma > 0 (the workloads use alpha_tilde^2 + sigma^2 = 1)
+ */
+dd_status dd_gaussian_latent_argmax(const int32_t* x, int32_t rows, int32_t V,
+                                    double alpha_tilde, double sigma, uint64_t seed,
+                                    uint32_t step, uint32_t row0, int32_t* z_out,
+                                    int32_t* dev_err, void* stream);
+
+/* ---------------------------------------------------------------- profiling */
+
+/*
+ * Per-launch timing with HIP events recorded on the launching stream.  While
+ * enabled, every kernel launch of the library is bracketed by an event pair and
+ * attributed to its kernel class.  Not thread-safe; meant for benchmarks.
+ */
+dd_status dd_profile_begin(int32_t max_launches);
+dd_status dd_profile_end(void);
+int32_t dd_profile_num_classes(void);
+/* Synchronises the recorded events; *name is a static string. */
+dd_status dd_profile_read(int32_t cls, const char** name, int64_t* launches, double* total_ms);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* DD_H */

@@ -72,12 +72,24 @@ def round_to(x, dtype):
 
 def normals(seed, tensor_id, count, start=0):
     """Standard normals for elements start .. start+count-1 of one tensor (float64)."""
-    e = np.arange(start, start + count, dtype=np.uint64)
+    return normals_at(seed, tensor_id, np.arange(start, start + count, dtype=np.uint64))
+
+
+def normals_at(seed, tensor_id, idx):
+    """Standard normals for the given flat element indices of one tensor (float64)."""
+    e = np.asarray(idx, dtype=np.uint64)
     pair = e >> np.uint64(1)
     k0, k1 = _ph.key_of(seed)
     w0, w1, _, _ = _ph.philox(pair & np.uint64(0xFFFFFFFF), pair >> np.uint64(32),
                               np.uint64(tensor_id), np.uint64(_ph.STREAM_PARAM), k0, k1)
     return _nz.box_muller(w0, w1, (e & np.uint64(1)).astype(bool))
+
+
+def values_at(cfg, seed, tensor_id, idx):
+    """Initial values of selected elements of one tensor, rounded like init_params."""
+    kind = specs(cfg)[tensor_id][2]
+    z = normals_at(seed, tensor_id, idx)
+    return round_to(0.02 * z if kind == "w" else 1.0 + 0.02 * z, cfg["dtype"])
 
 
 def init_params(cfg, seed):

@@ -1,0 +1,296 @@
+"""ctypes binding of libdd.so (include/dd.h).
+
+Argument marshalling only: every step of the reverse step runs in the HIP
+library.  Device buffers are torch tensors (data_ptr + the current HIP stream);
+each wrapper checks that the tensors it hands over are contiguous, on the GPU and
+large enough for the sizes it passes, so the library never reads or writes
+outside an allocation.  The library must have been built in-tree
+(python -m paper_2609_04010_amd.build); nothing falls back to another
+implementation when it is missing.
+"""
+import ctypes
+import os
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libdd.so")
+
+DD_BF16, DD_FP32 = 0, 1
+DD_PRIOR_MASK, DD_PRIOR_UNIFORM = 0, 1
+DD_GUMBEL_GROUP = 256
+DD_DEVERR_TOKEN = 1
+STATUS = {0: "DD_OK", 1: "DD_E_ARG", 2: "DD_E_SHAPE", 3: "DD_E_DTYPE", 4: "DD_E_WORKSPACE",
+          5: "DD_E_HIP", 6: "DD_E_UNSUPPORTED", 7: "DD_E_DEVICE"}
+
+EXPORTED = [
+    "dd_param_count", "dd_param_tensor", "dd_param_bytes", "dd_workspace_bytes",
+    "dd_loop_workspace_bytes", "dd_logits_ld", "dd_noise_width", "dd_status_str", "dd_last_error",
+    "dd_workspace_reset", "dd_read_device_error", "dd_init_params", "dd_denoise_forward",
+    "dd_posterior_sample", "dd_sample_loop", "dd_gaussian_latent_argmax", "dd_profile_begin",
+    "dd_profile_end", "dd_profile_num_classes", "dd_profile_read",
+]
+
+
+class DDConfig(ctypes.Structure):
+    _fields_ = [("n_layers", ctypes.c_int32), ("d_model", ctypes.c_int32),
+                ("n_heads", ctypes.c_int32), ("d_mlp", ctypes.c_int32),
+                ("vocab", ctypes.c_int32), ("max_len", ctypes.c_int32),
+                ("prior", ctypes.c_int32), ("dtype", ctypes.c_int32),
+                ("time_cond", ctypes.c_int32), ("norm_eps", ctypes.c_float)]
+
+
+class DDError(RuntimeError):
+    def __init__(self, status, msg):
+        super().__init__(f"{STATUS.get(status, status)}: {msg}")
+        self.status = status
+
+
+_lib = None
+
+
+def lib():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is not built; run `python -m paper_2609_04010_amd.build`")
+        L = ctypes.CDLL(LIB_PATH)
+        c = ctypes
+        P = c.c_void_p
+        cfgp = c.POINTER(DDConfig)
+        sig = {
+            "dd_param_count": (c.c_int32, [cfgp]),
+            "dd_param_tensor": (c.c_int32, [cfgp, c.c_int32, c.POINTER(c.c_size_t),
+                                            c.POINTER(c.c_int64), c.POINTER(c.c_int64)]),
+            "dd_param_bytes": (c.c_size_t, [cfgp]),
+            "dd_workspace_bytes": (c.c_size_t, [cfgp, c.c_int32, c.c_int32]),
+            "dd_loop_workspace_bytes": (c.c_size_t, [cfgp, c.c_int32, c.c_int32]),
+            "dd_logits_ld": (c.c_int64, [c.c_int32]),
+            "dd_noise_width": (c.c_int32, [c.c_int32, c.c_int32]),
+            "dd_status_str": (c.c_char_p, [c.c_int32]),
+            "dd_last_error": (c.c_char_p, []),
+            "dd_workspace_reset": (c.c_int32, [P, P]),
+            "dd_read_device_error": (c.c_int32, [P, c.POINTER(c.c_int32), P]),
+            "dd_init_params": (c.c_int32, [cfgp, P, c.c_size_t, c.c_uint64, P, P]),
+            "dd_denoise_forward": (c.c_int32, [cfgp, P, P, c.c_int32, c.c_int32, c.c_double, P,
+                                               c.c_int64, P, c.c_size_t, P]),
+            "dd_posterior_sample": (c.c_int32, [c.c_int32, P, c.c_int32, c.c_int64, c.c_int32,
+                                                c.c_int32, P, c.c_double, c.c_double, P,
+                                                c.c_uint64, c.c_uint32, c.c_uint32, P, P, P, P]),
+            "dd_sample_loop": (c.c_int32, [cfgp, P, c.c_int32, c.c_int32, c.c_int32,
+                                           c.POINTER(c.c_double), P, P, c.c_uint64, P, P,
+                                           c.c_size_t, P]),
+            "dd_gaussian_latent_argmax": (c.c_int32, [P, c.c_int32, c.c_int32, c.c_double,
+                                                      c.c_double, c.c_uint64, c.c_uint32,
+                                                      c.c_uint32, P, P, P]),
+            "dd_profile_begin": (c.c_int32, [c.c_int32]),
+            "dd_profile_end": (c.c_int32, []),
+            "dd_profile_num_classes": (c.c_int32, []),
+            "dd_profile_read": (c.c_int32, [c.c_int32, c.POINTER(c.c_char_p),
+                                            c.POINTER(c.c_int64), c.POINTER(c.c_double)]),
+        }
+        for name, (res, args) in sig.items():
+            f = getattr(L, name)
+            f.restype = res
+            f.argtypes = args
+        _lib = L
+    return _lib
+
+
+def _check(st):
+    if st != 0:
+        raise DDError(st, lib().dd_last_error().decode())
+
+
+def make_config(cfg):
+    """DDConfig from the architecture dictionary used by the workloads and the oracle."""
+    return DDConfig(int(cfg["n_layers"]), int(cfg["d_model"]), int(cfg["n_heads"]),
+                    int(cfg["d_mlp"]), int(cfg["vocab"]), int(cfg["max_len"]),
+                    DD_PRIOR_MASK if cfg["prior"] == "mask" else DD_PRIOR_UNIFORM,
+                    DD_BF16 if cfg["dtype"] == "bf16" else DD_FP32,
+                    1 if cfg.get("time_cond", True) else 0, float(cfg.get("norm_eps", 1e-5)))
+
+
+def prior_code(prior):
+    return DD_PRIOR_MASK if prior == "mask" else DD_PRIOR_UNIFORM
+
+
+def dtype_code(dtype):
+    return DD_BF16 if dtype == "bf16" else DD_FP32
+
+
+# ---------------------------------------------------------------- host-only queries
+
+def param_count(cfg):
+    return lib().dd_param_count(ctypes.byref(make_config(cfg)))
+
+
+def param_tensor(cfg, tid):
+    off, r, c = ctypes.c_size_t(), ctypes.c_int64(), ctypes.c_int64()
+    _check(lib().dd_param_tensor(ctypes.byref(make_config(cfg)), tid, ctypes.byref(off),
+                                 ctypes.byref(r), ctypes.byref(c)))
+    return off.value, r.value, c.value
+
+
+def param_bytes(cfg):
+    return lib().dd_param_bytes(ctypes.byref(make_config(cfg)))
+
+
+def workspace_bytes(cfg, B, L):
+    return lib().dd_workspace_bytes(ctypes.byref(make_config(cfg)), B, L)
+
+
+def loop_workspace_bytes(cfg, B, L):
+    return lib().dd_loop_workspace_bytes(ctypes.byref(make_config(cfg)), B, L)
+
+
+def logits_ld(V):
+    return lib().dd_logits_ld(V)
+
+
+def noise_width(prior, V):
+    return lib().dd_noise_width(prior_code(prior), V)
+
+
+def pack_params(cfg, tensors_by_id):
+    """Host blob in the library's parameter layout from a list of float arrays (id order)."""
+    nbytes = param_bytes(cfg)
+    blob = np.zeros(nbytes, dtype=np.uint8)
+    for tid, arr in enumerate(tensors_by_id):
+        off, r, c = param_tensor(cfg, tid)
+        a = np.asarray(arr, dtype=np.float64).reshape(-1)
+        assert a.size == r * c, (tid, a.shape, r, c)
+        f = a.astype(np.float32)
+        if cfg["dtype"] == "bf16":
+            u = f.view(np.uint32)
+            if not np.array_equal(u & 0xFFFF, np.zeros_like(u)):
+                raise ValueError(f"tensor {tid} is not exactly representable in bf16")
+            raw = (u >> 16).astype(np.uint16).view(np.uint8)
+        else:
+            raw = f.view(np.uint8)
+        blob[off:off + raw.size] = raw
+    return blob
+
+
+# ---------------------------------------------------------------- device calls
+
+def _torch():
+    import torch
+    return torch
+
+
+def _stream():
+    return ctypes.c_void_p(_torch().cuda.current_stream().cuda_stream)
+
+
+def _ptr(t, nbytes, name, dtype=None):
+    """Device pointer of a contiguous GPU tensor holding at least `nbytes` bytes."""
+    if t is None:
+        return None
+    torch = _torch()
+    if not isinstance(t, torch.Tensor) or not t.is_cuda:
+        raise TypeError(f"{name} must be a GPU tensor")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if dtype is not None and t.dtype != dtype:
+        raise TypeError(f"{name} must have dtype {dtype}, got {t.dtype}")
+    have = t.numel() * t.element_size()
+    if have < nbytes:
+        raise ValueError(f"{name} holds {have} bytes, needs {nbytes}")
+    return ctypes.c_void_p(t.data_ptr())
+
+
+def init_params(cfg, params, seed=0, host_blob=None):
+    need = param_bytes(cfg)
+    src = None
+    if host_blob is not None:
+        host_blob = np.ascontiguousarray(host_blob, dtype=np.uint8)
+        if host_blob.size < need:
+            raise ValueError("host blob too small")
+        src = host_blob.ctypes.data_as(ctypes.c_void_p)
+    _check(lib().dd_init_params(ctypes.byref(make_config(cfg)), _ptr(params, need, "params"),
+                                params.numel() * params.element_size(), int(seed), src, _stream()))
+    if host_blob is not None:
+        _torch().cuda.current_stream().synchronize()   # the host blob must outlive the copy
+
+
+def denoise_forward(cfg, params, z_t, B, L, alpha_t, logits, ld, ws):
+    torch = _torch()
+    es = 2 if cfg["dtype"] == "bf16" else 4
+    M = B * L
+    _check(lib().dd_denoise_forward(
+        ctypes.byref(make_config(cfg)), _ptr(params, param_bytes(cfg), "params"),
+        _ptr(z_t, 4 * M, "z_t", torch.int32), B, L, float(alpha_t),
+        _ptr(logits, es * M * ld, "logits"), int(ld),
+        _ptr(ws, workspace_bytes(cfg, B, L), "ws"), ws.numel() * ws.element_size(), _stream()))
+
+
+def posterior_sample(prior, logits, logits_dtype, ld, rows, V, z_t, alpha_t, alpha_s, z_s,
+                     noise_words=None, seed=0, step=0, row0=0, probs=None, dev_err=None):
+    torch = _torch()
+    es = 2 if logits_dtype == "bf16" else 4
+    K = V + 1 if prior == "mask" else V
+    nu = noise_width(prior, V)
+    lg = _ptr(logits, es * rows * ld, "logits") if rows > 0 else None
+    _check(lib().dd_posterior_sample(
+        prior_code(prior), lg, dtype_code(logits_dtype), int(ld), int(rows), int(V),
+        _ptr(z_t, 4 * rows, "z_t", torch.int32), float(alpha_t), float(alpha_s),
+        _ptr(noise_words, 4 * rows * nu, "noise_words", torch.int32) if noise_words is not None else None,
+        int(seed) & 0xFFFFFFFFFFFFFFFF, int(step), int(row0), _ptr(z_s, 4 * rows, "z_s", torch.int32),
+        _ptr(probs, 4 * rows * K, "probs", torch.float32) if probs is not None else None,
+        _ptr(dev_err, 4, "dev_err", torch.int32) if dev_err is not None else None, _stream()))
+
+
+def sample_loop(cfg, params, B, L, T, alphas, z, ws, noise_words=None, noise_seed=0, z_trace=None):
+    torch = _torch()
+    M = B * L
+    a = np.ascontiguousarray(alphas, dtype=np.float64)
+    if a.shape != (T + 1,):
+        raise ValueError("alphas must hold T + 1 values")
+    nu = noise_width(cfg["prior"], cfg["vocab"])
+    _check(lib().dd_sample_loop(
+        ctypes.byref(make_config(cfg)), _ptr(params, param_bytes(cfg), "params"), B, L, T,
+        a.ctypes.data_as(ctypes.POINTER(ctypes.c_double)), _ptr(z, 4 * M, "z", torch.int32),
+        _ptr(noise_words, 4 * T * M * nu, "noise_words", torch.int32) if noise_words is not None else None,
+        int(noise_seed) & 0xFFFFFFFFFFFFFFFF,
+        _ptr(z_trace, 4 * (T + 1) * M, "z_trace", torch.int32) if z_trace is not None else None,
+        _ptr(ws, loop_workspace_bytes(cfg, B, L), "ws"), ws.numel() * ws.element_size(), _stream()))
+
+
+def gaussian_latent_argmax(x, rows, V, alpha_tilde, sigma, seed, step, z_out, row0=0, dev_err=None):
+    torch = _torch()
+    _check(lib().dd_gaussian_latent_argmax(
+        _ptr(x, 4 * rows, "x", torch.int32), int(rows), int(V), float(alpha_tilde), float(sigma),
+        int(seed) & 0xFFFFFFFFFFFFFFFF, int(step), int(row0), _ptr(z_out, 4 * rows, "z_out", torch.int32),
+        _ptr(dev_err, 4, "dev_err", torch.int32) if dev_err is not None else None, _stream()))
+
+
+def workspace_reset(ws):
+    _check(lib().dd_workspace_reset(_ptr(ws, 4, "ws"), _stream()))
+
+
+def read_device_error(err):
+    code = ctypes.c_int32(0)
+    st = lib().dd_read_device_error(_ptr(err, 4, "err"), ctypes.byref(code), _stream())
+    if st not in (0, 7):
+        _check(st)
+    return code.value
+
+
+def profile_begin(max_launches):
+    _check(lib().dd_profile_begin(int(max_launches)))
+
+
+def profile_end():
+    _check(lib().dd_profile_end())
+
+
+def profile_read():
+    """{class name: (launches, total ms)} for every class with at least one launch."""
+    out = {}
+    for c in range(lib().dd_profile_num_classes()):
+        name, n, ms = ctypes.c_char_p(), ctypes.c_int64(), ctypes.c_double()
+        _check(lib().dd_profile_read(c, ctypes.byref(name), ctypes.byref(n), ctypes.byref(ms)))
+        if n.value:
+            out[name.value.decode()] = (n.value, ms.value)
+    return out

@@ -1,0 +1,80 @@
+// Shared device/host helpers of the gfx950 reverse-step library.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "dd.h"
+
+#define DD_DEV __device__ __forceinline__
+
+typedef uint16_t bf16_t;  // raw bfloat16 bits
+
+// ---------------------------------------------------------------- bf16 <-> fp32
+DD_DEV float bf16_lo(uint32_t pair) { return __uint_as_float(pair << 16); }
+DD_DEV float bf16_hi(uint32_t pair) { return __uint_as_float(pair & 0xFFFF0000u); }
+DD_DEV float bf16_to_f32(bf16_t b) { return __uint_as_float(((uint32_t)b) << 16); }
+
+// Round-to-nearest-even fp32 -> bf16 (finite inputs).
+DD_DEV bf16_t f32_to_bf16(float f) {
+    uint32_t u = __float_as_uint(f);
+    u += 0x7FFFu + ((u >> 16) & 1u);
+    return (bf16_t)(u >> 16);
+}
+DD_DEV uint32_t pack_bf16x2(float lo, float hi) {
+    return (uint32_t)f32_to_bf16(lo) | ((uint32_t)f32_to_bf16(hi) << 16);
+}
+
+// Round-to-nearest-even float64 -> bf16 directly (no intermediate fp32 rounding).
+DD_DEV bf16_t f64_to_bf16(double v) {
+    uint64_t b = (uint64_t)__double_as_longlong(v);
+    uint32_t sign = (uint32_t)(b >> 63);
+    uint64_t mag = b & 0x7FFFFFFFFFFFFFFFull;
+    if (mag == 0) return (bf16_t)(sign << 15);
+    // keep 7 mantissa bits of 52: round at bit 45, ties to even
+    uint64_t lsb = (mag >> 45) & 1ull;
+    mag += (1ull << 44) - 1ull + lsb;
+    int32_t e11 = (int32_t)(mag >> 52);
+    uint32_t m7 = (uint32_t)((mag >> 45) & 0x7Full);
+    int32_t e8 = e11 - 1023 + 127;
+    if (e8 <= 0) return (bf16_t)(sign << 15);           // below bf16 normals: flush
+    if (e8 >= 255) return (bf16_t)((sign << 15) | 0x7F80u);
+    return (bf16_t)((sign << 15) | ((uint32_t)e8 << 7) | m7);
+}
+
+// ---------------------------------------------------------------- wave helpers
+DD_DEV float wave_sum(float v) {
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+    return v;
+}
+DD_DEV float wave_max(float v) {
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
+    return v;
+}
+
+// ---------------------------------------------------------------- host helpers
+namespace dd {
+
+void set_error(const char* fmt, ...);
+dd_status launch_status(const char* what);
+
+// Profiling hooks around each launch (no-ops unless dd_profile_begin was called).
+enum KernelClass {
+    KC_TEMB = 0, KC_EMBED_LN, KC_LN, KC_GEMM_QKV, KC_ATTN, KC_GEMM_O, KC_GEMM_MLP1,
+    KC_GEMM_MLP2, KC_GEMM_VOCAB, KC_POSTERIOR, KC_LATENT, KC_INIT, KC_COPY, KC_COUNT
+};
+void prof_start(int cls, hipStream_t s);
+void prof_stop(int cls, hipStream_t s);
+
+struct ProfScope {
+    int cls;
+    hipStream_t s;
+    ProfScope(int c, hipStream_t st) : cls(c), s(st) { prof_start(cls, s); }
+    ~ProfScope() { prof_stop(cls, s); }
+};
+
+inline int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
+
+}  // namespace dd

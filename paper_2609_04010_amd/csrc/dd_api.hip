@@ -1,0 +1,502 @@
+// Host side of the C ABI declared in include/dd.h: validation, parameter and workspace layouts,
+// kernel dispatch, the T-step loop driver and the launch profiler.
+#include <math.h>
+#include <stdarg.h>
+#include <stdio.h>
+#include <string.h>
+
+#include <vector>
+
+#include "kernels.h"
+
+namespace dd {
+
+// ---------------------------------------------------------------- errors
+static thread_local char g_err[512] = "";
+
+void set_error(const char* fmt, ...) {
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(g_err, sizeof(g_err), fmt, ap);
+    va_end(ap);
+}
+
+dd_status launch_status(const char* what) {
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) {
+        set_error("%s: launch failed: %s", what, hipGetErrorString(e));
+        return DD_E_HIP;
+    }
+    return DD_OK;
+}
+
+#define DD_TRY(x)                            \
+    do {                                     \
+        const dd_status st_ = (x);           \
+        if (st_ != DD_OK) return st_;        \
+    } while (0)
+
+#define DD_CHECK(cond, code, ...)            \
+    do {                                     \
+        if (!(cond)) {                       \
+            set_error(__VA_ARGS__);          \
+            return code;                     \
+        }                                    \
+    } while (0)
+
+// ---------------------------------------------------------------- profiler
+static const char* kClassNames[KC_COUNT] = {
+    "time_embedding", "embed_layernorm", "layernorm", "gemm_qkv", "attention", "gemm_attn_out",
+    "gemm_mlp_up", "gemm_mlp_down", "gemm_vocab", "posterior_sample", "gaussian_latent",
+    "init_params", "copy"};
+
+struct Profiler {
+    bool on = false;
+    int cap = 0;
+    std::vector<hipEvent_t> ev;   // 2 per launch
+    std::vector<int> cls;         // class per launch
+    int open = -1;                // index of the launch whose start was recorded
+    int64_t dropped = 0;
+};
+static Profiler g_prof;
+
+void prof_start(int c, hipStream_t s) {
+    if (!g_prof.on) return;
+    const int n = (int)g_prof.cls.size();
+    if (n >= g_prof.cap) { g_prof.dropped++; g_prof.open = -1; return; }
+    (void)hipEventRecord(g_prof.ev[2 * n], s);
+    g_prof.cls.push_back(c);
+    g_prof.open = n;
+}
+
+void prof_stop(int c, hipStream_t s) {
+    if (!g_prof.on || g_prof.open < 0) return;
+    (void)hipEventRecord(g_prof.ev[2 * g_prof.open + 1], s);
+    (void)c;
+    g_prof.open = -1;
+}
+
+// ---------------------------------------------------------------- layouts
+struct Tensor {
+    size_t off;
+    int64_t rows, cols;
+};
+
+static size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+static size_t esize(int dtype) { return dtype == DD_BF16 ? 2 : 4; }
+
+static bool cfg_ok(const dd_config* c) {
+    if (!c) { set_error("config is NULL"); return false; }
+    if (c->n_layers < 0 || c->d_model <= 0 || c->n_heads <= 0 || c->d_mlp <= 0 || c->vocab <= 0 ||
+        c->max_len <= 0) {
+        set_error("config sizes must be positive");
+        return false;
+    }
+    if (c->d_model % c->n_heads != 0 || c->d_model % 2 != 0) {
+        set_error("d_model must be even and divisible by n_heads");
+        return false;
+    }
+    if (c->prior != DD_PRIOR_MASK && c->prior != DD_PRIOR_UNIFORM) { set_error("unknown prior"); return false; }
+    if (c->dtype != DD_BF16 && c->dtype != DD_FP32) { set_error("unknown dtype"); return false; }
+    if (!(c->norm_eps >= 0.f)) { set_error("norm_eps must be >= 0"); return false; }
+    return true;
+}
+
+static int n_tok(const dd_config* c) { return c->prior == DD_PRIOR_MASK ? c->vocab + 1 : c->vocab; }
+
+static std::vector<Tensor> tensor_list(const dd_config* c) {
+    const int64_t d = c->d_model, F = c->d_mlp, V = c->vocab;
+    std::vector<std::pair<int64_t, int64_t>> shapes;
+    shapes.push_back({n_tok(c), d});
+    shapes.push_back({c->max_len, d});
+    for (int l = 0; l < c->n_layers; ++l) {
+        shapes.push_back({1, d});      shapes.push_back({1, d});
+        shapes.push_back({3 * d, d});  shapes.push_back({1, 3 * d});
+        shapes.push_back({d, d});      shapes.push_back({1, d});
+        shapes.push_back({1, d});      shapes.push_back({1, d});
+        shapes.push_back({F, d});      shapes.push_back({1, F});
+        shapes.push_back({d, F});      shapes.push_back({1, d});
+    }
+    shapes.push_back({1, d});
+    shapes.push_back({1, d});
+    shapes.push_back({V, d});
+    std::vector<Tensor> t;
+    size_t off = 0;
+    const size_t es = esize(c->dtype);
+    for (auto& s : shapes) {
+        t.push_back({off, s.first, s.second});
+        off = align256(off + (size_t)(s.first * s.second) * es);
+    }
+    return t;
+}
+
+static bool is_gain(const dd_config* c, int id) {
+    const int nt = 2 + 12 * c->n_layers + 3;
+    if (id == nt - 3) return true;                  // lnf_g
+    if (id >= 2 && id < 2 + 12 * c->n_layers) {
+        const int k = (id - 2) % 12;
+        return k == 0 || k == 6;                      // ln1_g, ln2_g
+    }
+    return false;
+}
+
+struct WsLayout {
+    size_t err, temb, h, xln, qkv, att, mlp, logits, total_fwd, total_loop;
+};
+
+static WsLayout ws_layout(const dd_config* c, int64_t M) {
+    const size_t es = esize(c->dtype);
+    const int64_t d = c->d_model, F = c->d_mlp;
+    WsLayout w;
+    size_t off = 0;
+    w.err = off; off = align256(off + 4);
+    w.temb = off; off = align256(off + (size_t)d * 4);
+    w.h = off; off = align256(off + (size_t)(M * d) * 4);
+    w.xln = off; off = align256(off + (size_t)(M * d) * es);
+    w.qkv = off; off = align256(off + (size_t)(M * 3 * d) * es);
+    w.att = off; off = align256(off + (size_t)(M * d) * es);
+    w.mlp = off; off = align256(off + (size_t)(M * F) * es);
+    w.total_fwd = off;
+    w.logits = off;
+    const int64_t ld = (c->vocab + 63) / 64 * 64;
+    off = align256(off + (size_t)(M * ld) * es);
+    w.total_loop = off;
+    return w;
+}
+
+static bool forward_supported(const dd_config* c) {
+    const int dh = c->d_model / c->n_heads;
+    if (!ln_supported(c->d_model)) {
+        set_error("d_model %d: LayerNorm kernels need d_model %% 64 == 0 and d_model <= 2048", c->d_model);
+        return false;
+    }
+    if (!attn_supported(c->dtype, dh)) {
+        set_error("head dim %d unsupported for this dtype (bf16: 64; fp32: 16/32/64/128)", dh);
+        return false;
+    }
+    if (c->d_mlp % 8 != 0) { set_error("d_mlp must be a multiple of 8"); return false; }
+    return true;
+}
+
+static dd_status run_forward(const dd_config* c, const void* params, const int32_t* z, int32_t B,
+                             int32_t L, double alpha_t, void* logits, int64_t ld, char* ws,
+                             hipStream_t s) {
+    const std::vector<Tensor> T = tensor_list(c);
+    const WsLayout w = ws_layout(c, (int64_t)B * L);
+    const char* P = (const char*)params;
+    auto tp = [&](int id) -> const void* { return P + T[id].off; };
+    const int d = c->d_model, F = c->d_mlp, H = c->n_heads, V = c->vocab, nl = c->n_layers;
+    const int64_t M = (int64_t)B * L;
+    const int dt = c->dtype;
+    const size_t es = esize(dt);
+    int32_t* err = (int32_t*)(ws + w.err);
+    float* temb = (float*)(ws + w.temb);
+    float* h = (float*)(ws + w.h);
+    void* xln = ws + w.xln;
+    void* qkv = ws + w.qkv;
+    void* att = ws + w.att;
+    void* mlp = ws + w.mlp;
+    const int lnf = 2 + 12 * nl;
+
+    if (c->time_cond) DD_TRY(launch_temb(temb, d, 1000.0 * (1.0 - alpha_t), s));
+    const int g0 = nl > 0 ? 2 : lnf;
+    DD_TRY(launch_embed_ln(dt, z, M, L, n_tok(c), d, tp(0), tp(1), c->time_cond ? temb : nullptr,
+                           tp(g0), tp(g0 + 1), c->norm_eps, h, xln, err, s));
+    for (int l = 0; l < nl; ++l) {
+        const int b = 2 + 12 * l;
+        GemmArgs g;
+        g = {xln, d, tp(b + 2), d, tp(b + 3), qkv, 3 * d, (int)M, 3 * d, d};
+        DD_TRY(launch_gemm(dt, EPI_BIAS, KC_GEMM_QKV, g, s));
+        AttnArgs aa = {qkv, 3 * d, att, d, B, L, H, d,
+                       (float)(1.4426950408889634 / sqrt((double)(d / H)))};
+        DD_TRY(launch_attn(dt, aa, s));
+        g = {att, d, tp(b + 4), d, tp(b + 5), h, d, (int)M, d, d};
+        DD_TRY(launch_gemm(dt, EPI_BIAS_RESID, KC_GEMM_O, g, s));
+        DD_TRY(launch_ln(dt, h, M, d, tp(b + 6), tp(b + 7), c->norm_eps, xln, s));
+        g = {xln, d, tp(b + 8), d, tp(b + 9), mlp, F, (int)M, F, d};
+        DD_TRY(launch_gemm(dt, EPI_BIAS_GELU, KC_GEMM_MLP1, g, s));
+        g = {mlp, F, tp(b + 10), F, tp(b + 11), h, d, (int)M, d, F};
+        DD_TRY(launch_gemm(dt, EPI_BIAS_RESID, KC_GEMM_MLP2, g, s));
+        const int gn = (l + 1 < nl) ? b + 12 : lnf;
+        DD_TRY(launch_ln(dt, h, M, d, tp(gn), tp(gn + 1), c->norm_eps, xln, s));
+    }
+    GemmArgs g = {xln, d, tp(lnf + 2), d, nullptr, logits, ld, (int)M, V, d};
+    DD_TRY(launch_gemm(dt, EPI_PLAIN, KC_GEMM_VOCAB, g, s));
+    (void)es;
+    return DD_OK;
+}
+
+static dd_status check_schedule(double at, double as) {
+    DD_CHECK(at >= 0.0 && as <= 1.0 && at < as, DD_E_ARG,
+             "schedule values must satisfy 0 <= alpha_t < alpha_s <= 1 (got %.17g, %.17g)", at, as);
+    return DD_OK;
+}
+
+static int32_t ntop_of(int prior, int V) {
+    return (V + DD_GUMBEL_GROUP - 1) / DD_GUMBEL_GROUP + (prior == DD_PRIOR_MASK ? 1 : 0);
+}
+
+static PostArgs make_post(int prior, const void* logits, int64_t ld, int32_t rows, int32_t V,
+                          const int32_t* z_t, double at, double as, const uint32_t* noise,
+                          uint64_t seed, uint32_t step, uint32_t row0, int32_t* z_s, float* probs,
+                          int32_t* err) {
+    PostArgs a;
+    memset(&a, 0, sizeof(a));
+    a.logits = logits; a.ld = ld; a.rows = rows; a.V = V; a.prior = prior;
+    a.z_t = z_t; a.z_s = z_s;
+    if (prior == DD_PRIOR_MASK) {
+        a.wx = (as - at) / (1.0 - at);
+        a.wm = (1.0 - as) / (1.0 - at);
+        a.log_wx = log(a.wx);
+        a.log_wm = a.wm > 0.0 ? log(a.wm) : -INFINITY;
+    } else {
+        const double K = (double)V, ats = at / as;
+        a.c_x = as - at;
+        a.c_u = (1.0 - ats) * (1.0 - as) / K;
+        a.c_z = ats - at;
+        a.Ka_t = K * at;
+        a.one_m_at = 1.0 - at;
+    }
+    a.noise = noise;
+    a.ntop = ntop_of(prior, V);
+    a.nu = a.ntop + V;
+    a.seed = seed; a.step = step; a.row0 = row0;
+    a.probs = probs; a.err = err;
+    return a;
+}
+
+__global__ void fill_i32_kernel(int32_t* p, int32_t v, int64_t n) {
+    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i < n) p[i] = v;
+}
+
+}  // namespace dd
+
+using namespace dd;
+
+extern "C" {
+
+const char* dd_status_str(dd_status s) {
+    switch (s) {
+        case DD_OK: return "ok";
+        case DD_E_ARG: return "invalid argument";
+        case DD_E_SHAPE: return "inconsistent shape";
+        case DD_E_DTYPE: return "unknown dtype";
+        case DD_E_WORKSPACE: return "buffer too small";
+        case DD_E_HIP: return "HIP runtime error";
+        case DD_E_UNSUPPORTED: return "unsupported configuration";
+        case DD_E_DEVICE: return "device error word set";
+    }
+    return "unknown status";
+}
+
+const char* dd_last_error(void) { return g_err; }
+
+int32_t dd_param_count(const dd_config* cfg) {
+    if (!cfg_ok(cfg)) return 0;
+    return 2 + 12 * cfg->n_layers + 3;
+}
+
+dd_status dd_param_tensor(const dd_config* cfg, int32_t id, size_t* offset_bytes, int64_t* rows,
+                          int64_t* cols) {
+    DD_CHECK(cfg_ok(cfg), DD_E_ARG, "%s", g_err);
+    DD_CHECK(offset_bytes && rows && cols, DD_E_ARG, "output pointers must not be NULL");
+    const std::vector<Tensor> t = tensor_list(cfg);
+    DD_CHECK(id >= 0 && id < (int32_t)t.size(), DD_E_ARG, "tensor id %d out of range", id);
+    *offset_bytes = t[id].off;
+    *rows = t[id].rows;
+    *cols = t[id].cols;
+    return DD_OK;
+}
+
+size_t dd_param_bytes(const dd_config* cfg) {
+    if (!cfg_ok(cfg)) return 0;
+    const std::vector<Tensor> t = tensor_list(cfg);
+    const Tensor& l = t.back();
+    return align256(l.off + (size_t)(l.rows * l.cols) * esize(cfg->dtype));
+}
+
+size_t dd_workspace_bytes(const dd_config* cfg, int32_t B, int32_t L) {
+    if (!cfg_ok(cfg) || B <= 0 || L <= 0) return 0;
+    return ws_layout(cfg, (int64_t)B * L).total_fwd;
+}
+
+size_t dd_loop_workspace_bytes(const dd_config* cfg, int32_t B, int32_t L) {
+    if (!cfg_ok(cfg) || B <= 0 || L <= 0) return 0;
+    return ws_layout(cfg, (int64_t)B * L).total_loop;
+}
+
+int64_t dd_logits_ld(int32_t V) { return V <= 0 ? 0 : ((int64_t)V + 63) / 64 * 64; }
+
+int32_t dd_noise_width(int32_t prior, int32_t V) {
+    if (V <= 0 || (prior != DD_PRIOR_MASK && prior != DD_PRIOR_UNIFORM)) return 0;
+    return ntop_of(prior, V) + V;
+}
+
+dd_status dd_workspace_reset(void* ws, void* stream) {
+    DD_CHECK(ws, DD_E_ARG, "workspace is NULL");
+    hipLaunchKernelGGL(fill_i32_kernel, dim3(1), dim3(64), 0, (hipStream_t)stream, (int32_t*)ws, 0,
+                       (int64_t)1);
+    return launch_status("workspace_reset");
+}
+
+dd_status dd_read_device_error(const int32_t* err_word, int32_t* code_out, void* stream) {
+    DD_CHECK(err_word && code_out, DD_E_ARG, "NULL pointer");
+    hipError_t e = hipStreamSynchronize((hipStream_t)stream);
+    if (e == hipSuccess) e = hipMemcpy(code_out, err_word, sizeof(int32_t), hipMemcpyDeviceToHost);
+    DD_CHECK(e == hipSuccess, DD_E_HIP, "read_device_error: %s", hipGetErrorString(e));
+    return *code_out ? DD_E_DEVICE : DD_OK;
+}
+
+dd_status dd_init_params(const dd_config* cfg, void* params, size_t params_bytes, uint64_t seed,
+                         const void* host_src, void* stream) {
+    DD_CHECK(cfg_ok(cfg), DD_E_ARG, "%s", g_err);
+    DD_CHECK(params, DD_E_ARG, "params is NULL");
+    const size_t need = dd_param_bytes(cfg);
+    DD_CHECK(params_bytes >= need, DD_E_WORKSPACE, "parameter buffer has %zu bytes, needs %zu",
+             params_bytes, need);
+    hipStream_t s = (hipStream_t)stream;
+    if (host_src) {
+        const hipError_t e = hipMemcpyAsync(params, host_src, need, hipMemcpyHostToDevice, s);
+        DD_CHECK(e == hipSuccess, DD_E_HIP, "init_params copy: %s", hipGetErrorString(e));
+        return DD_OK;
+    }
+    const std::vector<Tensor> t = tensor_list(cfg);
+    for (int id = 0; id < (int)t.size(); ++id) {
+        DD_TRY(launch_init((char*)params + t[id].off, t[id].rows * t[id].cols, (uint32_t)id,
+                           is_gain(cfg, id) ? 1.0 : 0.0, cfg->dtype == DD_BF16, seed, s));
+    }
+    return DD_OK;
+}
+
+dd_status dd_denoise_forward(const dd_config* cfg, const void* params, const int32_t* z_t,
+                             int32_t B, int32_t L, double alpha_t, void* logits, int64_t ld,
+                             void* ws, size_t ws_bytes, void* stream) {
+    DD_CHECK(cfg_ok(cfg), DD_E_ARG, "%s", g_err);
+    DD_CHECK(params && z_t && logits && ws, DD_E_ARG, "NULL pointer argument");
+    DD_CHECK(B > 0 && L > 0, DD_E_ARG, "B and L must be positive");
+    DD_CHECK(L <= cfg->max_len, DD_E_SHAPE, "L = %d exceeds max_len = %d", L, cfg->max_len);
+    DD_CHECK(alpha_t >= 0.0 && alpha_t <= 1.0, DD_E_ARG, "alpha_t must lie in [0, 1]");
+    DD_CHECK(ld >= cfg->vocab && ld % 8 == 0, DD_E_SHAPE, "ld must be >= V and a multiple of 8");
+    DD_CHECK(forward_supported(cfg), DD_E_UNSUPPORTED, "%s", g_err);
+    const size_t need = dd_workspace_bytes(cfg, B, L);
+    DD_CHECK(ws_bytes >= need, DD_E_WORKSPACE, "workspace has %zu bytes, needs %zu", ws_bytes, need);
+    return run_forward(cfg, params, z_t, B, L, alpha_t, logits, ld, (char*)ws, (hipStream_t)stream);
+}
+
+dd_status dd_posterior_sample(int32_t prior, const void* logits, int32_t logits_dtype, int64_t ld,
+                              int32_t rows, int32_t V, const int32_t* z_t, double alpha_t,
+                              double alpha_s, const uint32_t* noise_words, uint64_t seed,
+                              uint32_t step, uint32_t row0, int32_t* z_s, float* probs,
+                              int32_t* dev_err, void* stream) {
+    DD_CHECK(prior == DD_PRIOR_MASK || prior == DD_PRIOR_UNIFORM, DD_E_ARG, "unknown prior %d", prior);
+    DD_CHECK(logits_dtype == DD_BF16 || logits_dtype == DD_FP32, DD_E_DTYPE, "unknown logits dtype");
+    DD_CHECK(rows >= 0 && V > 0, DD_E_ARG, "rows must be >= 0 and V > 0");
+    DD_CHECK(V <= (1 << 24), DD_E_UNSUPPORTED, "V > 2^24 unsupported");
+    DD_CHECK(ld >= V && ld % 8 == 0, DD_E_SHAPE, "ld must be >= V and a multiple of 8");
+    DD_TRY(check_schedule(alpha_t, alpha_s));
+    if (rows == 0) return DD_OK;
+    DD_CHECK(logits && z_t && z_s, DD_E_ARG, "NULL pointer argument");
+    const PostArgs a = make_post(prior, logits, ld, rows, V, z_t, alpha_t, alpha_s, noise_words,
+                                 seed, step, row0, z_s, probs, dev_err);
+    return launch_posterior(a, logits_dtype, (hipStream_t)stream);
+}
+
+dd_status dd_sample_loop(const dd_config* cfg, const void* params, int32_t B, int32_t L,
+                         int32_t T, const double* alphas, int32_t* z, const uint32_t* noise_words,
+                         uint64_t noise_seed, int32_t* z_trace, void* ws, size_t ws_bytes,
+                         void* stream) {
+    DD_CHECK(cfg_ok(cfg), DD_E_ARG, "%s", g_err);
+    DD_CHECK(params && z && ws && alphas, DD_E_ARG, "NULL pointer argument");
+    DD_CHECK(B > 0 && L > 0 && T > 0, DD_E_ARG, "B, L and T must be positive");
+    DD_CHECK(L <= cfg->max_len, DD_E_SHAPE, "L = %d exceeds max_len = %d", L, cfg->max_len);
+    DD_CHECK(forward_supported(cfg), DD_E_UNSUPPORTED, "%s", g_err);
+    for (int k = 1; k <= T; ++k) DD_TRY(check_schedule(alphas[k], alphas[k - 1]));
+    const size_t need = dd_loop_workspace_bytes(cfg, B, L);
+    DD_CHECK(ws_bytes >= need, DD_E_WORKSPACE, "workspace has %zu bytes, needs %zu", ws_bytes, need);
+    hipStream_t s = (hipStream_t)stream;
+    const int64_t M = (int64_t)B * L;
+    const WsLayout w = ws_layout(cfg, M);
+    char* wsc = (char*)ws;
+    void* logits = wsc + w.logits;
+    const int64_t ld = dd_logits_ld(cfg->vocab);
+    const int32_t nu = dd_noise_width(cfg->prior, cfg->vocab);
+    auto trace_copy = [&](int slot) -> dd_status {
+        if (!z_trace) return DD_OK;
+        ProfScope ps(KC_COPY, s);
+        const hipError_t e = hipMemcpyAsync(z_trace + (int64_t)slot * M, z, M * sizeof(int32_t),
+                                            hipMemcpyDeviceToDevice, s);
+        DD_CHECK(e == hipSuccess, DD_E_HIP, "trace copy: %s", hipGetErrorString(e));
+        return DD_OK;
+    };
+    DD_TRY(trace_copy(0));
+    for (int k = T; k >= 1; --k) {
+        DD_TRY(run_forward(cfg, params, z, B, L, alphas[k], logits, ld, wsc, s));
+        const uint32_t* nw = noise_words ? noise_words + (int64_t)(k - 1) * M * nu : nullptr;
+        const PostArgs a = make_post(cfg->prior, logits, ld, (int32_t)M, cfg->vocab, z, alphas[k],
+                                     alphas[k - 1], nw, noise_seed, (uint32_t)k, 0u, z, nullptr,
+                                     (int32_t*)(wsc + w.err));
+        DD_TRY(launch_posterior(a, cfg->dtype, s));
+        DD_TRY(trace_copy(T - k + 1));
+    }
+    return DD_OK;
+}
+
+dd_status dd_gaussian_latent_argmax(const int32_t* x, int32_t rows, int32_t V, double alpha_tilde,
+                                    double sigma, uint64_t seed, uint32_t step, uint32_t row0,
+                                    int32_t* z_out, int32_t* dev_err, void* stream) {
+    DD_CHECK(rows >= 0 && V > 0, DD_E_ARG, "rows must be >= 0 and V > 0");
+    DD_CHECK(alpha_tilde >= 0.0 && sigma > 0.0 && isfinite(alpha_tilde) && isfinite(sigma), DD_E_ARG,
+             "need alpha_tilde >= 0 and sigma > 0");
+    if (rows == 0) return DD_OK;
+    DD_CHECK(x && z_out, DD_E_ARG, "NULL pointer argument");
+    return launch_latent(x, rows, V, alpha_tilde, sigma, seed, step, row0, z_out, dev_err,
+                         (hipStream_t)stream);
+}
+
+dd_status dd_profile_begin(int32_t max_launches) {
+    DD_CHECK(max_launches > 0, DD_E_ARG, "max_launches must be positive");
+    if ((int)g_prof.ev.size() < 2 * max_launches) {
+        for (auto e : g_prof.ev) (void)hipEventDestroy(e);
+        g_prof.ev.assign(2 * max_launches, nullptr);
+        for (auto& e : g_prof.ev) {
+            const hipError_t r = hipEventCreate(&e);
+            DD_CHECK(r == hipSuccess, DD_E_HIP, "hipEventCreate: %s", hipGetErrorString(r));
+        }
+    }
+    g_prof.cap = max_launches;
+    g_prof.cls.clear();
+    g_prof.dropped = 0;
+    g_prof.open = -1;
+    g_prof.on = true;
+    return DD_OK;
+}
+
+dd_status dd_profile_end(void) {
+    g_prof.on = false;
+    return DD_OK;
+}
+
+int32_t dd_profile_num_classes(void) { return KC_COUNT; }
+
+dd_status dd_profile_read(int32_t cls, const char** name, int64_t* launches, double* total_ms) {
+    DD_CHECK(cls >= 0 && cls < KC_COUNT, DD_E_ARG, "class %d out of range", cls);
+    DD_CHECK(name && launches && total_ms, DD_E_ARG, "NULL pointer argument");
+    *name = kClassNames[cls];
+    int64_t n = 0;
+    double tot = 0.0;
+    for (size_t i = 0; i < g_prof.cls.size(); ++i) {
+        if (g_prof.cls[i] != cls) continue;
+        hipError_t e = hipEventSynchronize(g_prof.ev[2 * i + 1]);
+        float ms = 0.f;
+        if (e == hipSuccess) e = hipEventElapsedTime(&ms, g_prof.ev[2 * i], g_prof.ev[2 * i + 1]);
+        DD_CHECK(e == hipSuccess, DD_E_HIP, "event timing: %s", hipGetErrorString(e));
+        tot += ms;
+        ++n;
+    }
+    *launches = n;
+    *total_ms = tot;
+    return DD_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,237 @@
+// Non-causal multi-head attention softmax(q k^T / sqrt(dh)) v, flash style (no L x L tensor).
+//
+// bf16 path (dh = 64): a workgroup of 4 wavefronts owns 128 queries of one (batch, head); each
+// wavefront owns 32 queries.  Key/value tiles of 64 tokens are staged in LDS (double-buffered,
+// prefetched through registers): K row-major (padded rows), V transposed so the P.V contraction
+// reads contiguous 16-byte fragments.
+//   S^T = K Q^T with v_mfma_f32_32x32x16_bf16 (first operand: K rows from LDS; second: the wave's
+//         Q fragment, held in registers for the whole kernel).  Each lane then holds 32 scores of
+//         one query, the other 32 of the tile being in lane ^ 32.
+//   Online softmax in base 2 with the 1/sqrt(dh) scale folded into the exponent; the row max is
+//         combined with one cross-lane exchange; the running sum stays per lane until the end.
+//   O^T += V^T P^T: the probabilities are rounded to bf16 and used directly as the second MFMA
+//         operand (no shuffles: the key order of V^T in LDS is permuted to match the accumulator
+//         layout of S^T), so each lane's output column is again its own query.
+// fp32 path (validation): one thread per (batch, head, query), fp32 online softmax.
+#include <math.h>
+
+#include "kernels.h"
+
+namespace dd {
+
+typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8;
+typedef __attribute__((ext_vector_type(16))) float f32x16;
+
+constexpr int AQ = 128;  // queries per workgroup
+constexpr int AK = 64;   // keys per tile
+constexpr int DH = 64;
+constexpr int KSTR = DH + 8;
+constexpr int VSTR = AK + 8;
+
+// Position of key k (0..63) inside a transposed V row: within each 16-key step s the MFMA operand
+// slots of lane group g hold keys 16s + 4g + {0..3} and 16s + 8 + 4g + {0..3}; storing those eight
+// keys contiguously at 16s + 8g lets each lane read its operand with one 16-byte load.
+DD_DEV int vperm(int k) {
+    const int s = k >> 4, r = k & 3, g = (k >> 2) & 1, h = (k >> 3) & 1;
+    return 16 * s + 8 * g + 4 * h + r;
+}
+
+__global__ __launch_bounds__(256) void attn_bf16_kernel(AttnArgs a) {
+    __shared__ __attribute__((aligned(16))) bf16_t Ks[2][AK * KSTR];
+    __shared__ __attribute__((aligned(16))) bf16_t Vt[2][DH * VSTR];
+
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int h = blockIdx.y, b = blockIdx.z;
+    const int L = a.L, d = a.d;
+    const bf16_t* base = (const bf16_t*)a.qkv + (int64_t)b * L * a.ld;
+    const int q0 = blockIdx.x * AQ + wave * 32;
+    const int qi = q0 + (lane & 31);
+    const int grp = lane >> 5;
+
+    bf16x8 qf[4];
+#pragma unroll
+    for (int kk = 0; kk < 4; ++kk) {
+        if (qi < L) qf[kk] = *(const bf16x8*)(base + (int64_t)qi * a.ld + h * DH + kk * 16 + grp * 8);
+        else
+#pragma unroll
+            for (int e = 0; e < 8; ++e) qf[kk][e] = (__bf16)0.0f;
+    }
+
+    f32x16 o[2];
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) o[i][e] = 0.f;
+    float mrow = -INFINITY, lpart = 0.f;
+
+    uint4 rk[2], rv[2];
+    auto gload = [&](int kb0) {
+#pragma unroll
+        for (int r = 0; r < 2; ++r) {
+            const int c = tid + 256 * r, key = c >> 3, dc = (c & 7) * 8, t = kb0 + key;
+            if (t < L) {
+                const bf16_t* p = base + (int64_t)t * a.ld + h * DH + dc;
+                rk[r] = *(const uint4*)(p + d);
+                rv[r] = *(const uint4*)(p + 2 * d);
+            } else {
+                rk[r] = make_uint4(0u, 0u, 0u, 0u);
+                rv[r] = make_uint4(0u, 0u, 0u, 0u);
+            }
+        }
+    };
+    auto sstore = [&](int buf) {
+#pragma unroll
+        for (int r = 0; r < 2; ++r) {
+            const int c = tid + 256 * r, key = c >> 3, dc = (c & 7) * 8;
+            *(uint4*)&Ks[buf][key * KSTR + dc] = rk[r];
+            const int pk = vperm(key);
+            const uint32_t w[4] = {rv[r].x, rv[r].y, rv[r].z, rv[r].w};
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                Vt[buf][(dc + 2 * e) * VSTR + pk] = (bf16_t)(w[e] & 0xFFFFu);
+                Vt[buf][(dc + 2 * e + 1) * VSTR + pk] = (bf16_t)(w[e] >> 16);
+            }
+        }
+    };
+
+    const int ntiles = (L + AK - 1) / AK;
+    gload(0);
+    sstore(0);
+    __syncthreads();
+    for (int t = 0; t < ntiles; ++t) {
+        const int buf = t & 1, kb0 = t * AK;
+        if (t + 1 < ntiles) gload(kb0 + AK);
+
+        f32x16 sacc[2];
+#pragma unroll
+        for (int kb = 0; kb < 2; ++kb) {
+#pragma unroll
+            for (int e = 0; e < 16; ++e) sacc[kb][e] = 0.f;
+#pragma unroll
+            for (int kk = 0; kk < 4; ++kk) {
+                const bf16x8 kf = *(const bf16x8*)&Ks[buf][(kb * 32 + (lane & 31)) * KSTR + kk * 16 + grp * 8];
+                sacc[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[kk], sacc[kb], 0, 0, 0);
+            }
+        }
+        if (kb0 + AK > L) {
+#pragma unroll
+            for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+                for (int j = 0; j < 16; ++j) {
+                    const int key = kb0 + kb * 32 + 8 * (j >> 2) + 4 * grp + (j & 3);
+                    if (key >= L) sacc[kb][j] = -INFINITY;
+                }
+        }
+        float mloc = -INFINITY;
+#pragma unroll
+        for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+            for (int j = 0; j < 16; ++j) mloc = fmaxf(mloc, sacc[kb][j]);
+        mloc = fmaxf(mloc, __shfl_xor(mloc, 32, 64));
+        const float mnew = fmaxf(mrow, mloc * a.scale_log2);
+        const float corr = __builtin_amdgcn_exp2f(mrow - mnew);
+        float psum = 0.f;
+#pragma unroll
+        for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+            for (int j = 0; j < 16; ++j) {
+                const float p = __builtin_amdgcn_exp2f(fmaf(sacc[kb][j], a.scale_log2, -mnew));
+                sacc[kb][j] = p;
+                psum += p;
+            }
+        lpart = fmaf(lpart, corr, psum);
+        mrow = mnew;
+#pragma unroll
+        for (int i = 0; i < 2; ++i)
+#pragma unroll
+            for (int e = 0; e < 16; ++e) o[i][e] *= corr;
+
+#pragma unroll
+        for (int s = 0; s < 4; ++s) {
+            bf16x8 pf;
+#pragma unroll
+            for (int e = 0; e < 8; ++e) pf[e] = (__bf16)sacc[s >> 1][8 * (s & 1) + e];
+#pragma unroll
+            for (int blk = 0; blk < 2; ++blk) {
+                const bf16x8 vf = *(const bf16x8*)&Vt[buf][(blk * 32 + (lane & 31)) * VSTR + s * 16 + grp * 8];
+                o[blk] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf, o[blk], 0, 0, 0);
+            }
+        }
+        if (t + 1 < ntiles) sstore(buf ^ 1);
+        __syncthreads();
+    }
+
+    const float l = lpart + __shfl_xor(lpart, 32, 64);
+    const float inv = 1.0f / l;
+    if (qi < L) {
+        bf16_t* out = (bf16_t*)a.out + ((int64_t)b * L + qi) * a.ldo + h * DH;
+#pragma unroll
+        for (int blk = 0; blk < 2; ++blk)
+#pragma unroll
+            for (int j4 = 0; j4 < 4; ++j4) {
+                const int dv = blk * 32 + 8 * j4 + 4 * grp;
+                uint2 p;
+                p.x = pack_bf16x2(o[blk][4 * j4] * inv, o[blk][4 * j4 + 1] * inv);
+                p.y = pack_bf16x2(o[blk][4 * j4 + 2] * inv, o[blk][4 * j4 + 3] * inv);
+                *(uint2*)(out + dv) = p;
+            }
+    }
+}
+
+template <int D>
+__global__ __launch_bounds__(128) void attn_f32_kernel(AttnArgs a) {
+    const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    const int L = a.L, H = a.H, d = a.d;
+    if (idx >= (int64_t)a.B * H * L) return;
+    const int q = (int)(idx % L);
+    const int h = (int)((idx / L) % H);
+    const int b = (int)(idx / ((int64_t)L * H));
+    const float* base = (const float*)a.qkv + (int64_t)b * L * a.ld;
+    const float scale = 1.0f / sqrtf((float)D);
+    float qv[D], acc[D];
+#pragma unroll
+    for (int c = 0; c < D; ++c) { qv[c] = base[(int64_t)q * a.ld + h * D + c]; acc[c] = 0.f; }
+    float m = -INFINITY, l = 0.f;
+    for (int t = 0; t < L; ++t) {
+        const float* kr = base + (int64_t)t * a.ld + d + h * D;
+        float sdot = 0.f;
+#pragma unroll
+        for (int c = 0; c < D; ++c) sdot = fmaf(qv[c], kr[c], sdot);
+        sdot *= scale;
+        const float mn = fmaxf(m, sdot);
+        const float corr = expf(m - mn), p = expf(sdot - mn);
+        l = l * corr + p;
+        const float* vr = kr + d;
+#pragma unroll
+        for (int c = 0; c < D; ++c) acc[c] = fmaf(p, vr[c], acc[c] * corr);
+        m = mn;
+    }
+    float* out = (float*)a.out + ((int64_t)b * L + q) * a.ldo + h * D;
+#pragma unroll
+    for (int c = 0; c < D; ++c) out[c] = acc[c] / l;
+}
+
+bool attn_supported(int dtype, int dh) {
+    if (dtype == DD_BF16) return dh == DH;
+    return dh == 16 || dh == 32 || dh == 64 || dh == 128;
+}
+
+dd_status launch_attn(int dtype, const AttnArgs& a, hipStream_t s) {
+    const int dh = a.d / a.H;
+    ProfScope ps(KC_ATTN, s);
+    if (dtype == DD_BF16) {
+        hipLaunchKernelGGL(attn_bf16_kernel, dim3((a.L + AQ - 1) / AQ, a.H, a.B), dim3(256), 0, s, a);
+    } else {
+        const int64_t n = (int64_t)a.B * a.H * a.L;
+        const dim3 grid((unsigned)ceil_div(n, 128));
+        switch (dh) {
+            case 16: hipLaunchKernelGGL(attn_f32_kernel<16>, grid, dim3(128), 0, s, a); break;
+            case 32: hipLaunchKernelGGL(attn_f32_kernel<32>, grid, dim3(128), 0, s, a); break;
+            case 64: hipLaunchKernelGGL(attn_f32_kernel<64>, grid, dim3(128), 0, s, a); break;
+            default: hipLaunchKernelGGL(attn_f32_kernel<128>, grid, dim3(128), 0, s, a); break;
+        }
+    }
+    return launch_status("attention");
+}
+
+}  // namespace dd

@@ -1,0 +1,159 @@
+// Time embedding, token/position embedding + first LayerNorm, and LayerNorm.
+//
+// One wavefront per token row; statistics are reduced with cross-lane shuffles in
+// fp32 (mean first, then the biased variance of the centred values, from registers).
+#include <math.h>
+
+#include "kernels.h"
+
+namespace dd {
+
+// temb_j = sin(tau w_j) (j < d/2), cos(tau w_{j-d/2}) (j >= d/2), w_i = 10000^(-i/(d/2)),
+// evaluated in float64 and stored as fp32.
+__global__ void temb_kernel(float* temb, int d, double tau) {
+    const int j = blockIdx.x * blockDim.x + threadIdx.x;
+    if (j >= d) return;
+    const int half = d / 2;
+    const int i = j < half ? j : j - half;
+    const double w = pow(10000.0, -(double)i / (double)half);
+    temb[j] = (float)(j < half ? sin(tau * w) : cos(tau * w));
+}
+
+dd_status launch_temb(float* temb, int d, double tau, hipStream_t s) {
+    ProfScope ps(KC_TEMB, s);
+    hipLaunchKernelGGL(temb_kernel, dim3((d + 255) / 256), dim3(256), 0, s, temb, d, tau);
+    return launch_status("time_embedding");
+}
+
+template <typename W> DD_DEV float ldw(const W* p, int64_t i);
+template <> DD_DEV float ldw<bf16_t>(const bf16_t* p, int64_t i) { return bf16_to_f32(p[i]); }
+template <> DD_DEV float ldw<float>(const float* p, int64_t i) { return p[i]; }
+template <typename W> DD_DEV void stw(W* p, int64_t i, float v);
+template <> DD_DEV void stw<bf16_t>(bf16_t* p, int64_t i, float v) { p[i] = f32_to_bf16(v); }
+template <> DD_DEV void stw<float>(float* p, int64_t i, float v) { p[i] = v; }
+
+// NPL = d / 64 elements per lane (d % 64 == 0).
+template <typename W, int NPL>
+DD_DEV void ln_row(const float (&x)[NPL], int lane, int d, const W* g, const W* b, float eps,
+                   W* out) {
+    float s = 0.f;
+#pragma unroll
+    for (int k = 0; k < NPL; ++k) s += x[k];
+    const float mean = wave_sum(s) / (float)d;
+    float q = 0.f;
+#pragma unroll
+    for (int k = 0; k < NPL; ++k) { const float c = x[k] - mean; q += c * c; }
+    const float rstd = 1.0f / sqrtf(wave_sum(q) / (float)d + eps);
+#pragma unroll
+    for (int k = 0; k < NPL; ++k) {
+        const int c = lane + 64 * k;
+        stw<W>(out, c, (x[k] - mean) * rstd * ldw<W>(g, c) + ldw<W>(b, c));
+    }
+}
+
+template <typename W, int NPL>
+__global__ __launch_bounds__(256) void embed_ln_kernel(const int32_t* z, int64_t rows, int L,
+                                                       int n_tok, const W* tok, const W* pos,
+                                                       const float* temb, const W* g, const W* b,
+                                                       float eps, float* h, W* xln, int32_t* err) {
+    const int64_t row = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+    const int lane = threadIdx.x & 63;
+    if (row >= rows) return;
+    constexpr int d = NPL * 64;
+    int id = z[row];
+    if (id < 0 || id >= n_tok) {
+        if (lane == 0 && err) atomicOr(err, DD_DEVERR_TOKEN);
+        id = id < 0 ? 0 : n_tok - 1;
+    }
+    const int l = (int)(row % L);
+    float x[NPL];
+#pragma unroll
+    for (int k = 0; k < NPL; ++k) {
+        const int c = lane + 64 * k;
+        float v = ldw<W>(tok, (int64_t)id * d + c) + ldw<W>(pos, (int64_t)l * d + c);
+        if (temb) v += temb[c];
+        x[k] = v;
+        h[row * d + c] = v;
+    }
+    ln_row<W, NPL>(x, lane, d, g, b, eps, xln + row * d);
+}
+
+template <typename W, int NPL>
+__global__ __launch_bounds__(256) void ln_kernel(const float* h, int64_t rows, const W* g,
+                                                 const W* b, float eps, W* out) {
+    const int64_t row = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+    const int lane = threadIdx.x & 63;
+    if (row >= rows) return;
+    constexpr int d = NPL * 64;
+    float x[NPL];
+#pragma unroll
+    for (int k = 0; k < NPL; ++k) x[k] = h[row * d + lane + 64 * k];
+    ln_row<W, NPL>(x, lane, d, g, b, eps, out + row * d);
+}
+
+#define DD_NPL_CASES(X) X(1) X(2) X(4) X(8) X(12) X(16) X(24) X(32)
+
+template <typename W>
+dd_status launch_embed_ln_t(const int32_t* z, int64_t rows, int L, int n_tok, int d, const void* tok,
+                            const void* pos, const float* temb, const void* g, const void* b,
+                            float eps, float* h, void* xln, int32_t* err, hipStream_t s) {
+    const dim3 grid((unsigned)ceil_div(rows, 4)), blk(256);
+    ProfScope ps(KC_EMBED_LN, s);
+    switch (d / 64) {
+#define X(n)                                                                                     \
+    case n:                                                                                      \
+        hipLaunchKernelGGL((embed_ln_kernel<W, n>), grid, blk, 0, s, z, rows, L, n_tok,          \
+                           (const W*)tok, (const W*)pos, temb, (const W*)g, (const W*)b, eps, h,  \
+                           (W*)xln, err);                                                        \
+        break;
+        DD_NPL_CASES(X)
+#undef X
+        default: set_error("d_model %d unsupported by the LayerNorm kernels", d); return DD_E_UNSUPPORTED;
+    }
+    return launch_status("embed_ln");
+}
+
+dd_status launch_embed_ln(int dtype, const int32_t* z, int64_t rows, int L, int n_tok, int d,
+                          const void* tok, const void* pos, const float* temb, const void* g,
+                          const void* b, float eps, float* h, void* xln, int32_t* err,
+                          hipStream_t s) {
+    if (dtype == DD_BF16)
+        return launch_embed_ln_t<bf16_t>(z, rows, L, n_tok, d, tok, pos, temb, g, b, eps, h, xln, err, s);
+    return launch_embed_ln_t<float>(z, rows, L, n_tok, d, tok, pos, temb, g, b, eps, h, xln, err, s);
+}
+
+template <typename W>
+dd_status launch_ln_t(const float* h, int64_t rows, int d, const void* g, const void* b, float eps,
+                      void* out, hipStream_t s) {
+    const dim3 grid((unsigned)ceil_div(rows, 4)), blk(256);
+    ProfScope ps(KC_LN, s);
+    switch (d / 64) {
+#define X(n)                                                                                     \
+    case n:                                                                                      \
+        hipLaunchKernelGGL((ln_kernel<W, n>), grid, blk, 0, s, h, rows, (const W*)g,            \
+                           (const W*)b, eps, (W*)out);                                           \
+        break;
+        DD_NPL_CASES(X)
+#undef X
+        default: set_error("d_model %d unsupported by the LayerNorm kernels", d); return DD_E_UNSUPPORTED;
+    }
+    return launch_status("layernorm");
+}
+
+dd_status launch_ln(int dtype, const float* h, int64_t rows, int d, const void* g, const void* b,
+                    float eps, void* out, hipStream_t s) {
+    if (dtype == DD_BF16) return launch_ln_t<bf16_t>(h, rows, d, g, b, eps, out, s);
+    return launch_ln_t<float>(h, rows, d, g, b, eps, out, s);
+}
+
+bool ln_supported(int d) {
+    switch (d / 64) {
+#define X(n) case n:
+        DD_NPL_CASES(X)
+#undef X
+        return d % 64 == 0;
+        default: return false;
+    }
+}
+
+}  // namespace dd

@@ -1,0 +1,67 @@
+// Argument blocks and launchers shared by the host code (dd_api.hip) and the kernel files.
+#pragma once
+
+#include "common.h"
+
+namespace dd {
+
+struct PostArgs {
+    const void* logits;
+    int64_t ld;
+    int32_t rows, V, prior;
+    const int32_t* z_t;
+    int32_t* z_s;
+    // masked prior: w_x, w_m and their logs
+    double log_wx, log_wm, wx, wm;
+    // uniform prior: c_x = a_s - a_t, c_u = (1 - a_{t|s})(1 - a_s)/K, c_z = a_{t|s} - a_t,
+    // Ka_t = K a_t, one_m_at = 1 - a_t
+    double c_x, c_u, c_z, Ka_t, one_m_at;
+    const uint32_t* noise;  // explicit words [rows][nu] or NULL (Philox)
+    int32_t nu, ntop;
+    uint64_t seed;
+    uint32_t step, row0;
+    float* probs;
+    int32_t* err;
+};
+
+enum Epi { EPI_BIAS = 0, EPI_BIAS_GELU = 1, EPI_BIAS_RESID = 2, EPI_PLAIN = 3 };
+
+struct GemmArgs {
+    const void* A;   // [M][K], row stride lda
+    int64_t lda;
+    const void* W;   // [N][K], row stride ldw
+    int64_t ldw;
+    const void* bias;
+    void* C;         // [M][N], row stride ldc
+    int64_t ldc;
+    int M, N, K;
+};
+
+struct AttnArgs {
+    const void* qkv;  // [B*L][3d]: q | k | v, head h at columns h*dh
+    int64_t ld;
+    void* out;        // [B*L][d]
+    int64_t ldo;
+    int B, L, H, d;
+    float scale_log2;  // log2(e) / sqrt(dh)
+};
+
+dd_status launch_posterior(const PostArgs& a, int logits_dtype, hipStream_t s);
+dd_status launch_latent(const int32_t* x, int32_t rows, int32_t V, double at, double sigma,
+                        uint64_t seed, uint32_t step, uint32_t row0, int32_t* z, int32_t* err,
+                        hipStream_t s);
+dd_status launch_init(void* dst, int64_t count, uint32_t id, double shift, int is_bf16,
+                      uint64_t seed, hipStream_t s);
+dd_status launch_temb(float* temb, int d, double tau, hipStream_t s);
+dd_status launch_embed_ln(int dtype, const int32_t* z, int64_t rows, int L, int n_tok, int d,
+                          const void* tok, const void* pos, const float* temb, const void* g,
+                          const void* b, float eps, float* h, void* xln, int32_t* err,
+                          hipStream_t s);
+dd_status launch_ln(int dtype, const float* h, int64_t rows, int d, const void* g, const void* b,
+                    float eps, void* out, hipStream_t s);
+bool ln_supported(int d);
+dd_status launch_gemm(int dtype, int epi, int cls, const GemmArgs& g, hipStream_t s);
+dd_status launch_attn(int dtype, const AttnArgs& a, hipStream_t s);
+bool attn_supported(int dtype, int dh);
+
+}  // namespace dd

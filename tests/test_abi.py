@@ -1,0 +1,151 @@
+"""The C ABI: exported symbols, layouts and host-side validation (no GPU needed).
+
+Validation failures must return their status before any launch, so they can be
+exercised here with dummy non-null pointers that are never dereferenced.
+"""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+import workloads
+from oracle import params as oparams, sampler as osampler
+from paper_2609_04010_amd import _lib as dd
+
+HEADER = os.path.join(os.path.dirname(os.path.dirname(__file__)), "include", "dd.h")
+FAKE = ctypes.c_void_p(0x1000)   # never dereferenced: every call below fails validation first
+
+
+def _declared():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(dd_[a-z_]+)\s*\(", text)))
+
+
+def test_every_declared_symbol_is_exported():
+    L = dd.lib()
+    names = _declared()
+    assert len(names) >= 20
+    for n in names:
+        assert hasattr(L, n), n
+    assert sorted(dd.EXPORTED) == names
+
+
+@pytest.mark.parametrize("c", [1, 2, 5])
+def test_param_layout_matches_oracle_tensor_list(c):
+    cfg = workloads.model_cfg(c)
+    specs = oparams.specs(cfg)
+    assert dd.param_count(cfg) == len(specs)
+    es = 2 if cfg["dtype"] == "bf16" else 4
+    end = 0
+    for tid, (name, shape, _) in enumerate(specs):
+        off, r, cc = dd.param_tensor(cfg, tid)
+        n = int(np.prod(shape))
+        assert r * cc == n and (r == shape[0] if len(shape) == 2 else r == 1), name
+        assert off % 256 == 0 and off >= end
+        end = off + n * es
+    assert dd.param_bytes(cfg) >= end
+
+
+def test_sizes_and_noise_width():
+    cfg = workloads.model_cfg(2)
+    assert dd.logits_ld(50257) == 50304 and dd.logits_ld(32) == 64
+    for prior in ("mask", "uniform"):
+        for V in (1, 32, 256, 257, 50257):
+            assert dd.noise_width(prior, V) == osampler.noise_width(prior, V)
+    w1, w2 = dd.workspace_bytes(cfg, 1, 128), dd.workspace_bytes(cfg, 2, 128)
+    assert 0 < w1 < w2 < dd.loop_workspace_bytes(cfg, 2, 128)
+    assert dd.workspace_bytes(cfg, 0, 128) == 0
+
+
+def _post(**kw):
+    a = dict(prior=0, logits=FAKE, dtype=0, ld=64, rows=4, V=32, z_t=FAKE, at=0.2, as_=0.5,
+             noise=None, seed=0, step=1, row0=0, z_s=FAKE, probs=None, err=None)
+    a.update(kw)
+    return dd.lib().dd_posterior_sample(a["prior"], a["logits"], a["dtype"], a["ld"], a["rows"],
+                                        a["V"], a["z_t"], a["at"], a["as_"], a["noise"], a["seed"],
+                                        a["step"], a["row0"], a["z_s"], a["probs"], a["err"], None)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(prior=7), 1), (dict(dtype=9), 3), (dict(V=0), 1), (dict(rows=-1), 1),
+    (dict(ld=31), 2), (dict(ld=36), 2), (dict(at=0.5, as_=0.5), 1), (dict(at=0.6, as_=0.5), 1),
+    (dict(at=-0.1), 1), (dict(as_=1.5), 1), (dict(logits=None), 1), (dict(z_s=None), 1),
+])
+def test_posterior_validation(kw, status):
+    assert _post(**kw) == status
+
+
+def test_posterior_zero_rows_is_a_noop():
+    assert _post(rows=0, logits=None, z_t=None, z_s=None) == 0
+
+
+def _cfg_struct(**over):
+    cfg = workloads.model_cfg(2)
+    cfg.update(over)
+    return dd.make_config(cfg)
+
+
+def _fwd(cfg, B=1, L=16, at=0.5, ld=50304, ws_bytes=1 << 40):
+    return dd.lib().dd_denoise_forward(ctypes.byref(cfg), FAKE, FAKE, B, L, at, FAKE, ld, FAKE,
+                                       ws_bytes, None)
+
+
+def test_forward_validation():
+    assert _fwd(_cfg_struct(), L=2048) == 2            # L > max_len
+    assert _fwd(_cfg_struct(), B=0) == 1
+    assert _fwd(_cfg_struct(), at=1.5) == 1
+    assert _fwd(_cfg_struct(), ld=50257) == 2          # not a multiple of 8
+    assert _fwd(_cfg_struct(), ld=50000) == 2          # < V
+    assert _fwd(_cfg_struct(), ws_bytes=10) == 4
+    assert _fwd(_cfg_struct(n_heads=24)) == 6          # bf16 attention needs dh = 64
+    assert _fwd(_cfg_struct(d_model=100, n_heads=4)) in (1, 6)
+    bad = _cfg_struct()
+    bad.prior = 5
+    assert _fwd(bad) == 1
+    bad = _cfg_struct()
+    bad.dtype = 3
+    assert _fwd(bad) == 1
+
+
+def test_loop_validation():
+    cfg = _cfg_struct()
+    al = (ctypes.c_double * 3)(1.0, 0.5, 0.5)         # not strictly decreasing
+    assert dd.lib().dd_sample_loop(ctypes.byref(cfg), FAKE, 1, 16, 2, al, FAKE, None, 0, None, FAKE,
+                                   1 << 40, None) == 1
+    al = (ctypes.c_double * 3)(1.0, 0.5, 0.0)
+    assert dd.lib().dd_sample_loop(ctypes.byref(cfg), FAKE, 1, 16, 2, al, FAKE, None, 0, None, FAKE,
+                                   10, None) == 4
+    assert dd.lib().dd_sample_loop(ctypes.byref(cfg), FAKE, 1, 16, 0, al, FAKE, None, 0, None, FAKE,
+                                   1 << 40, None) == 1
+
+
+def test_latent_and_init_validation():
+    L = dd.lib()
+    assert L.dd_gaussian_latent_argmax(FAKE, 4, 0, 0.0, 1.0, 0, 0, 0, FAKE, None, None) == 1
+    assert L.dd_gaussian_latent_argmax(FAKE, 4, 8, 0.0, 0.0, 0, 0, 0, FAKE, None, None) == 1
+    assert L.dd_gaussian_latent_argmax(None, 0, 8, 0.0, 1.0, 0, 0, 0, None, None, None) == 0
+    cfg = _cfg_struct()
+    assert L.dd_init_params(ctypes.byref(cfg), FAKE, 100, 0, None, None) == 4
+    assert L.dd_init_params(ctypes.byref(cfg), None, 1 << 40, 0, None, None) == 1
+
+
+def test_status_strings_and_last_error():
+    L = dd.lib()
+    assert L.dd_status_str(0) == b"ok" and L.dd_status_str(4) == b"buffer too small"
+    _post(ld=31)
+    assert b"ld" in L.dd_last_error()
+
+
+def test_pack_params_rejects_non_bf16_values():
+    cfg = workloads.model_cfg(1, dtype="bf16", n_layers=1)
+    specs = oparams.specs(cfg)
+    P = workloads.host_params(cfg, 3, specs)
+    blob = dd.pack_params(cfg, [P[n] for n, _, _ in specs])
+    assert blob.size == dd.param_bytes(cfg)
+    bad = [P[n] for n, _, _ in specs]
+    bad[0] = bad[0] + 1e-5
+    with pytest.raises(ValueError):
+        dd.pack_params(cfg, bad)

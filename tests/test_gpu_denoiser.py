@@ -1,0 +1,156 @@
+"""GPU parity of the denoiser forward pass and the T-step loop, through the C ABI,
+against the float64 oracle on the same seeded inputs."""
+import numpy as np
+import pytest
+
+import workloads
+from oracle import forward as oforward, loop as oloop, params as oparams, sampler as osampler, \
+    schedule as osched
+from paper_2609_04010_amd import _lib as dd
+from tests.gpu_util import compare_ids, dev_i32, dev_words, say, torch_or_skip
+
+pytestmark = pytest.mark.gpu
+
+LOGIT_TOL = {"bf16": 5e-2, "fp32": 1e-4}
+
+
+def _params_host(torch, cfg, seed):
+    """Host-generated parameters (workloads) uploaded through the host-blob path."""
+    specs = oparams.specs(cfg)
+    P = workloads.host_params(cfg, seed, specs)
+    blob = dd.pack_params(cfg, [P[n] for n, _, _ in specs])
+    buf = torch.zeros(blob.size, dtype=torch.uint8, device="cuda")
+    dd.init_params(cfg, buf, host_blob=blob)
+    return P, buf
+
+
+def _params_seeded(torch, cfg, seed):
+    """In-kernel initialisation on the GPU; the oracle regenerates the same values itself."""
+    buf = torch.zeros(dd.param_bytes(cfg), dtype=torch.uint8, device="cuda")
+    dd.init_params(cfg, buf, seed=seed)
+    return oparams.init_params(cfg, seed), buf
+
+
+def _forward_gpu(torch, cfg, buf, z, at):
+    B, L = z.shape
+    V = cfg["vocab"]
+    ld = int(dd.logits_ld(V))
+    tdt = torch.bfloat16 if cfg["dtype"] == "bf16" else torch.float32
+    logits = torch.zeros((B * L, ld), dtype=tdt, device="cuda")
+    ws = torch.zeros(dd.workspace_bytes(cfg, B, L), dtype=torch.uint8, device="cuda")
+    dd.denoise_forward(cfg, buf, dev_i32(torch, z), B, L, at, logits, ld, ws)
+    err = dd.read_device_error(ws[:4].view(torch.int32))
+    assert err == 0
+    return logits[:, :V].float().cpu().numpy().astype(np.float64).reshape(B, L, V)
+
+
+FWD_CASES = [
+    # workload, overrides, B, L, alpha_t, mask fraction, params source
+    (1, {}, 4, 32, 0.0, 1.0, "seeded"),
+    (1, {}, 4, 32, 0.625, 0.375, "seeded"),
+    (1, {}, 3, 29, 0.9, 0.1, "host"),
+    (2, {}, 2, 200, 0.5, 0.5, "host"),
+    (2, {}, 1, 1024, 0.25, 0.75, "host"),
+    (3, {}, 2, 130, 0.4, 0.0, "host"),
+    (5, {"max_len": 4096}, 1, 300, 0.7, 0.3, "host"),
+]
+
+
+@pytest.mark.parametrize("case", FWD_CASES, ids=lambda c: f"w{c[0]}-B{c[2]}-L{c[3]}-a{c[4]}")
+def test_denoise_forward_parity(case):
+    torch = torch_or_skip()
+    c, over, B, L, at, mf, src = case
+    say("forward", case)
+    cfg = workloads.model_cfg(c, **over)
+    seed = workloads.seeds(c)["param"]
+    P, buf = (_params_seeded if src == "seeded" else _params_host)(torch, cfg, seed)
+    V = cfg["vocab"]
+    if cfg["prior"] == "mask":
+        z = workloads.masked_state(workloads.seeds(c)["data"], B, L, V, mf)
+    else:
+        z = workloads.uniform_state(workloads.seeds(c)["data"], B, L, V)
+    got = _forward_gpu(torch, cfg, buf, z, at)
+    ref = oforward.forward(cfg, P, z, at)
+    err = float(np.abs(got - ref).max())
+    say(f"max |dlogit| = {err:.3e} (logit std {ref.std():.3f})")
+    assert err <= LOGIT_TOL[cfg["dtype"]]
+
+
+def test_forward_out_of_range_token_sets_error_word():
+    torch = torch_or_skip()
+    cfg = workloads.model_cfg(1)
+    _, buf = _params_seeded(torch, cfg, 3)
+    z = workloads.all_mask(1, 8, cfg["vocab"])
+    z[0, 3] = 999
+    ld = int(dd.logits_ld(cfg["vocab"]))
+    logits = torch.zeros((8, ld), dtype=torch.float32, device="cuda")
+    ws = torch.zeros(dd.workspace_bytes(cfg, 1, 8), dtype=torch.uint8, device="cuda")
+    dd.denoise_forward(cfg, buf, dev_i32(torch, z), 1, 8, 0.5, logits, ld, ws)
+    assert dd.read_device_error(ws[:4].view(torch.int32)) == dd.DD_DEVERR_TOKEN
+    dd.workspace_reset(ws)
+    assert dd.read_device_error(ws[:4].view(torch.int32)) == 0
+
+
+def _loop_gpu(torch, cfg, buf, z1, T, alphas, words=None, seed=0):
+    B, L = z1.shape
+    z = dev_i32(torch, z1)
+    trace = torch.zeros(((T + 1) * B * L,), dtype=torch.int32, device="cuda")
+    ws = torch.zeros(dd.loop_workspace_bytes(cfg, B, L), dtype=torch.uint8, device="cuda")
+    dd.sample_loop(cfg, buf, B, L, T, alphas, z, ws,
+                   noise_words=dev_words(torch, words) if words is not None else None,
+                   noise_seed=seed, z_trace=trace)
+    assert dd.read_device_error(ws[:4].view(torch.int32)) == 0
+    return z.cpu().numpy().reshape(B, L), trace.cpu().numpy().reshape(T + 1, B, L)
+
+
+def test_loop_config1_free_running_matches_oracle():
+    """fp32 workload 1: the whole 8-step loop on explicit noise, free running on both sides."""
+    torch = torch_or_skip()
+    cfg = workloads.model_cfg(1)
+    w, s = workloads.CONFIGS[1], workloads.seeds(1)
+    B, L, V, T = w["B"], w["L"], w["vocab"], w["T"]
+    P, buf = _params_seeded(torch, cfg, s["param"])
+    words = workloads.noise_words(s["noise"], (T, B * L, osampler.noise_width("mask", V)))
+    z1 = workloads.all_mask(B, L, V)
+    al = osched.alphas(T)
+    z0, trace = _loop_gpu(torch, cfg, buf, z1, T, al, words=words)
+    rz0, rtrace, gaps = oloop.sample_loop(cfg, P, z1, T, al, noise_words=words)
+    say(f"loop: min gap {np.min(gaps):.3e}; trace agreement {np.mean(trace == rtrace):.6f}")
+    for k in range(T):
+        compare_ids(trace[k + 1].reshape(-1), rtrace[k + 1].reshape(-1), gaps[k], f"step {T - k}")
+    assert np.array_equal(z0, rz0)
+
+
+@pytest.mark.parametrize("c,B,L,T", [(2, 2, 128, 8), (4, 2, 96, 8)])
+def test_loop_bookkeeping_masked(c, B, L, T):
+    torch = torch_or_skip()
+    say("loop bookkeeping", c, B, L, T)
+    cfg = workloads.model_cfg(c)
+    V = cfg["vocab"]
+    _, buf = _params_seeded(torch, cfg, workloads.seeds(c)["param"])
+    z1 = workloads.all_mask(B, L, V)
+    z0, trace = _loop_gpu(torch, cfg, buf, z1, T, osched.alphas(T), seed=workloads.seeds(c)["noise"])
+    masked = (trace == V).sum(axis=(1, 2))
+    say("masked per step", masked.tolist())
+    assert masked[0] == B * L and masked[-1] == 0 and np.all(np.diff(masked) <= 0)
+    for k in range(1, T + 1):
+        was = trace[k - 1] != V
+        assert np.array_equal(trace[k][was], trace[k - 1][was])
+    assert np.all((z0 >= 0) & (z0 < V))
+    z0b, _ = _loop_gpu(torch, cfg, buf, z1, T, osched.alphas(T), seed=workloads.seeds(c)["noise"])
+    assert np.array_equal(z0, z0b)                                   # deterministic
+
+
+def test_loop_uniform_prior_runs_in_range():
+    torch = torch_or_skip()
+    cfg = workloads.model_cfg(3)
+    V = cfg["vocab"]
+    B, L, T = 2, 64, 4
+    _, buf = _params_seeded(torch, cfg, workloads.seeds(3)["param"])
+    x = workloads.clean_tokens(workloads.seeds(3)["data"], B, L, V)
+    z1d = torch.empty(B * L, dtype=torch.int32, device="cuda")
+    dd.gaussian_latent_argmax(dev_i32(torch, x), B * L, V, 0.0, 1.0, seed=9, step=0, z_out=z1d)
+    z1 = z1d.cpu().numpy().reshape(B, L)
+    z0, trace = _loop_gpu(torch, cfg, buf, z1, T, osched.alphas(T), seed=5)
+    assert np.all((trace >= 0) & (trace < V))
+    assert np.mean(trace[-1] != trace[0]) > 0.5          # the uniform prior keeps revising tokens
