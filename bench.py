@@ -1,0 +1,178 @@
+"""Throughput benchmark of the reverse-sampling loop on one MI355X.
+
+A benchmark step is one whole sampling job: dd_sample_loop over T reverse steps
+for a batch of B sequences of length L (denoiser forward + fused posterior /
+Gumbel-max draw per reverse step; workload 3 adds the Gaussian-latent start).
+Inputs (weights, start state, noise seed) are resident on the GPU before the
+timed region.  Prints ONE JSON line.
+
+  python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload 2] [--no-cpu-baseline]
+"""
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_BF16_TFLOPS = 2500.0     # MI355X dense bf16 MFMA
+PEAK_FP32_TFLOPS = 157.3      # MI355X fp32 vector
+PEAK_HBM_GBS = 8000.0         # MI355X HBM3E
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def algorithmic_units(cls, cfg, B, L):
+    """(amount per launch, unit, bound) for a kernel class (flops or bytes, see the design notes)."""
+    M, d, F, V, H = B * L, cfg["d_model"], cfg["d_mlp"], cfg["vocab"], cfg["n_heads"]
+    flops = {
+        "gemm_qkv": 2.0 * M * d * 3 * d,
+        "gemm_attn_out": 2.0 * M * d * d,
+        "gemm_mlp_up": 2.0 * M * d * F,
+        "gemm_mlp_down": 2.0 * M * F * d,
+        "gemm_vocab": 2.0 * M * d * V,
+        "attention": 4.0 * B * L * L * d,
+    }
+    if cls in flops:
+        return flops[cls], "TFLOP/s", "mfma"
+    return None, None, None
+
+
+def cpu_baseline(c, cfg, w):
+    """The float64 oracle on a bounded sample: one reverse step for ONE sequence."""
+    import workloads
+    from oracle import forward as ofw, params as opar, sampler as osm, schedule as osch
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:
+        threads = os.cpu_count()
+    L, V, T = w["L"], w["vocab"], w["T"]
+    P = workloads.host_params(cfg, workloads.seeds(c)["param"], opar.specs(cfg))
+    k = T // 2
+    al = osch.alphas(T)
+    if cfg["prior"] == "mask":
+        z = workloads.masked_state(workloads.seeds(c)["data"], 1, L, V, k / T)
+    else:
+        z = workloads.uniform_state(workloads.seeds(c)["data"], 1, L, V)
+    t0 = time.perf_counter()
+    logits = ofw.forward(cfg, P, z, al[k]).reshape(L, V)
+    osm.posterior_sample(cfg["prior"], logits, z.reshape(-1), al[k], al[k - 1],
+                         osm.PhiloxNoise(workloads.seeds(c)["noise"], k))
+    dt = time.perf_counter() - t0
+    # the oracle would need T such steps per sequence: generated tokens/s = L / (T dt)
+    return {"value": L / (T * dt), "unit": "tokens/s", "cores": int(threads), "kind": "oracle",
+            "sample": f"one reverse step (forward + posterior + draw) of 1 of {w['B']} sequences, "
+                      f"L={L}, step {k}/{T}: {dt:.2f} s; extrapolated x{T} steps"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=3)
+    ap.add_argument("--warmup", type=int, default=1)
+    ap.add_argument("--workload", type=int, default=2)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        log(f"bench.py measures one GPU only (asked for {args.gpus}); the sampling loop shards "
+            "along the batch with no communication, see the design notes.")
+        sys.exit(2)
+
+    import torch
+    import workloads
+    from paper_2609_04010_amd import _lib as dd
+
+    c = args.workload
+    w = workloads.CONFIGS[c]
+    cfg = workloads.model_cfg(c)
+    s = workloads.seeds(c)
+    B, L, T, V = w["B"], w["L"], w["T"], w["vocab"]
+    M = B * L
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+
+    params = torch.zeros(dd.param_bytes(cfg), dtype=torch.uint8, device=dev)
+    dd.init_params(cfg, params, seed=s["param"])
+    ws = torch.zeros(dd.loop_workspace_bytes(cfg, B, L), dtype=torch.uint8, device=dev)
+    alphas = 1.0 - np.arange(T + 1, dtype=np.float64) / T      # alpha_t = 1 - t on t_k = k / T
+    z = torch.empty(M, dtype=torch.int32, device=dev)
+    if cfg["prior"] == "mask":
+        z0 = torch.full((M,), V, dtype=torch.int32, device=dev)
+    else:
+        z0 = torch.from_numpy(workloads.clean_tokens(s["data"], B, L, V).reshape(-1)).to(dev)
+    torch.cuda.synchronize()
+
+    def job():
+        if cfg["prior"] == "mask":
+            z.copy_(z0)
+        else:   # z_1 = argmax of a pure-noise Gaussian latent (alpha_tilde = 0, sigma = 1)
+            dd.gaussian_latent_argmax(z0, M, V, 0.0, 1.0, seed=s["noise"], step=0, z_out=z)
+        dd.sample_loop(cfg, params, B, L, T, alphas, z, ws, noise_seed=s["noise"])
+
+    # warm-up; the first pass also times every kernel class to find the dominant one
+    per_job_launches = T * (8 * cfg["n_layers"] + 8) + 8
+    dominant = None
+    for i in range(max(1, args.warmup)):
+        if i == 0:
+            dd.profile_begin(per_job_launches)
+        job()
+        torch.cuda.synchronize()
+        if i == 0:
+            dd.profile_end()
+            prof = dd.profile_read()
+            ranked = sorted(prof.items(), key=lambda kv: -kv[1][1])
+            log("warm-up kernel classes (launches, ms):", {k: (v[0], round(v[1], 2)) for k, v in ranked})
+            dominant = next(k for k, _ in ranked if algorithmic_units(k, cfg, B, L)[0] is not None)
+    assert dd.read_device_error(ws[:4].view(torch.int32)) == 0
+
+    dd.profile_begin(args.steps * per_job_launches, classes=[dominant])
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        job()
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    dd.profile_end()
+    prof = dd.profile_read()
+    elapsed = t1 - t0
+    n_l, ms_l = prof[dominant]
+    per_launch, unit, bound = algorithmic_units(dominant, cfg, B, L)
+    achieved = per_launch / (ms_l / n_l * 1e-3) / 1e12
+    peak = PEAK_BF16_TFLOPS if cfg["dtype"] == "bf16" else PEAK_FP32_TFLOPS
+    tokens = args.steps * M
+    out = {
+        "metric": "generated tokens/sec at L=1024,B=16,T=128 on 1 GPU; ms per reverse step",
+        "value": tokens / elapsed,
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": elapsed / args.steps * 1e3,
+        "ms_per_reverse_step": elapsed / (args.steps * T) * 1e3,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": cfg["dtype"],
+        "data": "synthetic",
+        "config": {"workload": f"{w['name']}: {cfg['n_layers']}L d{cfg['d_model']} h{cfg['n_heads']} "
+                               f"F{cfg['d_mlp']} V{V}+{'mask' if cfg['prior'] == 'mask' else 'uniform'}, "
+                               f"random-init weights, all-mask start",
+                   "global_batch": B, "seq_len": L, "reverse_steps": T, "parallelism": "none (1 GPU)"},
+        "roofline": {"kernel": dominant, "bound": bound, "achieved": achieved, "peak": peak, "unit": unit,
+                     "frac": achieved / peak, "traffic": None, "launches": n_l,
+                     "avg_ms": ms_l / n_l},
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(c, cfg, w)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -145,6 +145,7 @@ dd_status dd_init_params(const dd_config* cfg, void* params, size_t params_bytes
  *   logits  device [B*L][ld] of cfg->dtype; columns >= V are left untouched
  *   ld      row stride in elements, ld >= V, ld % 8 == 0
  *   ws      device workspace of >= dd_workspace_bytes(cfg, B, L) bytes
+ * Alignment: logits 16 bytes, params and ws 256 bytes (DD_E_ARG otherwise).
  */
 dd_status dd_denoise_forward(const dd_config* cfg, const void* params,
                              const int32_t* z_t, int32_t B, int32_t L, double alpha_t,
@@ -215,10 +216,14 @@ dd_status dd_gaussian_latent_argmax(const int32_t* x, int32_t rows, int32_t V,
 
 /*
  * Per-launch timing with HIP events recorded on the launching stream.  While
- * enabled, every kernel launch of the library is bracketed by an event pair and
- * attributed to its kernel class.  Not thread-safe; meant for benchmarks.
+ * enabled, every launch of a kernel class whose bit is set in `class_mask`
+ * (bit c = class c; 0 selects every class) is bracketed by an event pair.  At
+ * most `max_launches` launches are recorded.  Not thread-safe; for benchmarks.
+ * Classes: 0 time_embedding, 1 embed_layernorm, 2 layernorm, 3 gemm_qkv,
+ * 4 attention, 5 gemm_attn_out, 6 gemm_mlp_up, 7 gemm_mlp_down, 8 gemm_vocab,
+ * 9 posterior_sample, 10 gaussian_latent, 11 init_params, 12 copy.
  */
-dd_status dd_profile_begin(int32_t max_launches);
+dd_status dd_profile_begin(int32_t max_launches, uint32_t class_mask);
 dd_status dd_profile_end(void);
 int32_t dd_profile_num_classes(void);
 /* Synchronises the recorded events; *name is a static string. */

@@ -83,7 +83,7 @@ def lib():
             "dd_gaussian_latent_argmax": (c.c_int32, [P, c.c_int32, c.c_int32, c.c_double,
                                                       c.c_double, c.c_uint64, c.c_uint32,
                                                       c.c_uint32, P, P, P]),
-            "dd_profile_begin": (c.c_int32, [c.c_int32]),
+            "dd_profile_begin": (c.c_int32, [c.c_int32, c.c_uint32]),
             "dd_profile_end": (c.c_int32, []),
             "dd_profile_num_classes": (c.c_int32, []),
             "dd_profile_read": (c.c_int32, [c.c_int32, c.POINTER(c.c_char_p),
@@ -277,8 +277,17 @@ def read_device_error(err):
     return code.value
 
 
-def profile_begin(max_launches):
-    _check(lib().dd_profile_begin(int(max_launches)))
+PROFILE_CLASSES = ["time_embedding", "embed_layernorm", "layernorm", "gemm_qkv", "attention",
+                   "gemm_attn_out", "gemm_mlp_up", "gemm_mlp_down", "gemm_vocab",
+                   "posterior_sample", "gaussian_latent", "init_params", "copy"]
+
+
+def profile_begin(max_launches, classes=None):
+    """Start event timing; `classes` is a list of class names (None: every class)."""
+    mask = 0
+    for name in classes or []:
+        mask |= 1 << PROFILE_CLASSES.index(name)
+    _check(lib().dd_profile_begin(int(max_launches), mask))
 
 
 def profile_end():

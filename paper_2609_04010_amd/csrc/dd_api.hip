@@ -3,6 +3,7 @@
 #include <math.h>
 #include <stdarg.h>
 #include <stdio.h>
+#include <stdint.h>
 #include <string.h>
 
 #include <vector>
@@ -53,6 +54,7 @@ static const char* kClassNames[KC_COUNT] = {
 struct Profiler {
     bool on = false;
     int cap = 0;
+    uint32_t mask = 0xFFFFFFFFu;
     std::vector<hipEvent_t> ev;   // 2 per launch
     std::vector<int> cls;         // class per launch
     int open = -1;                // index of the launch whose start was recorded
@@ -61,7 +63,7 @@ struct Profiler {
 static Profiler g_prof;
 
 void prof_start(int c, hipStream_t s) {
-    if (!g_prof.on) return;
+    if (!g_prof.on || !((g_prof.mask >> c) & 1u)) return;
     const int n = (int)g_prof.cls.size();
     if (n >= g_prof.cap) { g_prof.dropped++; g_prof.open = -1; return; }
     (void)hipEventRecord(g_prof.ev[2 * n], s);
@@ -378,6 +380,8 @@ dd_status dd_denoise_forward(const dd_config* cfg, const void* params, const int
     DD_CHECK(L <= cfg->max_len, DD_E_SHAPE, "L = %d exceeds max_len = %d", L, cfg->max_len);
     DD_CHECK(alpha_t >= 0.0 && alpha_t <= 1.0, DD_E_ARG, "alpha_t must lie in [0, 1]");
     DD_CHECK(ld >= cfg->vocab && ld % 8 == 0, DD_E_SHAPE, "ld must be >= V and a multiple of 8");
+    DD_CHECK(((uintptr_t)logits & 15) == 0 && ((uintptr_t)ws & 255) == 0 && ((uintptr_t)params & 255) == 0,
+             DD_E_ARG, "logits must be 16-byte aligned, params and ws 256-byte aligned");
     DD_CHECK(forward_supported(cfg), DD_E_UNSUPPORTED, "%s", g_err);
     const size_t need = dd_workspace_bytes(cfg, B, L);
     DD_CHECK(ws_bytes >= need, DD_E_WORKSPACE, "workspace has %zu bytes, needs %zu", ws_bytes, need);
@@ -411,6 +415,8 @@ dd_status dd_sample_loop(const dd_config* cfg, const void* params, int32_t B, in
     DD_CHECK(B > 0 && L > 0 && T > 0, DD_E_ARG, "B, L and T must be positive");
     DD_CHECK(L <= cfg->max_len, DD_E_SHAPE, "L = %d exceeds max_len = %d", L, cfg->max_len);
     DD_CHECK(forward_supported(cfg), DD_E_UNSUPPORTED, "%s", g_err);
+    DD_CHECK(((uintptr_t)ws & 255) == 0 && ((uintptr_t)params & 255) == 0, DD_E_ARG,
+             "params and ws must be 256-byte aligned");
     for (int k = 1; k <= T; ++k) DD_TRY(check_schedule(alphas[k], alphas[k - 1]));
     const size_t need = dd_loop_workspace_bytes(cfg, B, L);
     DD_CHECK(ws_bytes >= need, DD_E_WORKSPACE, "workspace has %zu bytes, needs %zu", ws_bytes, need);
@@ -454,7 +460,7 @@ dd_status dd_gaussian_latent_argmax(const int32_t* x, int32_t rows, int32_t V, d
                          (hipStream_t)stream);
 }
 
-dd_status dd_profile_begin(int32_t max_launches) {
+dd_status dd_profile_begin(int32_t max_launches, uint32_t class_mask) {
     DD_CHECK(max_launches > 0, DD_E_ARG, "max_launches must be positive");
     if ((int)g_prof.ev.size() < 2 * max_launches) {
         for (auto e : g_prof.ev) (void)hipEventDestroy(e);
@@ -465,6 +471,7 @@ dd_status dd_profile_begin(int32_t max_launches) {
         }
     }
     g_prof.cap = max_launches;
+    g_prof.mask = class_mask ? class_mask : 0xFFFFFFFFu;
     g_prof.cls.clear();
     g_prof.dropped = 0;
     g_prof.open = -1;

@@ -28,13 +28,10 @@ constexpr int DH = 64;
 constexpr int KSTR = DH + 8;
 constexpr int VSTR = AK + 8;
 
-// Position of key k (0..63) inside a transposed V row: within each 16-key step s the MFMA operand
-// slots of lane group g hold keys 16s + 4g + {0..3} and 16s + 8 + 4g + {0..3}; storing those eight
-// keys contiguously at 16s + 8g lets each lane read its operand with one 16-byte load.
-DD_DEV int vperm(int k) {
-    const int s = k >> 4, r = k & 3, g = (k >> 2) & 1, h = (k >> 3) & 1;
-    return 16 * s + 8 * g + 4 * h + r;
-}
+// Key order inside a transposed V row: within each 16-key step s the MFMA operand slots of lane
+// group g hold keys 16s + 4g + {0..3} and 16s + 8 + 4g + {0..3}; those eight keys are stored
+// contiguously at positions 16s + 8g .. + 7 (key 16s + 4g + 8h + r at position 16s + 8g + 4h + r),
+// so each lane reads its operand with one 16-byte load.
 
 __global__ __launch_bounds__(256) void attn_bf16_kernel(AttnArgs a) {
     __shared__ __attribute__((aligned(16))) bf16_t Ks[2][AK * KSTR];
@@ -64,19 +61,23 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(AttnArgs a) {
         for (int e = 0; e < 16; ++e) o[i][e] = 0.f;
     float mrow = -INFINITY, lpart = 0.f;
 
+    // K tile: thread handles 16-byte chunks c = tid + 256 r (key c / 8, columns 8 (c % 8) ..).
+    // V tile (stored transposed): thread handles dv chunk vc = tid / 32 and the pair of keys that
+    // sit at transposed positions 2 vp, 2 vp + 1 (vp = tid % 32); these are adjacent keys, so each
+    // dv row receives one 32-bit word per thread.  The upper half-wave visits the 8 dv rows of its
+    // chunk in rotated order so the two rows written by one instruction fall in different banks.
+    const int vc = tid >> 5, vp = tid & 31;
+    const int vkey = 16 * (vp >> 3) + 4 * ((vp >> 2) & 1) + 8 * ((vp >> 1) & 1) + 2 * (vp & 1);
     uint4 rk[2], rv[2];
     auto gload = [&](int kb0) {
 #pragma unroll
         for (int r = 0; r < 2; ++r) {
             const int c = tid + 256 * r, key = c >> 3, dc = (c & 7) * 8, t = kb0 + key;
-            if (t < L) {
-                const bf16_t* p = base + (int64_t)t * a.ld + h * DH + dc;
-                rk[r] = *(const uint4*)(p + d);
-                rv[r] = *(const uint4*)(p + 2 * d);
-            } else {
-                rk[r] = make_uint4(0u, 0u, 0u, 0u);
-                rv[r] = make_uint4(0u, 0u, 0u, 0u);
-            }
+            rk[r] = (t < L) ? *(const uint4*)(base + (int64_t)t * a.ld + d + h * DH + dc)
+                            : make_uint4(0u, 0u, 0u, 0u);
+            const int tv = kb0 + vkey + r;
+            rv[r] = (tv < L) ? *(const uint4*)(base + (int64_t)tv * a.ld + 2 * d + h * DH + 8 * vc)
+                             : make_uint4(0u, 0u, 0u, 0u);
         }
     };
     auto sstore = [&](int buf) {
@@ -84,13 +85,21 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(AttnArgs a) {
         for (int r = 0; r < 2; ++r) {
             const int c = tid + 256 * r, key = c >> 3, dc = (c & 7) * 8;
             *(uint4*)&Ks[buf][key * KSTR + dc] = rk[r];
-            const int pk = vperm(key);
-            const uint32_t w[4] = {rv[r].x, rv[r].y, rv[r].z, rv[r].w};
+        }
+        const uint32_t a0[4] = {rv[0].x, rv[0].y, rv[0].z, rv[0].w};
+        const uint32_t a1[4] = {rv[1].x, rv[1].y, rv[1].z, rv[1].w};
+        uint32_t wv[8];   // wv[e] = (V[key][8 vc + e], V[key + 1][8 vc + e]) as a bf16 pair
 #pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                Vt[buf][(dc + 2 * e) * VSTR + pk] = (bf16_t)(w[e] & 0xFFFFu);
-                Vt[buf][(dc + 2 * e + 1) * VSTR + pk] = (bf16_t)(w[e] >> 16);
-            }
+        for (int e = 0; e < 4; ++e) {
+            wv[2 * e] = __builtin_amdgcn_perm(a1[e], a0[e], 0x05040100u);
+            wv[2 * e + 1] = __builtin_amdgcn_perm(a1[e], a0[e], 0x07060302u);
+        }
+        const bool upper = (lane >> 5) != 0;
+        uint32_t* vt = (uint32_t*)&Vt[buf][0];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+            const int er = upper ? ((e + 4) & 7) : e;
+            vt[((8 * vc + er) * VSTR + 2 * vp) >> 1] = upper ? wv[(e + 4) & 7] : wv[e];
         }
     };
 

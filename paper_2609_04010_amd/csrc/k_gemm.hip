@@ -1,8 +1,8 @@
 // Dense layers of the denoiser: C = A W^T (+ epilogue), A [M][K] row-major, W [N][K] row-major
 // (weights stored [out][in]), so both operands are contiguous along K.
 //
-// bf16 path: 128x128x64 workgroup tiles, 4 wavefronts each owning a 64x64 sub-tile computed with
-// v_mfma_f32_32x32x16_bf16 (fp32 accumulation).  Global -> register prefetch of the next K-tile
+// bf16 path: workgroup tiles of 128 or 256 rows/columns by 64 along K, 4 wavefronts each owning a
+// quarter of the tile, computed with v_mfma_f32_32x32x16_bf16 (fp32 accumulation).  Global -> register prefetch of the next K-tile
 // overlaps the MFMAs on the current one; tiles are double-buffered in padded LDS rows (144 B) so
 // the 16-byte fragment reads are bank-conflict free.  The MFMA's first operand is the weight
 // fragment, so each lane ends with four consecutive output columns of one row, which the
@@ -15,6 +15,7 @@
 // Epilogues: bias -> bf16 (QKV), bias + GELU(tanh) -> bf16 (MLP up), bias + fp32 residual add in
 // place (attention output, MLP down), plain store (vocabulary projection).
 #include <math.h>
+#include <stdlib.h>
 
 #include "kernels.h"
 
@@ -24,9 +25,11 @@ typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8;
 typedef __attribute__((ext_vector_type(16))) float f32x16;
 
 // gelu_tanh(x) = 0.5 x (1 + tanh(y)) = x / (1 + exp(-2y)), y = sqrt(2/pi) (x + 0.044715 x^3)
+// (v_exp_f32 and v_rcp_f32, both about 1 ulp; the result is rounded to bf16 afterwards)
 DD_DEV float gelu_tanh(float x) {
     const float y = 0.7978845608028654f * fmaf(0.044715f * x, x * x, x);
-    return x / (1.0f + __expf(-2.0f * y));
+    const float e = __builtin_amdgcn_exp2f(-2.8853900817779268f * y);   // exp(-2y)
+    return x * __builtin_amdgcn_rcpf(1.0f + e);
 }
 
 DD_DEV void map_tile(int bid, int nblocks, int tiles_m, int tiles_n, int& tm, int& tn) {
@@ -44,15 +47,14 @@ DD_DEV void map_tile(int bid, int nblocks, int tiles_m, int tiles_n, int& tm, in
 }
 
 // ------------------------------------------------------------------------------ bf16 MFMA
-constexpr int BM = 128, BN = 128, BK = 64, LSTR = BK + 8;
+constexpr int BK = 64, LSTR = BK + 8;
 
 template <int EPI>
-DD_DEV void epilogue_bf16(const GemmArgs& g, int m, int n, const float* v) {
+DD_DEV void epilogue_bf16(const GemmArgs& g, int m, int n, const float* v, const float* bias4) {
     float o[4];
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
-        float x = v[e];
-        if (EPI != EPI_PLAIN && n + e < g.N) x += bf16_to_f32(((const bf16_t*)g.bias)[n + e]);
+        float x = v[e] + bias4[e];
         if (EPI == EPI_BIAS_GELU) x = gelu_tanh(x);
         o[e] = x;
     }
@@ -78,63 +80,73 @@ DD_DEV void epilogue_bf16(const GemmArgs& g, int m, int n, const float* v) {
     }
 }
 
-template <int EPI>
+// Workgroup tile TBM x TBN (x BK): 4 wavefronts in a 2 x 2 grid, each owning a (TBM/2) x (TBN/2)
+// sub-tile of MB x NB 32x32 MFMA blocks.  Larger wave tiles read fewer LDS bytes per MFMA flop
+// (64x64: 32 flop/B, 128x128: 64 flop/B).
+template <int TBM, int TBN, int EPI>
 __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmArgs g, int tiles_m, int tiles_n) {
-    __shared__ __attribute__((aligned(16))) bf16_t As[2][BM * LSTR];
-    __shared__ __attribute__((aligned(16))) bf16_t Ws[2][BN * LSTR];
+    constexpr int MB = TBM / 64, NB = TBN / 64;       // 32x32 blocks per wave along M and N
+    constexpr int RA = TBM / 32, RW = TBN / 32;       // 16-byte chunks per thread per K-tile
+    extern __shared__ __attribute__((aligned(16))) bf16_t smem[];
+    bf16_t* As = smem;                        // [2][TBM * LSTR]
+    bf16_t* Ws = smem + 2 * TBM * LSTR;       // [2][TBN * LSTR]
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int wm = wave >> 1, wn = wave & 1;
     int tm, tn;
     map_tile(blockIdx.x, gridDim.x, tiles_m, tiles_n, tm, tn);
-    const int m0 = tm * BM, n0 = tn * BN;
+    const int m0 = tm * TBM, n0 = tn * TBN;
     const bf16_t* A = (const bf16_t*)g.A;
     const bf16_t* W = (const bf16_t*)g.W;
 
-    f32x16 acc[2][2];
+    f32x16 acc[NB][MB];
 #pragma unroll
-    for (int i = 0; i < 2; ++i)
+    for (int i = 0; i < NB; ++i)
 #pragma unroll
-        for (int j = 0; j < 2; ++j)
+        for (int j = 0; j < MB; ++j)
 #pragma unroll
             for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
 
-    uint4 ra[4], rw[4];
+    uint4 ra[RA], rw[RW];
     const int lrow = tid >> 3, lk = (tid & 7) * 8;
     auto gload = [&](int k0) {
         const int gk = k0 + lk;
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-            const int row = lrow + 32 * r;
-            const int gm = m0 + row, gn = n0 + row;
+        for (int r = 0; r < RA; ++r) {
+            const int gm = m0 + lrow + 32 * r;
             ra[r] = (gm < g.M && gk < g.K) ? *(const uint4*)(A + (int64_t)gm * g.lda + gk)
                                            : make_uint4(0u, 0u, 0u, 0u);
+        }
+#pragma unroll
+        for (int r = 0; r < RW; ++r) {
+            const int gn = n0 + lrow + 32 * r;
             rw[r] = (gn < g.N && gk < g.K) ? *(const uint4*)(W + (int64_t)gn * g.ldw + gk)
                                            : make_uint4(0u, 0u, 0u, 0u);
         }
     };
     auto sstore = [&](int buf) {
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-            const int row = lrow + 32 * r;
-            *(uint4*)&As[buf][row * LSTR + lk] = ra[r];
-            *(uint4*)&Ws[buf][row * LSTR + lk] = rw[r];
-        }
+        for (int r = 0; r < RA; ++r)
+            *(uint4*)&As[buf * TBM * LSTR + (lrow + 32 * r) * LSTR + lk] = ra[r];
+#pragma unroll
+        for (int r = 0; r < RW; ++r)
+            *(uint4*)&Ws[buf * TBN * LSTR + (lrow + 32 * r) * LSTR + lk] = rw[r];
     };
     auto compute = [&](int buf) {
+        const bf16_t* Ab = As + buf * TBM * LSTR + (wm * (TBM / 2) + (lane & 31)) * LSTR;
+        const bf16_t* Wb = Ws + buf * TBN * LSTR + (wn * (TBN / 2) + (lane & 31)) * LSTR;
 #pragma unroll
         for (int kk = 0; kk < BK / 16; ++kk) {
             const int koff = kk * 16 + (lane >> 5) * 8;
-            bf16x8 af[2], wf[2];
+            bf16x8 af[MB], wf[NB];
 #pragma unroll
-            for (int i = 0; i < 2; ++i) {
-                af[i] = *(const bf16x8*)&As[buf][(wm * 64 + i * 32 + (lane & 31)) * LSTR + koff];
-                wf[i] = *(const bf16x8*)&Ws[buf][(wn * 64 + i * 32 + (lane & 31)) * LSTR + koff];
-            }
+            for (int i = 0; i < MB; ++i) af[i] = *(const bf16x8*)&Ab[i * 32 * LSTR + koff];
 #pragma unroll
-            for (int nb = 0; nb < 2; ++nb)
+            for (int i = 0; i < NB; ++i) wf[i] = *(const bf16x8*)&Wb[i * 32 * LSTR + koff];
 #pragma unroll
-                for (int mb = 0; mb < 2; ++mb)
+            for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+                for (int mb = 0; mb < MB; ++mb)
                     acc[nb][mb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(wf[nb], af[mb], acc[nb][mb], 0, 0, 0);
         }
     };
@@ -151,21 +163,202 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmArgs g, int tiles_m,
     }
 
 #pragma unroll
-    for (int nb = 0; nb < 2; ++nb)
+    for (int nb = 0; nb < NB; ++nb)
 #pragma unroll
-        for (int mb = 0; mb < 2; ++mb) {
-            const int m = m0 + wm * 64 + mb * 32 + (lane & 31);
-            if (m >= g.M) continue;
+        for (int j4 = 0; j4 < 4; ++j4) {
+            const int n = n0 + wn * (TBN / 2) + nb * 32 + 8 * j4 + 4 * (lane >> 5);
+            if (n >= g.N) continue;
+            float b4[4] = {0.f, 0.f, 0.f, 0.f};
+            if (EPI != EPI_PLAIN)
 #pragma unroll
-            for (int j4 = 0; j4 < 4; ++j4) {
-                const int n = n0 + wn * 64 + nb * 32 + 8 * j4 + 4 * (lane >> 5);
-                if (n >= g.N) continue;
+                for (int e = 0; e < 4; ++e)
+                    if (n + e < g.N) b4[e] = bf16_to_f32(((const bf16_t*)g.bias)[n + e]);
+#pragma unroll
+            for (int mb = 0; mb < MB; ++mb) {
+                const int m = m0 + wm * (TBM / 2) + mb * 32 + (lane & 31);
+                if (m >= g.M) continue;
                 float v[4] = {acc[nb][mb][4 * j4], acc[nb][mb][4 * j4 + 1], acc[nb][mb][4 * j4 + 2],
                               acc[nb][mb][4 * j4 + 3]};
-                epilogue_bf16<EPI>(g, m, n, v);
+                epilogue_bf16<EPI>(g, m, n, v, b4);
             }
         }
 }
+
+// ------------------------------------------------------------------------------ bf16, direct to LDS
+// 256 x 256 x 64 workgroup tile, 4 wavefronts of 128 x 128 (4 x 4 blocks of 32x32, 256 accumulator
+// registers).  Operand tiles travel global -> LDS with global_load_lds_dwordx4 (no staging
+// registers): each wave instruction fills 1 KB = 8 rows of 128 B.  Inside a row the eight 16-byte
+// K-chunks are stored XOR-swizzled (slot = chunk ^ (row & 7)) so that the MFMA fragment reads of
+// eight consecutive rows hit eight different bank groups.  Two LDS stages: the loads of K-tile t+1
+// are issued right after the barrier that publishes K-tile t and overlap its 64 MFMAs per wave;
+// fragments of the next 16-wide K step are read while the current step's MFMAs run.
+// Requires K % 64 == 0; rows past M or N are clamped (their results are never stored).
+constexpr int DT = 256;                       // tile rows / columns
+constexpr int DSTAGE = 2 * DT * BK;           // bf16 elements per stage (A tile, then W tile)
+constexpr int DCSTR = 128 + 8;                // epilogue staging row stride (bf16), 272 B
+constexpr size_t DL_LDS_BYTES = (size_t)4 * 128 * DCSTR * 2 > (size_t)2 * DSTAGE * 2
+                                    ? (size_t)4 * 128 * DCSTR * 2 : (size_t)2 * DSTAGE * 2;
+
+typedef __attribute__((address_space(3))) void lds_void;
+typedef __attribute__((address_space(1))) const void gbl_void;
+
+// ROLE (the profiler class of the layer) only separates the symbols of layers sharing an epilogue.
+template <int EPI, int ROLE>
+__global__ __launch_bounds__(256, 1) void gemm_bf16_dl_kernel(GemmArgs g, int tiles_m, int tiles_n) {
+    extern __shared__ __attribute__((aligned(1024))) bf16_t smem[];
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int wm = wave >> 1, wn = wave & 1;
+    int tm, tn;
+    map_tile(blockIdx.x, gridDim.x, tiles_m, tiles_n, tm, tn);
+    const int m0 = tm * DT, n0 = tn * DT;
+    const bf16_t* A = (const bf16_t*)g.A;
+    const bf16_t* W = (const bf16_t*)g.W;
+
+    // this lane's source rows: wave w fills rows 64 w + 8 i + lane / 8 (i = 0..7) of each tile,
+    // and its 16-byte slot lane % 8 holds K-chunk (lane % 8) ^ (row & 7) = (lane % 8) ^ (lane / 8)
+    const int lrow = 64 * wave + (lane >> 3);
+    const int lchunk = (lane & 7) ^ (lane >> 3);
+    int64_t offA[8], offW[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+        offA[i] = (int64_t)min(m0 + lrow + 8 * i, g.M - 1) * g.lda + lchunk * 8;
+        offW[i] = (int64_t)min(n0 + lrow + 8 * i, g.N - 1) * g.ldw + lchunk * 8;
+    }
+    auto issue = [&](int k0, int stage) {
+        bf16_t* sA = smem + stage * DSTAGE + (64 * wave) * BK;
+        bf16_t* sW = smem + stage * DSTAGE + DT * BK + (64 * wave) * BK;
+#pragma unroll
+        for (int i = 0; i < 8; ++i)
+            __builtin_amdgcn_global_load_lds((gbl_void*)(A + offA[i] + k0), (lds_void*)(sA + 8 * i * BK), 16, 0, 0);
+#pragma unroll
+        for (int i = 0; i < 8; ++i)
+            __builtin_amdgcn_global_load_lds((gbl_void*)(W + offW[i] + k0), (lds_void*)(sW + 8 * i * BK), 16, 0, 0);
+    };
+
+    f32x16 acc[4][4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+#pragma unroll
+            for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
+
+    // fragment rows of this lane; row & 7 == lane & 7 for every block (block bases are multiples of 32)
+    const int frow = lane & 31, fsw = lane & 7, fhalf = lane >> 5;
+    auto frag = [&](const bf16_t* tile, int row0, int kk) -> bf16x8 {
+        const int slot = (2 * kk + fhalf) ^ fsw;
+        return *(const bf16x8*)&tile[(row0 + frow) * BK + slot * 8];
+    };
+
+    const int nk = g.K / BK;
+    issue(0, 0);
+    for (int t = 0; t < nk; ++t) {
+        __builtin_amdgcn_s_waitcnt(0x3F70);      // vmcnt(0): this lane's loads of K-tile t landed
+        __syncthreads();                          // ... everyone's; and everyone left K-tile t-1
+        if (t + 1 < nk) issue((t + 1) * BK, (t + 1) & 1);
+        const bf16_t* sA = smem + (t & 1) * DSTAGE + (wm * 128) * BK;
+        const bf16_t* sW = smem + (t & 1) * DSTAGE + DT * BK + (wn * 128) * BK;
+        bf16x8 af[2][4], wf[2][4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) { af[0][i] = frag(sA, 32 * i, 0); wf[0][i] = frag(sW, 32 * i, 0); }
+#pragma unroll
+        for (int kk = 0; kk < BK / 16; ++kk) {
+            const int cur = kk & 1;
+#pragma unroll
+            for (int nb = 0; nb < 4; ++nb)
+#pragma unroll
+                for (int mb = 0; mb < 4; ++mb)
+                    acc[nb][mb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(wf[cur][nb], af[cur][mb], acc[nb][mb], 0, 0, 0);
+            if (kk + 1 < BK / 16) {
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    af[cur ^ 1][i] = frag(sA, 32 * i, kk + 1);
+                    wf[cur ^ 1][i] = frag(sW, 32 * i, kk + 1);
+                }
+                // issue order inside this step: two MFMAs, then one fragment read of the next step
+#pragma unroll
+                for (int i = 0; i < 8; ++i) {
+                    __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
+                    __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+                }
+            }
+            __builtin_amdgcn_sched_barrier(0);
+        }
+    }
+
+    if (EPI == EPI_BIAS_RESID) {     // fp32 read-modify-write of the residual stream, 16 B per lane
+#pragma unroll
+        for (int nb = 0; nb < 4; ++nb)
+#pragma unroll
+            for (int j4 = 0; j4 < 4; ++j4) {
+                const int n = n0 + wn * 128 + nb * 32 + 8 * j4 + 4 * (lane >> 5);
+                if (n >= g.N) continue;
+                float b4[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+                for (int e = 0; e < 4; ++e)
+                    if (n + e < g.N) b4[e] = bf16_to_f32(((const bf16_t*)g.bias)[n + e]);
+#pragma unroll
+                for (int mb = 0; mb < 4; ++mb) {
+                    const int m = m0 + wm * 128 + mb * 32 + (lane & 31);
+                    if (m >= g.M) continue;
+                    float v[4] = {acc[nb][mb][4 * j4], acc[nb][mb][4 * j4 + 1], acc[nb][mb][4 * j4 + 2],
+                                  acc[nb][mb][4 * j4 + 3]};
+                    epilogue_bf16<EPI>(g, m, n, v, b4);
+                }
+            }
+        return;
+    }
+
+    // bf16 outputs: each wave stages its 128 x 128 sub-tile in LDS (rows padded to 272 B), then
+    // writes whole 256-byte row segments with 16-byte stores.
+    __syncthreads();                              // every wave is done with the operand stages
+    bf16_t* cst = smem + wave * (128 * DCSTR);
+#pragma unroll
+    for (int nb = 0; nb < 4; ++nb)
+#pragma unroll
+        for (int j4 = 0; j4 < 4; ++j4) {
+            const int nl = nb * 32 + 8 * j4 + 4 * (lane >> 5);
+            const int n = n0 + wn * 128 + nl;
+            float b4[4] = {0.f, 0.f, 0.f, 0.f};
+            if (EPI != EPI_PLAIN)
+#pragma unroll
+                for (int e = 0; e < 4; ++e)
+                    if (n + e < g.N) b4[e] = bf16_to_f32(((const bf16_t*)g.bias)[n + e]);
+#pragma unroll
+            for (int mb = 0; mb < 4; ++mb) {
+                float o[4];
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    float x = acc[nb][mb][4 * j4 + e] + b4[e];
+                    if (EPI == EPI_BIAS_GELU) x = gelu_tanh(x);
+                    o[e] = x;
+                }
+                uint2 p;
+                p.x = pack_bf16x2(o[0], o[1]);
+                p.y = pack_bf16x2(o[2], o[3]);
+                *(uint2*)&cst[(mb * 32 + (lane & 31)) * DCSTR + nl] = p;
+            }
+        }
+    bf16_t* C = (bf16_t*)g.C;
+    const int mrow0 = m0 + wm * 128, ncol0 = n0 + wn * 128;
+#pragma unroll 4
+    for (int i = 0; i < 32; ++i) {
+        const int r = i * 4 + (lane >> 4), c = (lane & 15) * 8;
+        const int m = mrow0 + r, n = ncol0 + c;
+        if (m >= g.M || n >= g.N) continue;
+        const uint4 v = *(const uint4*)&cst[r * DCSTR + c];
+        bf16_t* dst = C + (int64_t)m * g.ldc + n;
+        if (n + 7 < g.N) {
+            *(uint4*)dst = v;
+        } else {
+            const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+            for (int e = 0; n + e < g.N; ++e) dst[e] = (bf16_t)((w[e >> 1] >> (16 * (e & 1))) & 0xFFFFu);
+        }
+    }
+}
+
+template <int TBM, int TBN>
+constexpr size_t gemm_lds_bytes() { return (size_t)2 * (TBM + TBN) * LSTR * sizeof(bf16_t); }
 
 // ------------------------------------------------------------------------------ fp32 (validation)
 constexpr int FT = 64, FK = 16;
@@ -219,11 +412,51 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmArgs g, int tiles_m, 
     }
 }
 
-template <int EPI>
+template <int TBM, int TBN, int EPI>
+static void launch_tile(const GemmArgs& g, hipStream_t s) {
+    const int tm = (g.M + TBM - 1) / TBM, tn = (g.N + TBN - 1) / TBN;
+    constexpr size_t lds = gemm_lds_bytes<TBM, TBN>();
+    static bool attr = false;   // one-time opt-in to more than 64 KB of LDS per workgroup
+    if (!attr) {
+        (void)hipFuncSetAttribute((const void*)gemm_bf16_kernel<TBM, TBN, EPI>,
+                                  hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+        attr = true;
+    }
+    hipLaunchKernelGGL((gemm_bf16_kernel<TBM, TBN, EPI>), dim3(tm * tn), dim3(256), lds, s, g, tm, tn);
+}
+
+// Tile choice: the direct-to-LDS 256 x 256 kernel whenever K % 64 == 0 (measured fastest on every
+// denoiser shape), else 128 x 128; DD_GEMM_TILE (0..4) forces one for tuning and tests.
+static int pick_tile(const GemmArgs& g) {
+    const char* e = getenv("DD_GEMM_TILE");
+    const int forced = e ? atoi(e) : -1;
+    if (forced >= 0 && forced <= 4) return (forced == 4 && g.K % BK != 0) ? 0 : forced;
+    return g.K % BK == 0 ? 4 : 0;     // direct-to-LDS 256 x 256 when K is a multiple of 64
+}
+
+template <int EPI, int ROLE>
+static void launch_dl(const GemmArgs& g, hipStream_t s) {
+    const int tm = (g.M + DT - 1) / DT, tn = (g.N + DT - 1) / DT;
+    constexpr size_t lds = DL_LDS_BYTES;
+    static bool attr = false;
+    if (!attr) {
+        (void)hipFuncSetAttribute((const void*)gemm_bf16_dl_kernel<EPI, ROLE>,
+                                  hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+        attr = true;
+    }
+    hipLaunchKernelGGL((gemm_bf16_dl_kernel<EPI, ROLE>), dim3(tm * tn), dim3(256), lds, s, g, tm, tn);
+}
+
+template <int EPI, int ROLE>
 static void launch_epi(int dtype, const GemmArgs& g, hipStream_t s) {
     if (dtype == DD_BF16) {
-        const int tm = (g.M + BM - 1) / BM, tn = (g.N + BN - 1) / BN;
-        hipLaunchKernelGGL(gemm_bf16_kernel<EPI>, dim3(tm * tn), dim3(256), 0, s, g, tm, tn);
+        switch (pick_tile(g)) {
+            case 4: launch_dl<EPI, ROLE>(g, s); break;
+            case 3: launch_tile<256, 256, EPI>(g, s); break;
+            case 2: launch_tile<256, 128, EPI>(g, s); break;
+            case 1: launch_tile<128, 256, EPI>(g, s); break;
+            default: launch_tile<128, 128, EPI>(g, s); break;
+        }
     } else {
         const int tm = (g.M + FT - 1) / FT, tn = (g.N + FT - 1) / FT;
         hipLaunchKernelGGL(gemm_f32_kernel<EPI>, dim3(tm * tn), dim3(256), 0, s, g, tm, tn);
@@ -234,10 +467,13 @@ dd_status launch_gemm(int dtype, int epi, int cls, const GemmArgs& g, hipStream_
     if (g.M == 0 || g.N == 0) return DD_OK;
     ProfScope ps(cls, s);
     switch (epi) {
-        case EPI_BIAS: launch_epi<EPI_BIAS>(dtype, g, s); break;
-        case EPI_BIAS_GELU: launch_epi<EPI_BIAS_GELU>(dtype, g, s); break;
-        case EPI_BIAS_RESID: launch_epi<EPI_BIAS_RESID>(dtype, g, s); break;
-        default: launch_epi<EPI_PLAIN>(dtype, g, s); break;
+        case EPI_BIAS: launch_epi<EPI_BIAS, KC_GEMM_QKV>(dtype, g, s); break;
+        case EPI_BIAS_GELU: launch_epi<EPI_BIAS_GELU, KC_GEMM_MLP1>(dtype, g, s); break;
+        case EPI_BIAS_RESID:
+            if (cls == KC_GEMM_O) launch_epi<EPI_BIAS_RESID, KC_GEMM_O>(dtype, g, s);
+            else launch_epi<EPI_BIAS_RESID, KC_GEMM_MLP2>(dtype, g, s);
+            break;
+        default: launch_epi<EPI_PLAIN, KC_GEMM_VOCAB>(dtype, g, s); break;
     }
     return launch_status("gemm");
 }

@@ -15,7 +15,7 @@ from oracle import params as oparams, sampler as osampler
 from paper_2609_04010_amd import _lib as dd
 
 HEADER = os.path.join(os.path.dirname(os.path.dirname(__file__)), "include", "dd.h")
-FAKE = ctypes.c_void_p(0x1000)   # never dereferenced: every call below fails validation first
+FAKE = ctypes.c_void_p(0x10000)  # never dereferenced: every call below fails validation first
 
 
 def _declared():

@@ -154,3 +154,19 @@ def test_loop_uniform_prior_runs_in_range():
     z0, trace = _loop_gpu(torch, cfg, buf, z1, T, osched.alphas(T), seed=5)
     assert np.all((trace >= 0) & (trace < V))
     assert np.mean(trace[-1] != trace[0]) > 0.5          # the uniform prior keeps revising tokens
+
+
+@pytest.mark.parametrize("tile", ["0", "1", "2", "3", "4"])
+def test_forward_parity_every_gemm_tile(tile, monkeypatch):
+    """Each GEMM tile variant (128/256 rows x 128/256 columns) on ragged M and N."""
+    torch = torch_or_skip()
+    monkeypatch.setenv("DD_GEMM_TILE", tile)
+    say("gemm tile", tile)
+    cfg = workloads.model_cfg(2, n_layers=2)
+    P, buf = _params_host(torch, cfg, 7)
+    z = workloads.masked_state(8, 3, 190, cfg["vocab"], 0.5)
+    got = _forward_gpu(torch, cfg, buf, z, 0.5)
+    ref = oforward.forward(cfg, P, z, 0.5)
+    err = float(np.abs(got - ref).max())
+    say(f"tile {tile}: max |dlogit| = {err:.3e}")
+    assert err <= LOGIT_TOL["bf16"]
