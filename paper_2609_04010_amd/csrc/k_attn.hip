@@ -64,8 +64,7 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(AttnArgs a) {
     // K tile: thread handles 16-byte chunks c = tid + 256 r (key c / 8, columns 8 (c % 8) ..).
     // V tile (stored transposed): thread handles dv chunk vc = tid / 32 and the pair of keys that
     // sit at transposed positions 2 vp, 2 vp + 1 (vp = tid % 32); these are adjacent keys, so each
-    // dv row receives one 32-bit word per thread.  The upper half-wave visits the 8 dv rows of its
-    // chunk in rotated order so the two rows written by one instruction fall in different banks.
+    // dv row receives one 32-bit word per thread (a half-wave writes 128 contiguous bytes).
     const int vc = tid >> 5, vp = tid & 31;
     const int vkey = 16 * (vp >> 3) + 4 * ((vp >> 2) & 1) + 8 * ((vp >> 1) & 1) + 2 * (vp & 1);
     uint4 rk[2], rv[2];
@@ -94,23 +93,18 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(AttnArgs a) {
             wv[2 * e] = __builtin_amdgcn_perm(a1[e], a0[e], 0x05040100u);
             wv[2 * e + 1] = __builtin_amdgcn_perm(a1[e], a0[e], 0x07060302u);
         }
-        const bool upper = (lane >> 5) != 0;
         uint32_t* vt = (uint32_t*)&Vt[buf][0];
 #pragma unroll
-        for (int e = 0; e < 8; ++e) {
-            const int er = upper ? ((e + 4) & 7) : e;
-            vt[((8 * vc + er) * VSTR + 2 * vp) >> 1] = upper ? wv[(e + 4) & 7] : wv[e];
-        }
+        for (int e = 0; e < 8; ++e) vt[((8 * vc + e) * VSTR + 2 * vp) >> 1] = wv[e];
     };
 
-    const int ntiles = (L + AK - 1) / AK;
-    gload(0);
-    sstore(0);
-    __syncthreads();
-    for (int t = 0; t < ntiles; ++t) {
+    // One 64-key tile.
+    // The exponent reference mref is raised only when a row's maximum exceeds it by more than
+    // RESCALE (base-2 units), so probabilities stay below 2^RESCALE and the O accumulators are
+    // rescaled only on those rare steps (checked once per wavefront).
+    constexpr float RESCALE = 8.0f;
+    auto tile = [&](int t) {
         const int buf = t & 1, kb0 = t * AK;
-        if (t + 1 < ntiles) gload(kb0 + AK);
-
         f32x16 sacc[2];
 #pragma unroll
         for (int kb = 0; kb < 2; ++kb) {
@@ -122,7 +116,7 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(AttnArgs a) {
                 sacc[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[kk], sacc[kb], 0, 0, 0);
             }
         }
-        if (kb0 + AK > L) {
+        if (kb0 + AK > L) {          // wave-uniform: only the last tile can run past L
 #pragma unroll
             for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
@@ -136,37 +130,48 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(AttnArgs a) {
         for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
             for (int j = 0; j < 16; ++j) mloc = fmaxf(mloc, sacc[kb][j]);
-        mloc = fmaxf(mloc, __shfl_xor(mloc, 32, 64));
-        const float mnew = fmaxf(mrow, mloc * a.scale_log2);
-        const float corr = __builtin_amdgcn_exp2f(mrow - mnew);
+        mloc = fmaxf(mloc, __shfl_xor(mloc, 32, 64)) * a.scale_log2;
+        const bool raise = mloc > mrow + RESCALE;
+        if (__any(raise)) {
+            const float mnew = raise ? mloc : mrow;
+            const float corr = __builtin_amdgcn_exp2f(mrow - mnew);
+            lpart *= corr;
+#pragma unroll
+            for (int i = 0; i < 2; ++i)
+#pragma unroll
+                for (int e = 0; e < 16; ++e) o[i][e] *= corr;
+            mrow = mnew;
+        }
         float psum = 0.f;
 #pragma unroll
         for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
             for (int j = 0; j < 16; ++j) {
-                const float p = __builtin_amdgcn_exp2f(fmaf(sacc[kb][j], a.scale_log2, -mnew));
+                const float p = __builtin_amdgcn_exp2f(fmaf(sacc[kb][j], a.scale_log2, -mrow));
                 sacc[kb][j] = p;
                 psum += p;
             }
-        lpart = fmaf(lpart, corr, psum);
-        mrow = mnew;
+        lpart += psum;
 #pragma unroll
-        for (int i = 0; i < 2; ++i)
-#pragma unroll
-            for (int e = 0; e < 16; ++e) o[i][e] *= corr;
-
-#pragma unroll
-        for (int s = 0; s < 4; ++s) {
+        for (int s4 = 0; s4 < 4; ++s4) {
             bf16x8 pf;
 #pragma unroll
-            for (int e = 0; e < 8; ++e) pf[e] = (__bf16)sacc[s >> 1][8 * (s & 1) + e];
+            for (int e = 0; e < 8; ++e) pf[e] = (__bf16)sacc[s4 >> 1][8 * (s4 & 1) + e];
 #pragma unroll
             for (int blk = 0; blk < 2; ++blk) {
-                const bf16x8 vf = *(const bf16x8*)&Vt[buf][(blk * 32 + (lane & 31)) * VSTR + s * 16 + grp * 8];
+                const bf16x8 vf = *(const bf16x8*)&Vt[buf][(blk * 32 + (lane & 31)) * VSTR + s4 * 16 + grp * 8];
                 o[blk] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf, o[blk], 0, 0, 0);
             }
         }
-        if (t + 1 < ntiles) sstore(buf ^ 1);
+    };
+    const int ntiles = (L + AK - 1) / AK;
+    gload(0);
+    sstore(0);
+    __syncthreads();
+    for (int t = 0; t < ntiles; ++t) {
+        if (t + 1 < ntiles) gload((t + 1) * AK);
+        tile(t);
+        if (t + 1 < ntiles) sstore((t + 1) & 1);
         __syncthreads();
     }
 

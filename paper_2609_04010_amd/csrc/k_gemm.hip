@@ -185,59 +185,69 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmArgs g, int tiles_m,
 }
 
 // ------------------------------------------------------------------------------ bf16, direct to LDS
-// 256 x 256 x 64 workgroup tile, 4 wavefronts of 128 x 128 (4 x 4 blocks of 32x32, 256 accumulator
-// registers).  Operand tiles travel global -> LDS with global_load_lds_dwordx4 (no staging
-// registers): each wave instruction fills 1 KB = 8 rows of 128 B.  Inside a row the eight 16-byte
-// K-chunks are stored XOR-swizzled (slot = chunk ^ (row & 7)) so that the MFMA fragment reads of
-// eight consecutive rows hit eight different bank groups.  Two LDS stages: the loads of K-tile t+1
-// are issued right after the barrier that publishes K-tile t and overlap its 64 MFMAs per wave;
-// fragments of the next 16-wide K step are read while the current step's MFMAs run.
-// Requires K % 64 == 0; rows past M or N are clamped (their results are never stored).
-constexpr int DT = 256;                       // tile rows / columns
-constexpr int DSTAGE = 2 * DT * BK;           // bf16 elements per stage (A tile, then W tile)
-constexpr int DCSTR = 128 + 8;                // epilogue staging row stride (bf16), 272 B
-constexpr size_t DL_LDS_BYTES = (size_t)4 * 128 * DCSTR * 2 > (size_t)2 * DSTAGE * 2
-                                    ? (size_t)4 * 128 * DCSTR * 2 : (size_t)2 * DSTAGE * 2;
+// 256 x TBN x 64 workgroup tile (TBN = 256 or 192), 4 wavefronts of 128 x TBN/2 (4 x NBW blocks of
+// 32x32 MFMA, NBW = 4 or 3).  Operand tiles travel global -> LDS with global_load_lds_dwordx4 (no
+// staging registers): each wave instruction fills 1 KB = 8 rows of 128 B.  Inside a row the eight
+// 16-byte K-chunks are stored XOR-swizzled (slot = chunk ^ (row & 7)) so that the MFMA fragment
+// reads of eight consecutive rows hit eight different bank groups.  Two LDS stages: the loads of
+// K-tile t+1 are issued right after the barrier that publishes K-tile t and overlap its MFMAs;
+// fragments of the next 16-wide K step are read between the current step's MFMAs.
+// bf16 outputs are staged per wave in padded LDS rows and written as 16-byte row segments.
+// The 192-wide variant exists for tile quantisation: with d = 768 it divides N = 768, 2304 and
+// 3072 into whole rounds of 256 CUs.  Requires K % 64 == 0; rows past M or N are clamped (their
+// results are never stored).
+constexpr int DM = 256;                       // tile rows (M)
+template <int NBW> struct DLShape {
+    static constexpr int TBN = 64 * NBW;                      // tile columns (N)
+    static constexpr int WN = 32 * NBW;                       // columns per wave
+    static constexpr int STAGE = (DM + TBN) * BK;             // bf16 elements per stage
+    static constexpr int CSTR = WN + 8;                       // epilogue staging row stride (bf16)
+    static constexpr size_t LDS = (size_t)4 * 128 * CSTR * 2 > (size_t)2 * STAGE * 2
+                                      ? (size_t)4 * 128 * CSTR * 2 : (size_t)2 * STAGE * 2;
+};
 
 typedef __attribute__((address_space(3))) void lds_void;
 typedef __attribute__((address_space(1))) const void gbl_void;
 
 // ROLE (the profiler class of the layer) only separates the symbols of layers sharing an epilogue.
-template <int EPI, int ROLE>
+template <int EPI, int ROLE, int NBW>
 __global__ __launch_bounds__(256, 1) void gemm_bf16_dl_kernel(GemmArgs g, int tiles_m, int tiles_n) {
+    using S = DLShape<NBW>;
+    constexpr int NIW = S::TBN / 32;          // W load instructions per wave per stage
     extern __shared__ __attribute__((aligned(1024))) bf16_t smem[];
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int wm = wave >> 1, wn = wave & 1;
     int tm, tn;
     map_tile(blockIdx.x, gridDim.x, tiles_m, tiles_n, tm, tn);
-    const int m0 = tm * DT, n0 = tn * DT;
+    const int m0 = tm * DM, n0 = tn * S::TBN;
     const bf16_t* A = (const bf16_t*)g.A;
     const bf16_t* W = (const bf16_t*)g.W;
 
-    // this lane's source rows: wave w fills rows 64 w + 8 i + lane / 8 (i = 0..7) of each tile,
-    // and its 16-byte slot lane % 8 holds K-chunk (lane % 8) ^ (row & 7) = (lane % 8) ^ (lane / 8)
-    const int lrow = 64 * wave + (lane >> 3);
+    // this lane's source rows: wave w fills A rows 64 w + 8 i + lane / 8 (i < 8) and W rows
+    // (TBN / 4) w + 8 i + lane / 8 (i < NIW); its 16-byte slot lane % 8 holds K-chunk
+    // (lane % 8) ^ (row & 7) = (lane % 8) ^ (lane / 8)
     const int lchunk = (lane & 7) ^ (lane >> 3);
-    int64_t offA[8], offW[8];
+    int64_t offA[8], offW[NIW];
 #pragma unroll
-    for (int i = 0; i < 8; ++i) {
-        offA[i] = (int64_t)min(m0 + lrow + 8 * i, g.M - 1) * g.lda + lchunk * 8;
-        offW[i] = (int64_t)min(n0 + lrow + 8 * i, g.N - 1) * g.ldw + lchunk * 8;
-    }
+    for (int i = 0; i < 8; ++i)
+        offA[i] = (int64_t)min(m0 + 64 * wave + 8 * i + (lane >> 3), g.M - 1) * g.lda + lchunk * 8;
+#pragma unroll
+    for (int i = 0; i < NIW; ++i)
+        offW[i] = (int64_t)min(n0 + (S::TBN / 4) * wave + 8 * i + (lane >> 3), g.N - 1) * g.ldw + lchunk * 8;
     auto issue = [&](int k0, int stage) {
-        bf16_t* sA = smem + stage * DSTAGE + (64 * wave) * BK;
-        bf16_t* sW = smem + stage * DSTAGE + DT * BK + (64 * wave) * BK;
+        bf16_t* sA = smem + stage * S::STAGE + (64 * wave) * BK;
+        bf16_t* sW = smem + stage * S::STAGE + DM * BK + ((S::TBN / 4) * wave) * BK;
 #pragma unroll
         for (int i = 0; i < 8; ++i)
             __builtin_amdgcn_global_load_lds((gbl_void*)(A + offA[i] + k0), (lds_void*)(sA + 8 * i * BK), 16, 0, 0);
 #pragma unroll
-        for (int i = 0; i < 8; ++i)
+        for (int i = 0; i < NIW; ++i)
             __builtin_amdgcn_global_load_lds((gbl_void*)(W + offW[i] + k0), (lds_void*)(sW + 8 * i * BK), 16, 0, 0);
     };
 
-    f32x16 acc[4][4];
+    f32x16 acc[NBW][4];
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
+    for (int i = 0; i < NBW; ++i)
 #pragma unroll
         for (int j = 0; j < 4; ++j)
 #pragma unroll
@@ -256,28 +266,29 @@ __global__ __launch_bounds__(256, 1) void gemm_bf16_dl_kernel(GemmArgs g, int ti
         __builtin_amdgcn_s_waitcnt(0x3F70);      // vmcnt(0): this lane's loads of K-tile t landed
         __syncthreads();                          // ... everyone's; and everyone left K-tile t-1
         if (t + 1 < nk) issue((t + 1) * BK, (t + 1) & 1);
-        const bf16_t* sA = smem + (t & 1) * DSTAGE + (wm * 128) * BK;
-        const bf16_t* sW = smem + (t & 1) * DSTAGE + DT * BK + (wn * 128) * BK;
-        bf16x8 af[2][4], wf[2][4];
+        const bf16_t* sA = smem + (t & 1) * S::STAGE + (wm * 128) * BK;
+        const bf16_t* sW = smem + (t & 1) * S::STAGE + DM * BK + (wn * S::WN) * BK;
+        bf16x8 af[2][4], wf[2][NBW];
 #pragma unroll
-        for (int i = 0; i < 4; ++i) { af[0][i] = frag(sA, 32 * i, 0); wf[0][i] = frag(sW, 32 * i, 0); }
+        for (int i = 0; i < 4; ++i) af[0][i] = frag(sA, 32 * i, 0);
+#pragma unroll
+        for (int i = 0; i < NBW; ++i) wf[0][i] = frag(sW, 32 * i, 0);
 #pragma unroll
         for (int kk = 0; kk < BK / 16; ++kk) {
             const int cur = kk & 1;
 #pragma unroll
-            for (int nb = 0; nb < 4; ++nb)
+            for (int nb = 0; nb < NBW; ++nb)
 #pragma unroll
                 for (int mb = 0; mb < 4; ++mb)
                     acc[nb][mb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(wf[cur][nb], af[cur][mb], acc[nb][mb], 0, 0, 0);
             if (kk + 1 < BK / 16) {
 #pragma unroll
-                for (int i = 0; i < 4; ++i) {
-                    af[cur ^ 1][i] = frag(sA, 32 * i, kk + 1);
-                    wf[cur ^ 1][i] = frag(sW, 32 * i, kk + 1);
-                }
-                // issue order inside this step: two MFMAs, then one fragment read of the next step
+                for (int i = 0; i < 4; ++i) af[cur ^ 1][i] = frag(sA, 32 * i, kk + 1);
 #pragma unroll
-                for (int i = 0; i < 8; ++i) {
+                for (int i = 0; i < NBW; ++i) wf[cur ^ 1][i] = frag(sW, 32 * i, kk + 1);
+                // issue order inside this step: MFMAs interleaved with the next step's reads
+#pragma unroll
+                for (int i = 0; i < 4 + NBW; ++i) {
                     __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
                     __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
                 }
@@ -288,10 +299,10 @@ __global__ __launch_bounds__(256, 1) void gemm_bf16_dl_kernel(GemmArgs g, int ti
 
     if (EPI == EPI_BIAS_RESID) {     // fp32 read-modify-write of the residual stream, 16 B per lane
 #pragma unroll
-        for (int nb = 0; nb < 4; ++nb)
+        for (int nb = 0; nb < NBW; ++nb)
 #pragma unroll
             for (int j4 = 0; j4 < 4; ++j4) {
-                const int n = n0 + wn * 128 + nb * 32 + 8 * j4 + 4 * (lane >> 5);
+                const int n = n0 + wn * S::WN + nb * 32 + 8 * j4 + 4 * (lane >> 5);
                 if (n >= g.N) continue;
                 float b4[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
@@ -309,16 +320,16 @@ __global__ __launch_bounds__(256, 1) void gemm_bf16_dl_kernel(GemmArgs g, int ti
         return;
     }
 
-    // bf16 outputs: each wave stages its 128 x 128 sub-tile in LDS (rows padded to 272 B), then
-    // writes whole 256-byte row segments with 16-byte stores.
+    // bf16 outputs: each wave stages its 128 x WN sub-tile in LDS (rows padded by 16 B), then
+    // writes whole row segments with 16-byte stores.
     __syncthreads();                              // every wave is done with the operand stages
-    bf16_t* cst = smem + wave * (128 * DCSTR);
+    bf16_t* cst = smem + wave * (128 * S::CSTR);
 #pragma unroll
-    for (int nb = 0; nb < 4; ++nb)
+    for (int nb = 0; nb < NBW; ++nb)
 #pragma unroll
         for (int j4 = 0; j4 < 4; ++j4) {
             const int nl = nb * 32 + 8 * j4 + 4 * (lane >> 5);
-            const int n = n0 + wn * 128 + nl;
+            const int n = n0 + wn * S::WN + nl;
             float b4[4] = {0.f, 0.f, 0.f, 0.f};
             if (EPI != EPI_PLAIN)
 #pragma unroll
@@ -336,17 +347,21 @@ __global__ __launch_bounds__(256, 1) void gemm_bf16_dl_kernel(GemmArgs g, int ti
                 uint2 p;
                 p.x = pack_bf16x2(o[0], o[1]);
                 p.y = pack_bf16x2(o[2], o[3]);
-                *(uint2*)&cst[(mb * 32 + (lane & 31)) * DCSTR + nl] = p;
+                *(uint2*)&cst[(mb * 32 + (lane & 31)) * S::CSTR + nl] = p;
             }
         }
     bf16_t* C = (bf16_t*)g.C;
-    const int mrow0 = m0 + wm * 128, ncol0 = n0 + wn * 128;
-#pragma unroll 4
-    for (int i = 0; i < 32; ++i) {
-        const int r = i * 4 + (lane >> 4), c = (lane & 15) * 8;
+    const int mrow0 = m0 + wm * 128, ncol0 = n0 + wn * S::WN;
+    // WN = 128: 16 chunks per row, 4 rows per wave instruction; WN = 96: 12 chunks per row, 5 rows
+    // per instruction (lanes 60..63 idle)
+    constexpr int CPR = S::WN / 8;                // 16-byte chunks per staged row
+    constexpr int RPI = 64 / CPR;                 // rows per wave instruction
+    for (int r0 = 0; r0 < 128; r0 += RPI) {
+        const int r = r0 + lane / CPR, c = (lane % CPR) * 8;
+        if (lane >= RPI * CPR || r >= 128) continue;
         const int m = mrow0 + r, n = ncol0 + c;
         if (m >= g.M || n >= g.N) continue;
-        const uint4 v = *(const uint4*)&cst[r * DCSTR + c];
+        const uint4 v = *(const uint4*)&cst[r * S::CSTR + c];
         bf16_t* dst = C + (int64_t)m * g.ldc + n;
         if (n + 7 < g.N) {
             *(uint4*)dst = v;
@@ -425,33 +440,50 @@ static void launch_tile(const GemmArgs& g, hipStream_t s) {
     hipLaunchKernelGGL((gemm_bf16_kernel<TBM, TBN, EPI>), dim3(tm * tn), dim3(256), lds, s, g, tm, tn);
 }
 
-// Tile choice: the direct-to-LDS 256 x 256 kernel whenever K % 64 == 0 (measured fastest on every
-// denoiser shape), else 128 x 128; DD_GEMM_TILE (0..4) forces one for tuning and tests.
+// Tile choice for the direct-to-LDS kernel: the N width (256 or 192) with the smaller estimated time,
+// counting whole rounds of workgroups over the CUs (a round of 192-wide tiles takes about 0.85 of a
+// round of 256-wide ones on MI355X).  K % 64 != 0 falls back to the 128 x 128 register-staged kernel.  DD_GEMM_TILE (0..5)
+// forces a variant for tuning and tests (4: 256 x 256, 5: 256 x 192).
+static int g_num_cus = 0;
+
 static int pick_tile(const GemmArgs& g) {
     const char* e = getenv("DD_GEMM_TILE");
     const int forced = e ? atoi(e) : -1;
-    if (forced >= 0 && forced <= 4) return (forced == 4 && g.K % BK != 0) ? 0 : forced;
-    return g.K % BK == 0 ? 4 : 0;     // direct-to-LDS 256 x 256 when K is a multiple of 64
+    if (forced >= 4 && forced <= 5 && g.K % BK != 0) return 0;
+    if (forced >= 0 && forced <= 5) return forced;
+    if (g.K % BK != 0) return 0;
+    if (g_num_cus == 0) {
+        int dev = 0;
+        (void)hipGetDevice(&dev);
+        if (hipDeviceGetAttribute(&g_num_cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+            g_num_cus <= 0)
+            g_num_cus = 256;
+    }
+    const int64_t tm = (g.M + DM - 1) / DM;
+    const int64_t r256 = (tm * ((g.N + 255) / 256) + g_num_cus - 1) / g_num_cus;
+    const int64_t r192 = (tm * ((g.N + 191) / 192) + g_num_cus - 1) / g_num_cus;
+    return (17 * r192 < 20 * r256) ? 5 : 4;
 }
 
-template <int EPI, int ROLE>
+template <int EPI, int ROLE, int NBW>
 static void launch_dl(const GemmArgs& g, hipStream_t s) {
-    const int tm = (g.M + DT - 1) / DT, tn = (g.N + DT - 1) / DT;
-    constexpr size_t lds = DL_LDS_BYTES;
+    using S = DLShape<NBW>;
+    const int tm = (g.M + DM - 1) / DM, tn = (g.N + S::TBN - 1) / S::TBN;
     static bool attr = false;
     if (!attr) {
-        (void)hipFuncSetAttribute((const void*)gemm_bf16_dl_kernel<EPI, ROLE>,
-                                  hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+        (void)hipFuncSetAttribute((const void*)gemm_bf16_dl_kernel<EPI, ROLE, NBW>,
+                                  hipFuncAttributeMaxDynamicSharedMemorySize, (int)S::LDS);
         attr = true;
     }
-    hipLaunchKernelGGL((gemm_bf16_dl_kernel<EPI, ROLE>), dim3(tm * tn), dim3(256), lds, s, g, tm, tn);
+    hipLaunchKernelGGL((gemm_bf16_dl_kernel<EPI, ROLE, NBW>), dim3(tm * tn), dim3(256), S::LDS, s, g, tm, tn);
 }
 
 template <int EPI, int ROLE>
 static void launch_epi(int dtype, const GemmArgs& g, hipStream_t s) {
     if (dtype == DD_BF16) {
         switch (pick_tile(g)) {
-            case 4: launch_dl<EPI, ROLE>(g, s); break;
+            case 5: launch_dl<EPI, ROLE, 3>(g, s); break;
+            case 4: launch_dl<EPI, ROLE, 4>(g, s); break;
             case 3: launch_tile<256, 256, EPI>(g, s); break;
             case 2: launch_tile<256, 128, EPI>(g, s); break;
             case 1: launch_tile<128, 256, EPI>(g, s); break;
