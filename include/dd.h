@@ -193,6 +193,9 @@ dd_status dd_posterior_sample(int32_t prior, const void* logits, int32_t logits_
  *   z_trace      NULL or device int32 [T + 1][B*L]: z_1 then the state after
  *                each step.
  *   ws           device workspace >= dd_loop_workspace_bytes(cfg, B, L).
+ * Masked prior (bf16): each step lists the still-masked rows and runs the vocabulary projection
+ * and the draw on those rows only; carried-over rows need no logits.  The result is identical to
+ * calling dd_denoise_forward and dd_posterior_sample on every row.
  */
 dd_status dd_sample_loop(const dd_config* cfg, const void* params, int32_t B, int32_t L,
                          int32_t T, const double* alphas, int32_t* z,
@@ -221,7 +224,7 @@ dd_status dd_gaussian_latent_argmax(const int32_t* x, int32_t rows, int32_t V,
  * most `max_launches` launches are recorded.  Not thread-safe; for benchmarks.
  * Classes: 0 time_embedding, 1 embed_layernorm, 2 layernorm, 3 gemm_qkv,
  * 4 attention, 5 gemm_attn_out, 6 gemm_mlp_up, 7 gemm_mlp_down, 8 gemm_vocab,
- * 9 posterior_sample, 10 gaussian_latent, 11 init_params, 12 copy.
+ * 9 posterior_sample, 10 gaussian_latent, 11 init_params, 12 copy, 13 compact_masked.
  */
 dd_status dd_profile_begin(int32_t max_launches, uint32_t class_mask);
 dd_status dd_profile_end(void);

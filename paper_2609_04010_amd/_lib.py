@@ -279,7 +279,7 @@ def read_device_error(err):
 
 PROFILE_CLASSES = ["time_embedding", "embed_layernorm", "layernorm", "gemm_qkv", "attention",
                    "gemm_attn_out", "gemm_mlp_up", "gemm_mlp_down", "gemm_vocab",
-                   "posterior_sample", "gaussian_latent", "init_params", "copy"]
+                   "posterior_sample", "gaussian_latent", "init_params", "copy", "compact_masked"]
 
 
 def profile_begin(max_launches, classes=None):

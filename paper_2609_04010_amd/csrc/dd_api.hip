@@ -49,7 +49,7 @@ dd_status launch_status(const char* what) {
 static const char* kClassNames[KC_COUNT] = {
     "time_embedding", "embed_layernorm", "layernorm", "gemm_qkv", "attention", "gemm_attn_out",
     "gemm_mlp_up", "gemm_mlp_down", "gemm_vocab", "posterior_sample", "gaussian_latent",
-    "init_params", "copy"};
+    "init_params", "copy", "compact_masked"};
 
 struct Profiler {
     bool on = false;
@@ -143,7 +143,7 @@ static bool is_gain(const dd_config* c, int id) {
 }
 
 struct WsLayout {
-    size_t err, temb, h, xln, qkv, att, mlp, logits, total_fwd, total_loop;
+    size_t err, temb, h, xln, qkv, att, mlp, logits, rows, count, total_fwd, total_loop;
 };
 
 static WsLayout ws_layout(const dd_config* c, int64_t M) {
@@ -162,6 +162,8 @@ static WsLayout ws_layout(const dd_config* c, int64_t M) {
     w.logits = off;
     const int64_t ld = (c->vocab + 63) / 64 * 64;
     off = align256(off + (size_t)(M * ld) * es);
+    w.rows = off; off = align256(off + (size_t)M * 4);
+    w.count = off; off = align256(off + 4);
     w.total_loop = off;
     return w;
 }
@@ -180,9 +182,12 @@ static bool forward_supported(const dd_config* c) {
     return true;
 }
 
+// vocab_rows / vocab_count (device, nullable): restrict the vocabulary projection to the listed
+// rows, written compacted (row j of `logits` belongs to token row vocab_rows[j]).
 static dd_status run_forward(const dd_config* c, const void* params, const int32_t* z, int32_t B,
                              int32_t L, double alpha_t, void* logits, int64_t ld, char* ws,
-                             hipStream_t s) {
+                             hipStream_t s, const int32_t* vocab_rows = nullptr,
+                             const int32_t* vocab_count = nullptr) {
     const std::vector<Tensor> T = tensor_list(c);
     const WsLayout w = ws_layout(c, (int64_t)B * L);
     const char* P = (const char*)params;
@@ -207,23 +212,28 @@ static dd_status run_forward(const dd_config* c, const void* params, const int32
     for (int l = 0; l < nl; ++l) {
         const int b = 2 + 12 * l;
         GemmArgs g;
-        g = {xln, d, tp(b + 2), d, tp(b + 3), qkv, 3 * d, (int)M, 3 * d, d};
+        g = {xln, d, tp(b + 2), d, tp(b + 3), qkv, 3 * d, (int)M, 3 * d, d, nullptr, nullptr};
         DD_TRY(launch_gemm(dt, EPI_BIAS, KC_GEMM_QKV, g, s));
         AttnArgs aa = {qkv, 3 * d, att, d, B, L, H, d,
                        (float)(1.4426950408889634 / sqrt((double)(d / H)))};
         DD_TRY(launch_attn(dt, aa, s));
-        g = {att, d, tp(b + 4), d, tp(b + 5), h, d, (int)M, d, d};
+        g = {att, d, tp(b + 4), d, tp(b + 5), h, d, (int)M, d, d, nullptr, nullptr};
         DD_TRY(launch_gemm(dt, EPI_BIAS_RESID, KC_GEMM_O, g, s));
         DD_TRY(launch_ln(dt, h, M, d, tp(b + 6), tp(b + 7), c->norm_eps, xln, s));
-        g = {xln, d, tp(b + 8), d, tp(b + 9), mlp, F, (int)M, F, d};
+        g = {xln, d, tp(b + 8), d, tp(b + 9), mlp, F, (int)M, F, d, nullptr, nullptr};
         DD_TRY(launch_gemm(dt, EPI_BIAS_GELU, KC_GEMM_MLP1, g, s));
-        g = {mlp, F, tp(b + 10), F, tp(b + 11), h, d, (int)M, d, F};
+        g = {mlp, F, tp(b + 10), F, tp(b + 11), h, d, (int)M, d, F, nullptr, nullptr};
         DD_TRY(launch_gemm(dt, EPI_BIAS_RESID, KC_GEMM_MLP2, g, s));
         const int gn = (l + 1 < nl) ? b + 12 : lnf;
         DD_TRY(launch_ln(dt, h, M, d, tp(gn), tp(gn + 1), c->norm_eps, xln, s));
     }
-    GemmArgs g = {xln, d, tp(lnf + 2), d, nullptr, logits, ld, (int)M, V, d};
-    DD_TRY(launch_gemm(dt, EPI_PLAIN, KC_GEMM_VOCAB, g, s));
+    if (vocab_rows) {   // only the listed rows (count on the device) get logits, compacted
+        GemmArgs g = {xln, d, tp(lnf + 2), d, nullptr, logits, ld, (int)M, V, d, vocab_rows, vocab_count};
+        DD_TRY(launch_gemm(dt, EPI_PLAIN, KC_GEMM_VOCAB, g, s));
+    } else {
+        GemmArgs g = {xln, d, tp(lnf + 2), d, nullptr, logits, ld, (int)M, V, d, nullptr, nullptr};
+        DD_TRY(launch_gemm(dt, EPI_PLAIN, KC_GEMM_VOCAB, g, s));
+    }
     (void)es;
     return DD_OK;
 }
@@ -435,13 +445,22 @@ dd_status dd_sample_loop(const dd_config* cfg, const void* params, int32_t B, in
         DD_CHECK(e == hipSuccess, DD_E_HIP, "trace copy: %s", hipGetErrorString(e));
         return DD_OK;
     };
+    // Masked prior: rows already unmasked are carried over and need no logits, so the vocabulary
+    // projection and the draw run on the compacted list of still-masked rows (same per-row
+    // arithmetic and noise counters as the full path, so the result is identical).
+    const bool compact = cfg->prior == DD_PRIOR_MASK && gemm_gather_supported(cfg->dtype, cfg->d_model);
+    int32_t* rows = (int32_t*)(wsc + w.rows);
+    int32_t* count = (int32_t*)(wsc + w.count);
     DD_TRY(trace_copy(0));
     for (int k = T; k >= 1; --k) {
-        DD_TRY(run_forward(cfg, params, z, B, L, alphas[k], logits, ld, wsc, s));
+        if (compact) DD_TRY(launch_compact(z, M, cfg->vocab, rows, count, s));
+        DD_TRY(run_forward(cfg, params, z, B, L, alphas[k], logits, ld, wsc, s,
+                           compact ? rows : nullptr, compact ? count : nullptr));
         const uint32_t* nw = noise_words ? noise_words + (int64_t)(k - 1) * M * nu : nullptr;
-        const PostArgs a = make_post(cfg->prior, logits, ld, (int32_t)M, cfg->vocab, z, alphas[k],
-                                     alphas[k - 1], nw, noise_seed, (uint32_t)k, 0u, z, nullptr,
-                                     (int32_t*)(wsc + w.err));
+        PostArgs a = make_post(cfg->prior, logits, ld, (int32_t)M, cfg->vocab, z, alphas[k],
+                               alphas[k - 1], nw, noise_seed, (uint32_t)k, 0u, z, nullptr,
+                               (int32_t*)(wsc + w.err));
+        if (compact) { a.rows_idx = rows; a.count = count; }
         DD_TRY(launch_posterior(a, cfg->dtype, s));
         DD_TRY(trace_copy(T - k + 1));
     }

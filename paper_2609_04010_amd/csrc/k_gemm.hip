@@ -217,8 +217,18 @@ __global__ __launch_bounds__(256, 1) void gemm_bf16_dl_kernel(GemmArgs g, int ti
     extern __shared__ __attribute__((aligned(1024))) bf16_t smem[];
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int wm = wave >> 1, wn = wave & 1;
+    // Gathered mode: only the first *m_count output rows exist; the tile grid is re-derived from
+    // that device-side count so the active tiles are spread over every XCD, and surplus
+    // workgroups leave at once.
+    int M = g.M, nblocks = gridDim.x;
+    if (g.m_count) {
+        M = *g.m_count;
+        tiles_m = (M + DM - 1) / DM;
+        nblocks = tiles_m * tiles_n;
+        if ((int)blockIdx.x >= nblocks) return;
+    }
     int tm, tn;
-    map_tile(blockIdx.x, gridDim.x, tiles_m, tiles_n, tm, tn);
+    map_tile(blockIdx.x, nblocks, tiles_m, tiles_n, tm, tn);
     const int m0 = tm * DM, n0 = tn * S::TBN;
     const bf16_t* A = (const bf16_t*)g.A;
     const bf16_t* W = (const bf16_t*)g.W;
@@ -229,8 +239,10 @@ __global__ __launch_bounds__(256, 1) void gemm_bf16_dl_kernel(GemmArgs g, int ti
     const int lchunk = (lane & 7) ^ (lane >> 3);
     int64_t offA[8], offW[NIW];
 #pragma unroll
-    for (int i = 0; i < 8; ++i)
-        offA[i] = (int64_t)min(m0 + 64 * wave + 8 * i + (lane >> 3), g.M - 1) * g.lda + lchunk * 8;
+    for (int i = 0; i < 8; ++i) {
+        const int r = min(m0 + 64 * wave + 8 * i + (lane >> 3), M - 1);
+        offA[i] = (int64_t)(g.a_rows ? g.a_rows[r] : r) * g.lda + lchunk * 8;
+    }
 #pragma unroll
     for (int i = 0; i < NIW; ++i)
         offW[i] = (int64_t)min(n0 + (S::TBN / 4) * wave + 8 * i + (lane >> 3), g.N - 1) * g.ldw + lchunk * 8;
@@ -311,7 +323,7 @@ __global__ __launch_bounds__(256, 1) void gemm_bf16_dl_kernel(GemmArgs g, int ti
 #pragma unroll
                 for (int mb = 0; mb < 4; ++mb) {
                     const int m = m0 + wm * 128 + mb * 32 + (lane & 31);
-                    if (m >= g.M) continue;
+                    if (m >= M) continue;
                     float v[4] = {acc[nb][mb][4 * j4], acc[nb][mb][4 * j4 + 1], acc[nb][mb][4 * j4 + 2],
                                   acc[nb][mb][4 * j4 + 3]};
                     epilogue_bf16<EPI>(g, m, n, v, b4);
@@ -360,7 +372,7 @@ __global__ __launch_bounds__(256, 1) void gemm_bf16_dl_kernel(GemmArgs g, int ti
         const int r = r0 + lane / CPR, c = (lane % CPR) * 8;
         if (lane >= RPI * CPR || r >= 128) continue;
         const int m = mrow0 + r, n = ncol0 + c;
-        if (m >= g.M || n >= g.N) continue;
+        if (m >= M || n >= g.N) continue;
         const uint4 v = *(const uint4*)&cst[r * S::CSTR + c];
         bf16_t* dst = C + (int64_t)m * g.ldc + n;
         if (n + 7 < g.N) {
@@ -450,7 +462,7 @@ static int pick_tile(const GemmArgs& g) {
     const char* e = getenv("DD_GEMM_TILE");
     const int forced = e ? atoi(e) : -1;
     if (forced >= 4 && forced <= 5 && g.K % BK != 0) return 0;
-    if (forced >= 0 && forced <= 5) return forced;
+    if (forced >= 0 && forced <= 5 && !(g.a_rows && forced < 4)) return forced;
     if (g.K % BK != 0) return 0;
     if (g_num_cus == 0) {
         int dev = 0;
@@ -495,8 +507,14 @@ static void launch_epi(int dtype, const GemmArgs& g, hipStream_t s) {
     }
 }
 
+bool gemm_gather_supported(int dtype, int K) { return dtype == DD_BF16 && K % BK == 0; }
+
 dd_status launch_gemm(int dtype, int epi, int cls, const GemmArgs& g, hipStream_t s) {
     if (g.M == 0 || g.N == 0) return DD_OK;
+    if (g.a_rows && !gemm_gather_supported(dtype, g.K)) {
+        set_error("row-gathered GEMM needs the bf16 path and K %% 64 == 0");
+        return DD_E_UNSUPPORTED;
+    }
     ProfScope ps(cls, s);
     switch (epi) {
         case EPI_BIAS: launch_epi<EPI_BIAS, KC_GEMM_QKV>(dtype, g, s); break;

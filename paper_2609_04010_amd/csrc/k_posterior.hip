@@ -98,7 +98,11 @@ __global__ __launch_bounds__(PT) void posterior_kernel(PostArgs a) {
 
     constexpr int E = Elem<T>::E;
     constexpr int LPG = DD_GUMBEL_GROUP / E;  // lanes per group (32 bf16, 64 fp32)
-    const int row = blockIdx.x;
+    int row = blockIdx.x;                     // token row; the logits row is blockIdx.x
+    if (a.count) {                            // compacted: logits row j holds token row rows_idx[j]
+        if ((int)blockIdx.x >= *a.count) return;
+        row = a.rows_idx[blockIdx.x];
+    }
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int V = a.V;
@@ -118,7 +122,7 @@ __global__ __launch_bounds__(PT) void posterior_kernel(PostArgs a) {
         return;
     }
 
-    const char* rowp = (const char*)a.logits + (size_t)row * (size_t)a.ld * sizeof(T);
+    const char* rowp = (const char*)a.logits + (size_t)blockIdx.x * (size_t)a.ld * sizeof(T);
     const int nchunk = (V + E - 1) / E;
     const int ngroups = (V + DD_GUMBEL_GROUP - 1) / DD_GUMBEL_GROUP;
 
@@ -245,6 +249,40 @@ __global__ __launch_bounds__(PT) void posterior_kernel(PostArgs a) {
             a.probs[(int64_t)row * K + j] = (float)p;
         }
     }
+}
+
+// Ascending list of the rows whose token is the mask id, and its length (one workgroup: each thread
+// counts a contiguous slice, a workgroup scan gives the slice offsets, then the slices are written).
+constexpr int CT = 1024;
+
+__global__ __launch_bounds__(CT) void compact_masked_kernel(const int32_t* z, int64_t M,
+                                                            int32_t mask_id, int32_t* idx,
+                                                            int32_t* count) {
+    __shared__ int sh[CT];
+    const int tid = threadIdx.x;
+    const int64_t per = (M + CT - 1) / CT;
+    const int64_t lo = (int64_t)tid * per, hi = lo + per < M ? lo + per : M;
+    int c = 0;
+    for (int64_t r = lo; r < hi; ++r) c += (z[r] == mask_id);
+    sh[tid] = c;
+    __syncthreads();
+    for (int off = 1; off < CT; off <<= 1) {
+        const int v = tid >= off ? sh[tid - off] : 0;
+        __syncthreads();
+        sh[tid] += v;
+        __syncthreads();
+    }
+    int pos = sh[tid] - c;
+    for (int64_t r = lo; r < hi; ++r)
+        if (z[r] == mask_id) idx[pos++] = (int32_t)r;
+    if (tid == CT - 1) *count = sh[CT - 1];
+}
+
+dd_status launch_compact(const int32_t* z, int64_t M, int32_t mask_id, int32_t* idx, int32_t* count,
+                         hipStream_t s) {
+    ProfScope ps(KC_COMPACT, s);
+    hipLaunchKernelGGL(compact_masked_kernel, dim3(1), dim3(CT), 0, s, z, M, mask_id, idx, count);
+    return launch_status("compact_masked");
 }
 
 dd_status launch_posterior(const PostArgs& a, int logits_dtype, hipStream_t s) {

@@ -22,6 +22,9 @@ struct PostArgs {
     uint32_t step, row0;
     float* probs;
     int32_t* err;
+    // compacted mode (masked prior): logits row j belongs to token row rows_idx[j], j < *count
+    const int32_t* rows_idx;
+    const int32_t* count;
 };
 
 enum Epi { EPI_BIAS = 0, EPI_BIAS_GELU = 1, EPI_BIAS_RESID = 2, EPI_PLAIN = 3 };
@@ -35,6 +38,9 @@ struct GemmArgs {
     void* C;         // [M][N], row stride ldc
     int64_t ldc;
     int M, N, K;
+    // optional row gather (bf16 path, K % 64 == 0): output row m < *m_count takes A row a_rows[m]
+    const int32_t* a_rows;
+    const int32_t* m_count;
 };
 
 struct AttnArgs {
@@ -63,5 +69,8 @@ bool ln_supported(int d);
 dd_status launch_gemm(int dtype, int epi, int cls, const GemmArgs& g, hipStream_t s);
 dd_status launch_attn(int dtype, const AttnArgs& a, hipStream_t s);
 bool attn_supported(int dtype, int dh);
+dd_status launch_compact(const int32_t* z, int64_t M, int32_t mask_id, int32_t* idx, int32_t* count,
+                         hipStream_t s);
+bool gemm_gather_supported(int dtype, int K);
 
 }  // namespace dd

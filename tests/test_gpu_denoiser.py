@@ -170,3 +170,28 @@ def test_forward_parity_every_gemm_tile(tile, monkeypatch):
     err = float(np.abs(got - ref).max())
     say(f"tile {tile}: max |dlogit| = {err:.3e}")
     assert err <= LOGIT_TOL["bf16"]
+
+
+@pytest.mark.parametrize("c,over,B,L,T", [(2, dict(n_layers=2), 2, 300, 6), (5, dict(n_layers=1), 1, 520, 4)])
+def test_compacted_loop_equals_full_path_loop(c, over, B, L, T):
+    """dd_sample_loop (vocabulary projection and draw on the still-masked rows only) must give the
+    same trajectory as dd_denoise_forward + dd_posterior_sample applied to every row."""
+    torch = torch_or_skip()
+    say("compacted loop", c, over, B, L, T)
+    cfg = workloads.model_cfg(c, **over)
+    V = cfg["vocab"]
+    _, buf = _params_seeded(torch, cfg, 41)
+    z1 = workloads.all_mask(B, L, V)
+    al = osched.alphas(T)
+    _, trace = _loop_gpu(torch, cfg, buf, z1, T, al, seed=77)
+    M = B * L
+    ld = int(dd.logits_ld(V))
+    logits = torch.zeros((M, ld), dtype=torch.bfloat16, device="cuda")
+    ws = torch.zeros(dd.workspace_bytes(cfg, B, L), dtype=torch.uint8, device="cuda")
+    z = dev_i32(torch, z1)
+    for k in range(T, 0, -1):
+        dd.denoise_forward(cfg, buf, z, B, L, al[k], logits, ld, ws)
+        dd.posterior_sample("mask", logits, "bf16", ld, M, V, z, al[k], al[k - 1], z, seed=77, step=k)
+        got = z.cpu().numpy().reshape(B, L)
+        assert np.array_equal(got, trace[T - k + 1]), f"step {k}"
+    say("masked per step", [(t == V).sum() for t in trace])
