@@ -91,6 +91,47 @@ __global__ __launch_bounds__(256) void ln_kernel(const float* h, int64_t rows, c
     ln_row<W, NPL>(x, lane, d, g, b, eps, out + row * d);
 }
 
+// bf16 output, d % 256 == 0: each lane holds NV = d / 256 groups of four consecutive features,
+// read as one 16-byte fp32 load and written as one 8-byte bf16 store.
+template <int NV>
+__global__ __launch_bounds__(256) void ln_bf16_v4_kernel(const float* h, int64_t rows,
+                                                         const bf16_t* g, const bf16_t* b,
+                                                         float eps, bf16_t* out) {
+    const int64_t row = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+    const int lane = threadIdx.x & 63;
+    if (row >= rows) return;
+    constexpr int d = NV * 256;
+    float4 x[NV];
+    const float4* hr = (const float4*)(h + row * d);
+#pragma unroll
+    for (int k = 0; k < NV; ++k) x[k] = hr[lane + 64 * k];
+    float s = 0.f;
+#pragma unroll
+    for (int k = 0; k < NV; ++k) s += (x[k].x + x[k].y) + (x[k].z + x[k].w);
+    const float mean = wave_sum(s) / (float)d;
+    float q = 0.f;
+#pragma unroll
+    for (int k = 0; k < NV; ++k) {
+        const float a0 = x[k].x - mean, a1 = x[k].y - mean, a2 = x[k].z - mean, a3 = x[k].w - mean;
+        q += (a0 * a0 + a1 * a1) + (a2 * a2 + a3 * a3);
+    }
+    const float rstd = 1.0f / sqrtf(wave_sum(q) / (float)d + eps);
+    uint2* orow = (uint2*)(out + row * d);
+    const uint2* gv = (const uint2*)g;
+    const uint2* bv = (const uint2*)b;
+#pragma unroll
+    for (int k = 0; k < NV; ++k) {
+        const int c = lane + 64 * k;
+        const uint2 gg = gv[c], bb = bv[c];
+        uint2 o;
+        o.x = pack_bf16x2((x[k].x - mean) * rstd * bf16_lo(gg.x) + bf16_lo(bb.x),
+                          (x[k].y - mean) * rstd * bf16_hi(gg.x) + bf16_hi(bb.x));
+        o.y = pack_bf16x2((x[k].z - mean) * rstd * bf16_lo(gg.y) + bf16_lo(bb.y),
+                          (x[k].w - mean) * rstd * bf16_hi(gg.y) + bf16_hi(bb.y));
+        orow[c] = o;
+    }
+}
+
 #define DD_NPL_CASES(X) X(1) X(2) X(4) X(8) X(12) X(16) X(24) X(32)
 
 template <typename W>
@@ -142,6 +183,17 @@ dd_status launch_ln_t(const float* h, int64_t rows, int d, const void* g, const 
 
 dd_status launch_ln(int dtype, const float* h, int64_t rows, int d, const void* g, const void* b,
                     float eps, void* out, hipStream_t s) {
+    if (dtype == DD_BF16 && (d == 768 || d == 1024 || d == 2048)) {
+        const dim3 grid((unsigned)ceil_div(rows, 4)), blk(256);
+        ProfScope ps(KC_LN, s);
+        const bf16_t* gg = (const bf16_t*)g;
+        const bf16_t* bb = (const bf16_t*)b;
+        bf16_t* o = (bf16_t*)out;
+        if (d == 768) hipLaunchKernelGGL(ln_bf16_v4_kernel<3>, grid, blk, 0, s, h, rows, gg, bb, eps, o);
+        else if (d == 1024) hipLaunchKernelGGL(ln_bf16_v4_kernel<4>, grid, blk, 0, s, h, rows, gg, bb, eps, o);
+        else hipLaunchKernelGGL(ln_bf16_v4_kernel<8>, grid, blk, 0, s, h, rows, gg, bb, eps, o);
+        return launch_status("layernorm");
+    }
     if (dtype == DD_BF16) return launch_ln_t<bf16_t>(h, rows, d, g, b, eps, out, s);
     return launch_ln_t<float>(h, rows, d, g, b, eps, out, s);
 }
