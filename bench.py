@@ -7,7 +7,10 @@ Inputs (weights, start state, noise seed) are resident on the GPU before the
 timed region.  Prints ONE JSON line.
 
   python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload 2] [--no-cpu-baseline]
+  python bench.py --traffic-probe     (for rocprofv3 --pmc FETCH_SIZE / WRITE_SIZE runs: one 256 MiB
+                                       device copy for calibration, then one forward pass; no output)
 """
+import hashlib
 import argparse
 import json
 import os
@@ -72,6 +75,46 @@ def cpu_baseline(c, cfg, w):
                       f"L={L}, step {k}/{T}: {dt:.2f} s; extrapolated x{T} steps"}
 
 
+def recorded_traffic(cls):
+    """HBM-side bytes per launch of `cls` from the committed counter summary, or None when there is
+    none or the kernel source changed since the counters were taken."""
+    import glob
+    for f in glob.glob(os.path.join(ROOT, "profiles", "traffic_*.md")):
+        for line in open(f):
+            if not line.startswith("traffic-json: "):
+                continue
+            rec = json.loads(line[len("traffic-json: "):])
+            if rec.get("kernel_class") != cls:
+                continue
+            src = os.path.join(ROOT, rec["source"])
+            if hashlib.sha256(open(src, "rb").read()).hexdigest() != rec["source_sha256"]:
+                return None
+            return rec["traffic_bytes_per_launch"]
+    return None
+
+
+def traffic_probe(c):
+    import torch
+    import workloads
+    from paper_2609_04010_amd import _lib as dd
+    src = torch.empty(256 * 2 ** 20, dtype=torch.uint8, device="cuda")
+    src.fill_(1)
+    dst = torch.empty_like(src)
+    torch.cuda.synchronize()
+    dst.copy_(src)
+    torch.cuda.synchronize()
+    cfg, w = workloads.model_cfg(c), workloads.CONFIGS[c]
+    B, L, V = w["B"], w["L"], w["vocab"]
+    params = torch.zeros(dd.param_bytes(cfg), dtype=torch.uint8, device="cuda")
+    dd.init_params(cfg, params, seed=workloads.seeds(c)["param"])
+    ld = int(dd.logits_ld(V))
+    logits = torch.empty((B * L, ld), dtype=torch.bfloat16, device="cuda")
+    ws = torch.zeros(dd.workspace_bytes(cfg, B, L), dtype=torch.uint8, device="cuda")
+    z = torch.from_numpy(workloads.masked_state(workloads.seeds(c)["data"], B, L, V, 0.5).reshape(-1)).cuda()
+    dd.denoise_forward(cfg, params, z, B, L, 0.5, logits, ld, ws)
+    torch.cuda.synchronize()
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -79,7 +122,11 @@ def main():
     ap.add_argument("--warmup", type=int, default=1)
     ap.add_argument("--workload", type=int, default=2)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--traffic-probe", action="store_true")
     args = ap.parse_args()
+    if args.traffic_probe:
+        traffic_probe(args.workload)
+        return
     if args.gpus != 1:
         log(f"bench.py measures one GPU only (asked for {args.gpus}); the sampling loop shards "
             "along the batch with no communication, see the design notes.")
@@ -166,8 +213,9 @@ def main():
                                f"random-init weights, all-mask start",
                    "global_batch": B, "seq_len": L, "reverse_steps": T, "parallelism": "none (1 GPU)"},
         "roofline": {"kernel": dominant, "bound": bound, "achieved": achieved, "peak": peak, "unit": unit,
-                     "frac": achieved / peak, "traffic": None, "launches": n_l,
-                     "avg_ms": ms_l / n_l},
+                     "frac": achieved / peak, "traffic": recorded_traffic(dominant),
+                     "traffic_unit": "bytes per launch (L2-miss reads + writes, copy-calibrated)",
+                     "launches": n_l, "avg_ms": ms_l / n_l},
     }
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(c, cfg, w)
