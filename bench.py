@@ -129,7 +129,7 @@ def main():
         return
     if args.gpus != 1:
         log(f"bench.py measures one GPU only (asked for {args.gpus}); the sampling loop shards "
-            "along the batch with no communication, see the design notes.")
+            "along the batch with no communication between GPUs.")
         sys.exit(2)
 
     import torch

@@ -17,8 +17,14 @@ LIB = os.path.join(PKG, "libdd.so")
 SOURCES = ["dd_api.hip", "k_posterior.hip", "k_latent_init.hip", "k_norm.hip", "k_gemm.hip",
            "k_attn.hip"]
 
+# Per-file extra flags.  Attention keeps its MFMA accumulators in ordinary VGPRs (the softmax reads
+# every score with VALU instructions; AGPR accumulators would need a copy per score).  The GEMMs need
+# the AGPR file for their 256 accumulators and keep the default.
+EXTRA = {"k_attn.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"]}
+
 FLAGS = ["-O3", "-std=c++17", "-fPIC", "--offload-arch=gfx950",
-         # no packed-fp32 instructions anywhere (see the design notes on packed FP32)
+         # packed-FP32 instructions stay off everywhere: some of their forms have given wrong results
+         # on this hardware without any error
          "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
          "-I", os.path.join(ROOT, "include"), "-I", CSRC,
          "-Wno-unused-result"]
@@ -33,7 +39,7 @@ def _hipcc():
 
 def _compile(src, verbose):
     obj = os.path.join(BUILD, os.path.splitext(src)[0] + ".o")
-    cmd = [_hipcc(), *FLAGS, "-c", os.path.join(CSRC, src), "-o", obj]
+    cmd = [_hipcc(), *FLAGS, *EXTRA.get(src, []), "-c", os.path.join(CSRC, src), "-o", obj]
     r = subprocess.run(cmd, capture_output=True, text=True)
     out = (r.stdout + r.stderr)
     # the host pass does not know the packed-fp32 feature and says so; that line is noise
