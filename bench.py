@@ -32,7 +32,8 @@ def log(*a):
 
 
 def algorithmic_units(cls, cfg, B, L):
-    """(amount per launch, unit, bound) for a kernel class (flops or bytes, see the design notes)."""
+    """(algorithmic amount per launch, unit, bound) of a kernel class: 2 M N K flops per GEMM,
+    4 B L^2 d flops per attention launch."""
     M, d, F, V, H = B * L, cfg["d_model"], cfg["d_mlp"], cfg["vocab"], cfg["n_heads"]
     flops = {
         "gemm_qkv": 2.0 * M * d * 3 * d,

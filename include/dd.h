@@ -173,6 +173,9 @@ dd_status dd_denoise_forward(const dd_config* cfg, const void* params,
  * mass of the group of DD_GUMBEL_GROUP consecutive classes; the mask class is a
  * group of its own), level 2 picks the class in g by argmax of log p_j + Gumbel;
  * the lowest index wins ties.  Masked prior: rows with z_t != mask are copied.
+ * Arithmetic: log-sum-exp, group masses and Gumbel scores in fp32 (so a draw
+ * can differ from an exact one only where two scores lie within ~1e-5); the
+ * debug probabilities in float64.
  */
 dd_status dd_posterior_sample(int32_t prior, const void* logits, int32_t logits_dtype,
                               int64_t ld, int32_t rows, int32_t V, const int32_t* z_t,

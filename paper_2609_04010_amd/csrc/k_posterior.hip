@@ -1,12 +1,14 @@
 // Fused logits -> softmax -> reverse posterior -> two-level Gumbel-max draw.
 //
 // One workgroup (256 threads) per row.  The row is streamed once from HBM in
-// 16-byte chunks; each thread keeps up to 16 chunks of a tile in registers, so
+// 16-byte chunks; each thread keeps TILE_IT chunks of a tile in registers, so
 // the per-wave maximum and the per-group sums of exp(l - max) come from
 // registers without a second read.  Only the per-group log-sum-exp values
-// (one float per DD_GUMBEL_GROUP classes) go to LDS.  The level-1 draw then
-// runs over the groups, and the level-2 draw re-reads the 256 logits of the
-// winning group (an L2 hit).
+// (one float per DD_GUMBEL_GROUP classes) go to LDS.  One wavefront then
+// finishes the row in fp32: the level-1 draw over the groups, and the level-2
+// draw over the 256 logits of the winning group (re-read, an L2 hit).  The
+// optional full posterior row (a debug output) comes from a separate kernel in
+// float64.
 //
 // Masked prior (App. A.1, eq. mdm-posterior, x = softmax(logits)):
 //   z_t == mask:  p_v = w_x x_v (v < V), p_mask = w_m,
@@ -23,12 +25,28 @@
 namespace dd {
 
 constexpr int PT = 256;       // threads per workgroup
-constexpr int TILE_IT = 16;   // 16-byte chunks per thread held in registers per tile
+#ifndef DD_POST_TILE_IT
+#define DD_POST_TILE_IT 8
+#endif
+constexpr int TILE_IT = DD_POST_TILE_IT;   // 16-byte chunks per thread held in registers per tile
+static_assert(TILE_IT >= 1 && TILE_IT <= 32 && (TILE_IT & (TILE_IT - 1)) == 0,
+              "the group butterfly needs a power of two no larger than the lanes of a group");
 constexpr float LOG2E = 1.4426950408889634f;
 
 template <typename T> struct Elem;
 template <> struct Elem<bf16_t> {
     static constexpr int E = 8;  // elements per 16-byte chunk
+    static constexpr uint4 NEG_INF4 = {0xFF80FF80u, 0xFF80FF80u, 0xFF80FF80u, 0xFF80FF80u};
+    // elements n.. of the chunk become -inf (0 < n < E)
+    DD_DEV static void clip(uint4& c, int n) {
+        uint32_t w[4] = {c.x, c.y, c.z, c.w};
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+            const uint32_t hi_cut = (w[k] & 0xFFFFu) | 0xFF800000u;
+            w[k] = (2 * k + 1 < n) ? w[k] : (2 * k < n) ? hi_cut : 0xFF80FF80u;
+        }
+        c = make_uint4(w[0], w[1], w[2], w[3]);
+    }
     DD_DEV static float get(const uint4& c, int e) {
         const uint32_t w = (e < 2) ? c.x : (e < 4) ? c.y : (e < 6) ? c.z : c.w;
         return (e & 1) ? bf16_hi(w) : bf16_lo(w);
@@ -37,6 +55,13 @@ template <> struct Elem<bf16_t> {
 };
 template <> struct Elem<float> {
     static constexpr int E = 4;
+    static constexpr uint4 NEG_INF4 = {0xFF800000u, 0xFF800000u, 0xFF800000u, 0xFF800000u};
+    DD_DEV static void clip(uint4& c, int n) {
+        uint32_t w[4] = {c.x, c.y, c.z, c.w};
+#pragma unroll
+        for (int k = 0; k < 4; ++k) w[k] = (k < n) ? w[k] : 0xFF800000u;
+        c = make_uint4(w[0], w[1], w[2], w[3]);
+    }
     DD_DEV static float get(const uint4& c, int e) {
         const uint32_t w = (e == 0) ? c.x : (e == 1) ? c.y : (e == 2) ? c.z : c.w;
         return __uint_as_float(w);
@@ -44,57 +69,19 @@ template <> struct Elem<float> {
     DD_DEV static float load1(const void* p, int64_t i) { return ((const float*)p)[i]; }
 };
 
-DD_DEV void better(double& s, int& i, double s2, int i2) {
-    if (s2 > s || (s2 == s && i2 < i)) { s = s2; i = i2; }
-}
-
-// Block-wide argmax of (score, index); the lowest index wins ties.  Result in lane 0 of every wave
-// is broadcast through LDS to all threads.
-DD_DEV void block_argmax(double& s, int& i, double* sh_s, int* sh_i) {
+// Wavefront argmax of (score, index); the lowest index wins ties; every lane gets the result.
+DD_DEV void wave_argmax(float& s, int& i) {
 #pragma unroll
     for (int o = 32; o > 0; o >>= 1) {
-        double s2 = __shfl_xor(s, o, 64);
-        int i2 = __shfl_xor(i, o, 64);
-        better(s, i, s2, i2);
+        const float s2 = __shfl_xor(s, o, 64);
+        const int i2 = __shfl_xor(i, o, 64);
+        if (s2 > s || (s2 == s && i2 < i)) { s = s2; i = i2; }
     }
-    const int w = threadIdx.x >> 6;
-    __syncthreads();
-    if ((threadIdx.x & 63) == 0) { sh_s[w] = s; sh_i[w] = i; }
-    __syncthreads();
-    s = sh_s[0]; i = sh_i[0];
-#pragma unroll
-    for (int k = 1; k < PT / 64; ++k) better(s, i, sh_s[k], sh_i[k]);
-}
-
-DD_DEV double block_max_d(double v, double* sh) {
-#pragma unroll
-    for (int o = 32; o > 0; o >>= 1) v = fmax(v, __shfl_xor(v, o, 64));
-    __syncthreads();
-    if ((threadIdx.x & 63) == 0) sh[threadIdx.x >> 6] = v;
-    __syncthreads();
-    double r = sh[0];
-#pragma unroll
-    for (int k = 1; k < PT / 64; ++k) r = fmax(r, sh[k]);
-    return r;
-}
-
-DD_DEV double block_sum_d(double v, double* sh) {
-#pragma unroll
-    for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
-    __syncthreads();
-    if ((threadIdx.x & 63) == 0) sh[threadIdx.x >> 6] = v;
-    __syncthreads();
-    double r = sh[0];
-#pragma unroll
-    for (int k = 1; k < PT / 64; ++k) r += sh[k];
-    return r;
 }
 
 template <typename T>
 __global__ __launch_bounds__(PT) void posterior_kernel(PostArgs a) {
     extern __shared__ float s_lse[];  // one log-sum-exp per group
-    __shared__ double sh_d[PT / 64];
-    __shared__ int sh_i[PT / 64];
 
     constexpr int E = Elem<T>::E;
     constexpr int LPG = DD_GUMBEL_GROUP / E;  // lanes per group (32 bf16, 64 fp32)
@@ -117,8 +104,6 @@ __global__ __launch_bounds__(PT) void posterior_kernel(PostArgs a) {
     }
     if (mask_prior && zt != V) {  // carry-over: the row's logits are never read
         if (tid == 0) a.z_s[row] = zt;
-        if (a.probs)
-            for (int j = tid; j < K; j += PT) a.probs[(int64_t)row * K + j] = (j == zt) ? 1.f : 0.f;
         return;
     }
 
@@ -127,127 +112,214 @@ __global__ __launch_bounds__(PT) void posterior_kernel(PostArgs a) {
     const int ngroups = (V + DD_GUMBEL_GROUP - 1) / DD_GUMBEL_GROUP;
 
     // ---- pass over the row: per-group log-sum-exp ---------------------------------------
+    // Elements past V count as -inf: chunks past the row are filled with -inf bits, and the one
+    // ragged chunk (V not a multiple of E) is clipped in registers.  Each lane ends a tile with TILE_IT
+    // partial sums (one per iteration, i.e. per group slice); a butterfly over the LPG lanes of a
+    // group halves the list at every step, so TILE_IT sums cost log2(LPG) steps and TILE_IT
+    // shuffles in total instead of TILE_IT * log2(LPG).
     for (int tile0 = 0; tile0 < nchunk; tile0 += TILE_IT * PT) {
         uint4 buf[TILE_IT];
+        if ((tile0 + TILE_IT * PT) * E <= V) {   // every element of the tile is in the row
 #pragma unroll
-        for (int it = 0; it < TILE_IT; ++it) {
-            const int c = tile0 + it * PT + tid;
-            if (c < nchunk) buf[it] = *(const uint4*)(rowp + (size_t)c * 16);
-            else buf[it] = make_uint4(0u, 0u, 0u, 0u);
-        }
-        float m = -INFINITY;
-#pragma unroll
-        for (int it = 0; it < TILE_IT; ++it) {
-            const int c = tile0 + it * PT + tid;
-#pragma unroll
-            for (int e = 0; e < E; ++e)
-                if (c * E + e < V) m = fmaxf(m, Elem<T>::get(buf[it], e));
-        }
-        m = wave_max(m);
-        const float mref = (m == -INFINITY) ? 0.f : m;
-        const float moff = -mref * LOG2E;
-        float part[TILE_IT];
-#pragma unroll
-        for (int it = 0; it < TILE_IT; ++it) {
-            const int c = tile0 + it * PT + tid;
-            float s = 0.f;
-#pragma unroll
-            for (int e = 0; e < E; ++e)
-                if (c * E + e < V) s += __builtin_amdgcn_exp2f(fmaf(Elem<T>::get(buf[it], e), LOG2E, moff));
-            part[it] = s;
-        }
-#pragma unroll
-        for (int it = 0; it < TILE_IT; ++it) {
-#pragma unroll
-            for (int o = LPG / 2; o > 0; o >>= 1) part[it] += __shfl_xor(part[it], o, 64);
-        }
-        if ((lane % LPG) == 0) {
+            for (int it = 0; it < TILE_IT; ++it)
+                buf[it] = *(const uint4*)(rowp + (size_t)(tile0 + it * PT + tid) * 16);
+        } else {   // last tile: clamped loads, -inf past the row, the ragged chunk clipped
 #pragma unroll
             for (int it = 0; it < TILE_IT; ++it) {
                 const int c = tile0 + it * PT + tid;
-                if (c < nchunk) s_lse[c / LPG] = mref + logf(part[it]);
+                const uint4 x = *(const uint4*)(rowp + (size_t)min(c, nchunk - 1) * 16);
+                buf[it] = (c < nchunk) ? x : Elem<T>::NEG_INF4;
             }
+            if (V % E != 0) {
+#pragma unroll
+                for (int it = 0; it < TILE_IT; ++it)
+                    if (tile0 + it * PT + tid == nchunk - 1) Elem<T>::clip(buf[it], V % E);
+            }
+        }
+        float m = -INFINITY;
+#pragma unroll
+        for (int it = 0; it < TILE_IT; ++it)
+#pragma unroll
+            for (int e = 0; e < E; ++e) m = fmaxf(m, Elem<T>::get(buf[it], e));
+        m = wave_max(m);
+        const float mref = (m == -INFINITY) ? 0.f : m;
+        const float moff = -mref * LOG2E;
+        float v[TILE_IT];
+#pragma unroll
+        for (int it = 0; it < TILE_IT; ++it) {
+            float sum = 0.f;
+#pragma unroll
+            for (int e = 0; e < E; ++e) sum += __builtin_amdgcn_exp2f(fmaf(Elem<T>::get(buf[it], e), LOG2E, moff));
+            v[it] = sum;
+        }
+        int idx = 0;   // iteration whose group sum this lane holds at the end
+#pragma unroll
+        for (int o = LPG / 2, n = TILE_IT; o >= 1; o >>= 1) {
+            if (n > 1) {
+                n >>= 1;
+                const bool up = (lane & o) != 0;
+                // the swap is written with bit masks: as a select of two array elements the compiler
+                // turns it into a dynamically indexed register array (a compare-select chain)
+                const uint32_t mk = up ? 0xFFFFFFFFu : 0u;
+#pragma unroll
+                for (int i = 0; i < TILE_IT / 2; ++i) {
+                    if (i < n) {
+                        const uint32_t lo = __float_as_uint(v[i]), hi = __float_as_uint(v[n + i]);
+                        const float send = __uint_as_float((lo & mk) | (hi & ~mk));
+                        const float keep = __uint_as_float((hi & mk) | (lo & ~mk));
+                        v[i] = keep + __shfl_xor(send, o, 64);
+                    }
+                }
+                if (up) idx += n;
+            } else {
+                v[0] += __shfl_xor(v[0], o, 64);
+            }
+        }
+        constexpr int DUP = (LPG / TILE_IT) > 1 ? LPG / TILE_IT : 1;   // lanes holding the same sum
+        if ((lane & (DUP - 1)) == 0) {
+            const int c = tile0 + idx * PT + (tid & ~(LPG - 1));
+            if (c < nchunk) s_lse[c / LPG] = mref + logf(v[0]);
         }
     }
     __syncthreads();
 
-    // ---- row log-sum-exp ---------------------------------------------------------------
-    double lmax = -INFINITY;
-    for (int g = tid; g < ngroups; g += PT) lmax = fmax(lmax, (double)s_lse[g]);
-    lmax = block_max_d(lmax, sh_d);
-    const double lref = isinf(lmax) ? 0.0 : lmax;
-    double lsum = 0.0;
-    for (int g = tid; g < ngroups; g += PT) lsum += exp((double)s_lse[g] - lref);
-    lsum = block_sum_d(lsum, sh_d);
-    const double lse = lref + log(lsum);
+    // ---- tail: one wavefront finishes the row (no further workgroup barrier) ---------------
+    // Row log-sum-exp over the group values, level 1 over the groups (4 per lane: one Philox block
+    // gives their 4 words) and level 2 over the 256 classes of the chosen group (4 per lane), all in
+    // fp32 with wavefront shuffles.  The other wavefronts leave unless the debug output is wanted.
+    if ((tid >> 6) != 0) return;
+    {
+        float m = -INFINITY;
+        for (int g = lane; g < ngroups; g += 64) m = fmaxf(m, s_lse[g]);
+        m = wave_max(m);
+        const float mref = isinf(m) ? 0.f : m;
+        float sum = 0.f;
+        for (int g = lane; g < ngroups; g += 64) sum += expf(s_lse[g] - mref);
+        const float lse = mref + logf(wave_sum(sum));
 
-    // uniform prior: x_r and the row-specific coefficients
+        float c_r = 0.f, Dn = 1.f;
+        if (!mask_prior) {   // uniform prior: x_r enters the mass of the current token's class
+            const float xr = expf(Elem<T>::load1(rowp, zt) - lse);
+            c_r = (float)a.Ka_t * xr + (float)a.c_z;
+            Dn = (float)a.Ka_t * xr + (float)a.one_m_at;
+        }
+        const float log_wx = (float)a.log_wx, log_wm = (float)a.log_wm;
+        const float c_x = (float)a.c_x, c_u = (float)a.c_u, log_dn = logf(Dn);
+        const uint32_t k0 = (uint32_t)a.seed, k1 = (uint32_t)(a.seed >> 32);
+
+        // level 1: group g has log mass log w_x + lse_g - lse (mask prior; the mask class is group
+        // `ngroups`) or log((c_x X_g + n_g c_u + [r in g] c_r) / D) (uniform prior)
+        float best = -INFINITY;
+        int bi = 0x7FFFFFFF;
+        for (int gb = 0; gb < a.ntop; gb += 256) {
+            const int base = gb + 4 * lane;
+            if (base >= a.ntop) break;
+            uint32_t wd[4];
+            if (a.noise) {
+                for (int i = 0; i < 4; ++i)
+                    wd[i] = (base + i < a.ntop) ? a.noise[(int64_t)row * a.nu + base + i] : 0u;
+            } else {
+                const Words4 W = philox4x32_10((uint32_t)(base >> 2), grow, a.step, STREAM_TOP, k0, k1);
+                for (int i = 0; i < 4; ++i) wd[i] = W.w[i];
+            }
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const int g = base + i;
+                if (g >= a.ntop) break;
+                float logm;
+                if (mask_prior) {
+                    logm = (g < ngroups) ? log_wx + (s_lse[g] - lse) : log_wm;
+                } else {
+                    const int lo = g * DD_GUMBEL_GROUP;
+                    const int n = min(DD_GUMBEL_GROUP, V - lo);
+                    const float X = expf(s_lse[g] - lse);
+                    logm = logf(c_x * X + (float)n * c_u + ((zt >= lo && zt < lo + n) ? c_r : 0.f)) - log_dn;
+                }
+                const float sc = logm + word_gumbel_f(wd[i]);
+                if (sc > best || (sc == best && g < bi)) { best = sc; bi = g; }
+            }
+        }
+        wave_argmax(best, bi);
+        const int gstar = bi;
+
+        int result = V;
+        if (!(mask_prior && gstar == ngroups)) {   // level 2 inside the chosen group
+            best = -INFINITY;
+            bi = 0x7FFFFFFF;
+            const int base = gstar * DD_GUMBEL_GROUP + 4 * lane;
+            if (base < V) {
+                uint32_t wd[4];
+                if (a.noise) {
+                    for (int i = 0; i < 4; ++i)
+                        wd[i] = (base + i < V) ? a.noise[(int64_t)row * a.nu + a.ntop + base + i] : 0u;
+                } else {
+                    const Words4 W = philox4x32_10((uint32_t)(base >> 2), grow, a.step, STREAM_CLASS, k0, k1);
+                    for (int i = 0; i < 4; ++i) wd[i] = W.w[i];
+                }
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    const int j = base + i;
+                    if (j >= V) break;
+                    const float l = Elem<T>::load1(rowp, j);
+                    float logp;
+                    if (mask_prior) logp = log_wx + (l - lse);
+                    else logp = logf(c_x * expf(l - lse) + c_u + (j == zt ? c_r : 0.f)) - log_dn;
+                    const float sc = logp + word_gumbel_f(wd[i]);
+                    if (sc > best || (sc == best && j < bi)) { best = sc; bi = j; }
+                }
+            }
+            wave_argmax(best, bi);
+            result = bi;
+        }
+        if (lane == 0) a.z_s[row] = result;
+    }
+
+}
+
+// Debug output: the full posterior row in float64 arithmetic (two passes over the logits).
+template <typename T>
+__global__ __launch_bounds__(PT) void posterior_probs_kernel(PostArgs a) {
+    __shared__ double sh[PT / 64];
+    const int row = blockIdx.x, tid = threadIdx.x;
+    const int V = a.V;
+    const bool mask_prior = a.prior == DD_PRIOR_MASK;
+    const int K = mask_prior ? V + 1 : V;
+    int zt = a.z_t[row];
+    zt = zt < 0 ? 0 : (zt >= K ? K - 1 : zt);
+    float* out = a.probs + (int64_t)row * K;
+    if (mask_prior && zt != V) {
+        for (int j = tid; j < K; j += PT) out[j] = (j == zt) ? 1.f : 0.f;
+        return;
+    }
+    const char* rowp = (const char*)a.logits + (size_t)row * (size_t)a.ld * sizeof(T);
+    double m = -INFINITY;
+    for (int j = tid; j < V; j += PT) m = fmax(m, (double)Elem<T>::load1(rowp, j));
+    for (int o = 32; o > 0; o >>= 1) m = fmax(m, __shfl_xor(m, o, 64));
+    if ((tid & 63) == 0) sh[tid >> 6] = m;
+    __syncthreads();
+    m = fmax(fmax(sh[0], sh[1]), fmax(sh[2], sh[3]));
+    __syncthreads();
+    double sum = 0.0;
+    for (int j = tid; j < V; j += PT) sum += exp((double)Elem<T>::load1(rowp, j) - m);
+    for (int o = 32; o > 0; o >>= 1) sum += __shfl_xor(sum, o, 64);
+    if ((tid & 63) == 0) sh[tid >> 6] = sum;
+    __syncthreads();
+    const double lse = m + log(sh[0] + sh[1] + sh[2] + sh[3]);
     double c_r = 0.0, Dn = 1.0;
     if (!mask_prior) {
         const double xr = exp((double)Elem<T>::load1(rowp, zt) - lse);
         c_r = a.Ka_t * xr + a.c_z;
         Dn = a.Ka_t * xr + a.one_m_at;
     }
-
-    // ---- level 1: choose a group ------------------------------------------------------
-    double best = -INFINITY;
-    int bi = 0x7FFFFFFF;
-    for (int g = tid; g < a.ntop; g += PT) {
-        double logm;
+    for (int j = tid; j < K; j += PT) {
+        double p;
         if (mask_prior) {
-            logm = (g < ngroups) ? a.log_wx + ((double)s_lse[g] - lse) : a.log_wm;
+            p = (j < V) ? a.wx * exp((double)Elem<T>::load1(rowp, j) - lse) : a.wm;
         } else {
-            const int lo = g * DD_GUMBEL_GROUP;
-            const int n = min(DD_GUMBEL_GROUP, V - lo);
-            const double X = exp((double)s_lse[g] - lse);
-            const double M = a.c_x * X + n * a.c_u + ((zt >= lo && zt < lo + n) ? c_r : 0.0);
-            logm = log(M / Dn);
+            const double x = exp((double)Elem<T>::load1(rowp, j) - lse);
+            p = (a.c_x * x + a.c_u + (j == zt ? c_r : 0.0)) / Dn;
         }
-        const uint32_t w = a.noise ? a.noise[(int64_t)row * a.nu + g]
-                                   : counter_word(a.seed, STREAM_TOP, a.step, grow, (uint32_t)g);
-        better(best, bi, logm + word_gumbel(w), g);
-    }
-    block_argmax(best, bi, sh_d, sh_i);
-    const int gstar = bi;
-
-    // ---- level 2: choose a class inside the group ---------------------------------------
-    int result;
-    if (mask_prior && gstar == ngroups) {
-        result = V;
-    } else {
-        best = -INFINITY;
-        bi = 0x7FFFFFFF;
-        const int j = gstar * DD_GUMBEL_GROUP + tid;
-        if (j < V) {
-            const double l = (double)Elem<T>::load1(rowp, j);
-            double logp;
-            if (mask_prior) {
-                logp = a.log_wx + (l - lse);
-            } else {
-                const double x = exp(l - lse);
-                logp = log((a.c_x * x + a.c_u + (j == zt ? c_r : 0.0)) / Dn);
-            }
-            const uint32_t w = a.noise ? a.noise[(int64_t)row * a.nu + a.ntop + j]
-                                       : counter_word(a.seed, STREAM_CLASS, a.step, grow, (uint32_t)j);
-            best = logp + word_gumbel(w);
-            bi = j;
-        }
-        block_argmax(best, bi, sh_d, sh_i);
-        result = bi;
-    }
-    if (tid == 0) a.z_s[row] = result;
-
-    if (a.probs) {  // debug output of the full posterior row
-        for (int j = tid; j < K; j += PT) {
-            double p;
-            if (mask_prior) {
-                p = (j < V) ? a.wx * exp((double)Elem<T>::load1(rowp, j) - lse) : a.wm;
-            } else {
-                const double x = exp((double)Elem<T>::load1(rowp, j) - lse);
-                p = (a.c_x * x + a.c_u + (j == zt ? c_r : 0.0)) / Dn;
-            }
-            a.probs[(int64_t)row * K + j] = (float)p;
-        }
+        out[j] = (float)p;
     }
 }
 
@@ -289,11 +361,19 @@ dd_status launch_posterior(const PostArgs& a, int logits_dtype, hipStream_t s) {
     if (a.rows == 0) return DD_OK;
     const int ngroups = (a.V + DD_GUMBEL_GROUP - 1) / DD_GUMBEL_GROUP;
     const size_t shmem = (size_t)ngroups * sizeof(float);
-    ProfScope ps(KC_POSTERIOR, s);
-    if (logits_dtype == DD_BF16)
-        hipLaunchKernelGGL(posterior_kernel<bf16_t>, dim3(a.rows), dim3(PT), shmem, s, a);
-    else
-        hipLaunchKernelGGL(posterior_kernel<float>, dim3(a.rows), dim3(PT), shmem, s, a);
+    {
+        ProfScope ps(KC_POSTERIOR, s);
+        if (logits_dtype == DD_BF16)
+            hipLaunchKernelGGL(posterior_kernel<bf16_t>, dim3(a.rows), dim3(PT), shmem, s, a);
+        else
+            hipLaunchKernelGGL(posterior_kernel<float>, dim3(a.rows), dim3(PT), shmem, s, a);
+    }
+    if (a.probs && !a.count) {
+        if (logits_dtype == DD_BF16)
+            hipLaunchKernelGGL(posterior_probs_kernel<bf16_t>, dim3(a.rows), dim3(PT), 0, s, a);
+        else
+            hipLaunchKernelGGL(posterior_probs_kernel<float>, dim3(a.rows), dim3(PT), 0, s, a);
+    }
     return launch_status("posterior");
 }
 

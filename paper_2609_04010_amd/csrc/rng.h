@@ -61,6 +61,15 @@ DD_DEV double word_exponential(uint32_t w) {
 
 DD_DEV double word_gumbel(uint32_t w) { return -log(word_exponential(w)); }
 
+// The same transforms in fp32 (relative error of E about 2^-23, so G is within ~1e-7 of the
+// float64 value); the complement c = 1 - u keeps E accurate as u -> 1.
+DD_DEV float word_gumbel_f(uint32_t w) {
+    float e;
+    if (w >= 0x80000000u) e = -log1pf(-(((float)(0xFFFFFFFFu - w) + 0.5f) * 0x1p-32f));
+    else e = -logf(((float)w + 0.5f) * 0x1p-32f);
+    return -logf(e);
+}
+
 DD_DEV double word_normal(uint32_t w) {
     if (w >= 0x80000000u) return -normcdfinv(((double)(0xFFFFFFFFu - w) + 0.5) * 0x1p-32);
     return normcdfinv(((double)w + 0.5) * 0x1p-32);
