@@ -15,15 +15,14 @@ DD_DEV float bf16_lo(uint32_t pair) { return __uint_as_float(pair << 16); }
 DD_DEV float bf16_hi(uint32_t pair) { return __uint_as_float(pair & 0xFFFF0000u); }
 DD_DEV float bf16_to_f32(bf16_t b) { return __uint_as_float(((uint32_t)b) << 16); }
 
-// Round-to-nearest-even fp32 -> bf16 (finite inputs).
-DD_DEV bf16_t f32_to_bf16(float f) {
-    uint32_t u = __float_as_uint(f);
-    u += 0x7FFFu + ((u >> 16) & 1u);
-    return (bf16_t)(u >> 16);
-}
+// Round-to-nearest-even fp32 -> bf16 with the hardware conversion (v_cvt_pk_bf16_f32, which rounds
+// in the default round-to-nearest-even mode).
+typedef __attribute__((ext_vector_type(2))) __bf16 bf16x2_hw;
 DD_DEV uint32_t pack_bf16x2(float lo, float hi) {
-    return (uint32_t)f32_to_bf16(lo) | ((uint32_t)f32_to_bf16(hi) << 16);
+    const bf16x2_hw v = {(__bf16)lo, (__bf16)hi};
+    return __builtin_bit_cast(uint32_t, v);
 }
+DD_DEV bf16_t f32_to_bf16(float f) { return (bf16_t)(pack_bf16x2(f, 0.f) & 0xFFFFu); }
 
 // Round-to-nearest-even float64 -> bf16 directly (no intermediate fp32 rounding).
 DD_DEV bf16_t f64_to_bf16(double v) {

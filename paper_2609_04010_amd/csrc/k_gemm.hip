@@ -17,6 +17,8 @@
 #include <math.h>
 #include <stdlib.h>
 
+#include <type_traits>
+
 #include "kernels.h"
 
 namespace dd {
@@ -24,11 +26,11 @@ namespace dd {
 typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8;
 typedef __attribute__((ext_vector_type(16))) float f32x16;
 
-// gelu_tanh(x) = 0.5 x (1 + tanh(y)) = x / (1 + exp(-2y)), y = sqrt(2/pi) (x + 0.044715 x^3)
-// (v_exp_f32 and v_rcp_f32, both about 1 ulp; the result is rounded to bf16 afterwards)
+// gelu_tanh(x) = 0.5 x (1 + tanh(y)) = x / (1 + exp(-2y)), y = sqrt(2/pi) (x + 0.044715 x^3), with
+// exp(-2y) = 2^(x (a + b x^2)), a = -2 sqrt(2/pi) log2(e), b = 0.044715 a: five VALU operations plus
+// v_exp_f32 and v_rcp_f32 (about 1 ulp each; the result is rounded to bf16 afterwards)
 DD_DEV float gelu_tanh(float x) {
-    const float y = 0.7978845608028654f * fmaf(0.044715f * x, x * x, x);
-    const float e = __builtin_amdgcn_exp2f(-2.8853900817779268f * y);   // exp(-2y)
+    const float e = __builtin_amdgcn_exp2f(x * fmaf(x * x, -0.1029432395800235f, -2.302208198144325f));
     return x * __builtin_amdgcn_rcpf(1.0f + e);
 }
 
@@ -187,11 +189,15 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmArgs g, int tiles_m,
 // ------------------------------------------------------------------------------ bf16, direct to LDS
 // 256 x TBN x 64 workgroup tile (TBN = 256 or 192), 4 wavefronts of 128 x TBN/2 (4 x NBW blocks of
 // 32x32 MFMA, NBW = 4 or 3).  Operand tiles travel global -> LDS with global_load_lds_dwordx4 (no
-// staging registers): each wave instruction fills 1 KB = 8 rows of 128 B.  Inside a row the eight
-// 16-byte K-chunks are stored XOR-swizzled (slot = chunk ^ (row & 7)) so that the MFMA fragment
-// reads of eight consecutive rows hit eight different bank groups.  Two LDS stages: the loads of
-// K-tile t+1 are issued right after the barrier that publishes K-tile t and overlap its MFMAs;
-// fragments of the next 16-wide K step are read between the current step's MFMAs.
+// staging registers): each wave instruction fills 1 KB = 8 rows of 128 B.  The LDS serves a
+// 16-byte read for 16 lanes (256 B, 64 banks) per cycle, and a fragment read covers rows r..r+15 of
+// one K-chunk, so the eight 16-byte K-chunks of a row are stored XOR-swizzled with
+// slot = chunk ^ ((row >> 1) & 7): the eight even and the eight odd rows of the group each land on
+// eight different bank groups.  Two LDS stages.  After the barrier that publishes K-tile t, the
+// 16-wide K steps of t run their MFMAs with, between them, the fragment reads of the next step and
+// (during the first LD_STEPS steps) the global->LDS loads of K-tile t+1: a load waits in the
+// vector-memory queue behind the other wavefronts' loads, and with MFMAs already issued ahead of it
+// the matrix core keeps working meanwhile.
 // bf16 outputs are staged per wave in padded LDS rows and written as 16-byte row segments.
 // The 192-wide variant exists for tile quantisation: with d = 768 it divides N = 768, 2304 and
 // 3072 into whole rounds of 256 CUs.  Requires K % 64 == 0; rows past M or N are clamped (their
@@ -235,27 +241,31 @@ __global__ __launch_bounds__(256, 1) void gemm_bf16_dl_kernel(GemmArgs g, int ti
 
     // this lane's source rows: wave w fills A rows 64 w + 8 i + lane / 8 (i < 8) and W rows
     // (TBN / 4) w + 8 i + lane / 8 (i < NIW); its 16-byte slot lane % 8 holds K-chunk
-    // (lane % 8) ^ (row & 7) = (lane % 8) ^ (lane / 8)
-    const int lchunk = (lane & 7) ^ (lane >> 3);
+    // (lane % 8) ^ ((row >> 1) & 7) = (lane % 8) ^ ((4 i + lane / 16) & 7)  (row bases are
+    // multiples of 16)
+    auto lchunk = [&](int i) { return (lane & 7) ^ ((4 * (i & 1) + (lane >> 4)) & 7); };
     int64_t offA[8], offW[NIW];
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
         const int r = min(m0 + 64 * wave + 8 * i + (lane >> 3), M - 1);
-        offA[i] = (int64_t)(g.a_rows ? g.a_rows[r] : r) * g.lda + lchunk * 8;
+        offA[i] = (int64_t)(g.a_rows ? g.a_rows[r] : r) * g.lda + lchunk(i) * 8;
     }
 #pragma unroll
     for (int i = 0; i < NIW; ++i)
-        offW[i] = (int64_t)min(n0 + (S::TBN / 4) * wave + 8 * i + (lane >> 3), g.N - 1) * g.ldw + lchunk * 8;
-    auto issue = [&](int k0, int stage) {
-        bf16_t* sA = smem + stage * S::STAGE + (64 * wave) * BK;
-        bf16_t* sW = smem + stage * S::STAGE + DM * BK + ((S::TBN / 4) * wave) * BK;
-#pragma unroll
-        for (int i = 0; i < 8; ++i)
-            __builtin_amdgcn_global_load_lds((gbl_void*)(A + offA[i] + k0), (lds_void*)(sA + 8 * i * BK), 16, 0, 0);
-#pragma unroll
-        for (int i = 0; i < NIW; ++i)
-            __builtin_amdgcn_global_load_lds((gbl_void*)(W + offW[i] + k0), (lds_void*)(sW + 8 * i * BK), 16, 0, 0);
+        offW[i] = (int64_t)min(n0 + (S::TBN / 4) * wave + 8 * i + (lane >> 3), g.N - 1) * g.ldw + lchunk(i) * 8;
+    // load j of a stage: j < 8 fills A rows 8 j.., otherwise W rows 8 (j - 8)..
+    auto issue_one = [&](int k0, int stage, int j) {
+        if (j < 8) {
+            bf16_t* sA = smem + stage * S::STAGE + (64 * wave) * BK;
+            __builtin_amdgcn_global_load_lds((gbl_void*)(A + offA[j] + k0), (lds_void*)(sA + 8 * j * BK), 16, 0, 0);
+        } else {
+            bf16_t* sW = smem + stage * S::STAGE + DM * BK + ((S::TBN / 4) * wave) * BK;
+            __builtin_amdgcn_global_load_lds((gbl_void*)(W + offW[j - 8] + k0), (lds_void*)(sW + 8 * (j - 8) * BK), 16, 0, 0);
+        }
     };
+    constexpr int NL = 8 + NIW;                        // load instructions per wave per stage
+    constexpr int LD_STEPS = 3;                        // K steps over which they are spread
+    constexpr int LPS = (NL + LD_STEPS - 1) / LD_STEPS;
 
     f32x16 acc[NBW][4];
 #pragma unroll
@@ -265,19 +275,20 @@ __global__ __launch_bounds__(256, 1) void gemm_bf16_dl_kernel(GemmArgs g, int ti
 #pragma unroll
             for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
 
-    // fragment rows of this lane; row & 7 == lane & 7 for every block (block bases are multiples of 32)
-    const int frow = lane & 31, fsw = lane & 7, fhalf = lane >> 5;
+    // fragment rows of this lane: row0 + lane % 32 with row0 a multiple of 32, so
+    // (row >> 1) & 7 == (lane >> 1) & 7
+    const int frow = lane & 31, fsw = (lane >> 1) & 7, fhalf = lane >> 5;
     auto frag = [&](const bf16_t* tile, int row0, int kk) -> bf16x8 {
         const int slot = (2 * kk + fhalf) ^ fsw;
         return *(const bf16x8*)&tile[(row0 + frow) * BK + slot * 8];
     };
 
-    const int nk = g.K / BK;
-    issue(0, 0);
-    for (int t = 0; t < nk; ++t) {
+    // one K-tile; the last one (with_loads false) has no next tile to fetch, which keeps the load
+    // issue free of branches inside the MFMA sequence
+    auto ktile = [&](const int t, auto with_loads) {
+        constexpr bool more = decltype(with_loads)::value;
         __builtin_amdgcn_s_waitcnt(0x3F70);      // vmcnt(0): this lane's loads of K-tile t landed
         __syncthreads();                          // ... everyone's; and everyone left K-tile t-1
-        if (t + 1 < nk) issue((t + 1) * BK, (t + 1) & 1);
         const bf16_t* sA = smem + (t & 1) * S::STAGE + (wm * 128) * BK;
         const bf16_t* sW = smem + (t & 1) * S::STAGE + DM * BK + (wn * S::WN) * BK;
         bf16x8 af[2][4], wf[2][NBW];
@@ -285,29 +296,75 @@ __global__ __launch_bounds__(256, 1) void gemm_bf16_dl_kernel(GemmArgs g, int ti
         for (int i = 0; i < 4; ++i) af[0][i] = frag(sA, 32 * i, 0);
 #pragma unroll
         for (int i = 0; i < NBW; ++i) wf[0][i] = frag(sW, 32 * i, 0);
+        __builtin_amdgcn_s_waitcnt(0xC07F);       // lgkmcnt(0): the first step's fragments
+        __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
         for (int kk = 0; kk < BK / 16; ++kk) {
             const int cur = kk & 1;
+            // issue slot i: MFMAs 2i and 2i+1, fragment reads 2i-2 and 2i-1 of the next step and
+            // load i of the next K-tile, fenced so the scheduler keeps the slots in order.  The reads
+            // go out early in the step (after its first MFMAs) and are waited for at its end, so no
+            // MFMA waits on a read of its own step.
+            constexpr int NPAIR = 2 * NBW, NREAD = 4 + NBW;
+            constexpr int NSLOT = NPAIR > LPS ? NPAIR : LPS;
+            const int nload = (more && kk < LD_STEPS) ? min(LPS, NL - kk * LPS) : 0;
 #pragma unroll
-            for (int nb = 0; nb < NBW; ++nb)
+            for (int i = 0; i < NSLOT; ++i) {
+                if (i < NPAIR) {
 #pragma unroll
-                for (int mb = 0; mb < 4; ++mb)
-                    acc[nb][mb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(wf[cur][nb], af[cur][mb], acc[nb][mb], 0, 0, 0);
-            if (kk + 1 < BK / 16) {
-#pragma unroll
-                for (int i = 0; i < 4; ++i) af[cur ^ 1][i] = frag(sA, 32 * i, kk + 1);
-#pragma unroll
-                for (int i = 0; i < NBW; ++i) wf[cur ^ 1][i] = frag(sW, 32 * i, kk + 1);
-                // issue order inside this step: MFMAs interleaved with the next step's reads
-#pragma unroll
-                for (int i = 0; i < 4 + NBW; ++i) {
-                    __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
-                    __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+                    for (int h = 0; h < 2; ++h) {
+                        const int q = 2 * i + h, nb = q / 4, mb = q % 4;
+                        acc[nb][mb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(wf[cur][nb], af[cur][mb], acc[nb][mb], 0, 0, 0);
+                    }
                 }
+                if (kk + 1 < BK / 16 && i >= 1) {
+#pragma unroll
+                    for (int h = 0; h < 2; ++h) {
+                        const int r = 2 * (i - 1) + h;
+                        if (r < 4) af[cur ^ 1][r] = frag(sA, 32 * r, kk + 1);
+                        else if (r < NREAD) wf[cur ^ 1][r - 4] = frag(sW, 32 * (r - 4), kk + 1);
+                    }
+                }
+                if constexpr (more)
+                    if (i < nload) issue_one((t + 1) * BK, (t + 1) & 1, kk * LPS + i);
+                __builtin_amdgcn_sched_barrier(0);
             }
+            if (kk + 1 < BK / 16) __builtin_amdgcn_s_waitcnt(0xC07F);   // lgkmcnt(0)
             __builtin_amdgcn_sched_barrier(0);
         }
+    };
+
+    // bias of this lane's output columns (4 consecutive per (nb, j4)); the bf16-output epilogues
+    // fetch it before the K loop, the residual epilogue (short of registers) when it needs it
+    auto load_bias4 = [&](int nb, int j4) -> uint2 {
+        const int n = n0 + wn * S::WN + nb * 32 + 8 * j4 + 4 * (lane >> 5);
+        const bf16_t* bp = (const bf16_t*)g.bias + n;
+        if (n + 3 < g.N) return *(const uint2*)bp;
+        uint32_t h[4] = {0u, 0u, 0u, 0u};
+        for (int e = 0; e < 4; ++e)
+            if (n + e < g.N) h[e] = bp[e];
+        return make_uint2(h[0] | (h[1] << 16), h[2] | (h[3] << 16));
+    };
+    constexpr bool PREFETCH_BIAS = EPI == EPI_BIAS || EPI == EPI_BIAS_GELU;
+    uint2 braw[PREFETCH_BIAS ? NBW : 1][4];
+    if constexpr (PREFETCH_BIAS) {
+#pragma unroll
+        for (int nb = 0; nb < NBW; ++nb)
+#pragma unroll
+            for (int j4 = 0; j4 < 4; ++j4) braw[nb][j4] = load_bias4(nb, j4);
     }
+    auto bias4 = [&](int nb, int j4, float* b4) {
+        uint2 r = make_uint2(0u, 0u);
+        if constexpr (PREFETCH_BIAS) r = braw[nb][j4];
+        else if constexpr (EPI != EPI_PLAIN) r = load_bias4(nb, j4);
+        b4[0] = bf16_lo(r.x); b4[1] = bf16_hi(r.x); b4[2] = bf16_lo(r.y); b4[3] = bf16_hi(r.y);
+    };
+
+    const int nk = g.K / BK;
+#pragma unroll
+    for (int j = 0; j < NL; ++j) issue_one(0, 0, j);
+    for (int t = 0; t + 1 < nk; ++t) ktile(t, std::true_type{});
+    ktile(nk - 1, std::false_type{});
 
     if (EPI == EPI_BIAS_RESID) {     // fp32 read-modify-write of the residual stream, 16 B per lane
 #pragma unroll
@@ -316,10 +373,8 @@ __global__ __launch_bounds__(256, 1) void gemm_bf16_dl_kernel(GemmArgs g, int ti
             for (int j4 = 0; j4 < 4; ++j4) {
                 const int n = n0 + wn * S::WN + nb * 32 + 8 * j4 + 4 * (lane >> 5);
                 if (n >= g.N) continue;
-                float b4[4] = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-                for (int e = 0; e < 4; ++e)
-                    if (n + e < g.N) b4[e] = bf16_to_f32(((const bf16_t*)g.bias)[n + e]);
+                float b4[4];
+                bias4(nb, j4, b4);
 #pragma unroll
                 for (int mb = 0; mb < 4; ++mb) {
                     const int m = m0 + wm * 128 + mb * 32 + (lane & 31);
@@ -342,11 +397,9 @@ __global__ __launch_bounds__(256, 1) void gemm_bf16_dl_kernel(GemmArgs g, int ti
         for (int j4 = 0; j4 < 4; ++j4) {
             const int nl = nb * 32 + 8 * j4 + 4 * (lane >> 5);
             const int n = n0 + wn * S::WN + nl;
-            float b4[4] = {0.f, 0.f, 0.f, 0.f};
-            if (EPI != EPI_PLAIN)
-#pragma unroll
-                for (int e = 0; e < 4; ++e)
-                    if (n + e < g.N) b4[e] = bf16_to_f32(((const bf16_t*)g.bias)[n + e]);
+            float b4[4];
+            bias4(nb, j4, b4);
+            (void)n;
 #pragma unroll
             for (int mb = 0; mb < 4; ++mb) {
                 float o[4];
@@ -511,6 +564,10 @@ bool gemm_gather_supported(int dtype, int K) { return dtype == DD_BF16 && K % BK
 
 dd_status launch_gemm(int dtype, int epi, int cls, const GemmArgs& g, hipStream_t s) {
     if (g.M == 0 || g.N == 0) return DD_OK;
+    if (g.K <= 0) {
+        set_error("GEMM with K = %d", g.K);
+        return DD_E_ARG;
+    }
     if (g.a_rows && !gemm_gather_supported(dtype, g.K)) {
         set_error("row-gathered GEMM needs the bf16 path and K %% 64 == 0");
         return DD_E_UNSUPPORTED;
