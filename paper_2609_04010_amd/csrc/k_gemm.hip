@@ -187,8 +187,9 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmArgs g, int tiles_m,
 }
 
 // ------------------------------------------------------------------------------ bf16, direct to LDS
-// 256 x TBN x 64 workgroup tile (TBN = 256 or 192), 4 wavefronts of 128 x TBN/2 (4 x NBW blocks of
-// 32x32 MFMA, NBW = 4 or 3).  Operand tiles travel global -> LDS with global_load_lds_dwordx4 (no
+// 256 x TBN x 64 workgroup tile (TBN = 256 or 192) over a WGM x WGN grid of wavefronts (2 x 2 with
+// 128 x TBN/2 sub-tiles, or 8 wavefronts: 2 x 4 of 128 x 64 / 4 x 2 of 64 x 96), each sub-tile a set
+// of 32x32 MFMA blocks.  Operand tiles travel global -> LDS with global_load_lds_dwordx4 (no
 // staging registers): each wave instruction fills 1 KB = 8 rows of 128 B.  The LDS serves a
 // 16-byte read for 16 lanes (256 B, 64 banks) per cycle, and a fragment read covers rows r..r+15 of
 // one K-chunk, so the eight 16-byte K-chunks of a row are stored XOR-swizzled with
@@ -203,26 +204,36 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmArgs g, int tiles_m,
 // 3072 into whole rounds of 256 CUs.  Requires K % 64 == 0; rows past M or N are clamped (their
 // results are never stored).
 constexpr int DM = 256;                       // tile rows (M)
-template <int NBW> struct DLShape {
-    static constexpr int TBN = 64 * NBW;                      // tile columns (N)
-    static constexpr int WN = 32 * NBW;                       // columns per wave
+// WGM x WGN wavefronts, each owning a WM x WN sub-tile of MB x NB 32x32 MFMA blocks.
+template <int TBN_, int WGM_, int WGN_> struct DLShape {
+    static constexpr int TBN = TBN_;                          // tile columns (N)
+    static constexpr int WGM = WGM_, WGN = WGN_, NW = WGM * WGN;
+    static constexpr int THREADS = 64 * NW;
+    static constexpr int WM = DM / WGM, WN = TBN / WGN;       // wave sub-tile
+    static constexpr int MB = WM / 32, NB = WN / 32;
+    static constexpr int ALOADS = DM / 8 / NW;                // A load instructions per wave per stage
+    static constexpr int WLOADS = TBN / 8 / NW;               // W load instructions per wave per stage
     static constexpr int STAGE = (DM + TBN) * BK;             // bf16 elements per stage
     static constexpr int CSTR = WN + 8;                       // epilogue staging row stride (bf16)
-    static constexpr size_t LDS = (size_t)4 * 128 * CSTR * 2 > (size_t)2 * STAGE * 2
-                                      ? (size_t)4 * 128 * CSTR * 2 : (size_t)2 * STAGE * 2;
+    static constexpr size_t LDS = (size_t)NW * WM * CSTR * 2 > (size_t)2 * STAGE * 2
+                                      ? (size_t)NW * WM * CSTR * 2 : (size_t)2 * STAGE * 2;
+    static_assert(WM % 32 == 0 && WN % 32 == 0 && (MB * NB) % 2 == 0, "wave sub-tile");
+    static_assert(DM % (8 * NW) == 0 && TBN % (8 * NW) == 0, "load split");
+    static_assert(LDS <= 160 * 1024, "LDS");
 };
 
 typedef __attribute__((address_space(3))) void lds_void;
 typedef __attribute__((address_space(1))) const void gbl_void;
 
 // ROLE (the profiler class of the layer) only separates the symbols of layers sharing an epilogue.
-template <int EPI, int ROLE, int NBW>
-__global__ __launch_bounds__(256, 1) void gemm_bf16_dl_kernel(GemmArgs g, int tiles_m, int tiles_n) {
-    using S = DLShape<NBW>;
-    constexpr int NIW = S::TBN / 32;          // W load instructions per wave per stage
+template <int EPI, int ROLE, int TBN_, int WGM_, int WGN_>
+__global__ __launch_bounds__(64 * WGM_ * WGN_, 1) void gemm_bf16_dl_kernel(GemmArgs g, int tiles_m, int tiles_n) {
+    using S = DLShape<TBN_, WGM_, WGN_>;
+    constexpr int MB = S::MB, NB = S::NB, NA = S::ALOADS, NWL = S::WLOADS;
+    constexpr int AROWS = DM / S::NW, WROWS = S::TBN / S::NW;   // operand rows each wave loads
     extern __shared__ __attribute__((aligned(1024))) bf16_t smem[];
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int wm = wave >> 1, wn = wave & 1;
+    const int wm = wave / S::WGN, wn = wave % S::WGN;
     // Gathered mode: only the first *m_count output rows exist; the tile grid is re-derived from
     // that device-side count so the active tiles are spread over every XCD, and surplus
     // workgroups leave at once.
@@ -239,39 +250,40 @@ __global__ __launch_bounds__(256, 1) void gemm_bf16_dl_kernel(GemmArgs g, int ti
     const bf16_t* A = (const bf16_t*)g.A;
     const bf16_t* W = (const bf16_t*)g.W;
 
-    // this lane's source rows: wave w fills A rows 64 w + 8 i + lane / 8 (i < 8) and W rows
-    // (TBN / 4) w + 8 i + lane / 8 (i < NIW); its 16-byte slot lane % 8 holds K-chunk
-    // (lane % 8) ^ ((row >> 1) & 7) = (lane % 8) ^ ((4 i + lane / 16) & 7)  (row bases are
-    // multiples of 16)
-    auto lchunk = [&](int i) { return (lane & 7) ^ ((4 * (i & 1) + (lane >> 4)) & 7); };
-    int64_t offA[8], offW[NIW];
+    // this lane's source rows: wave w fills A rows AROWS w + 8 i + lane / 8 and W rows
+    // WROWS w + 8 i + lane / 8; its 16-byte slot lane % 8 holds K-chunk (lane % 8) ^ ((row >> 1) & 7)
+    auto lchunk = [&](int row) { return (lane & 7) ^ ((row >> 1) & 7); };
+    int64_t offA[NA], offW[NWL];
 #pragma unroll
-    for (int i = 0; i < 8; ++i) {
-        const int r = min(m0 + 64 * wave + 8 * i + (lane >> 3), M - 1);
-        offA[i] = (int64_t)(g.a_rows ? g.a_rows[r] : r) * g.lda + lchunk(i) * 8;
+    for (int i = 0; i < NA; ++i) {
+        const int rl = AROWS * wave + 8 * i + (lane >> 3);
+        const int r = min(m0 + rl, M - 1);
+        offA[i] = (int64_t)(g.a_rows ? g.a_rows[r] : r) * g.lda + lchunk(rl) * 8;
     }
 #pragma unroll
-    for (int i = 0; i < NIW; ++i)
-        offW[i] = (int64_t)min(n0 + (S::TBN / 4) * wave + 8 * i + (lane >> 3), g.N - 1) * g.ldw + lchunk(i) * 8;
-    // load j of a stage: j < 8 fills A rows 8 j.., otherwise W rows 8 (j - 8)..
+    for (int i = 0; i < NWL; ++i) {
+        const int rl = WROWS * wave + 8 * i + (lane >> 3);
+        offW[i] = (int64_t)min(n0 + rl, g.N - 1) * g.ldw + lchunk(rl) * 8;
+    }
+    // load j of a stage: j < NA fills A rows AROWS w + 8 j.., otherwise W rows WROWS w + 8 (j - NA)..
     auto issue_one = [&](int k0, int stage, int j) {
-        if (j < 8) {
-            bf16_t* sA = smem + stage * S::STAGE + (64 * wave) * BK;
+        if (j < NA) {
+            bf16_t* sA = smem + stage * S::STAGE + (AROWS * wave) * BK;
             __builtin_amdgcn_global_load_lds((gbl_void*)(A + offA[j] + k0), (lds_void*)(sA + 8 * j * BK), 16, 0, 0);
         } else {
-            bf16_t* sW = smem + stage * S::STAGE + DM * BK + ((S::TBN / 4) * wave) * BK;
-            __builtin_amdgcn_global_load_lds((gbl_void*)(W + offW[j - 8] + k0), (lds_void*)(sW + 8 * (j - 8) * BK), 16, 0, 0);
+            bf16_t* sW = smem + stage * S::STAGE + DM * BK + (WROWS * wave) * BK;
+            __builtin_amdgcn_global_load_lds((gbl_void*)(W + offW[j - NA] + k0), (lds_void*)(sW + 8 * (j - NA) * BK), 16, 0, 0);
         }
     };
-    constexpr int NL = 8 + NIW;                        // load instructions per wave per stage
+    constexpr int NL = NA + NWL;                       // load instructions per wave per stage
     constexpr int LD_STEPS = 3;                        // K steps over which they are spread
     constexpr int LPS = (NL + LD_STEPS - 1) / LD_STEPS;
 
-    f32x16 acc[NBW][4];
+    f32x16 acc[NB][MB];
 #pragma unroll
-    for (int i = 0; i < NBW; ++i)
+    for (int i = 0; i < NB; ++i)
 #pragma unroll
-        for (int j = 0; j < 4; ++j)
+        for (int j = 0; j < MB; ++j)
 #pragma unroll
             for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
 
@@ -289,13 +301,13 @@ __global__ __launch_bounds__(256, 1) void gemm_bf16_dl_kernel(GemmArgs g, int ti
         constexpr bool more = decltype(with_loads)::value;
         __builtin_amdgcn_s_waitcnt(0x3F70);      // vmcnt(0): this lane's loads of K-tile t landed
         __syncthreads();                          // ... everyone's; and everyone left K-tile t-1
-        const bf16_t* sA = smem + (t & 1) * S::STAGE + (wm * 128) * BK;
+        const bf16_t* sA = smem + (t & 1) * S::STAGE + (wm * S::WM) * BK;
         const bf16_t* sW = smem + (t & 1) * S::STAGE + DM * BK + (wn * S::WN) * BK;
-        bf16x8 af[2][4], wf[2][NBW];
+        bf16x8 af[2][MB], wf[2][NB];
 #pragma unroll
-        for (int i = 0; i < 4; ++i) af[0][i] = frag(sA, 32 * i, 0);
+        for (int i = 0; i < MB; ++i) af[0][i] = frag(sA, 32 * i, 0);
 #pragma unroll
-        for (int i = 0; i < NBW; ++i) wf[0][i] = frag(sW, 32 * i, 0);
+        for (int i = 0; i < NB; ++i) wf[0][i] = frag(sW, 32 * i, 0);
         __builtin_amdgcn_s_waitcnt(0xC07F);       // lgkmcnt(0): the first step's fragments
         __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
@@ -305,15 +317,20 @@ __global__ __launch_bounds__(256, 1) void gemm_bf16_dl_kernel(GemmArgs g, int ti
             // load i of the next K-tile, fenced so the scheduler keeps the slots in order.  The reads
             // go out early in the step (after its first MFMAs) and are waited for at its end, so no
             // MFMA waits on a read of its own step.
-            constexpr int NPAIR = 2 * NBW, NREAD = 4 + NBW;
-            constexpr int NSLOT = NPAIR > LPS ? NPAIR : LPS;
+            constexpr int NPAIR = NB * MB / 2, NREAD = MB + NB;
+            // enough slots for every MFMA pair, every load and every read (two per slot from slot 1)
+            constexpr int NRSLOT = (NREAD + 1) / 2 + 1;
+            constexpr int NSLOT0 = NPAIR > LPS ? NPAIR : LPS;
+            constexpr int NSLOT = NSLOT0 > NRSLOT ? NSLOT0 : NRSLOT;
+            static_assert(2 * (NSLOT - 1) >= NREAD && NSLOT >= NPAIR && LD_STEPS * LPS >= NL &&
+                          LD_STEPS < BK / 16 + 1, "every read, MFMA pair and load has a slot");
             const int nload = (more && kk < LD_STEPS) ? min(LPS, NL - kk * LPS) : 0;
 #pragma unroll
             for (int i = 0; i < NSLOT; ++i) {
                 if (i < NPAIR) {
 #pragma unroll
                     for (int h = 0; h < 2; ++h) {
-                        const int q = 2 * i + h, nb = q / 4, mb = q % 4;
+                        const int q = 2 * i + h, nb = q / MB, mb = q % MB;
                         acc[nb][mb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(wf[cur][nb], af[cur][mb], acc[nb][mb], 0, 0, 0);
                     }
                 }
@@ -321,8 +338,8 @@ __global__ __launch_bounds__(256, 1) void gemm_bf16_dl_kernel(GemmArgs g, int ti
 #pragma unroll
                     for (int h = 0; h < 2; ++h) {
                         const int r = 2 * (i - 1) + h;
-                        if (r < 4) af[cur ^ 1][r] = frag(sA, 32 * r, kk + 1);
-                        else if (r < NREAD) wf[cur ^ 1][r - 4] = frag(sW, 32 * (r - 4), kk + 1);
+                        if (r < MB) af[cur ^ 1][r] = frag(sA, 32 * r, kk + 1);
+                        else if (r < NREAD) wf[cur ^ 1][r - MB] = frag(sW, 32 * (r - MB), kk + 1);
                     }
                 }
                 if constexpr (more)
@@ -346,10 +363,10 @@ __global__ __launch_bounds__(256, 1) void gemm_bf16_dl_kernel(GemmArgs g, int ti
         return make_uint2(h[0] | (h[1] << 16), h[2] | (h[3] << 16));
     };
     constexpr bool PREFETCH_BIAS = EPI == EPI_BIAS || EPI == EPI_BIAS_GELU;
-    uint2 braw[PREFETCH_BIAS ? NBW : 1][4];
+    uint2 braw[PREFETCH_BIAS ? NB : 1][4];
     if constexpr (PREFETCH_BIAS) {
 #pragma unroll
-        for (int nb = 0; nb < NBW; ++nb)
+        for (int nb = 0; nb < NB; ++nb)
 #pragma unroll
             for (int j4 = 0; j4 < 4; ++j4) braw[nb][j4] = load_bias4(nb, j4);
     }
@@ -368,7 +385,7 @@ __global__ __launch_bounds__(256, 1) void gemm_bf16_dl_kernel(GemmArgs g, int ti
 
     if (EPI == EPI_BIAS_RESID) {     // fp32 read-modify-write of the residual stream, 16 B per lane
 #pragma unroll
-        for (int nb = 0; nb < NBW; ++nb)
+        for (int nb = 0; nb < NB; ++nb)
 #pragma unroll
             for (int j4 = 0; j4 < 4; ++j4) {
                 const int n = n0 + wn * S::WN + nb * 32 + 8 * j4 + 4 * (lane >> 5);
@@ -376,8 +393,8 @@ __global__ __launch_bounds__(256, 1) void gemm_bf16_dl_kernel(GemmArgs g, int ti
                 float b4[4];
                 bias4(nb, j4, b4);
 #pragma unroll
-                for (int mb = 0; mb < 4; ++mb) {
-                    const int m = m0 + wm * 128 + mb * 32 + (lane & 31);
+                for (int mb = 0; mb < MB; ++mb) {
+                    const int m = m0 + wm * S::WM + mb * 32 + (lane & 31);
                     if (m >= M) continue;
                     float v[4] = {acc[nb][mb][4 * j4], acc[nb][mb][4 * j4 + 1], acc[nb][mb][4 * j4 + 2],
                                   acc[nb][mb][4 * j4 + 3]};
@@ -387,12 +404,12 @@ __global__ __launch_bounds__(256, 1) void gemm_bf16_dl_kernel(GemmArgs g, int ti
         return;
     }
 
-    // bf16 outputs: each wave stages its 128 x WN sub-tile in LDS (rows padded by 16 B), then
+    // bf16 outputs: each wave stages its WM x WN sub-tile in LDS (rows padded by 16 B), then
     // writes whole row segments with 16-byte stores.
     __syncthreads();                              // every wave is done with the operand stages
-    bf16_t* cst = smem + wave * (128 * S::CSTR);
+    bf16_t* cst = smem + wave * (S::WM * S::CSTR);
 #pragma unroll
-    for (int nb = 0; nb < NBW; ++nb)
+    for (int nb = 0; nb < NB; ++nb)
 #pragma unroll
         for (int j4 = 0; j4 < 4; ++j4) {
             const int nl = nb * 32 + 8 * j4 + 4 * (lane >> 5);
@@ -401,7 +418,7 @@ __global__ __launch_bounds__(256, 1) void gemm_bf16_dl_kernel(GemmArgs g, int ti
             bias4(nb, j4, b4);
             (void)n;
 #pragma unroll
-            for (int mb = 0; mb < 4; ++mb) {
+            for (int mb = 0; mb < MB; ++mb) {
                 float o[4];
 #pragma unroll
                 for (int e = 0; e < 4; ++e) {
@@ -416,14 +433,14 @@ __global__ __launch_bounds__(256, 1) void gemm_bf16_dl_kernel(GemmArgs g, int ti
             }
         }
     bf16_t* C = (bf16_t*)g.C;
-    const int mrow0 = m0 + wm * 128, ncol0 = n0 + wn * S::WN;
-    // WN = 128: 16 chunks per row, 4 rows per wave instruction; WN = 96: 12 chunks per row, 5 rows
-    // per instruction (lanes 60..63 idle)
+    const int mrow0 = m0 + wm * S::WM, ncol0 = n0 + wn * S::WN;
+    // e.g. WN = 128: 16 chunks per row, 4 rows per wave instruction; WN = 96: 12 chunks per row,
+    // 5 rows per instruction (lanes 60..63 idle)
     constexpr int CPR = S::WN / 8;                // 16-byte chunks per staged row
     constexpr int RPI = 64 / CPR;                 // rows per wave instruction
-    for (int r0 = 0; r0 < 128; r0 += RPI) {
+    for (int r0 = 0; r0 < S::WM; r0 += RPI) {
         const int r = r0 + lane / CPR, c = (lane % CPR) * 8;
-        if (lane >= RPI * CPR || r >= 128) continue;
+        if (lane >= RPI * CPR || r >= S::WM) continue;
         const int m = mrow0 + r, n = ncol0 + c;
         if (m >= M || n >= g.N) continue;
         const uint4 v = *(const uint4*)&cst[r * S::CSTR + c];
@@ -507,15 +524,17 @@ static void launch_tile(const GemmArgs& g, hipStream_t s) {
 
 // Tile choice for the direct-to-LDS kernel: the N width (256 or 192) with the smaller estimated time,
 // counting whole rounds of workgroups over the CUs (a round of 192-wide tiles takes about 0.85 of a
-// round of 256-wide ones on MI355X).  K % 64 != 0 falls back to the 128 x 128 register-staged kernel.  DD_GEMM_TILE (0..5)
-// forces a variant for tuning and tests (4: 256 x 256, 5: 256 x 192).
+// round of 256-wide ones on MI355X), in the 8-wavefront form (two wavefronts per SIMD, measured 2-6%
+// faster than four wavefronts of twice the sub-tile).  K % 64 != 0 falls back to the 128 x 128
+// register-staged kernel.  DD_GEMM_TILE (0..7) forces a variant for tuning and tests
+// (4: 256 x 256 / 4 waves, 5: 256 x 192 / 4 waves, 6: 256 x 256 / 8 waves, 7: 256 x 192 / 8 waves).
 static int g_num_cus = 0;
 
 static int pick_tile(const GemmArgs& g) {
     const char* e = getenv("DD_GEMM_TILE");
     const int forced = e ? atoi(e) : -1;
-    if (forced >= 4 && forced <= 5 && g.K % BK != 0) return 0;
-    if (forced >= 0 && forced <= 5 && !(g.a_rows && forced < 4)) return forced;
+    if (forced >= 4 && forced <= 7 && g.K % BK != 0) return 0;
+    if (forced >= 0 && forced <= 7 && !(g.a_rows && forced < 4)) return forced;
     if (g.K % BK != 0) return 0;
     if (g_num_cus == 0) {
         int dev = 0;
@@ -527,28 +546,31 @@ static int pick_tile(const GemmArgs& g) {
     const int64_t tm = (g.M + DM - 1) / DM;
     const int64_t r256 = (tm * ((g.N + 255) / 256) + g_num_cus - 1) / g_num_cus;
     const int64_t r192 = (tm * ((g.N + 191) / 192) + g_num_cus - 1) / g_num_cus;
-    return (17 * r192 < 20 * r256) ? 5 : 4;
+    return (17 * r192 < 20 * r256) ? 7 : 6;
 }
 
-template <int EPI, int ROLE, int NBW>
+template <int EPI, int ROLE, int TBN, int WGM, int WGN>
 static void launch_dl(const GemmArgs& g, hipStream_t s) {
-    using S = DLShape<NBW>;
+    using S = DLShape<TBN, WGM, WGN>;
     const int tm = (g.M + DM - 1) / DM, tn = (g.N + S::TBN - 1) / S::TBN;
     static bool attr = false;
     if (!attr) {
-        (void)hipFuncSetAttribute((const void*)gemm_bf16_dl_kernel<EPI, ROLE, NBW>,
+        (void)hipFuncSetAttribute((const void*)gemm_bf16_dl_kernel<EPI, ROLE, TBN, WGM, WGN>,
                                   hipFuncAttributeMaxDynamicSharedMemorySize, (int)S::LDS);
         attr = true;
     }
-    hipLaunchKernelGGL((gemm_bf16_dl_kernel<EPI, ROLE, NBW>), dim3(tm * tn), dim3(256), S::LDS, s, g, tm, tn);
+    hipLaunchKernelGGL((gemm_bf16_dl_kernel<EPI, ROLE, TBN, WGM, WGN>), dim3(tm * tn), dim3(S::THREADS), S::LDS, s,
+                       g, tm, tn);
 }
 
 template <int EPI, int ROLE>
 static void launch_epi(int dtype, const GemmArgs& g, hipStream_t s) {
     if (dtype == DD_BF16) {
         switch (pick_tile(g)) {
-            case 5: launch_dl<EPI, ROLE, 3>(g, s); break;
-            case 4: launch_dl<EPI, ROLE, 4>(g, s); break;
+            case 7: launch_dl<EPI, ROLE, 192, 4, 2>(g, s); break;
+            case 6: launch_dl<EPI, ROLE, 256, 2, 4>(g, s); break;
+            case 5: launch_dl<EPI, ROLE, 192, 2, 2>(g, s); break;
+            case 4: launch_dl<EPI, ROLE, 256, 2, 2>(g, s); break;
             case 3: launch_tile<256, 256, EPI>(g, s); break;
             case 2: launch_tile<256, 128, EPI>(g, s); break;
             case 1: launch_tile<128, 256, EPI>(g, s); break;
