@@ -17,6 +17,7 @@
 #include <math.h>
 #include <stdlib.h>
 
+#include <algorithm>
 #include <type_traits>
 
 #include "kernels.h"
@@ -201,7 +202,7 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmArgs g, int tiles_m,
 // the matrix core keeps working meanwhile.
 // bf16 outputs are staged per wave in padded LDS rows and written as 16-byte row segments.
 // The 192-wide variant exists for tile quantisation: with d = 768 it divides N = 768, 2304 and
-// 3072 into whole rounds of 256 CUs.  Requires K % 64 == 0; rows past M or N are clamped (their
+// 3072 into whole rounds of 256 CUs.  Requires K % 128 == 0; rows past M or N are clamped (their
 // results are never stored).
 constexpr int DM = 256;                       // tile rows (M)
 // WGM x WGN wavefronts, each owning a WM x WN sub-tile of MB x NB 32x32 MFMA blocks.
@@ -215,9 +216,10 @@ template <int TBN_, int WGM_, int WGN_> struct DLShape {
     static constexpr int WLOADS = TBN / 8 / NW;               // W load instructions per wave per stage
     static constexpr int STAGE = (DM + TBN) * BK;             // bf16 elements per stage
     static constexpr int CSTR = WN + 8;                       // epilogue staging row stride (bf16)
-    static constexpr size_t LDS = (size_t)NW * WM * CSTR * 2 > (size_t)2 * STAGE * 2
-                                      ? (size_t)NW * WM * CSTR * 2 : (size_t)2 * STAGE * 2;
-    static_assert(WM % 32 == 0 && WN % 32 == 0 && (MB * NB) % 2 == 0, "wave sub-tile");
+    // two operand stages; the epilogue stages half a sub-tile per wave above stage 0
+    static constexpr size_t STAGING = (size_t)STAGE * 2 + (size_t)NW * (WM / 2) * CSTR * 2;
+    static constexpr size_t LDS = STAGING > (size_t)2 * STAGE * 2 ? STAGING : (size_t)2 * STAGE * 2;
+    static_assert(WM % 64 == 0 && WN % 32 == 0 && (MB * NB) % 2 == 0, "wave sub-tile (two row halves)");
     static_assert(DM % (8 * NW) == 0 && TBN % (8 * NW) == 0, "load split");
     static_assert(LDS <= 160 * 1024, "LDS");
 };
@@ -226,6 +228,9 @@ typedef __attribute__((address_space(3))) void lds_void;
 typedef __attribute__((address_space(1))) const void gbl_void;
 
 // ROLE (the profiler class of the layer) only separates the symbols of layers sharing an epilogue.
+// Persistent: workgroup b takes tiles b, b + G, b + 2G, ... (G = grid size).  The number of K-tiles
+// is even, so the loads of the next tile's first K-tile go out during the last K-tile of the
+// current one into stage 0, which the staged epilogue leaves alone: they land while it runs.
 template <int EPI, int ROLE, int TBN_, int WGM_, int WGN_>
 __global__ __launch_bounds__(64 * WGM_ * WGN_, 1) void gemm_bf16_dl_kernel(GemmArgs g, int tiles_m, int tiles_n) {
     using S = DLShape<TBN_, WGM_, WGN_>;
@@ -235,36 +240,41 @@ __global__ __launch_bounds__(64 * WGM_ * WGN_, 1) void gemm_bf16_dl_kernel(GemmA
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int wm = wave / S::WGN, wn = wave % S::WGN;
     // Gathered mode: only the first *m_count output rows exist; the tile grid is re-derived from
-    // that device-side count so the active tiles are spread over every XCD, and surplus
-    // workgroups leave at once.
-    int M = g.M, nblocks = gridDim.x;
+    // that device-side count.
+    int M = g.M;
     if (g.m_count) {
         M = *g.m_count;
         tiles_m = (M + DM - 1) / DM;
-        nblocks = tiles_m * tiles_n;
-        if ((int)blockIdx.x >= nblocks) return;
     }
-    int tm, tn;
-    map_tile(blockIdx.x, nblocks, tiles_m, tiles_n, tm, tn);
-    const int m0 = tm * DM, n0 = tn * S::TBN;
+    const int nblocks = tiles_m * tiles_n;
+    int L = blockIdx.x;
+    if (L >= nblocks) return;
     const bf16_t* A = (const bf16_t*)g.A;
     const bf16_t* W = (const bf16_t*)g.W;
+    const int nk = g.K / BK;                     // even (the launcher checks K % 128 == 0)
 
     // this lane's source rows: wave w fills A rows AROWS w + 8 i + lane / 8 and W rows
     // WROWS w + 8 i + lane / 8; its 16-byte slot lane % 8 holds K-chunk (lane % 8) ^ ((row >> 1) & 7)
     auto lchunk = [&](int row) { return (lane & 7) ^ ((row >> 1) & 7); };
+    int m0 = 0, n0 = 0;
     int64_t offA[NA], offW[NWL];
+    auto setup_tile = [&](int tile) {
+        int tm, tn;
+        map_tile(tile, nblocks, tiles_m, tiles_n, tm, tn);
+        m0 = tm * DM;
+        n0 = tn * S::TBN;
 #pragma unroll
-    for (int i = 0; i < NA; ++i) {
-        const int rl = AROWS * wave + 8 * i + (lane >> 3);
-        const int r = min(m0 + rl, M - 1);
-        offA[i] = (int64_t)(g.a_rows ? g.a_rows[r] : r) * g.lda + lchunk(rl) * 8;
-    }
+        for (int i = 0; i < NA; ++i) {
+            const int rl = AROWS * wave + 8 * i + (lane >> 3);
+            const int r = min(m0 + rl, M - 1);
+            offA[i] = (int64_t)(g.a_rows ? g.a_rows[r] : r) * g.lda + lchunk(rl) * 8;
+        }
 #pragma unroll
-    for (int i = 0; i < NWL; ++i) {
-        const int rl = WROWS * wave + 8 * i + (lane >> 3);
-        offW[i] = (int64_t)min(n0 + rl, g.N - 1) * g.ldw + lchunk(rl) * 8;
-    }
+        for (int i = 0; i < NWL; ++i) {
+            const int rl = WROWS * wave + 8 * i + (lane >> 3);
+            offW[i] = (int64_t)min(n0 + rl, g.N - 1) * g.ldw + lchunk(rl) * 8;
+        }
+    };
     // load j of a stage: j < NA fills A rows AROWS w + 8 j.., otherwise W rows WROWS w + 8 (j - NA)..
     auto issue_one = [&](int k0, int stage, int j) {
         if (j < NA) {
@@ -280,12 +290,6 @@ __global__ __launch_bounds__(64 * WGM_ * WGN_, 1) void gemm_bf16_dl_kernel(GemmA
     constexpr int LPS = (NL + LD_STEPS - 1) / LD_STEPS;
 
     f32x16 acc[NB][MB];
-#pragma unroll
-    for (int i = 0; i < NB; ++i)
-#pragma unroll
-        for (int j = 0; j < MB; ++j)
-#pragma unroll
-            for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
 
     // fragment rows of this lane: row0 + lane % 32 with row0 a multiple of 32, so
     // (row >> 1) & 7 == (lane >> 1) & 7
@@ -295,9 +299,9 @@ __global__ __launch_bounds__(64 * WGM_ * WGN_, 1) void gemm_bf16_dl_kernel(GemmA
         return *(const bf16x8*)&tile[(row0 + frow) * BK + slot * 8];
     };
 
-    // one K-tile; the last one (with_loads false) has no next tile to fetch, which keeps the load
-    // issue free of branches inside the MFMA sequence
-    auto ktile = [&](const int t, auto with_loads) {
+    // one K-tile; with_loads: also fetch K offset next_k0 (of the tile offA/offW describe) into the
+    // other stage; without, the load issue stays free of branches inside the MFMA sequence
+    auto ktile = [&](const int t, const int next_k0, auto with_loads) {
         constexpr bool more = decltype(with_loads)::value;
         __builtin_amdgcn_s_waitcnt(0x3F70);      // vmcnt(0): this lane's loads of K-tile t landed
         __syncthreads();                          // ... everyone's; and everyone left K-tile t-1
@@ -343,7 +347,7 @@ __global__ __launch_bounds__(64 * WGM_ * WGN_, 1) void gemm_bf16_dl_kernel(GemmA
                     }
                 }
                 if constexpr (more)
-                    if (i < nload) issue_one((t + 1) * BK, (t + 1) & 1, kk * LPS + i);
+                    if (i < nload) issue_one(next_k0, (t + 1) & 1, kk * LPS + i);
                 __builtin_amdgcn_sched_barrier(0);
             }
             if (kk + 1 < BK / 16) __builtin_amdgcn_s_waitcnt(0xC07F);   // lgkmcnt(0)
@@ -352,7 +356,7 @@ __global__ __launch_bounds__(64 * WGM_ * WGN_, 1) void gemm_bf16_dl_kernel(GemmA
     };
 
     // bias of this lane's output columns (4 consecutive per (nb, j4)); the bf16-output epilogues
-    // fetch it before the K loop, the residual epilogue (short of registers) when it needs it
+    // fetch it ahead of the K loop, the residual epilogue (short of registers) when it needs it
     auto load_bias4 = [&](int nb, int j4) -> uint2 {
         const int n = n0 + wn * S::WN + nb * 32 + 8 * j4 + 4 * (lane >> 5);
         const bf16_t* bp = (const bf16_t*)g.bias + n;
@@ -364,12 +368,14 @@ __global__ __launch_bounds__(64 * WGM_ * WGN_, 1) void gemm_bf16_dl_kernel(GemmA
     };
     constexpr bool PREFETCH_BIAS = EPI == EPI_BIAS || EPI == EPI_BIAS_GELU;
     uint2 braw[PREFETCH_BIAS ? NB : 1][4];
-    if constexpr (PREFETCH_BIAS) {
+    auto prefetch_bias = [&]() {
+        if constexpr (PREFETCH_BIAS) {
 #pragma unroll
-        for (int nb = 0; nb < NB; ++nb)
+            for (int nb = 0; nb < NB; ++nb)
 #pragma unroll
-            for (int j4 = 0; j4 < 4; ++j4) braw[nb][j4] = load_bias4(nb, j4);
-    }
+                for (int j4 = 0; j4 < 4; ++j4) braw[nb][j4] = load_bias4(nb, j4);
+        }
+    };
     auto bias4 = [&](int nb, int j4, float* b4) {
         uint2 r = make_uint2(0u, 0u);
         if constexpr (PREFETCH_BIAS) r = braw[nb][j4];
@@ -377,81 +383,115 @@ __global__ __launch_bounds__(64 * WGM_ * WGN_, 1) void gemm_bf16_dl_kernel(GemmA
         b4[0] = bf16_lo(r.x); b4[1] = bf16_hi(r.x); b4[2] = bf16_lo(r.y); b4[3] = bf16_hi(r.y);
     };
 
-    const int nk = g.K / BK;
+    // epilogue of the tile at (m0, n0); n0 and the bias are read through the lambdas above, so the
+    // caller keeps them describing this tile until the epilogue is done
+    auto epilogue = [&](const int tm0) {
+        if constexpr (EPI == EPI_BIAS_RESID) {   // fp32 read-modify-write of the residual stream
+#pragma unroll
+            for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+                for (int j4 = 0; j4 < 4; ++j4) {
+                    const int n = n0 + wn * S::WN + nb * 32 + 8 * j4 + 4 * (lane >> 5);
+                    if (n >= g.N) continue;
+                    float b4[4];
+                    bias4(nb, j4, b4);
+#pragma unroll
+                    for (int mb = 0; mb < MB; ++mb) {
+                        const int m = tm0 + wm * S::WM + mb * 32 + (lane & 31);
+                        if (m >= M) continue;
+                        float v[4] = {acc[nb][mb][4 * j4], acc[nb][mb][4 * j4 + 1], acc[nb][mb][4 * j4 + 2],
+                                      acc[nb][mb][4 * j4 + 3]};
+                        epilogue_bf16<EPI>(g, m, n, v, b4);
+                    }
+                }
+        } else {
+            // bf16 outputs: each wave stages half of its WM x WN sub-tile at a time in LDS (rows
+            // padded by 16 B, above stage 0), then writes whole row segments with 16-byte stores.
+            __syncthreads();                      // every wave is done with the operand stages
+            bf16_t* cst = smem + S::STAGE + wave * (S::WM / 2 * S::CSTR);
+            bf16_t* C = (bf16_t*)g.C;
+            const int mrow0 = tm0 + wm * S::WM, ncol0 = n0 + wn * S::WN;
+            // e.g. WN = 64: 8 chunks per row, 8 rows per wave instruction; WN = 96: 12 chunks per
+            // row, 5 rows per instruction (lanes 60..63 idle)
+            constexpr int CPR = S::WN / 8;            // 16-byte chunks per staged row
+            constexpr int RPI = 64 / CPR;             // rows per wave instruction
+#pragma unroll
+            for (int half = 0; half < 2; ++half) {
+#pragma unroll
+                for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+                    for (int j4 = 0; j4 < 4; ++j4) {
+                        const int nl = nb * 32 + 8 * j4 + 4 * (lane >> 5);
+                        float b4[4];
+                        bias4(nb, j4, b4);
+#pragma unroll
+                        for (int mh = 0; mh < MB / 2; ++mh) {
+                            const int mb = half * (MB / 2) + mh;
+                            float o[4];
+#pragma unroll
+                            for (int e = 0; e < 4; ++e) {
+                                float x = acc[nb][mb][4 * j4 + e] + b4[e];
+                                if (EPI == EPI_BIAS_GELU) x = gelu_tanh(x);
+                                o[e] = x;
+                            }
+                            uint2 pk;
+                            pk.x = pack_bf16x2(o[0], o[1]);
+                            pk.y = pack_bf16x2(o[2], o[3]);
+                            *(uint2*)&cst[(mh * 32 + (lane & 31)) * S::CSTR + nl] = pk;
+                        }
+                    }
+                for (int r0 = 0; r0 < S::WM / 2; r0 += RPI) {
+                    const int r = r0 + lane / CPR, c = (lane % CPR) * 8;
+                    if (lane >= RPI * CPR || r >= S::WM / 2) continue;
+                    const int m = mrow0 + half * (S::WM / 2) + r, n = ncol0 + c;
+                    if (m >= M || n >= g.N) continue;
+                    const uint4 v = *(const uint4*)&cst[r * S::CSTR + c];
+                    bf16_t* dst = C + (int64_t)m * g.ldc + n;
+                    if (n + 7 < g.N) {
+                        *(uint4*)dst = v;
+                    } else {
+                        const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+                        for (int e = 0; n + e < g.N; ++e) dst[e] = (bf16_t)((w[e >> 1] >> (16 * (e & 1))) & 0xFFFFu);
+                    }
+                }
+            }
+        }
+    };
+
+    setup_tile(L);
+    prefetch_bias();
 #pragma unroll
     for (int j = 0; j < NL; ++j) issue_one(0, 0, j);
-    for (int t = 0; t + 1 < nk; ++t) ktile(t, std::true_type{});
-    ktile(nk - 1, std::false_type{});
-
-    if (EPI == EPI_BIAS_RESID) {     // fp32 read-modify-write of the residual stream, 16 B per lane
+    while (true) {
 #pragma unroll
-        for (int nb = 0; nb < NB; ++nb)
+        for (int i = 0; i < NB; ++i)
 #pragma unroll
-            for (int j4 = 0; j4 < 4; ++j4) {
-                const int n = n0 + wn * S::WN + nb * 32 + 8 * j4 + 4 * (lane >> 5);
-                if (n >= g.N) continue;
-                float b4[4];
-                bias4(nb, j4, b4);
+            for (int j = 0; j < MB; ++j)
 #pragma unroll
-                for (int mb = 0; mb < MB; ++mb) {
-                    const int m = m0 + wm * S::WM + mb * 32 + (lane & 31);
-                    if (m >= M) continue;
-                    float v[4] = {acc[nb][mb][4 * j4], acc[nb][mb][4 * j4 + 1], acc[nb][mb][4 * j4 + 2],
-                                  acc[nb][mb][4 * j4 + 3]};
-                    epilogue_bf16<EPI>(g, m, n, v, b4);
-                }
+                for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
+        const int Ln = L + (int)gridDim.x;
+        const bool next = Ln < nblocks;
+        const int tm0 = m0;
+        for (int t = 0; t < nk; ++t) {
+            if (t == nk - 1 && next) {            // the last K-tile fetches the next tile's first one
+                const int tn0 = n0;
+                setup_tile(Ln);
+                n0 = tn0;                         // the epilogue still describes this tile
             }
-        return;
-    }
-
-    // bf16 outputs: each wave stages its WM x WN sub-tile in LDS (rows padded by 16 B), then
-    // writes whole row segments with 16-byte stores.
-    __syncthreads();                              // every wave is done with the operand stages
-    bf16_t* cst = smem + wave * (S::WM * S::CSTR);
-#pragma unroll
-    for (int nb = 0; nb < NB; ++nb)
-#pragma unroll
-        for (int j4 = 0; j4 < 4; ++j4) {
-            const int nl = nb * 32 + 8 * j4 + 4 * (lane >> 5);
-            const int n = n0 + wn * S::WN + nl;
-            float b4[4];
-            bias4(nb, j4, b4);
-            (void)n;
-#pragma unroll
-            for (int mb = 0; mb < MB; ++mb) {
-                float o[4];
-#pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                    float x = acc[nb][mb][4 * j4 + e] + b4[e];
-                    if (EPI == EPI_BIAS_GELU) x = gelu_tanh(x);
-                    o[e] = x;
-                }
-                uint2 p;
-                p.x = pack_bf16x2(o[0], o[1]);
-                p.y = pack_bf16x2(o[2], o[3]);
-                *(uint2*)&cst[(mb * 32 + (lane & 31)) * S::CSTR + nl] = p;
-            }
+            // after the very last K-tile this re-fetches K-tile 0 into stage 0 (unused, in bounds):
+            // one call site keeps the MFMA sequence in one copy
+            ktile(t, t + 1 < nk ? (t + 1) * BK : 0, std::true_type{});
         }
-    bf16_t* C = (bf16_t*)g.C;
-    const int mrow0 = m0 + wm * S::WM, ncol0 = n0 + wn * S::WN;
-    // e.g. WN = 128: 16 chunks per row, 4 rows per wave instruction; WN = 96: 12 chunks per row,
-    // 5 rows per instruction (lanes 60..63 idle)
-    constexpr int CPR = S::WN / 8;                // 16-byte chunks per staged row
-    constexpr int RPI = 64 / CPR;                 // rows per wave instruction
-    for (int r0 = 0; r0 < S::WM; r0 += RPI) {
-        const int r = r0 + lane / CPR, c = (lane % CPR) * 8;
-        if (lane >= RPI * CPR || r >= S::WM) continue;
-        const int m = mrow0 + r, n = ncol0 + c;
-        if (m >= M || n >= g.N) continue;
-        const uint4 v = *(const uint4*)&cst[r * S::CSTR + c];
-        bf16_t* dst = C + (int64_t)m * g.ldc + n;
-        if (n + 7 < g.N) {
-            *(uint4*)dst = v;
-        } else {
-            const uint32_t w[4] = {v.x, v.y, v.z, v.w};
-            for (int e = 0; n + e < g.N; ++e) dst[e] = (bf16_t)((w[e >> 1] >> (16 * (e & 1))) & 0xFFFFu);
-        }
+        epilogue(tm0);
+        if (!next) break;
+        int tm_n, tn_n;
+        map_tile(Ln, nblocks, tiles_m, tiles_n, tm_n, tn_n);
+        m0 = tm_n * DM;
+        n0 = tn_n * S::TBN;
+        prefetch_bias();
+        L = Ln;
     }
+    __builtin_amdgcn_s_waitcnt(0x3F70);           // vmcnt(0): no LDS write in flight at exit
 }
 
 template <int TBM, int TBN>
@@ -525,27 +565,29 @@ static void launch_tile(const GemmArgs& g, hipStream_t s) {
 // Tile choice for the direct-to-LDS kernel: the N width (256 or 192) with the smaller estimated time,
 // counting whole rounds of workgroups over the CUs (a round of 192-wide tiles takes about 0.85 of a
 // round of 256-wide ones on MI355X), in the 8-wavefront form (two wavefronts per SIMD, measured 2-6%
-// faster than four wavefronts of twice the sub-tile).  K % 64 != 0 falls back to the 128 x 128
+// faster than four wavefronts of twice the sub-tile).  K % 128 != 0 falls back to the 128 x 128
 // register-staged kernel.  DD_GEMM_TILE (0..7) forces a variant for tuning and tests
 // (4: 256 x 256 / 4 waves, 5: 256 x 192 / 4 waves, 6: 256 x 256 / 8 waves, 7: 256 x 192 / 8 waves).
-static int g_num_cus = 0;
+static int num_cus() {
+    static int n = 0;
+    if (n == 0) {
+        int dev = 0, v = 0;
+        (void)hipGetDevice(&dev);
+        n = (hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess && v > 0) ? v : 256;
+    }
+    return n;
+}
 
 static int pick_tile(const GemmArgs& g) {
     const char* e = getenv("DD_GEMM_TILE");
     const int forced = e ? atoi(e) : -1;
-    if (forced >= 4 && forced <= 7 && g.K % BK != 0) return 0;
+    if (forced >= 4 && forced <= 7 && g.K % (2 * BK) != 0) return 0;
     if (forced >= 0 && forced <= 7 && !(g.a_rows && forced < 4)) return forced;
-    if (g.K % BK != 0) return 0;
-    if (g_num_cus == 0) {
-        int dev = 0;
-        (void)hipGetDevice(&dev);
-        if (hipDeviceGetAttribute(&g_num_cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
-            g_num_cus <= 0)
-            g_num_cus = 256;
-    }
+    if (g.K % (2 * BK) != 0) return 0;
+    const int64_t ncu = num_cus();
     const int64_t tm = (g.M + DM - 1) / DM;
-    const int64_t r256 = (tm * ((g.N + 255) / 256) + g_num_cus - 1) / g_num_cus;
-    const int64_t r192 = (tm * ((g.N + 191) / 192) + g_num_cus - 1) / g_num_cus;
+    const int64_t r256 = (tm * ((g.N + 255) / 256) + ncu - 1) / ncu;
+    const int64_t r192 = (tm * ((g.N + 191) / 192) + ncu - 1) / ncu;
     return (17 * r192 < 20 * r256) ? 7 : 6;
 }
 
@@ -559,7 +601,9 @@ static void launch_dl(const GemmArgs& g, hipStream_t s) {
                                   hipFuncAttributeMaxDynamicSharedMemorySize, (int)S::LDS);
         attr = true;
     }
-    hipLaunchKernelGGL((gemm_bf16_dl_kernel<EPI, ROLE, TBN, WGM, WGN>), dim3(tm * tn), dim3(S::THREADS), S::LDS, s,
+    // persistent: at most one workgroup per CU (the LDS footprint allows no second one)
+    const int grid = (int)std::min<int64_t>((int64_t)tm * tn, num_cus());
+    hipLaunchKernelGGL((gemm_bf16_dl_kernel<EPI, ROLE, TBN, WGM, WGN>), dim3(grid), dim3(S::THREADS), S::LDS, s,
                        g, tm, tn);
 }
 
@@ -582,7 +626,7 @@ static void launch_epi(int dtype, const GemmArgs& g, hipStream_t s) {
     }
 }
 
-bool gemm_gather_supported(int dtype, int K) { return dtype == DD_BF16 && K % BK == 0; }
+bool gemm_gather_supported(int dtype, int K) { return dtype == DD_BF16 && K % (2 * BK) == 0; }
 
 dd_status launch_gemm(int dtype, int epi, int cls, const GemmArgs& g, hipStream_t s) {
     if (g.M == 0 || g.N == 0) return DD_OK;
@@ -591,7 +635,7 @@ dd_status launch_gemm(int dtype, int epi, int cls, const GemmArgs& g, hipStream_
         return DD_E_ARG;
     }
     if (g.a_rows && !gemm_gather_supported(dtype, g.K)) {
-        set_error("row-gathered GEMM needs the bf16 path and K %% 64 == 0");
+        set_error("row-gathered GEMM needs the bf16 path and K %% 128 == 0");
         return DD_E_UNSUPPORTED;
     }
     ProfScope ps(cls, s);
