@@ -53,6 +53,14 @@ DD_DEV float wave_max(float v) {
     return v;
 }
 
+// Workgroup id -> work index such that each of the 8 XCDs (which receive workgroups round-robin by
+// id) walks one contiguous eighth of the work indices; work that shares operands and sits close in
+// index order then shares that XCD's L2.  Ids past the largest multiple of 8 map to themselves.
+DD_DEV int xcd_linear(int bid, int nblocks) {
+    const int per = nblocks / 8;
+    return bid < per * 8 ? (bid & 7) * per + (bid >> 3) : bid;
+}
+
 // ---------------------------------------------------------------- host helpers
 namespace dd {
 

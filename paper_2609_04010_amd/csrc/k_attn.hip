@@ -38,10 +38,15 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(AttnArgs a) {
     __shared__ __attribute__((aligned(16))) bf16_t Vt[2][DH * VSTR];
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int h = blockIdx.y, b = blockIdx.z;
+    // one-dimensional grid: the query blocks of one (batch, head) run on one XCD, one after another,
+    // so that head's K and V are fetched into that XCD's L2 once and then re-read from it
+    const int nqb = (a.L + AQ - 1) / AQ;
+    const int work = xcd_linear(blockIdx.x, gridDim.x);
+    const int qb = work % nqb, bh = work / nqb;
+    const int h = bh % a.H, b = bh / a.H;
     const int L = a.L, d = a.d;
     const bf16_t* base = (const bf16_t*)a.qkv + (int64_t)b * L * a.ld;
-    const int q0 = blockIdx.x * AQ + wave * 32;
+    const int q0 = qb * AQ + wave * 32;
     const int qi = q0 + (lane & 31);
     const int grp = lane >> 5;
 
@@ -234,7 +239,7 @@ dd_status launch_attn(int dtype, const AttnArgs& a, hipStream_t s) {
     const int dh = a.d / a.H;
     ProfScope ps(KC_ATTN, s);
     if (dtype == DD_BF16) {
-        hipLaunchKernelGGL(attn_bf16_kernel, dim3((a.L + AQ - 1) / AQ, a.H, a.B), dim3(256), 0, s, a);
+        hipLaunchKernelGGL(attn_bf16_kernel, dim3((unsigned)(ceil_div(a.L, AQ) * a.H * a.B)), dim3(256), 0, s, a);
     } else {
         const int64_t n = (int64_t)a.B * a.H * a.L;
         const dim3 grid((unsigned)ceil_div(n, 128));

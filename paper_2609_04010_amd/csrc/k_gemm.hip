@@ -36,9 +36,7 @@ DD_DEV float gelu_tanh(float x) {
 }
 
 DD_DEV void map_tile(int bid, int nblocks, int tiles_m, int tiles_n, int& tm, int& tn) {
-    int t = bid;
-    const int per = nblocks / 8;
-    if (bid < per * 8) t = (bid & 7) * per + (bid >> 3);
+    const int t = xcd_linear(bid, nblocks);
     constexpr int GM = 8;
     const int in_group = GM * tiles_n;
     const int grp = t / in_group;
