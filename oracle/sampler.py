@@ -24,8 +24,17 @@ probability p_j / M_g (the Gumbel-max property; Maddison, Tarlow, Minka,
 Explicit-noise layout per row: NU = n_top + V words, the n_top level-1
 words first, then one level-2 word per real class.
 
+psi_sample draws from the Psi transition (App. A.4, eq. (psi-sampler), in the
+closed forms eqs. (psi-mdm) and (psi-usdm)) with correction strength kappa in
+[0, 1]; kappa = 1 is the ancestral step above.  For the masked prior an
+unmasked position's x_theta is the one-hot of its token (the carry-over
+parameterisation that makes kappa = 1 keep it), so under eq. (psi-mdm) the
+token is kept with probability a_s + kappa (1 - a_s) and remasked with
+probability (1 - kappa)(1 - a_s); its logits are never read.
+
 Pinned by chi-square tests of many draws against the enumerated posterior and
-against the flat (one Gumbel per class) Gumbel-max draw.
+against the flat (one Gumbel per class) Gumbel-max draw; psi_sample by equality
+with posterior_sample at kappa = 1 and chi-square tests of its draws.
 """
 import numpy as np
 
@@ -142,6 +151,36 @@ def posterior_sample(prior, logits, z_t, alpha_t, alpha_s, noise, rows=None, ret
         x = np.exp(l - l.max())
         x /= x.sum()
         p = _post.posterior(prior, x, zt, alpha_t, alpha_s)
+        if return_probs:
+            probs[i] = p
+        out[i], gaps[i, 0], gaps[i, 1] = sample_from_probs(prior, p, int(rows[i]), noise)
+    return (out, gaps, probs) if return_probs else (out, gaps)
+
+
+def psi_sample(prior, logits, z_t, alpha_t, alpha_s, kappa, noise, rows=None, return_probs=False):
+    """One Psi-sampler step (App. A.4, eq. (psi-sampler)) on a [R, V] logit matrix.
+
+    Same outputs as posterior_sample; every row draws (masked prior: unmasked rows
+    choose between keeping their token and the mask)."""
+    logits = np.asarray(logits, dtype=np.float64)
+    z_t = np.asarray(z_t)
+    R, V = logits.shape
+    rows = np.arange(R) if rows is None else np.asarray(rows)
+    out = np.array(z_t, dtype=np.int64).copy()
+    gaps = np.full((R, 2), np.inf)
+    K = V + 1 if prior == "mask" else V
+    probs = np.zeros((R, K)) if return_probs else None
+    for i in range(R):
+        zt = int(z_t[i])
+        if prior == "mask" and zt != V:
+            x = np.zeros(V)
+            x[zt] = 1.0
+            p = _post.psi_mdm(x, zt, alpha_t, alpha_s, kappa)
+        else:
+            l = logits[i]
+            x = np.exp(l - l.max())
+            x /= x.sum()
+            p = (_post.psi_mdm if prior == "mask" else _post.psi_usdm)(x, zt, alpha_t, alpha_s, kappa)
         if return_probs:
             probs[i] = p
         out[i], gaps[i, 0], gaps[i, 1] = sample_from_probs(prior, p, int(rows[i]), noise)

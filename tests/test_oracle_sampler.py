@@ -171,3 +171,73 @@ def test_loop_uniform_prior_runs():
     z1 = workloads.uniform_state(3, B, L, V)
     z0, trace, _ = loop.sample_loop(cfg, P, z1, T, schedule.alphas(T), noise_seed=17)
     assert z0.shape == (B, L) and (trace >= 0).all() and (trace < V).all()
+
+
+# ---------------------------------------------------------------- Psi sampler (kappa < 1)
+
+@pytest.mark.parametrize("prior", ["mask", "uniform"])
+def test_psi_sample_at_kappa_one_is_the_ancestral_step(prior):
+    V, R = 300, 24
+    logits = workloads.synthetic_logits(21, R, V)
+    if prior == "mask":
+        zt = workloads.masked_state(22, 1, R, V, 0.6).reshape(-1)
+    else:
+        zt = workloads.uniform_state(22, 1, R, V).reshape(-1)
+    a, _ = sampler.posterior_sample(prior, logits, zt, 0.3, 0.45, sampler.PhiloxNoise(4, 7))
+    b, _ = sampler.psi_sample(prior, logits, zt, 0.3, 0.45, 1.0, sampler.PhiloxNoise(4, 7))
+    assert np.array_equal(a, b)
+
+
+def test_psi_unmasked_token_keep_or_remask_chi2():
+    """Masked prior, unmasked z_t: eq. (psi-mdm) with x_theta = one-hot(z_t) keeps the token with
+    probability a_s + kappa (1 - a_s) and remasks otherwise; the logits are never read."""
+    V, n, at, as_, kappa = 40, 20000, 0.35, 0.5, 0.3
+    logits = np.full((n, V), np.nan)                     # unread
+    zt = np.full(n, 17)
+    z, _ = sampler.psi_sample("mask", logits, zt, at, as_, kappa, sampler.PhiloxNoise(3, 2))
+    assert set(np.unique(z)) <= {17, V}
+    keep = as_ + kappa * (1 - as_)
+    counts = np.array([(z == 17).sum(), (z == V).sum()])
+    assert chi2_pvalue(counts, np.array([keep, 1 - keep])) > 1e-3
+
+
+@pytest.mark.parametrize("prior", ["mask", "uniform"])
+@pytest.mark.parametrize("kappa", [0.0, 0.45])
+def test_psi_draws_match_psi_probabilities_chi2(prior, kappa):
+    V, n = 600, 20000                                    # three real groups
+    r = np.random.default_rng(5)
+    l = 1.5 * r.standard_normal(V)
+    l[r.integers(0, V, 3)] += 4.0
+    x = np.exp(l - l.max())
+    x /= x.sum()
+    zt = V if prior == "mask" else 123
+    f = posterior.psi_mdm if prior == "mask" else posterior.psi_usdm
+    p = f(x, zt, 0.4, 0.55, kappa)
+    z = np.empty(n, dtype=np.int64)
+    for i in range(n):
+        z[i] = sampler.sample_from_probs(prior, p, 3, sampler.PhiloxNoise(13, i))[0]
+    assert chi2_pvalue(np.bincount(z, minlength=p.shape[0]), p) > 1e-3
+    # the draw routine on a logit row gives exactly these probabilities
+    _, _, pr = sampler.psi_sample(prior, l[None, :], np.array([zt]), 0.4, 0.55, kappa,
+                                  sampler.PhiloxNoise(13, 0), return_probs=True)
+    assert np.allclose(pr[0], p, rtol=0, atol=1e-15)
+
+
+def test_psi_loop_bookkeeping_masked_config1():
+    """kappa < 1 lets decoded tokens be remasked, tokens change only by unmasking or remasking, and
+    the last step (a_s = 1) still leaves no mask."""
+    c = 1
+    cfg = workloads.model_cfg(c)
+    V, T = cfg["vocab"], 8
+    P = workloads.host_params(cfg, workloads.seeds(c)["param"], params.specs(cfg))
+    z1 = workloads.all_mask(4, 32, V)
+    al = schedule.alphas(T)
+    kap = np.full(T + 1, 0.3)
+    z0, trace, _ = loop.sample_loop(cfg, P, z1, T, al, noise_seed=9, kappas=kap)
+    assert (trace[-1] == V).sum() == 0
+    remasked = sum(int(((a != V) & (b == V)).sum()) for a, b in zip(trace[:-1], trace[1:]))
+    assert remasked > 0                                   # decoded tokens were remasked
+    for a, b in zip(trace[:-1], trace[1:]):
+        changed = a != b
+        # a change is either mask -> token or token -> mask
+        assert np.all((a[changed] == V) ^ (b[changed] == V))
