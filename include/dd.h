@@ -184,6 +184,25 @@ dd_status dd_posterior_sample(int32_t prior, const void* logits, int32_t logits_
                               float* probs, int32_t* dev_err, void* stream);
 
 /*
+ * dd_psi_posterior_sample - one Psi-sampler draw per row (App. A.4, eq. psi:
+ * kappa q_{s|t} + (1 - kappa) q_s, with x = softmax(logits); closed forms
+ * eqs. psi-mdm and psi-usdm).  Arguments as dd_posterior_sample, plus
+ *   kappa        correction strength in [0, 1] (DD_E_ARG otherwise); 1 gives
+ *                exactly dd_posterior_sample.
+ * Masked prior, z_t != mask: x_theta is taken as the one-hot of z_t (the
+ * carry-over parameterisation), so the token is kept with probability
+ * a_s + kappa (1 - a_s) and remasked otherwise, by the level-1 Gumbel scores of
+ * its own group and of the mask group; its logits are never read.  Uniform
+ * prior: every class keeps non-zero probability for kappa < 1.
+ */
+dd_status dd_psi_posterior_sample(int32_t prior, const void* logits, int32_t logits_dtype,
+                                  int64_t ld, int32_t rows, int32_t V, const int32_t* z_t,
+                                  double alpha_t, double alpha_s, double kappa,
+                                  const uint32_t* noise_words, uint64_t seed, uint32_t step,
+                                  uint32_t row0, int32_t* z_s, float* probs, int32_t* dev_err,
+                                  void* stream);
+
+/*
  * dd_sample_loop - T ancestral steps z_1 -> z_0 on the grid t_k = k/T.
  *   alphas       host double [T + 1], alphas[k] = alpha(k / T): alphas[0] = 1,
  *                alphas[T] = 0 is not required but the values must strictly
@@ -204,6 +223,25 @@ dd_status dd_sample_loop(const dd_config* cfg, const void* params, int32_t B, in
                          int32_t T, const double* alphas, int32_t* z,
                          const uint32_t* noise_words, uint64_t noise_seed,
                          int32_t* z_trace, void* ws, size_t ws_bytes, void* stream);
+
+/*
+ * dd_psi_sample_loop - dd_sample_loop with the Psi transition (App. A.4,
+ * eq. psi-sampler): step k draws with dd_psi_posterior_sample at
+ * kappa = kappas[k].
+ *   kappas       NULL (every kappa 1: exactly dd_sample_loop) or host double
+ *                [T + 1], each used entry (k = 1..T) in [0, 1].
+ * With kappa < 1 decoded tokens can be remasked and T may exceed the number of
+ * positions (inference-time scaling, Sec. 4); a step with alpha_s = 1 (the
+ * last one) still unmasks every position.  Masked prior (bf16): the rows
+ * unmasked before a step first keep or remask (no logits), then the
+ * still-masked rows run the vocabulary projection and the draw as in
+ * dd_sample_loop; the result equals dd_denoise_forward followed by
+ * dd_psi_posterior_sample on every row.
+ */
+dd_status dd_psi_sample_loop(const dd_config* cfg, const void* params, int32_t B, int32_t L,
+                             int32_t T, const double* alphas, const double* kappas, int32_t* z,
+                             const uint32_t* noise_words, uint64_t noise_seed,
+                             int32_t* z_trace, void* ws, size_t ws_bytes, void* stream);
 
 /*
  * dd_gaussian_latent_argmax - z = argmax_v (alpha_tilde [v == x] + sigma eps_v)

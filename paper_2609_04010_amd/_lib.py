@@ -27,7 +27,8 @@ EXPORTED = [
     "dd_param_count", "dd_param_tensor", "dd_param_bytes", "dd_workspace_bytes",
     "dd_loop_workspace_bytes", "dd_logits_ld", "dd_noise_width", "dd_status_str", "dd_last_error",
     "dd_workspace_reset", "dd_read_device_error", "dd_init_params", "dd_denoise_forward",
-    "dd_posterior_sample", "dd_sample_loop", "dd_gaussian_latent_argmax", "dd_profile_begin",
+    "dd_posterior_sample", "dd_psi_posterior_sample", "dd_sample_loop", "dd_psi_sample_loop",
+    "dd_gaussian_latent_argmax", "dd_profile_begin",
     "dd_profile_end", "dd_profile_num_classes", "dd_profile_read",
 ]
 
@@ -77,9 +78,16 @@ def lib():
             "dd_posterior_sample": (c.c_int32, [c.c_int32, P, c.c_int32, c.c_int64, c.c_int32,
                                                 c.c_int32, P, c.c_double, c.c_double, P,
                                                 c.c_uint64, c.c_uint32, c.c_uint32, P, P, P, P]),
+            "dd_psi_posterior_sample": (c.c_int32, [c.c_int32, P, c.c_int32, c.c_int64, c.c_int32,
+                                                    c.c_int32, P, c.c_double, c.c_double, c.c_double,
+                                                    P, c.c_uint64, c.c_uint32, c.c_uint32, P, P, P,
+                                                    P]),
             "dd_sample_loop": (c.c_int32, [cfgp, P, c.c_int32, c.c_int32, c.c_int32,
                                            c.POINTER(c.c_double), P, P, c.c_uint64, P, P,
                                            c.c_size_t, P]),
+            "dd_psi_sample_loop": (c.c_int32, [cfgp, P, c.c_int32, c.c_int32, c.c_int32,
+                                               c.POINTER(c.c_double), c.POINTER(c.c_double), P, P,
+                                               c.c_uint64, P, P, c.c_size_t, P]),
             "dd_gaussian_latent_argmax": (c.c_int32, [P, c.c_int32, c.c_int32, c.c_double,
                                                       c.c_double, c.c_uint64, c.c_uint32,
                                                       c.c_uint32, P, P, P]),
@@ -225,36 +233,61 @@ def denoise_forward(cfg, params, z_t, B, L, alpha_t, logits, ld, ws):
         _ptr(ws, workspace_bytes(cfg, B, L), "ws"), ws.numel() * ws.element_size(), _stream()))
 
 
-def posterior_sample(prior, logits, logits_dtype, ld, rows, V, z_t, alpha_t, alpha_s, z_s,
-                     noise_words=None, seed=0, step=0, row0=0, probs=None, dev_err=None):
+def _posterior_args(prior, logits, logits_dtype, ld, rows, V, z_t, noise_words, z_s, probs, dev_err):
     torch = _torch()
     es = 2 if logits_dtype == "bf16" else 4
     K = V + 1 if prior == "mask" else V
     nu = noise_width(prior, V)
     lg = _ptr(logits, es * rows * ld, "logits") if rows > 0 else None
+    return (lg, _ptr(z_t, 4 * rows, "z_t", torch.int32),
+            _ptr(noise_words, 4 * rows * nu, "noise_words", torch.int32) if noise_words is not None else None,
+            _ptr(z_s, 4 * rows, "z_s", torch.int32),
+            _ptr(probs, 4 * rows * K, "probs", torch.float32) if probs is not None else None,
+            _ptr(dev_err, 4, "dev_err", torch.int32) if dev_err is not None else None)
+
+
+def posterior_sample(prior, logits, logits_dtype, ld, rows, V, z_t, alpha_t, alpha_s, z_s,
+                     noise_words=None, seed=0, step=0, row0=0, probs=None, dev_err=None):
+    lg, zt, nw, zs, pr, er = _posterior_args(prior, logits, logits_dtype, ld, rows, V, z_t, noise_words,
+                                             z_s, probs, dev_err)
     _check(lib().dd_posterior_sample(
-        prior_code(prior), lg, dtype_code(logits_dtype), int(ld), int(rows), int(V),
-        _ptr(z_t, 4 * rows, "z_t", torch.int32), float(alpha_t), float(alpha_s),
-        _ptr(noise_words, 4 * rows * nu, "noise_words", torch.int32) if noise_words is not None else None,
-        int(seed) & 0xFFFFFFFFFFFFFFFF, int(step), int(row0), _ptr(z_s, 4 * rows, "z_s", torch.int32),
-        _ptr(probs, 4 * rows * K, "probs", torch.float32) if probs is not None else None,
-        _ptr(dev_err, 4, "dev_err", torch.int32) if dev_err is not None else None, _stream()))
+        prior_code(prior), lg, dtype_code(logits_dtype), int(ld), int(rows), int(V), zt, float(alpha_t),
+        float(alpha_s), nw, int(seed) & 0xFFFFFFFFFFFFFFFF, int(step), int(row0), zs, pr, er, _stream()))
 
 
-def sample_loop(cfg, params, B, L, T, alphas, z, ws, noise_words=None, noise_seed=0, z_trace=None):
+def psi_posterior_sample(prior, logits, logits_dtype, ld, rows, V, z_t, alpha_t, alpha_s, kappa, z_s,
+                         noise_words=None, seed=0, step=0, row0=0, probs=None, dev_err=None):
+    lg, zt, nw, zs, pr, er = _posterior_args(prior, logits, logits_dtype, ld, rows, V, z_t, noise_words,
+                                             z_s, probs, dev_err)
+    _check(lib().dd_psi_posterior_sample(
+        prior_code(prior), lg, dtype_code(logits_dtype), int(ld), int(rows), int(V), zt, float(alpha_t),
+        float(alpha_s), float(kappa), nw, int(seed) & 0xFFFFFFFFFFFFFFFF, int(step), int(row0), zs, pr, er,
+        _stream()))
+
+
+def sample_loop(cfg, params, B, L, T, alphas, z, ws, noise_words=None, noise_seed=0, z_trace=None,
+                kappas=None):
+    """dd_sample_loop, or dd_psi_sample_loop when kappas (T + 1 values) is given."""
     torch = _torch()
     M = B * L
     a = np.ascontiguousarray(alphas, dtype=np.float64)
     if a.shape != (T + 1,):
         raise ValueError("alphas must hold T + 1 values")
     nu = noise_width(cfg["prior"], cfg["vocab"])
-    _check(lib().dd_sample_loop(
-        ctypes.byref(make_config(cfg)), _ptr(params, param_bytes(cfg), "params"), B, L, T,
-        a.ctypes.data_as(ctypes.POINTER(ctypes.c_double)), _ptr(z, 4 * M, "z", torch.int32),
-        _ptr(noise_words, 4 * T * M * nu, "noise_words", torch.int32) if noise_words is not None else None,
-        int(noise_seed) & 0xFFFFFFFFFFFFFFFF,
-        _ptr(z_trace, 4 * (T + 1) * M, "z_trace", torch.int32) if z_trace is not None else None,
-        _ptr(ws, loop_workspace_bytes(cfg, B, L), "ws"), ws.numel() * ws.element_size(), _stream()))
+    dp = ctypes.POINTER(ctypes.c_double)
+    head = (ctypes.byref(make_config(cfg)), _ptr(params, param_bytes(cfg), "params"), B, L, T, a.ctypes.data_as(dp))
+    tail = (_ptr(z, 4 * M, "z", torch.int32),
+            _ptr(noise_words, 4 * T * M * nu, "noise_words", torch.int32) if noise_words is not None else None,
+            int(noise_seed) & 0xFFFFFFFFFFFFFFFF,
+            _ptr(z_trace, 4 * (T + 1) * M, "z_trace", torch.int32) if z_trace is not None else None,
+            _ptr(ws, loop_workspace_bytes(cfg, B, L), "ws"), ws.numel() * ws.element_size(), _stream())
+    if kappas is None:
+        _check(lib().dd_sample_loop(*head, *tail))
+    else:
+        k = np.ascontiguousarray(kappas, dtype=np.float64)
+        if k.shape != (T + 1,):
+            raise ValueError("kappas must hold T + 1 values")
+        _check(lib().dd_psi_sample_loop(*head, k.ctypes.data_as(dp), *tail))
 
 
 def gaussian_latent_argmax(x, rows, V, alpha_tilde, sigma, seed, step, z_out, row0=0, dev_err=None):

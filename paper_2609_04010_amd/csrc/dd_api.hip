@@ -248,25 +248,41 @@ static int32_t ntop_of(int prior, int V) {
     return (V + DD_GUMBEL_GROUP - 1) / DD_GUMBEL_GROUP + (prior == DD_PRIOR_MASK ? 1 : 0);
 }
 
+// Coefficients of the Psi transition (App. A.4, eq. (psi-sampler) in the closed forms eqs.
+// (psi-mdm), (psi-usdm)); kappa = 1 is the ancestral posterior (App. A.1 / A.2).  Each term is
+// written as its kappa = 1 value plus a (1 - kappa) correction, so kappa = 1 reproduces the
+// ancestral coefficients bit for bit.
 static PostArgs make_post(int prior, const void* logits, int64_t ld, int32_t rows, int32_t V,
-                          const int32_t* z_t, double at, double as, const uint32_t* noise,
-                          uint64_t seed, uint32_t step, uint32_t row0, int32_t* z_s, float* probs,
-                          int32_t* err) {
+                          const int32_t* z_t, double at, double as, double kappa,
+                          const uint32_t* noise, uint64_t seed, uint32_t step, uint32_t row0,
+                          int32_t* z_s, float* probs, int32_t* err) {
     PostArgs a;
     memset(&a, 0, sizeof(a));
     a.logits = logits; a.ld = ld; a.rows = rows; a.V = V; a.prior = prior;
     a.z_t = z_t; a.z_s = z_s;
+    const double omk = 1.0 - kappa;
     if (prior == DD_PRIOR_MASK) {
-        a.wx = (as - at) / (1.0 - at);
-        a.wm = (1.0 - as) / (1.0 - at);
+        // masked rows: (a_s - k a_t (1 - a_s)/(1 - a_t)) x + (1 - a_s + k a_t (1 - a_s)/(1 - a_t)) m
+        const double corr = omk * at * (1.0 - as) / (1.0 - at);
+        a.wx = (as - at) / (1.0 - at) + corr;
+        a.wm = (1.0 - as) / (1.0 - at) - corr;
         a.log_wx = log(a.wx);
         a.log_wm = a.wm > 0.0 ? log(a.wm) : -INFINITY;
+        // unmasked rows (x_theta = one-hot of the token): keep a_s + k (1 - a_s), remask the rest
+        a.rmask = omk * (1.0 - as);
+        a.keep = 1.0 - a.rmask;
+        a.remask = a.rmask > 0.0;
+        a.log_keep = log(a.keep);
+        a.log_rmask = a.rmask > 0.0 ? log(a.rmask) : -INFINITY;
     } else {
         const double K = (double)V, ats = at / as;
-        a.c_x = as - at;
-        a.c_u = (1.0 - ats) * (1.0 - as) / K;
-        a.c_z = ats - at;
+        const double cu1 = (1.0 - ats) * (1.0 - as) / K;
+        a.c_x = (as - at) + omk * at * (1.0 - as);
+        a.c_u = cu1 - omk * cu1;
+        a.u1 = omk * (1.0 - as) / K;
+        a.c_z = (ats - at) - omk * (1.0 - as) * ats;
         a.Ka_t = K * at;
+        a.Ka_r = K * at * (1.0 - omk * (1.0 - as));
         a.one_m_at = 1.0 - at;
     }
     a.noise = noise;
@@ -398,28 +414,38 @@ dd_status dd_denoise_forward(const dd_config* cfg, const void* params, const int
     return run_forward(cfg, params, z_t, B, L, alpha_t, logits, ld, (char*)ws, (hipStream_t)stream);
 }
 
-dd_status dd_posterior_sample(int32_t prior, const void* logits, int32_t logits_dtype, int64_t ld,
-                              int32_t rows, int32_t V, const int32_t* z_t, double alpha_t,
-                              double alpha_s, const uint32_t* noise_words, uint64_t seed,
-                              uint32_t step, uint32_t row0, int32_t* z_s, float* probs,
-                              int32_t* dev_err, void* stream) {
+dd_status dd_psi_posterior_sample(int32_t prior, const void* logits, int32_t logits_dtype, int64_t ld,
+                                  int32_t rows, int32_t V, const int32_t* z_t, double alpha_t,
+                                  double alpha_s, double kappa, const uint32_t* noise_words,
+                                  uint64_t seed, uint32_t step, uint32_t row0, int32_t* z_s,
+                                  float* probs, int32_t* dev_err, void* stream) {
     DD_CHECK(prior == DD_PRIOR_MASK || prior == DD_PRIOR_UNIFORM, DD_E_ARG, "unknown prior %d", prior);
     DD_CHECK(logits_dtype == DD_BF16 || logits_dtype == DD_FP32, DD_E_DTYPE, "unknown logits dtype");
     DD_CHECK(rows >= 0 && V > 0, DD_E_ARG, "rows must be >= 0 and V > 0");
     DD_CHECK(V <= (1 << 24), DD_E_UNSUPPORTED, "V > 2^24 unsupported");
     DD_CHECK(ld >= V && ld % 8 == 0, DD_E_SHAPE, "ld must be >= V and a multiple of 8");
     DD_TRY(check_schedule(alpha_t, alpha_s));
+    DD_CHECK(kappa >= 0.0 && kappa <= 1.0, DD_E_ARG, "kappa must lie in [0, 1] (got %.17g)", kappa);
     if (rows == 0) return DD_OK;
     DD_CHECK(logits && z_t && z_s, DD_E_ARG, "NULL pointer argument");
-    const PostArgs a = make_post(prior, logits, ld, rows, V, z_t, alpha_t, alpha_s, noise_words,
+    const PostArgs a = make_post(prior, logits, ld, rows, V, z_t, alpha_t, alpha_s, kappa, noise_words,
                                  seed, step, row0, z_s, probs, dev_err);
     return launch_posterior(a, logits_dtype, (hipStream_t)stream);
 }
 
-dd_status dd_sample_loop(const dd_config* cfg, const void* params, int32_t B, int32_t L,
-                         int32_t T, const double* alphas, int32_t* z, const uint32_t* noise_words,
-                         uint64_t noise_seed, int32_t* z_trace, void* ws, size_t ws_bytes,
-                         void* stream) {
+dd_status dd_posterior_sample(int32_t prior, const void* logits, int32_t logits_dtype, int64_t ld,
+                              int32_t rows, int32_t V, const int32_t* z_t, double alpha_t,
+                              double alpha_s, const uint32_t* noise_words, uint64_t seed,
+                              uint32_t step, uint32_t row0, int32_t* z_s, float* probs,
+                              int32_t* dev_err, void* stream) {
+    return dd_psi_posterior_sample(prior, logits, logits_dtype, ld, rows, V, z_t, alpha_t, alpha_s, 1.0,
+                                   noise_words, seed, step, row0, z_s, probs, dev_err, stream);
+}
+
+dd_status dd_psi_sample_loop(const dd_config* cfg, const void* params, int32_t B, int32_t L,
+                             int32_t T, const double* alphas, const double* kappas, int32_t* z,
+                             const uint32_t* noise_words, uint64_t noise_seed, int32_t* z_trace,
+                             void* ws, size_t ws_bytes, void* stream) {
     DD_CHECK(cfg_ok(cfg), DD_E_ARG, "%s", g_err);
     DD_CHECK(params && z && ws && alphas, DD_E_ARG, "NULL pointer argument");
     DD_CHECK(B > 0 && L > 0 && T > 0, DD_E_ARG, "B, L and T must be positive");
@@ -428,6 +454,10 @@ dd_status dd_sample_loop(const dd_config* cfg, const void* params, int32_t B, in
     DD_CHECK(((uintptr_t)ws & 255) == 0 && ((uintptr_t)params & 255) == 0, DD_E_ARG,
              "params and ws must be 256-byte aligned");
     for (int k = 1; k <= T; ++k) DD_TRY(check_schedule(alphas[k], alphas[k - 1]));
+    if (kappas)
+        for (int k = 1; k <= T; ++k)
+            DD_CHECK(kappas[k] >= 0.0 && kappas[k] <= 1.0, DD_E_ARG, "kappas[%d] = %.17g is outside [0, 1]",
+                     k, kappas[k]);
     const size_t need = dd_loop_workspace_bytes(cfg, B, L);
     DD_CHECK(ws_bytes >= need, DD_E_WORKSPACE, "workspace has %zu bytes, needs %zu", ws_bytes, need);
     hipStream_t s = (hipStream_t)stream;
@@ -458,13 +488,27 @@ dd_status dd_sample_loop(const dd_config* cfg, const void* params, int32_t B, in
                            compact ? rows : nullptr, compact ? count : nullptr));
         const uint32_t* nw = noise_words ? noise_words + (int64_t)(k - 1) * M * nu : nullptr;
         PostArgs a = make_post(cfg->prior, logits, ld, (int32_t)M, cfg->vocab, z, alphas[k],
-                               alphas[k - 1], nw, noise_seed, (uint32_t)k, 0u, z, nullptr,
-                               (int32_t*)(wsc + w.err));
-        if (compact) { a.rows_idx = rows; a.count = count; }
+                               alphas[k - 1], kappas ? kappas[k] : 1.0, nw, noise_seed, (uint32_t)k,
+                               0u, z, nullptr, (int32_t*)(wsc + w.err));
+        if (compact) {
+            // kappa < 1: the rows unmasked before this step keep or remask first (they read no
+            // logits and are not in the compacted list, which was taken before the step)
+            if (a.remask) DD_TRY(launch_remask(a, s));
+            a.rows_idx = rows;
+            a.count = count;
+        }
         DD_TRY(launch_posterior(a, cfg->dtype, s));
         DD_TRY(trace_copy(T - k + 1));
     }
     return DD_OK;
+}
+
+dd_status dd_sample_loop(const dd_config* cfg, const void* params, int32_t B, int32_t L,
+                         int32_t T, const double* alphas, int32_t* z, const uint32_t* noise_words,
+                         uint64_t noise_seed, int32_t* z_trace, void* ws, size_t ws_bytes,
+                         void* stream) {
+    return dd_psi_sample_loop(cfg, params, B, L, T, alphas, nullptr, z, noise_words, noise_seed, z_trace,
+                              ws, ws_bytes, stream);
 }
 
 dd_status dd_gaussian_latent_argmax(const int32_t* x, int32_t rows, int32_t V, double alpha_tilde,

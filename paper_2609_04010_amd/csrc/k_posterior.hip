@@ -10,13 +10,17 @@
 // optional full posterior row (a debug output) comes from a separate kernel in
 // float64.
 //
-// Masked prior (App. A.1, eq. mdm-posterior, x = softmax(logits)):
-//   z_t == mask:  p_v = w_x x_v (v < V), p_mask = w_m,
+// The transition is the Psi sampler step (App. A.4, eq. psi-sampler) with correction strength
+// kappa; kappa = 1 is the ancestral posterior.  The host folds kappa into the coefficients.
+// Masked prior (App. A.1, eq. mdm-posterior; App. A.4, eq. psi-mdm), x = softmax(logits):
+//   z_t == mask:  p_v = w_x x_v (v < V), p_mask = w_m; at kappa = 1
 //                 w_x = (a_s - a_t)/(1 - a_t), w_m = (1 - a_s)/(1 - a_t)
-//   z_t != mask:  carry-over, z_s = z_t (the row is not read).
-// Uniform prior (App. A.2, eq. uniform_true_reverse_posterior), K = V, r = z_t:
-//   p_j = [c_x x_j + c_u + [j == r](K a_t x_r + c_z)] / (K a_t x_r + 1 - a_t)
-//   c_x = a_s - a_t, c_z = a_{t|s} - a_t, c_u = (1 - a_{t|s})(1 - a_s)/K.
+//   z_t != mask:  kappa = 1: carry-over, z_s = z_t; kappa < 1: keep z_t or remask (probabilities
+//                 a_s + kappa (1 - a_s) and the rest).  The row's logits are never read.
+// Uniform prior (App. A.2, eq. uniform_true_reverse_posterior; App. A.4, eq. psi-usdm), K = V,
+// r = z_t, D = K a_t x_r + 1 - a_t:
+//   p_j = [c_x x_j + c_u + u1 D + [j == r](Ka_r x_r + c_z)] / D; at kappa = 1
+//   c_x = a_s - a_t, c_z = a_{t|s} - a_t, c_u = (1 - a_{t|s})(1 - a_s)/K, u1 = 0, Ka_r = K a_t.
 #include <math.h>
 
 #include "kernels.h"
@@ -79,6 +83,26 @@ DD_DEV void wave_argmax(float& s, int& i) {
     }
 }
 
+// Keep-or-remask draw of an unmasked row (masked prior, kappa < 1): the two-level draw over a
+// distribution whose only classes are the token (in group zt / GROUP) and the mask (its own group,
+// index ngroups), so level 1 decides; ties go to the token's (lower) group.
+DD_DEV int32_t keep_or_remask(const PostArgs& a, int row, int zt) {
+    const int ngroups = (a.V + DD_GUMBEL_GROUP - 1) / DD_GUMBEL_GROUP;
+    const int gr = zt / DD_GUMBEL_GROUP;
+    uint32_t wr, wm;
+    if (a.noise) {
+        wr = a.noise[(int64_t)row * a.nu + gr];
+        wm = a.noise[(int64_t)row * a.nu + ngroups];
+    } else {
+        const uint32_t grow = a.row0 + (uint32_t)row;
+        wr = counter_word(a.seed, STREAM_TOP, a.step, grow, (uint32_t)gr);
+        wm = counter_word(a.seed, STREAM_TOP, a.step, grow, (uint32_t)ngroups);
+    }
+    const float sr = (float)a.log_keep + word_gumbel_f(wr);
+    const float sm = (float)a.log_rmask + word_gumbel_f(wm);
+    return sm > sr ? a.V : zt;
+}
+
 template <typename T>
 __global__ __launch_bounds__(PT) void posterior_kernel(PostArgs a) {
     extern __shared__ float s_lse[];  // one log-sum-exp per group
@@ -102,8 +126,8 @@ __global__ __launch_bounds__(PT) void posterior_kernel(PostArgs a) {
         if (tid == 0 && a.err) atomicOr(a.err, DD_DEVERR_TOKEN);
         zt = zt < 0 ? 0 : K - 1;
     }
-    if (mask_prior && zt != V) {  // carry-over: the row's logits are never read
-        if (tid == 0) a.z_s[row] = zt;
+    if (mask_prior && zt != V) {  // carry-over or keep/remask: the row's logits are never read
+        if (tid == 0) a.z_s[row] = a.remask ? keep_or_remask(a, row, zt) : zt;
         return;
     }
 
@@ -197,14 +221,15 @@ __global__ __launch_bounds__(PT) void posterior_kernel(PostArgs a) {
         for (int g = lane; g < ngroups; g += 64) sum += expf(s_lse[g] - mref);
         const float lse = mref + logf(wave_sum(sum));
 
-        float c_r = 0.f, Dn = 1.f;
+        float c_r = 0.f, Dn = 1.f, c_u = 0.f;
         if (!mask_prior) {   // uniform prior: x_r enters the mass of the current token's class
             const float xr = expf(Elem<T>::load1(rowp, zt) - lse);
-            c_r = (float)a.Ka_t * xr + (float)a.c_z;
+            c_r = (float)a.Ka_r * xr + (float)a.c_z;
             Dn = (float)a.Ka_t * xr + (float)a.one_m_at;
+            c_u = (float)a.c_u + (float)a.u1 * Dn;
         }
         const float log_wx = (float)a.log_wx, log_wm = (float)a.log_wm;
-        const float c_x = (float)a.c_x, c_u = (float)a.c_u, log_dn = logf(Dn);
+        const float c_x = (float)a.c_x, log_dn = logf(Dn);
         const uint32_t k0 = (uint32_t)a.seed, k1 = (uint32_t)(a.seed >> 32);
 
         // level 1: group g has log mass log w_x + lse_g - lse (mask prior; the mask class is group
@@ -288,7 +313,8 @@ __global__ __launch_bounds__(PT) void posterior_probs_kernel(PostArgs a) {
     zt = zt < 0 ? 0 : (zt >= K ? K - 1 : zt);
     float* out = a.probs + (int64_t)row * K;
     if (mask_prior && zt != V) {
-        for (int j = tid; j < K; j += PT) out[j] = (j == zt) ? 1.f : 0.f;
+        const double keep = a.remask ? a.keep : 1.0, rm = a.remask ? a.rmask : 0.0;
+        for (int j = tid; j < K; j += PT) out[j] = (j == zt) ? (float)keep : (j == V ? (float)rm : 0.f);
         return;
     }
     const char* rowp = (const char*)a.logits + (size_t)row * (size_t)a.ld * sizeof(T);
@@ -305,11 +331,12 @@ __global__ __launch_bounds__(PT) void posterior_probs_kernel(PostArgs a) {
     if ((tid & 63) == 0) sh[tid >> 6] = sum;
     __syncthreads();
     const double lse = m + log(sh[0] + sh[1] + sh[2] + sh[3]);
-    double c_r = 0.0, Dn = 1.0;
+    double c_r = 0.0, Dn = 1.0, c_u = 0.0;
     if (!mask_prior) {
         const double xr = exp((double)Elem<T>::load1(rowp, zt) - lse);
-        c_r = a.Ka_t * xr + a.c_z;
+        c_r = a.Ka_r * xr + a.c_z;
         Dn = a.Ka_t * xr + a.one_m_at;
+        c_u = a.c_u + a.u1 * Dn;
     }
     for (int j = tid; j < K; j += PT) {
         double p;
@@ -317,10 +344,32 @@ __global__ __launch_bounds__(PT) void posterior_probs_kernel(PostArgs a) {
             p = (j < V) ? a.wx * exp((double)Elem<T>::load1(rowp, j) - lse) : a.wm;
         } else {
             const double x = exp((double)Elem<T>::load1(rowp, j) - lse);
-            p = (a.c_x * x + a.c_u + (j == zt ? c_r : 0.0)) / Dn;
+            p = (a.c_x * x + c_u + (j == zt ? c_r : 0.0)) / Dn;
         }
         out[j] = (float)p;
     }
+}
+
+// Keep-or-remask draws of all unmasked rows (masked prior, kappa < 1), one thread per row; masked
+// rows are left untouched (the posterior kernel draws them).
+__global__ __launch_bounds__(256) void remask_kernel(PostArgs a) {
+    const int row = blockIdx.x * 256 + threadIdx.x;
+    if (row >= a.rows) return;
+    int zt = a.z_t[row];
+    if (zt == a.V) return;
+    if (zt < 0 || zt > a.V) {   // flagged; ids past the mask count as masked (left to the posterior)
+        if (a.err) atomicOr(a.err, DD_DEVERR_TOKEN);
+        if (zt > a.V) return;
+        zt = 0;
+    }
+    a.z_s[row] = keep_or_remask(a, row, zt);
+}
+
+dd_status launch_remask(const PostArgs& a, hipStream_t s) {
+    if (a.rows == 0) return DD_OK;
+    ProfScope ps(KC_POSTERIOR, s);
+    hipLaunchKernelGGL(remask_kernel, dim3((a.rows + 255) / 256), dim3(256), 0, s, a);
+    return launch_status("remask");
 }
 
 // Ascending list of the rows whose token is the mask id, and its length (one workgroup: each thread

@@ -11,11 +11,15 @@ struct PostArgs {
     int32_t rows, V, prior;
     const int32_t* z_t;
     int32_t* z_s;
-    // masked prior: w_x, w_m and their logs
+    // masked prior, masked rows: p_v = w_x x_v, p_mask = w_m (and their logs)
     double log_wx, log_wm, wx, wm;
-    // uniform prior: c_x = a_s - a_t, c_u = (1 - a_{t|s})(1 - a_s)/K, c_z = a_{t|s} - a_t,
-    // Ka_t = K a_t, one_m_at = 1 - a_t
-    double c_x, c_u, c_z, Ka_t, one_m_at;
+    // masked prior, unmasked rows under a Psi transition with kappa < 1: keep the token with
+    // probability keep, remask with probability rmask (remask != 0 when rmask > 0)
+    double keep, rmask, log_keep, log_rmask;
+    int32_t remask;
+    // uniform prior: p_j = (c_x x_j + c_u + u1 D + [j == r](Ka_r x_r + c_z)) / D,
+    // D = Ka_t x_r + one_m_at
+    double c_x, c_u, u1, c_z, Ka_t, Ka_r, one_m_at;
     const uint32_t* noise;  // explicit words [rows][nu] or NULL (Philox)
     int32_t nu, ntop;
     uint64_t seed;
@@ -53,6 +57,8 @@ struct AttnArgs {
 };
 
 dd_status launch_posterior(const PostArgs& a, int logits_dtype, hipStream_t s);
+// keep-or-remask draw of every unmasked row (masked prior, kappa < 1), one thread per row
+dd_status launch_remask(const PostArgs& a, hipStream_t s);
 dd_status launch_latent(const int32_t* x, int32_t rows, int32_t V, double at, double sigma,
                         uint64_t seed, uint32_t step, uint32_t row0, int32_t* z, int32_t* err,
                         hipStream_t s);

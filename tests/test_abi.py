@@ -149,3 +149,18 @@ def test_pack_params_rejects_non_bf16_values():
     bad[0] = bad[0] + 1e-5
     with pytest.raises(ValueError):
         dd.pack_params(cfg, bad)
+
+
+def test_psi_entry_points_validate_kappa():
+    """kappa outside [0, 1] is rejected before anything reaches the GPU."""
+    L = dd.lib()
+    for kappa, status in ((-0.1, 1), (1.5, 1), (float("nan"), 1)):
+        assert L.dd_psi_posterior_sample(0, FAKE, 0, 64, 4, 32, FAKE, 0.2, 0.5, kappa, None, 0, 1, 0, FAKE,
+                                         None, None, None) == status
+    assert L.dd_psi_posterior_sample(0, None, 0, 64, 0, 32, None, 0.2, 0.5, 0.5, None, 0, 1, 0, None,
+                                     None, None, None) == 0      # zero rows: nothing to do
+    cfg = _cfg_struct()
+    al = (ctypes.c_double * 3)(1.0, 0.5, 0.0)
+    bad = (ctypes.c_double * 3)(1.0, 0.5, 2.0)
+    assert L.dd_psi_sample_loop(ctypes.byref(cfg), FAKE, 1, 16, 2, al, bad, FAKE, None, 0, None, FAKE,
+                                1 << 40, None) == 1

@@ -91,14 +91,14 @@ def test_forward_out_of_range_token_sets_error_word():
     assert dd.read_device_error(ws[:4].view(torch.int32)) == 0
 
 
-def _loop_gpu(torch, cfg, buf, z1, T, alphas, words=None, seed=0):
+def _loop_gpu(torch, cfg, buf, z1, T, alphas, words=None, seed=0, kappas=None):
     B, L = z1.shape
     z = dev_i32(torch, z1)
     trace = torch.zeros(((T + 1) * B * L,), dtype=torch.int32, device="cuda")
     ws = torch.zeros(dd.loop_workspace_bytes(cfg, B, L), dtype=torch.uint8, device="cuda")
     dd.sample_loop(cfg, buf, B, L, T, alphas, z, ws,
                    noise_words=dev_words(torch, words) if words is not None else None,
-                   noise_seed=seed, z_trace=trace)
+                   noise_seed=seed, z_trace=trace, kappas=kappas)
     assert dd.read_device_error(ws[:4].view(torch.int32)) == 0
     return z.cpu().numpy().reshape(B, L), trace.cpu().numpy().reshape(T + 1, B, L)
 
@@ -196,3 +196,57 @@ def test_compacted_loop_equals_full_path_loop(c, over, B, L, T):
         got = z.cpu().numpy().reshape(B, L)
         assert np.array_equal(got, trace[T - k + 1]), f"step {k}"
     say("masked per step", [(t == V).sum() for t in trace])
+
+
+# ---------------------------------------------------------------- Psi sampler loop (kappa < 1)
+
+def test_psi_loop_config1_free_running_matches_oracle():
+    """fp32 workload 1 with kappa = 0.5 at every step (App. A.4): decoded tokens can be remasked;
+    the whole loop on explicit noise, free running on both sides."""
+    torch = torch_or_skip()
+    cfg = workloads.model_cfg(1)
+    w, s = workloads.CONFIGS[1], workloads.seeds(1)
+    B, L, V, T = w["B"], w["L"], w["vocab"], w["T"]
+    P, buf = _params_seeded(torch, cfg, s["param"])
+    words = workloads.noise_words(s["noise"] + 1, (T, B * L, osampler.noise_width("mask", V)))
+    z1 = workloads.all_mask(B, L, V)
+    al = osched.alphas(T)
+    kap = np.full(T + 1, 0.5)
+    z0, trace = _loop_gpu(torch, cfg, buf, z1, T, al, words=words, kappas=kap)
+    rz0, rtrace, gaps = oloop.sample_loop(cfg, P, z1, T, al, noise_words=words, kappas=kap)
+    remasked = sum(int(((a != V) & (b == V)).sum()) for a, b in zip(trace[:-1], trace[1:]))
+    say(f"psi loop: min gap {np.min(gaps):.3e}; remasked {remasked}; agreement {np.mean(trace == rtrace):.6f}")
+    for k in range(T):
+        compare_ids(trace[k + 1].reshape(-1), rtrace[k + 1].reshape(-1), gaps[k], f"step {T - k}")
+    assert np.array_equal(z0, rz0)
+    assert remasked > 0 and (z0 != V).all()
+
+
+@pytest.mark.parametrize("kappa", [0.0, 0.4])
+def test_psi_compacted_loop_equals_full_path_loop(kappa):
+    """dd_psi_sample_loop (keep/remask of decoded rows, then the vocabulary projection and draw on
+    the still-masked rows) must give the same trajectory as dd_denoise_forward +
+    dd_psi_posterior_sample on every row."""
+    torch = torch_or_skip()
+    say("psi compacted loop", kappa)
+    cfg = workloads.model_cfg(2, n_layers=2)
+    V = cfg["vocab"]
+    B, L, T = 2, 300, 6
+    _, buf = _params_seeded(torch, cfg, 43)
+    z1 = workloads.all_mask(B, L, V)
+    al = osched.alphas(T)
+    kap = np.full(T + 1, kappa)
+    _, trace = _loop_gpu(torch, cfg, buf, z1, T, al, seed=78, kappas=kap)
+    M = B * L
+    ld = int(dd.logits_ld(V))
+    logits = torch.zeros((M, ld), dtype=torch.bfloat16, device="cuda")
+    ws = torch.zeros(dd.workspace_bytes(cfg, B, L), dtype=torch.uint8, device="cuda")
+    z = dev_i32(torch, z1)
+    for k in range(T, 0, -1):
+        dd.denoise_forward(cfg, buf, z, B, L, al[k], logits, ld, ws)
+        dd.psi_posterior_sample("mask", logits, "bf16", ld, M, V, z, al[k], al[k - 1], kappa, z, seed=78, step=k)
+        got = z.cpu().numpy().reshape(B, L)
+        assert np.array_equal(got, trace[T - k + 1]), f"step {k}"
+    remasked = sum(int(((a != V) & (b == V)).sum()) for a, b in zip(trace[:-1], trace[1:]))
+    say("masked per step", [(t == V).sum() for t in trace], "remasked", remasked)
+    assert remasked > 0 and (trace[-1] != V).all()

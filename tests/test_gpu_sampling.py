@@ -78,7 +78,7 @@ POST_CASES = [
 
 
 def _run_posterior(torch, prior, V, R, dt, noise, t, s, mf, scale, spikes, seed=5, step=3,
-                   want_probs=True, row0=0):
+                   want_probs=True, row0=0, kappa=None):
     at, as_ = 1.0 - t, 1.0 - s
     lv = round_to_dtype(workloads.synthetic_logits(seed, R, V, scale=scale, spike_frac=spikes), dt)
     if prior == "mask":
@@ -99,11 +99,17 @@ def _run_posterior(torch, prior, V, R, dt, noise, t, s, mf, scale, spikes, seed=
     else:
         nz = osampler.PhiloxNoise(seed + 3, step)
         wd = None
-    dd.posterior_sample(prior, lg, dt, ld, R, V, zt_d, at, as_, zs_d, noise_words=wd, seed=seed + 3,
-                        step=step, row0=row0, probs=probs)
     rows = np.arange(R) + row0
-    ref, gaps, rprobs = osampler.posterior_sample(prior, lv, zt, at, as_, nz, rows=rows,
-                                                  return_probs=True)
+    if kappa is None:
+        dd.posterior_sample(prior, lg, dt, ld, R, V, zt_d, at, as_, zs_d, noise_words=wd, seed=seed + 3,
+                            step=step, row0=row0, probs=probs)
+        ref, gaps, rprobs = osampler.posterior_sample(prior, lv, zt, at, as_, nz, rows=rows,
+                                                      return_probs=True)
+    else:
+        dd.psi_posterior_sample(prior, lg, dt, ld, R, V, zt_d, at, as_, kappa, zs_d, noise_words=wd,
+                                seed=seed + 3, step=step, row0=row0, probs=probs)
+        ref, gaps, rprobs = osampler.psi_sample(prior, lv, zt, at, as_, kappa, nz, rows=rows,
+                                                return_probs=True)
     return zt, zs_d.cpu().numpy(), ref, gaps, rprobs, (probs.cpu().numpy() if want_probs else None)
 
 
@@ -122,6 +128,69 @@ def test_posterior_parity(case):
         assert np.array_equal(got[keep], zt[keep])          # carry-over, bit exact
         assert np.all(got[~keep] <= V)
     assert np.all((got >= 0) & (got < (V + 1 if prior == "mask" else V)))
+
+
+PSI_CASES = [
+    # prior, V, rows, logit dtype, noise, t, s, mask fraction, logit scale, spikes, kappa
+    ("mask", 32, 256, "fp32", "explicit", 0.5, 0.375, 0.5, 2.0, 0.0, 0.0),
+    ("mask", 300, 256, "bf16", "philox", 0.6, 0.4, 0.5, 3.0, 0.01, 0.5),
+    ("mask", 50257, 48, "bf16", "philox", 0.75, 0.5, 0.6, 2.0, 0.0, 0.3),
+    ("uniform", 32, 128, "fp32", "explicit", 0.9, 0.8, 0.0, 2.0, 0.0, 0.0),
+    ("uniform", 1000, 64, "bf16", "philox", 0.3, 0.1, 0.0, 3.0, 0.01, 0.6),
+    ("uniform", 50257, 32, "bf16", "philox", 0.75, 0.5, 0.0, 2.0, 0.0, 0.25),
+]
+
+
+@pytest.mark.parametrize("case", PSI_CASES, ids=lambda c: f"{c[0]}-V{c[1]}-{c[3]}-{c[4]}-k{c[10]}")
+def test_psi_posterior_parity(case):
+    """App. A.4 Psi transition with kappa < 1 against the oracle on the same (device-rounded)
+    logits and noise; masked prior: unmasked rows keep their token or become the mask."""
+    torch = torch_or_skip()
+    say("psi posterior", case)
+    prior, V, kappa = case[0], case[1], case[10]
+    zt, got, ref, gaps, rprobs, gprobs = _run_posterior(torch, *case[:10], kappa=kappa)
+    compare_ids(got, ref, gaps, f"psi {prior} V={V} kappa={kappa}")
+    perr = float(np.abs(gprobs - rprobs).max())
+    say(f"max |dp| = {perr:.3e}")
+    assert perr <= PROB_TOL
+    if prior == "mask":
+        dec = zt != V
+        assert np.all((got[dec] == zt[dec]) | (got[dec] == V))
+        assert np.any(got[dec] == V)                       # some decoded tokens were remasked
+    assert np.all((got >= 0) & (got < (V + 1 if prior == "mask" else V)))
+
+
+def test_psi_at_kappa_one_equals_the_posterior_entry_point():
+    torch = torch_or_skip()
+    for case in (POST_CASES[2], POST_CASES[3], POST_CASES[8]):
+        say("psi kappa=1", case)
+        _, a, _, _, _, pa = _run_posterior(torch, *case)
+        _, b, _, _, _, pb = _run_posterior(torch, *case, kappa=1.0)
+        assert np.array_equal(a, b) and np.array_equal(pa, pb)
+
+
+def test_psi_explicit_words_equal_in_kernel_philox_and_unmasked_logits_unread():
+    torch = torch_or_skip()
+    V, R = 600, 96
+    lv = round_to_dtype(workloads.synthetic_logits(3, R, V, scale=0.5), "bf16")
+    zt = workloads.masked_state(4, 1, R, V, 0.5).reshape(-1)
+    ld = int(dd.logits_ld(V))
+    lg = logits_dev(torch, lv, "bf16", ld)
+    poisoned = lv.copy()
+    poisoned[zt != V] = np.nan
+    lp = logits_dev(torch, poisoned, "bf16", ld)
+    rows = np.arange(R)[:, None]
+    ntop = osampler.n_top("mask", V)
+    words = np.concatenate([ophilox.counter_words(5, ophilox.STREAM_TOP, 2, rows, np.arange(ntop)[None]),
+                            ophilox.counter_words(5, ophilox.STREAM_CLASS, 2, rows, np.arange(V)[None])], 1)
+    zd = dev_i32(torch, zt)
+    outs = []
+    for logits, wd in ((lg, None), (lg, dev_words(torch, words)), (lp, None)):
+        o = torch.empty(R, dtype=torch.int32, device="cuda")
+        dd.psi_posterior_sample("mask", logits, "bf16", ld, R, V, zd, 0.4, 0.6, 0.2, o, noise_words=wd,
+                                seed=5, step=2)
+        outs.append(o.cpu().numpy())
+    assert np.array_equal(outs[0], outs[1]) and np.array_equal(outs[0], outs[2])
 
 
 def test_posterior_row_offset_keys_noise_by_global_row():
