@@ -30,7 +30,7 @@ namespace dd {
 
 constexpr int PT = 256;       // threads per workgroup
 #ifndef DD_POST_TILE_IT
-#define DD_POST_TILE_IT 8
+#define DD_POST_TILE_IT 4
 #endif
 constexpr int TILE_IT = DD_POST_TILE_IT;   // 16-byte chunks per thread held in registers per tile
 static_assert(TILE_IT >= 1 && TILE_IT <= 32 && (TILE_IT & (TILE_IT - 1)) == 0,
@@ -73,14 +73,36 @@ template <> struct Elem<float> {
     DD_DEV static float load1(const void* p, int64_t i) { return ((const float*)p)[i]; }
 };
 
-// Wavefront argmax of (score, index); the lowest index wins ties; every lane gets the result.
-DD_DEV void wave_argmax(float& s, int& i) {
+// Wavefront maximum with DPP lane moves (VALU latency) instead of LDS-routed shuffles: two
+// quad permutations, the half-row and row mirrors (each row of 16 lanes then holds its maximum),
+// then the row broadcasts of lanes 15 and 31; lane 63 ends with the result.
+template <int CTRL, int ROW_MASK>
+DD_DEV float dpp_max(float v) {
+    const int m = __builtin_amdgcn_update_dpp(__float_as_int(v), __float_as_int(v), CTRL, ROW_MASK, 0xF, false);
+    return fmaxf(v, __int_as_float(m));
+}
+DD_DEV float wave_max_dpp(float v) {
+    v = dpp_max<0xB1, 0xF>(v);    // quad_perm [1, 0, 3, 2]
+    v = dpp_max<0x4E, 0xF>(v);    // quad_perm [2, 3, 0, 1]
+    v = dpp_max<0x141, 0xF>(v);   // row_half_mirror
+    v = dpp_max<0x140, 0xF>(v);   // row_mirror
+    v = dpp_max<0x142, 0xA>(v);   // row_bcast15 into rows 1 and 3
+    v = dpp_max<0x143, 0xC>(v);   // row_bcast31 into rows 2 and 3
+    return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 63));
+}
+
+// Wavefront argmax of (score, index); the lowest index wins ties; every lane gets the index.
+// (Values in and out, with selects: by-reference updates inside branches ended up in scratch.)
+DD_DEV int wave_argmax(float s, int i) {
 #pragma unroll
     for (int o = 32; o > 0; o >>= 1) {
         const float s2 = __shfl_xor(s, o, 64);
         const int i2 = __shfl_xor(i, o, 64);
-        if (s2 > s || (s2 == s && i2 < i)) { s = s2; i = i2; }
+        const bool take = s2 > s || (s2 == s && i2 < i);
+        s = take ? s2 : s;
+        i = take ? i2 : i;
     }
+    return i;
 }
 
 // Keep-or-remask draw of an unmasked row (masked prior, kappa < 1): the two-level draw over a
@@ -141,8 +163,9 @@ __global__ __launch_bounds__(PT) void posterior_kernel(PostArgs a) {
     // partial sums (one per iteration, i.e. per group slice); a butterfly over the LPG lanes of a
     // group halves the list at every step, so TILE_IT sums cost log2(LPG) steps and TILE_IT
     // shuffles in total instead of TILE_IT * log2(LPG).
-    for (int tile0 = 0; tile0 < nchunk; tile0 += TILE_IT * PT) {
-        uint4 buf[TILE_IT];
+    // tiles of TILE_IT * PT chunks; the loads of the next tile are issued before the current one
+    // is reduced (two register buffers), so a wavefront always has a tile in flight
+    auto load_tile = [&](uint4 (&buf)[TILE_IT], const int tile0) {
         if ((tile0 + TILE_IT * PT) * E <= V) {   // every element of the tile is in the row
 #pragma unroll
             for (int it = 0; it < TILE_IT; ++it)
@@ -160,12 +183,14 @@ __global__ __launch_bounds__(PT) void posterior_kernel(PostArgs a) {
                     if (tile0 + it * PT + tid == nchunk - 1) Elem<T>::clip(buf[it], V % E);
             }
         }
+    };
+    auto reduce_tile = [&](uint4 (&buf)[TILE_IT], const int tile0) {
         float m = -INFINITY;
 #pragma unroll
         for (int it = 0; it < TILE_IT; ++it)
 #pragma unroll
             for (int e = 0; e < E; ++e) m = fmaxf(m, Elem<T>::get(buf[it], e));
-        m = wave_max(m);
+        m = wave_max_dpp(m);
         const float mref = (m == -INFINITY) ? 0.f : m;
         const float moff = -mref * LOG2E;
         float v[TILE_IT];
@@ -204,6 +229,17 @@ __global__ __launch_bounds__(PT) void posterior_kernel(PostArgs a) {
             const int c = tile0 + idx * PT + (tid & ~(LPG - 1));
             if (c < nchunk) s_lse[c / LPG] = mref + logf(v[0]);
         }
+    };
+    constexpr int TS = TILE_IT * PT;
+    uint4 ba[TILE_IT], bb[TILE_IT];
+    load_tile(ba, 0);
+    for (int t0 = 0; t0 < nchunk; t0 += 2 * TS) {
+        const bool next_b = t0 + TS < nchunk;
+        if (next_b) load_tile(bb, t0 + TS);
+        reduce_tile(ba, t0);
+        if (!next_b) break;
+        if (t0 + 2 * TS < nchunk) load_tile(ba, t0 + 2 * TS);
+        reduce_tile(bb, t0 + TS);
     }
     __syncthreads();
 
@@ -241,16 +277,18 @@ __global__ __launch_bounds__(PT) void posterior_kernel(PostArgs a) {
             if (base >= a.ntop) break;
             uint32_t wd[4];
             if (a.noise) {
+#pragma unroll
                 for (int i = 0; i < 4; ++i)
                     wd[i] = (base + i < a.ntop) ? a.noise[(int64_t)row * a.nu + base + i] : 0u;
             } else {
                 const Words4 W = philox4x32_10((uint32_t)(base >> 2), grow, a.step, STREAM_TOP, k0, k1);
+#pragma unroll
                 for (int i = 0; i < 4; ++i) wd[i] = W.w[i];
             }
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
                 const int g = base + i;
-                if (g >= a.ntop) break;
+                if (g >= a.ntop) continue;
                 float logm;
                 if (mask_prior) {
                     logm = (g < ngroups) ? log_wx + (s_lse[g] - lse) : log_wm;
@@ -261,11 +299,12 @@ __global__ __launch_bounds__(PT) void posterior_kernel(PostArgs a) {
                     logm = logf(c_x * X + (float)n * c_u + ((zt >= lo && zt < lo + n) ? c_r : 0.f)) - log_dn;
                 }
                 const float sc = logm + word_gumbel_f(wd[i]);
-                if (sc > best || (sc == best && g < bi)) { best = sc; bi = g; }
+                const bool take = sc > best || (sc == best && g < bi);
+                best = take ? sc : best;
+                bi = take ? g : bi;
             }
         }
-        wave_argmax(best, bi);
-        const int gstar = bi;
+        const int gstar = wave_argmax(best, bi);
 
         int result = V;
         if (!(mask_prior && gstar == ngroups)) {   // level 2 inside the chosen group
@@ -275,26 +314,29 @@ __global__ __launch_bounds__(PT) void posterior_kernel(PostArgs a) {
             if (base < V) {
                 uint32_t wd[4];
                 if (a.noise) {
+#pragma unroll
                     for (int i = 0; i < 4; ++i)
                         wd[i] = (base + i < V) ? a.noise[(int64_t)row * a.nu + a.ntop + base + i] : 0u;
                 } else {
                     const Words4 W = philox4x32_10((uint32_t)(base >> 2), grow, a.step, STREAM_CLASS, k0, k1);
+#pragma unroll
                     for (int i = 0; i < 4; ++i) wd[i] = W.w[i];
                 }
 #pragma unroll
                 for (int i = 0; i < 4; ++i) {
                     const int j = base + i;
-                    if (j >= V) break;
+                    if (j >= V) continue;
                     const float l = Elem<T>::load1(rowp, j);
                     float logp;
                     if (mask_prior) logp = log_wx + (l - lse);
                     else logp = logf(c_x * expf(l - lse) + c_u + (j == zt ? c_r : 0.f)) - log_dn;
                     const float sc = logp + word_gumbel_f(wd[i]);
-                    if (sc > best || (sc == best && j < bi)) { best = sc; bi = j; }
+                    const bool take = sc > best || (sc == best && j < bi);
+                    best = take ? sc : best;
+                    bi = take ? j : bi;
                 }
             }
-            wave_argmax(best, bi);
-            result = bi;
+            result = wave_argmax(best, bi);
         }
         if (lane == 0) a.z_s[row] = result;
     }

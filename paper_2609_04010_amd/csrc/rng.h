@@ -46,9 +46,11 @@ DD_DEV Words4 philox4x32_10(uint32_t c0, uint32_t c1, uint32_t c2, uint32_t c3,
 // Word for (stream, step, row, index): counter (index >> 2, row, step, stream), word index & 3.
 DD_DEV uint32_t counter_word(uint64_t seed, uint32_t stream, uint32_t step, uint32_t row,
                              uint32_t index) {
-    Words4 b = philox4x32_10(index >> 2, row, step, stream, (uint32_t)seed,
-                             (uint32_t)(seed >> 32));
-    return b.w[index & 3u];
+    const Words4 b = philox4x32_10(index >> 2, row, step, stream, (uint32_t)seed,
+                                   (uint32_t)(seed >> 32));
+    // selects, not an indexed load: a runtime index into the array would put it in scratch memory
+    const uint32_t i = index & 3u;
+    return i == 0 ? b.w[0] : i == 1 ? b.w[1] : i == 2 ? b.w[2] : b.w[3];
 }
 
 DD_DEV double word_exponential(uint32_t w) {
