@@ -25,6 +25,7 @@ STREAM_TOP = 0      # group-level Gumbels of the two-level sampler
 STREAM_CLASS = 1    # per-class Gumbels of the two-level sampler
 STREAM_LATENT = 2   # Gaussian latents (uniform-state start / probes)
 STREAM_PARAM = 3    # parameter initialisation
+STREAM_VERIFY = 4   # acceptance uniforms of speculative verification
 
 
 def philox_scalar(ctr, key, rounds=10):

@@ -102,3 +102,35 @@ def test_chi2_pin_catches_gumbel_sign(monkeypatch):
 def test_kat_pin_catches_wrong_multiplier(monkeypatch):
     monkeypatch.setattr(philox, "_M0", 0xD2511F55)
     assert philox.philox_scalar((0, 0, 0, 0), (0, 0))[0] != 0x6627e8d5
+
+
+def test_lossless_pin_catches_a_wrong_residual(monkeypatch):
+    """Replacing the residual [p - q]_+ by [q - p]_+, or by p itself, must break the lossless
+    chi-square pin of the speculative verification."""
+    from oracle import verify
+    from tests import test_oracle_verify as tv
+
+    def make_wrong(kind):
+        def wrong_verify_one(p_logits, q_logits, draft, seq, nz):
+            B, V = p_logits.shape
+            u = verify.word_uniform(nz.accept(seq, B - 1))
+            n = B
+            for i in range(B - 1):
+                p, q = verify._softmax(p_logits[i]), verify._softmax(q_logits[i])
+                if u[i] > min(1.0, p[draft[i]] / q[draft[i]]):
+                    n = i + 1
+                    break
+            if n == B:
+                dist = verify._softmax(p_logits[B - 1])
+            else:
+                p, q = verify._softmax(p_logits[n - 1]), verify._softmax(q_logits[n - 1])
+                dist = np.maximum(q - p, 0.0) if kind == "swapped" else p
+                dist = dist / dist.sum()
+            z, g1, g2 = sampler.sample_from_probs("uniform", dist, seq, nz)
+            return n, z, None, (g1, g2)
+        return wrong_verify_one
+
+    for kind in ("swapped", "plain_p"):
+        monkeypatch.setattr(verify, "verify_one", make_wrong(kind))
+        with pytest.raises(AssertionError):
+            tv.test_first_emitted_token_is_distributed_as_the_target()
