@@ -244,6 +244,42 @@ dd_status dd_psi_sample_loop(const dd_config* cfg, const void* params, int32_t B
                              int32_t* z_trace, void* ws, size_t ws_bytes, void* stream);
 
 /*
+ * dd_spec_verify - speculative verification of S drafted blocks (Alg. 1,
+ * linear sampler; the rejection correction of speculative decoding).
+ *   p_logits     device [S*B][ld] target logits: row s*B + i is p_{i+1} of
+ *                sequence s (the last row of a block gives the bonus draw)
+ *   q_logits     device [S*(B-1)][ld] draft logits, row s*(B-1) + i is q_{i+1}
+ *   draft        device int32 [S][B-1], the drafted tokens x_i (drawn from q_i)
+ *   logits_dtype bf16 or fp32; ld >= V, ld % 8 == 0; B >= 1 (q_logits and draft
+ *                may be NULL when B == 1)
+ *   noise_words  NULL: Philox under `seed` — acceptance uniform u_i from the word
+ *                (i >> 2, row0 + s, step, 4), the draw's words as for the
+ *                posterior (streams 0 and 1, row row0 + s); otherwise device
+ *                uint32 [S][dd_spec_verify_noise_width(B, V)]: B - 1
+ *                acceptance words, then the draw's level-1 and level-2 words.
+ *   n_out        device int32 [S]: n = the first i (1-based) with
+ *                u_i > min(1, p_i(x_i) / q_i(x_i)), or B if none; the block
+ *                keeps x_1 .. x_{n-1}
+ *   z_out        device int32 [S]: the token that follows them, drawn from
+ *                Norm([p_n - q_n]_+) (from p_n if that has no mass) when n < B
+ *                and from p_B when n == B, by the two-level Gumbel-max draw
+ *   ws           device scratch >= dd_spec_verify_workspace_bytes(S, B) (row
+ *                log-sum-exps)
+ *   dev_err      NULL or device int32 error word (DD_DEVERR_TOKEN for a draft
+ *                token outside [0, V), which is clamped).
+ * Arithmetic in fp32.  Each emitted token is distributed as the target (the
+ * tokens per verification forward pass are (n + 1) / 2 with the block's
+ * always-accepted first token counted, between 1 and (B + 1) / 2).
+ */
+size_t dd_spec_verify_workspace_bytes(int32_t S, int32_t B);
+int32_t dd_spec_verify_noise_width(int32_t B, int32_t V);
+dd_status dd_spec_verify(const void* p_logits, const void* q_logits, int32_t logits_dtype,
+                         int64_t ld, int32_t S, int32_t B, int32_t V, const int32_t* draft,
+                         const uint32_t* noise_words, uint64_t seed, uint32_t step,
+                         uint32_t row0, int32_t* n_out, int32_t* z_out, void* ws,
+                         size_t ws_bytes, int32_t* dev_err, void* stream);
+
+/*
  * dd_gaussian_latent_argmax - z = argmax_v (alpha_tilde [v == x] + sigma eps_v)
  * per row (App. A.5: uniform-state diffusion is the argmax projection of a
  * Gaussian diffusion on one-hot vectors).  eps_v = Phi^-1(u) of the Philox word

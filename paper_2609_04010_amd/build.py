@@ -15,7 +15,7 @@ BUILD = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libdd.so")
 
 SOURCES = ["dd_api.hip", "k_posterior.hip", "k_latent_init.hip", "k_norm.hip", "k_gemm.hip",
-           "k_attn.hip"]
+           "k_attn.hip", "k_verify.hip"]
 
 # Per-file extra flags.  Attention keeps its MFMA accumulators in ordinary VGPRs (the softmax reads
 # every score with VALU instructions; AGPR accumulators would need a copy per score).  The GEMMs need

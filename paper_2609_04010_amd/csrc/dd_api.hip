@@ -511,6 +511,42 @@ dd_status dd_sample_loop(const dd_config* cfg, const void* params, int32_t B, in
                               ws, ws_bytes, stream);
 }
 
+size_t dd_spec_verify_workspace_bytes(int32_t S, int32_t B) {
+    if (S <= 0 || B <= 0) return 0;
+    return ((size_t)S * (2 * (size_t)B - 1) * sizeof(float) + 255) & ~(size_t)255;
+}
+
+int32_t dd_spec_verify_noise_width(int32_t B, int32_t V) {
+    return (B - 1) + ntop_of(DD_PRIOR_UNIFORM, V) + V;
+}
+
+dd_status dd_spec_verify(const void* p_logits, const void* q_logits, int32_t logits_dtype, int64_t ld,
+                         int32_t S, int32_t B, int32_t V, const int32_t* draft,
+                         const uint32_t* noise_words, uint64_t seed, uint32_t step, uint32_t row0,
+                         int32_t* n_out, int32_t* z_out, void* ws, size_t ws_bytes, int32_t* dev_err,
+                         void* stream) {
+    DD_CHECK(logits_dtype == DD_BF16 || logits_dtype == DD_FP32, DD_E_DTYPE, "unknown logits dtype");
+    DD_CHECK(S >= 0 && B >= 1 && V > 0, DD_E_ARG, "need S >= 0, B >= 1 and V > 0");
+    DD_CHECK(V <= (1 << 24), DD_E_UNSUPPORTED, "V > 2^24 unsupported");
+    DD_CHECK((int64_t)S * (2 * (int64_t)B - 1) <= INT32_MAX, DD_E_UNSUPPORTED, "too many rows");
+    DD_CHECK(ld >= V && ld % 8 == 0, DD_E_SHAPE, "ld must be >= V and a multiple of 8");
+    if (S == 0) return DD_OK;
+    DD_CHECK(p_logits && n_out && z_out && ws, DD_E_ARG, "NULL pointer argument");
+    DD_CHECK(B == 1 || (q_logits && draft), DD_E_ARG, "B > 1 needs draft logits and tokens");
+    const size_t need = dd_spec_verify_workspace_bytes(S, B);
+    DD_CHECK(ws_bytes >= need, DD_E_WORKSPACE, "workspace has %zu bytes, needs %zu", ws_bytes, need);
+    VerifyArgs a;
+    memset(&a, 0, sizeof(a));
+    a.p = p_logits; a.q = q_logits; a.ld = ld;
+    a.S = S; a.B = B; a.V = V;
+    a.draft = draft;
+    a.noise = noise_words;
+    a.nu = dd_spec_verify_noise_width(B, V);
+    a.seed = seed; a.step = step; a.row0 = row0;
+    a.n_out = n_out; a.z_out = z_out; a.err = dev_err;
+    return launch_verify(a, logits_dtype, (float*)ws, (hipStream_t)stream);
+}
+
 dd_status dd_gaussian_latent_argmax(const int32_t* x, int32_t rows, int32_t V, double alpha_tilde,
                                     double sigma, uint64_t seed, uint32_t step, uint32_t row0,
                                     int32_t* z_out, int32_t* dev_err, void* stream) {

@@ -23,6 +23,7 @@
 //   c_x = a_s - a_t, c_z = a_{t|s} - a_t, c_u = (1 - a_{t|s})(1 - a_s)/K, u1 = 0, Ka_r = K a_t.
 #include <math.h>
 
+#include "elem.h"
 #include "kernels.h"
 #include "rng.h"
 
@@ -35,43 +36,6 @@ constexpr int PT = 256;       // threads per workgroup
 constexpr int TILE_IT = DD_POST_TILE_IT;   // 16-byte chunks per thread held in registers per tile
 static_assert(TILE_IT >= 1 && TILE_IT <= 32 && (TILE_IT & (TILE_IT - 1)) == 0,
               "the group butterfly needs a power of two no larger than the lanes of a group");
-constexpr float LOG2E = 1.4426950408889634f;
-
-template <typename T> struct Elem;
-template <> struct Elem<bf16_t> {
-    static constexpr int E = 8;  // elements per 16-byte chunk
-    static constexpr uint4 NEG_INF4 = {0xFF80FF80u, 0xFF80FF80u, 0xFF80FF80u, 0xFF80FF80u};
-    // elements n.. of the chunk become -inf (0 < n < E)
-    DD_DEV static void clip(uint4& c, int n) {
-        uint32_t w[4] = {c.x, c.y, c.z, c.w};
-#pragma unroll
-        for (int k = 0; k < 4; ++k) {
-            const uint32_t hi_cut = (w[k] & 0xFFFFu) | 0xFF800000u;
-            w[k] = (2 * k + 1 < n) ? w[k] : (2 * k < n) ? hi_cut : 0xFF80FF80u;
-        }
-        c = make_uint4(w[0], w[1], w[2], w[3]);
-    }
-    DD_DEV static float get(const uint4& c, int e) {
-        const uint32_t w = (e < 2) ? c.x : (e < 4) ? c.y : (e < 6) ? c.z : c.w;
-        return (e & 1) ? bf16_hi(w) : bf16_lo(w);
-    }
-    DD_DEV static float load1(const void* p, int64_t i) { return bf16_to_f32(((const bf16_t*)p)[i]); }
-};
-template <> struct Elem<float> {
-    static constexpr int E = 4;
-    static constexpr uint4 NEG_INF4 = {0xFF800000u, 0xFF800000u, 0xFF800000u, 0xFF800000u};
-    DD_DEV static void clip(uint4& c, int n) {
-        uint32_t w[4] = {c.x, c.y, c.z, c.w};
-#pragma unroll
-        for (int k = 0; k < 4; ++k) w[k] = (k < n) ? w[k] : 0xFF800000u;
-        c = make_uint4(w[0], w[1], w[2], w[3]);
-    }
-    DD_DEV static float get(const uint4& c, int e) {
-        const uint32_t w = (e == 0) ? c.x : (e == 1) ? c.y : (e == 2) ? c.z : c.w;
-        return __uint_as_float(w);
-    }
-    DD_DEV static float load1(const void* p, int64_t i) { return ((const float*)p)[i]; }
-};
 
 // Wavefront maximum with DPP lane moves (VALU latency) instead of LDS-routed shuffles: two
 // quad permutations, the half-row and row mirrors (each row of 16 lanes then holds its maximum),

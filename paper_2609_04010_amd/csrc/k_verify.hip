@@ -1,0 +1,219 @@
+// Speculative verification of drafted blocks (Alg. 1, linear sampler).
+//
+// For sequence s the target logits p_1..p_B and the draft logits q_1..q_{B-1} are rows of two
+// [rows][ld] matrices, the drafted tokens x_1..x_{B-1} a [S][B-1] array.  With acceptance uniforms
+// u_i (word (STREAM_VERIFY, step, row0 + s, i)):
+//   n = first i with u_i > min(1, p_i(x_i) / q_i(x_i)), else B
+//   z ~ Norm([p_n - q_n]_+) if n < B, else z ~ p_B     (p_n itself if the residual has no mass)
+// z is drawn with the two-level Gumbel-max of the posterior kernel (groups of DD_GUMBEL_GROUP
+// classes, no mask group): the draw is invariant to the normaliser, so group masses and class
+// scores use the unnormalised residual.
+//
+// Kernel 1 (one workgroup per logit row): row log-sum-exp in fp32.
+// Kernel 2 (one workgroup per sequence): n from the B - 1 acceptance tests, then one pass over the
+// chosen row pair for the group masses and the two-level draw.
+#include <math.h>
+
+#include "elem.h"
+#include "kernels.h"
+#include "rng.h"
+
+namespace dd {
+
+namespace {
+
+constexpr int VT = 256;   // threads per workgroup
+
+DD_DEV float block_reduce(float v, bool is_max, float* sh) {
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    v = is_max ? wave_max(v) : wave_sum(v);
+    if (lane == 0) sh[wave] = v;
+    __syncthreads();
+    float r = sh[0];
+#pragma unroll
+    for (int w = 1; w < VT / 64; ++w) r = is_max ? fmaxf(r, sh[w]) : r + sh[w];
+    __syncthreads();
+    return r;
+}
+
+// Row r < S B is target row r; otherwise draft row r - S B.
+template <typename T>
+__global__ __launch_bounds__(VT) void row_lse_kernel(VerifyArgs a, float* lse) {
+    __shared__ float sh[VT / 64];
+    constexpr int E = Elem<T>::E;
+    const int r = blockIdx.x;
+    const int np = a.S * a.B;
+    const char* rowp = r < np ? (const char*)a.p + (size_t)r * a.ld * sizeof(T)
+                              : (const char*)a.q + (size_t)(r - np) * a.ld * sizeof(T);
+    const int V = a.V, nchunk = (V + E - 1) / E;
+    float m = -INFINITY;
+    for (int c = threadIdx.x; c < nchunk; c += VT) {
+        const uint4 x = *(const uint4*)(rowp + (size_t)c * 16);
+#pragma unroll
+        for (int e = 0; e < E; ++e)
+            if (c * E + e < V) m = fmaxf(m, Elem<T>::get(x, e));
+    }
+    m = block_reduce(m, true, sh);
+    const float mref = isinf(m) ? 0.f : m;
+    float sum = 0.f;
+    for (int c = threadIdx.x; c < nchunk; c += VT) {
+        const uint4 x = *(const uint4*)(rowp + (size_t)c * 16);
+#pragma unroll
+        for (int e = 0; e < E; ++e)
+            if (c * E + e < V) sum += __builtin_amdgcn_exp2f((Elem<T>::get(x, e) - mref) * LOG2E);
+    }
+    sum = block_reduce(sum, false, sh);
+    if (threadIdx.x == 0) lse[r] = mref + logf(sum);
+}
+
+DD_DEV uint32_t verify_word(const VerifyArgs& a, int s, uint32_t stream, int idx, int explicit_off) {
+    if (a.noise) return a.noise[(int64_t)s * a.nu + explicit_off + idx];
+    return counter_word(a.seed, stream, a.step, a.row0 + (uint32_t)s, (uint32_t)idx);
+}
+
+DD_DEV float word_uniform_f(uint32_t w) { return ((float)w + 0.5f) * 0x1p-32f; }
+
+template <typename T>
+__global__ __launch_bounds__(VT) void verify_kernel(VerifyArgs a, const float* lse) {
+    extern __shared__ float s_mass[];   // one mass per group
+    __shared__ int sh_n;
+    __shared__ float sh_tot[VT / 64];
+    constexpr int E = Elem<T>::E;
+    constexpr int LPG = DD_GUMBEL_GROUP / E;   // chunks (lanes) per group
+    const int s = blockIdx.x, tid = threadIdx.x, lane = tid & 63;
+    const int B = a.B, V = a.V;
+    const int ngroups = (V + DD_GUMBEL_GROUP - 1) / DD_GUMBEL_GROUP;
+    const float* lse_p = lse + (size_t)s * B;
+    const float* lse_q = lse + (size_t)a.S * B + (size_t)s * (B - 1);
+    auto prow = [&](int i) { return (const char*)a.p + ((size_t)s * B + i) * a.ld * sizeof(T); };
+    auto qrow = [&](int i) { return (const char*)a.q + ((size_t)s * (B - 1) + i) * a.ld * sizeof(T); };
+
+    // ---- acceptance: the first rejected draft position (1-based), or B ----
+    if (tid == 0) {
+        int n = B;
+        for (int i = 0; i < B - 1; ++i) {
+            int x = a.draft[(int64_t)s * (B - 1) + i];
+            if (x < 0 || x >= V) {
+                if (a.err) atomicOr(a.err, DD_DEVERR_TOKEN);
+                x = x < 0 ? 0 : V - 1;
+            }
+            const float lp = Elem<T>::load1(prow(i), x) - lse_p[i];
+            const float lq = Elem<T>::load1(qrow(i), x) - lse_q[i];
+            const float ratio = fminf(1.f, __builtin_amdgcn_exp2f((lp - lq) * LOG2E));
+            const float u = word_uniform_f(verify_word(a, s, STREAM_VERIFY, i, 0));
+            if (u > ratio) { n = i + 1; break; }
+        }
+        sh_n = n;
+    }
+    __syncthreads();
+    const int n = sh_n;
+    const bool resid = n < B;
+    const char* pr = prow(n - 1);
+    const char* qr = resid ? qrow(n - 1) : nullptr;
+    const float lp0 = lse_p[n - 1], lq0 = resid ? lse_q[n - 1] : 0.f;
+
+    // unnormalised class mass: [p - q]_+ for a rejection, p for the bonus (use_p: residual empty)
+    auto cls_mass = [&](float lpv, float lqv, bool use_p) -> float {
+        const float ep = __builtin_amdgcn_exp2f((lpv - lp0) * LOG2E);
+        if (!resid || use_p) return ep;
+        return fmaxf(ep - __builtin_amdgcn_exp2f((lqv - lq0) * LOG2E), 0.f);
+    };
+
+    // ---- group masses: lanes of a group hold consecutive chunks; reduce over LPG lanes ----
+    const int nchunk = (V + E - 1) / E;
+    auto masses = [&](bool use_p) -> float {
+        float tot = 0.f;
+        for (int c0 = 0; c0 < nchunk; c0 += VT) {
+            const int c = c0 + tid;
+            float sum = 0.f;
+            if (c < nchunk) {
+                const uint4 xp = *(const uint4*)(pr + (size_t)c * 16);
+                uint4 xq = make_uint4(0u, 0u, 0u, 0u);
+                if (resid && !use_p) xq = *(const uint4*)(qr + (size_t)c * 16);
+#pragma unroll
+                for (int e = 0; e < E; ++e)
+                    if (c * E + e < V) sum += cls_mass(Elem<T>::get(xp, e), Elem<T>::get(xq, e), use_p);
+            }
+#pragma unroll
+            for (int o = 1; o < LPG; o <<= 1) sum += __shfl_xor(sum, o, 64);
+            if ((lane & (LPG - 1)) == 0 && c < nchunk) s_mass[c / LPG] = sum;
+            tot += ((lane & (LPG - 1)) == 0 && c < nchunk) ? sum : 0.f;
+        }
+        tot = wave_sum(tot);
+        if (lane == 0) sh_tot[tid >> 6] = tot;
+        __syncthreads();
+        float t = 0.f;
+#pragma unroll
+        for (int w = 0; w < VT / 64; ++w) t += sh_tot[w];
+        __syncthreads();
+        return t;
+    };
+    bool use_p = false;
+    if (!(masses(false) > 0.f)) {   // empty residual: draw from p_n
+        use_p = true;
+        masses(true);
+    }
+
+    // ---- two-level draw (one wavefront) ----
+    if ((tid >> 6) != 0) return;
+    float best = -INFINITY;
+    int bi = 0x7FFFFFFF;
+    for (int g = lane; g < ngroups; g += 64) {
+        const float sc = logf(s_mass[g]) + word_gumbel_f(verify_word(a, s, STREAM_TOP, g, B - 1));
+        const bool take = sc > best || (sc == best && g < bi);
+        best = take ? sc : best;
+        bi = take ? g : bi;
+    }
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) {
+        const float s2 = __shfl_xor(best, o, 64);
+        const int i2 = __shfl_xor(bi, o, 64);
+        const bool take = s2 > best || (s2 == best && i2 < bi);
+        best = take ? s2 : best;
+        bi = take ? i2 : bi;
+    }
+    const int gstar = bi;
+    best = -INFINITY;
+    bi = 0x7FFFFFFF;
+    const int ntop = ngroups;
+    for (int j = gstar * DD_GUMBEL_GROUP + lane; j < min(V, (gstar + 1) * DD_GUMBEL_GROUP); j += 64) {
+        const float lpv = Elem<T>::load1(pr, j);
+        const float lqv = (resid && !use_p) ? Elem<T>::load1(qr, j) : 0.f;
+        const float sc = logf(cls_mass(lpv, lqv, use_p)) +
+                         word_gumbel_f(verify_word(a, s, STREAM_CLASS, j, B - 1 + ntop));
+        const bool take = sc > best || (sc == best && j < bi);
+        best = take ? sc : best;
+        bi = take ? j : bi;
+    }
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) {
+        const float s2 = __shfl_xor(best, o, 64);
+        const int i2 = __shfl_xor(bi, o, 64);
+        const bool take = s2 > best || (s2 == best && i2 < bi);
+        best = take ? s2 : best;
+        bi = take ? i2 : bi;
+    }
+    if (lane == 0) {
+        a.n_out[s] = n;
+        a.z_out[s] = bi;
+    }
+}
+
+}  // namespace
+
+dd_status launch_verify(const VerifyArgs& a, int logits_dtype, float* lse, hipStream_t s) {
+    if (a.S == 0) return DD_OK;
+    const int rows = a.S * (2 * a.B - 1);
+    const int ngroups = (a.V + DD_GUMBEL_GROUP - 1) / DD_GUMBEL_GROUP;
+    const size_t shmem = (size_t)ngroups * sizeof(float);
+    if (logits_dtype == DD_BF16) {
+        hipLaunchKernelGGL(row_lse_kernel<bf16_t>, dim3(rows), dim3(VT), 0, s, a, lse);
+        hipLaunchKernelGGL(verify_kernel<bf16_t>, dim3(a.S), dim3(VT), shmem, s, a, (const float*)lse);
+    } else {
+        hipLaunchKernelGGL(row_lse_kernel<float>, dim3(rows), dim3(VT), 0, s, a, lse);
+        hipLaunchKernelGGL(verify_kernel<float>, dim3(a.S), dim3(VT), shmem, s, a, (const float*)lse);
+    }
+    return launch_status("spec_verify");
+}
+
+}  // namespace dd

@@ -59,6 +59,24 @@ struct AttnArgs {
 dd_status launch_posterior(const PostArgs& a, int logits_dtype, hipStream_t s);
 // keep-or-remask draw of every unmasked row (masked prior, kappa < 1), one thread per row
 dd_status launch_remask(const PostArgs& a, hipStream_t s);
+
+// Speculative verification: target rows p [S*B][ld], draft rows q [S*(B-1)][ld], drafted tokens
+// [S][B-1]; outputs n (first rejected position, 1-based, or B) and the replacement / bonus token.
+struct VerifyArgs {
+    const void* p;
+    const void* q;
+    int64_t ld;
+    int32_t S, B, V;
+    const int32_t* draft;
+    const uint32_t* noise;  // explicit words [S][nu] or NULL (Philox)
+    int32_t nu;
+    uint64_t seed;
+    uint32_t step, row0;
+    int32_t* n_out;
+    int32_t* z_out;
+    int32_t* err;
+};
+dd_status launch_verify(const VerifyArgs& a, int logits_dtype, float* lse, hipStream_t s);
 dd_status launch_latent(const int32_t* x, int32_t rows, int32_t V, double at, double sigma,
                         uint64_t seed, uint32_t step, uint32_t row0, int32_t* z, int32_t* err,
                         hipStream_t s);

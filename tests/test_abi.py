@@ -164,3 +164,24 @@ def test_psi_entry_points_validate_kappa():
     bad = (ctypes.c_double * 3)(1.0, 0.5, 2.0)
     assert L.dd_psi_sample_loop(ctypes.byref(cfg), FAKE, 1, 16, 2, al, bad, FAKE, None, 0, None, FAKE,
                                 1 << 40, None) == 1
+
+
+def test_spec_verify_validation_and_sizes():
+    from oracle import verify as overify
+    L = dd.lib()
+    args = lambda **k: dict(dict(p=FAKE, q=FAKE, dt=0, ld=64, S=4, B=3, V=32, draft=FAKE, noise=None, seed=0,
+                                 step=0, row0=0, n=FAKE, z=FAKE, ws=FAKE, wsb=1 << 20, err=None), **k)
+
+    def call(**k):
+        a = args(**k)
+        return L.dd_spec_verify(a["p"], a["q"], a["dt"], a["ld"], a["S"], a["B"], a["V"], a["draft"], a["noise"],
+                                a["seed"], a["step"], a["row0"], a["n"], a["z"], a["ws"], a["wsb"], a["err"], None)
+    assert call(dt=7) == 3
+    assert call(B=0) == 1
+    assert call(ld=30) == 2 and call(ld=36) == 2
+    assert call(wsb=8) == 4
+    assert call(q=None) == 1                       # B > 1 needs draft logits
+    assert call(S=0, p=None, n=None, z=None, ws=None) == 0
+    assert dd.spec_verify_workspace_bytes(4, 3) == 256 and dd.spec_verify_workspace_bytes(100, 8) == 6144
+    for B, V in ((1, 32), (4, 300), (16, 50257)):
+        assert dd.spec_verify_noise_width(B, V) == overify.noise_width(B, V)
