@@ -11,7 +11,7 @@ GPT-2-shaped, non-causal transformer.  This build's reading:
   temb_j = sin(tau w_j) (j < d/2), cos(tau w_{j-d/2}) (j >= d/2),
            w_i = 10000 ** (-i / (d/2)), tau = 1000 (1 - alpha_t)
   per layer:  a = LN1(h); [q|k|v] = a W_qkv^T + b_qkv
-              h += softmax(q k^T / sqrt(dh)) v  W_o^T + b_o   (no mask, per head)
+              h += softmax(q k^T / sqrt(dh)) v  W_o^T + b_o   (per head)
               a = LN2(h); h += gelu_tanh(a W_1^T + b_1) W_2^T + b_2
   logits = LN_f(h) W_out^T                        (V columns, no bias)
 
@@ -19,10 +19,26 @@ LayerNorm uses the biased variance and eps = cfg['norm_eps'].  x_theta is the
 softmax of the logits over the V real tokens (the mask class gets zero mass,
 App. A.1: clean data contains no mask token).
 
+Two extensions toward the paper's drafting pathway (Sec. 3.1 - 3.2, Sec. 4.1):
+  vis   [L, L] boolean attention pattern (oracle.masks): query i attends only
+        to keys j with vis[i, j]; the softmax runs over those keys alone.
+        None is the bidirectional pattern.
+  gated LoRA (cfg['lora_rank'] = r > 0): each projection y = a W^T + b becomes
+        y = a W^T + b + g_l (alpha/r) (a A^T) B^T
+        at sequence position l, with g_l in {0, 1} the per-position adapter
+        gate (Sec. 3.2 and Sec. 4.1: adapters off at clean positions, on at
+        noisy ones); gate None switches them on everywhere.  With g_l = 1 this
+        is the merged weight W + (alpha/r) B A of App. "Varying LoRA alpha / r".
+
 Parity unpinned by the paper (the architecture is a convention): pinned by a
 second, independent scalar-loop implementation (forward_loops), by LayerNorm
 moments, by permutation equivariance with zero position embeddings and by
-non-causality.
+non-causality.  The extensions are pinned by forward_loops under every
+pattern and gate, by the reach of a perturbation under each pattern (it
+changes exactly the positions that can see it), by the merged-weight identity
+(all gates on == base weights W + (alpha/r) B A) and by the teacher property
+of Sec. 3.2 (under the [x, z_1] pattern with adapters on z_1 only, the logits
+at x equal the base model's causal logits on x alone).
 """
 import numpy as np
 
@@ -44,44 +60,58 @@ def gelu_tanh(x):
     return 0.5 * x * (1.0 + np.tanh(np.sqrt(2.0 / np.pi) * (x + 0.044715 * x ** 3)))
 
 
-def attention(q, k, v):
-    """Non-causal softmax attention for one head: q, k, v are [L, dh]."""
+def attention(q, k, v, vis=None):
+    """Softmax attention for one head: q, k, v are [L, dh]; vis [L, L] or None (all visible)."""
     s = q @ k.T / np.sqrt(q.shape[-1])
+    if vis is not None:
+        s = np.where(vis, s, -np.inf)
     s = s - s.max(axis=-1, keepdims=True)
     p = np.exp(s)
     p /= p.sum(axis=-1, keepdims=True)
     return p @ v
 
 
-def forward_hidden(cfg, P, z, alpha_t):
+def projection(cfg, P, l, name, a, gate):
+    """a W^T + b of projection `name` (qkv, o, 1, 2) of layer l, plus the gated adapter term."""
+    y = a @ P[f"l{l}.w_{name}"].T + P[f"l{l}.b_{name}"]
+    r = int(cfg.get("lora_rank", 0) or 0)
+    if r:
+        scale = float(cfg["lora_alpha"]) / r
+        u = a @ P[f"l{l}.lora_a_{name}"].T
+        y = y + (gate[None, :, None] * scale) * (u @ P[f"l{l}.lora_b_{name}"].T)
+    return y
+
+
+def forward_hidden(cfg, P, z, alpha_t, vis=None, gate=None):
     """Final-LN activations [B, L, d] for token ids z [B, L]."""
     z = np.asarray(z)
     B, L = z.shape
     d, H = cfg["d_model"], cfg["n_heads"]
     dh = d // H
     eps = cfg["norm_eps"]
+    g = np.ones(L) if gate is None else np.asarray(gate, dtype=np.float64)
     h = P["tok_emb"][z] + P["pos_emb"][:L][None]
     if cfg.get("time_cond", True):
         h = h + time_embedding(alpha_t, d)[None, None]
     for l in range(cfg["n_layers"]):
         p = lambda n: P[f"l{l}.{n}"]
         a = layer_norm(h, p("ln1_g"), p("ln1_b"), eps)
-        qkv = a @ p("w_qkv").T + p("b_qkv")
+        qkv = projection(cfg, P, l, "qkv", a, g)
         q, k, v = qkv[..., :d], qkv[..., d:2 * d], qkv[..., 2 * d:]
         o = np.empty_like(q)
         for b in range(B):
             for hh in range(H):
                 cs = slice(hh * dh, (hh + 1) * dh)
-                o[b, :, cs] = attention(q[b, :, cs], k[b, :, cs], v[b, :, cs])
-        h = h + o @ p("w_o").T + p("b_o")
+                o[b, :, cs] = attention(q[b, :, cs], k[b, :, cs], v[b, :, cs], vis)
+        h = h + projection(cfg, P, l, "o", o, g)
         a = layer_norm(h, p("ln2_g"), p("ln2_b"), eps)
-        h = h + gelu_tanh(a @ p("w_1").T + p("b_1")) @ p("w_2").T + p("b_2")
+        h = h + projection(cfg, P, l, "2", gelu_tanh(projection(cfg, P, l, "1", a, g)), g)
     return layer_norm(h, P["lnf_g"], P["lnf_b"], eps)
 
 
-def forward(cfg, P, z, alpha_t):
+def forward(cfg, P, z, alpha_t, vis=None, gate=None):
     """Logits [B, L, V] (float64) of the denoiser at noise level alpha_t."""
-    return forward_hidden(cfg, P, z, alpha_t) @ P["w_out"].T
+    return forward_hidden(cfg, P, z, alpha_t, vis, gate) @ P["w_out"].T
 
 
 def x_theta(logits):

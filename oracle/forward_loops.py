@@ -34,10 +34,15 @@ def _gelu(x):
     return 0.5 * x * (1.0 + math.tanh(c * (x + 0.044715 * x * x * x)))
 
 
-def forward_loops(cfg, P, z, alpha_t):
-    """Logits as nested lists [B][L][V]; P values may be numpy arrays."""
+def forward_loops(cfg, P, z, alpha_t, vis=None, gate=None):
+    """Logits as nested lists [B][L][V]; P values may be numpy arrays.
+
+    vis[i][j] false hides key j from query i (None: all visible); gate[l] in
+    {0, 1} switches the adapters of position l (None: all on)."""
     tl = lambda a: a.tolist()
     d, H, V = cfg["d_model"], cfg["n_heads"], cfg["vocab"]
+    r = int(cfg.get("lora_rank", 0) or 0)
+    scale = float(cfg["lora_alpha"]) / r if r else 0.0
     dh = d // H
     eps = cfg["norm_eps"]
     tok, pos = tl(P["tok_emb"]), tl(P["pos_emb"])
@@ -55,16 +60,28 @@ def forward_loops(cfg, P, z, alpha_t):
         hs = [[tok[int(seq[l])][j] + pos[l][j] + temb[j] for j in range(d)] for l in range(L)]
         for layer in range(cfg["n_layers"]):
             g = lambda n: tl(P[f"l{layer}.{n}"])
-            ln1g, ln1b, wqkv, bqkv = g("ln1_g"), g("ln1_b"), g("w_qkv"), g("b_qkv")
-            wo, bo, ln2g, ln2b = g("w_o"), g("b_o"), g("ln2_g"), g("ln2_b")
-            w1, b1, w2, b2 = g("w_1"), g("b_1"), g("w_2"), g("b_2")
-            qkv = [_linear(_ln(hs[l], ln1g, ln1b, eps), wqkv, bqkv) for l in range(L)]
+            ln1g, ln1b, ln2g, ln2b = g("ln1_g"), g("ln1_b"), g("ln2_g"), g("ln2_b")
+            proj = {}
+            for p in ("qkv", "o", "1", "2"):
+                ad = (g(f"lora_a_{p}"), g(f"lora_b_{p}")) if r else None
+                proj[p] = (g(f"w_{p}"), g(f"b_{p}"), ad)
+
+            def lin(p, vec, l):
+                W, bias, ad = proj[p]
+                y = _linear(vec, W, bias)
+                if ad is not None and (gate is None or gate[l]):
+                    t = _linear(_linear(vec, ad[0], None), ad[1], None)
+                    y = [y[o] + scale * t[o] for o in range(len(y))]
+                return y
+
+            qkv = [lin("qkv", _ln(hs[l], ln1g, ln1b, eps), l) for l in range(L)]
             att = [[0.0] * d for _ in range(L)]
             for hh in range(H):
                 off = hh * dh
                 for i in range(L):
+                    keys = [j for j in range(L) if vis is None or vis[i][j]]
                     scores = []
-                    for j in range(L):
+                    for j in keys:
                         s = 0.0
                         for c in range(dh):
                             s += qkv[i][off + c] * qkv[j][d + off + c]
@@ -74,14 +91,14 @@ def forward_loops(cfg, P, z, alpha_t):
                     tot = sum(ws)
                     for c in range(dh):
                         acc = 0.0
-                        for j in range(L):
-                            acc += ws[j] * qkv[j][2 * d + off + c]
+                        for wj, j in zip(ws, keys):
+                            acc += wj * qkv[j][2 * d + off + c]
                         att[i][off + c] = acc / tot
             for l in range(L):
-                o = _linear(att[l], wo, bo)
+                o = lin("o", att[l], l)
                 hs[l] = [hs[l][j] + o[j] for j in range(d)]
-                u = [_gelu(x) for x in _linear(_ln(hs[l], ln2g, ln2b, eps), w1, b1)]
-                m = _linear(u, w2, b2)
+                u = [_gelu(x) for x in lin("1", _ln(hs[l], ln2g, ln2b, eps), l)]
+                m = lin("2", u, l)
                 hs[l] = [hs[l][j] + m[j] for j in range(d)]
         lnfg, lnfb, wout = tl(P["lnf_g"]), tl(P["lnf_b"]), tl(P["w_out"])
         out.append([_linear(_ln(hs[l], lnfg, lnfb, eps), wout, None) for l in range(L)])

@@ -13,6 +13,14 @@ each tensor is its index in this list), every matrix stored [out][in]:
      ln2_g [d], ln2_b [d], w_1 [F, d], b_1 [F], w_2 [d, F], b_2 [d]
   then lnf_g [d], lnf_b [d], w_out [V, d]
 
+Adapters (cfg['lora_rank'] = r > 0, Sec. 3.1: every projection of a layer has
+a LoRA adapter W + (alpha/r) B A, App. "Varying LoRA alpha / r"): the
+projection tensors w_qkv, w_o, w_1, w_2 are stored [out, in + r] with row o
+holding W[o, :] followed by B[o, :] (B [out, r]); the A matrices [r, in] follow
+w_out, per layer l at ids 2 + 12 L + 3 + 4 l + (0..3) for qkv, o, 1, 2
+(L = n_layers).  `init_params` splits each stored row into P['l.w_*'] and
+P['l.lora_b_*']; `storage_tensors` joins them again in id order.
+
 Initialisation (this build's reading of "weights ~ N(0, 0.02)"): element e of
 tensor `id` takes the Box-Muller normal of Philox block
 (e >> 1 low, e >> 1 high, id, STREAM_PARAM) under key `seed`, using words 0
@@ -33,20 +41,68 @@ def n_tok(cfg):
     return cfg["vocab"] + 1 if cfg["prior"] == "mask" else cfg["vocab"]
 
 
+PROJ = ("qkv", "o", "1", "2")
+
+
+def lora_rank(cfg):
+    return int(cfg.get("lora_rank", 0) or 0)
+
+
+def proj_shape(cfg, name):
+    """(out, in) of projection `name` in PROJ."""
+    d, F = cfg["d_model"], cfg["d_mlp"]
+    return {"qkv": (3 * d, d), "o": (d, d), "1": (F, d), "2": (d, F)}[name]
+
+
 def specs(cfg):
-    """List of (name, shape, kind) in id order; kind is 'w' or 'gain'."""
+    """List of (name, stored shape, kind) in id order; kind is 'w' or 'gain'.
+
+    With adapters the projections are listed with their stored shape
+    [out, in + r] (W and B side by side) under the name of W."""
     d, F, V = cfg["d_model"], cfg["d_mlp"], cfg["vocab"]
+    r = lora_rank(cfg)
     out = [("tok_emb", (n_tok(cfg), d), "w"), ("pos_emb", (cfg["max_len"], d), "w")]
     for l in range(cfg["n_layers"]):
+        wq, wo, w1, w2 = ((o, i + r) for o, i in (proj_shape(cfg, p) for p in PROJ))
         out += [
             (f"l{l}.ln1_g", (d,), "gain"), (f"l{l}.ln1_b", (d,), "w"),
-            (f"l{l}.w_qkv", (3 * d, d), "w"), (f"l{l}.b_qkv", (3 * d,), "w"),
-            (f"l{l}.w_o", (d, d), "w"), (f"l{l}.b_o", (d,), "w"),
+            (f"l{l}.w_qkv", wq, "w"), (f"l{l}.b_qkv", (3 * d,), "w"),
+            (f"l{l}.w_o", wo, "w"), (f"l{l}.b_o", (d,), "w"),
             (f"l{l}.ln2_g", (d,), "gain"), (f"l{l}.ln2_b", (d,), "w"),
-            (f"l{l}.w_1", (F, d), "w"), (f"l{l}.b_1", (F,), "w"),
-            (f"l{l}.w_2", (d, F), "w"), (f"l{l}.b_2", (d,), "w"),
+            (f"l{l}.w_1", w1, "w"), (f"l{l}.b_1", (F,), "w"),
+            (f"l{l}.w_2", w2, "w"), (f"l{l}.b_2", (d,), "w"),
         ]
     out += [("lnf_g", (d,), "gain"), ("lnf_b", (d,), "w"), ("w_out", (V, d), "w")]
+    if r:
+        for l in range(cfg["n_layers"]):
+            out += [(f"l{l}.lora_a_{p}", (r, proj_shape(cfg, p)[1]), "w") for p in PROJ]
+    return out
+
+
+def split_storage(cfg, P):
+    """Split stored [W | B] projections into P['l.w_*'] and P['l.lora_b_*'] (in place)."""
+    if not lora_rank(cfg):
+        return P
+    for l in range(cfg["n_layers"]):
+        for p in PROJ:
+            k = f"l{l}.w_{p}"
+            m = proj_shape(cfg, p)[1]
+            if P[k].shape[1] == m:
+                continue
+            P[f"l{l}.lora_b_{p}"] = P[k][:, m:].copy()
+            P[k] = P[k][:, :m].copy()
+    return P
+
+
+def storage_tensors(cfg, P):
+    """The tensors of P in id order and stored shape (the inverse of split_storage)."""
+    out = []
+    for name, shape, _ in specs(cfg):
+        a = P[name]
+        if a.shape != tuple(shape) and len(shape) == 2:
+            l, p = name.split(".w_")
+            a = np.concatenate([a, P[f"{l}.lora_b_{p}"]], axis=1)
+        out.append(a)
     return out
 
 
@@ -99,4 +155,4 @@ def init_params(cfg, seed):
         z = normals(seed, tid, int(np.prod(shape))).reshape(shape)
         v = 0.02 * z if kind == "w" else 1.0 + 0.02 * z
         P[name] = round_to(v, cfg["dtype"])
-    return P
+    return split_storage(cfg, P)

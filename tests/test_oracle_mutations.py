@@ -62,7 +62,7 @@ def _forward_mismatch():
 
 
 def test_loop_pin_catches_missing_attention_scale(monkeypatch):
-    def att(q, k, v):
+    def att(q, k, v, vis=None):
         s = q @ k.T
         p = np.exp(s - s.max(-1, keepdims=True))
         return (p / p.sum(-1, keepdims=True)) @ v
@@ -134,3 +134,35 @@ def test_lossless_pin_catches_a_wrong_residual(monkeypatch):
         monkeypatch.setattr(verify, "verify_one", make_wrong(kind))
         with pytest.raises(AssertionError):
             tv.test_first_emitted_token_is_distributed_as_the_target()
+
+
+def test_pattern_pins_catch_transposed_visibility(monkeypatch):
+    """A pattern applied as vis^T (keys and queries swapped) fails the scalar-loop pin."""
+    from tests import test_oracle_masked_lora as t
+    orig = forward.attention
+    monkeypatch.setattr(forward, "attention", lambda q, k, v, vis=None: orig(q, k, v, None if vis is None else vis.T))
+    with pytest.raises(AssertionError):
+        t.test_masked_forward_equals_scalar_loops("causal")
+
+
+def test_lora_pins_catch_wrong_adapter_scale(monkeypatch):
+    """r / alpha in place of alpha / r fails the merged-weight identity."""
+    from tests import test_oracle_masked_lora as t
+    orig = forward.projection
+
+    def proj(cfg, P, l, name, a, gate):
+        if cfg.get("lora_rank"):
+            cfg = dict(cfg, lora_alpha=cfg["lora_rank"] ** 2 / cfg["lora_alpha"])
+        return orig(cfg, P, l, name, a, gate)
+    monkeypatch.setattr(forward, "projection", proj)
+    with pytest.raises(AssertionError):
+        t.test_all_gates_on_equals_merged_weights()
+
+
+def test_lora_pins_catch_gate_on_the_wrong_positions(monkeypatch):
+    """A gate indexed from the end of the sequence fails the teacher property of the [x, z_1] pass."""
+    from tests import test_oracle_masked_lora as t
+    orig = forward.projection
+    monkeypatch.setattr(forward, "projection", lambda cfg, P, l, name, a, gate: orig(cfg, P, l, name, a, gate[::-1]))
+    with pytest.raises(AssertionError):
+        t.test_teacher_logits_from_one_pass_over_x_and_z()
