@@ -60,9 +60,11 @@ typedef enum { DD_PRIOR_MASK = 0, DD_PRIOR_UNIFORM = 1 } dd_prior;
 #define DD_GUMBEL_GROUP 256
 /* Device error word bits. */
 #define DD_DEVERR_TOKEN 1
+#define DD_DEVERR_MASK 2   /* an attention-pattern entry was invalid (see dd_denoise_forward_ex) */
 
 /*
- * Denoiser architecture.  Pre-LN transformer, non-causal attention:
+ * Denoiser architecture.  Pre-LN transformer, bidirectional attention (other
+ * patterns: dd_denoise_forward_ex):
  *   h = tok_emb[z] + pos_emb[l] + temb(alpha_t)       (temb only if time_cond)
  *   temb_j = sin(tau w_j) (j < d/2), cos(tau w_{j-d/2}) (j >= d/2),
  *   w_i = 10000^(-i/(d/2)), tau = 1000 (1 - alpha_t)
@@ -71,6 +73,16 @@ typedef enum { DD_PRIOR_MASK = 0, DD_PRIOR_UNIFORM = 1 } dd_prior;
  * d_model even, d_model % n_heads == 0.  dtype DD_BF16: bf16 weights and
  * activations, fp32 accumulation, fp32 residual stream, LayerNorm and softmax;
  * DD_FP32: everything fp32 (validation build).
+ *
+ * Adapters (lora_rank = r > 0; the diffusion weights of Sec. 3.1, a LoRA
+ * adapter on every projection W_qkv, W_o, W_1, W_2): at sequence position l
+ * each projection y = W a + b becomes
+ *   y = W a + b + g_l (lora_alpha / r) B (A a)
+ * with the per-position gate g_l in {0, 1} of dd_denoise_forward_ex (Sec. 3.2,
+ * Sec. 4.1: adapters off at clean positions, on at noisy ones; every other
+ * entry point runs with all gates on).  g_l = 1 everywhere is the merged weight
+ * W + (alpha/r) B A.  r % 8 == 0, lora_alpha > 0; r = 0 disables adapters
+ * (lora_alpha is then ignored).
  */
 typedef struct {
     int32_t n_layers;
@@ -83,6 +95,8 @@ typedef struct {
     int32_t dtype;      /* dd_dtype of weights, activations and logits */
     int32_t time_cond;  /* 1: add the sinusoidal time embedding */
     float norm_eps;     /* LayerNorm epsilon (biased variance) */
+    int32_t lora_rank;  /* r: adapter rank, 0 = no adapters */
+    float lora_alpha;   /* adapter scale numerator: scale = lora_alpha / r */
 } dd_config;
 
 /* ---------------------------------------------------------------- layout */
@@ -96,6 +110,11 @@ typedef struct {
  *     0 ln1_g [d]  1 ln1_b [d]  2 w_qkv [3d][d]  3 b_qkv [3d]  4 w_o [d][d]  5 b_o [d]
  *     6 ln2_g [d]  7 ln2_b [d]  8 w_1 [F][d]     9 b_1 [F]    10 w_2 [d][F] 11 b_2 [d]
  *   then lnf_g [d], lnf_b [d], w_out [V][d].
+ * With adapters (lora_rank = r > 0) the four projections are stored with r more
+ * columns, row o holding W[o][:] then B[o][:] (w_qkv [3d][d+r], w_o [d][d+r],
+ * w_1 [F][d+r], w_2 [d][F+r]), and the A matrices follow w_out: per layer l,
+ * ids 2 + 12 n_layers + 3 + 4 l + : 0 a_qkv [r][d]  1 a_o [r][d]  2 a_1 [r][d]
+ * 3 a_2 [r][F].
  * A vector reports rows = 1, cols = length.
  */
 int32_t dd_param_count(const dd_config* cfg);
@@ -151,6 +170,46 @@ dd_status dd_denoise_forward(const dd_config* cfg, const void* params,
                              const int32_t* z_t, int32_t B, int32_t L, double alpha_t,
                              void* logits, int64_t ld, void* ws, size_t ws_bytes,
                              void* stream);
+
+/* Attention patterns (visibility of key j to query i). */
+typedef enum {
+    DD_ATTN_BIDIRECTIONAL = 0, /* every key (the denoiser's own pattern)                     */
+    DD_ATTN_CAUSAL = 1,        /* j <= i: the AR pathway (Sec. 3.1) and the drafting pass over
+                                  [context, clean, z_t] (Sec. 4.1)                          */
+    DD_ATTN_BLOCK_CAUSAL = 2,  /* blocks of `block` positions: block(j) <= block(i)          */
+    DD_ATTN_DRAFT_TRAIN = 3    /* [x, z_1], x and z_1 of L/2 positions in blocks of `block`
+                                  (Sec. 3.2, Block Diffusion): causal within x; a token of
+                                  noisy block b sees x^(<b) and, causally, its own block     */
+} dd_attn_pattern;
+
+/*
+ * dd_attn_mask_build - write a pattern in the form the forward pass reads:
+ * host int32 out[3*L] = pre[L] | lo[L] | hi[L], key j visible to query i iff
+ * j < pre[i] or lo[i] <= j < hi[i].  `block` is used by BLOCK_CAUSAL (>= 1) and
+ * DRAFT_TRAIN (>= 1, L even, (L/2) % block == 0); DD_E_ARG / DD_E_SHAPE
+ * otherwise.  Host only (no device work).
+ */
+dd_status dd_attn_mask_build(int32_t pattern, int32_t L, int32_t block, int32_t* out);
+
+/*
+ * dd_denoise_forward_ex - dd_denoise_forward with an attention pattern and the
+ * per-position adapter gate.
+ *   attn_mask  NULL (bidirectional) or device int32 [3*L] in the form of
+ *              dd_attn_mask_build, shared by the B sequences.  Needs
+ *              0 <= pre <= L, 0 <= lo <= hi <= L and at least one visible key
+ *              per query: a query whose entry breaks this sets DD_DEVERR_MASK in
+ *              the device error word (first int32 of ws) and sees every key.
+ *   lora_gate  NULL (all adapters on) or device int32 [L]: position l uses its
+ *              adapters iff lora_gate[l] != 0; shared by the B sequences.
+ *              Must be NULL when cfg->lora_rank == 0 (DD_E_ARG).
+ * Other arguments, alignment and errors as dd_denoise_forward; the workspace
+ * size is dd_workspace_bytes (which accounts for the adapters).
+ */
+dd_status dd_denoise_forward_ex(const dd_config* cfg, const void* params,
+                                const int32_t* z_t, int32_t B, int32_t L, double alpha_t,
+                                const int32_t* attn_mask, const int32_t* lora_gate,
+                                void* logits, int64_t ld, void* ws, size_t ws_bytes,
+                                void* stream);
 
 /*
  * dd_posterior_sample - one reverse-posterior draw per row (App. A.1 / A.2 with

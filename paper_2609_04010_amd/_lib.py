@@ -20,6 +20,8 @@ DD_BF16, DD_FP32 = 0, 1
 DD_PRIOR_MASK, DD_PRIOR_UNIFORM = 0, 1
 DD_GUMBEL_GROUP = 256
 DD_DEVERR_TOKEN = 1
+DD_DEVERR_MASK = 2
+ATTN_PATTERNS = {"bidirectional": 0, "causal": 1, "block_causal": 2, "draft_train": 3}
 STATUS = {0: "DD_OK", 1: "DD_E_ARG", 2: "DD_E_SHAPE", 3: "DD_E_DTYPE", 4: "DD_E_WORKSPACE",
           5: "DD_E_HIP", 6: "DD_E_UNSUPPORTED", 7: "DD_E_DEVICE"}
 
@@ -27,6 +29,7 @@ EXPORTED = [
     "dd_param_count", "dd_param_tensor", "dd_param_bytes", "dd_workspace_bytes",
     "dd_loop_workspace_bytes", "dd_logits_ld", "dd_noise_width", "dd_status_str", "dd_last_error",
     "dd_workspace_reset", "dd_read_device_error", "dd_init_params", "dd_denoise_forward",
+    "dd_attn_mask_build", "dd_denoise_forward_ex",
     "dd_posterior_sample", "dd_psi_posterior_sample", "dd_sample_loop", "dd_psi_sample_loop",
     "dd_gaussian_latent_argmax", "dd_spec_verify_workspace_bytes", "dd_spec_verify_noise_width",
     "dd_spec_verify", "dd_profile_begin",
@@ -39,7 +42,8 @@ class DDConfig(ctypes.Structure):
                 ("n_heads", ctypes.c_int32), ("d_mlp", ctypes.c_int32),
                 ("vocab", ctypes.c_int32), ("max_len", ctypes.c_int32),
                 ("prior", ctypes.c_int32), ("dtype", ctypes.c_int32),
-                ("time_cond", ctypes.c_int32), ("norm_eps", ctypes.c_float)]
+                ("time_cond", ctypes.c_int32), ("norm_eps", ctypes.c_float),
+                ("lora_rank", ctypes.c_int32), ("lora_alpha", ctypes.c_float)]
 
 
 class DDError(RuntimeError):
@@ -76,6 +80,9 @@ def lib():
             "dd_init_params": (c.c_int32, [cfgp, P, c.c_size_t, c.c_uint64, P, P]),
             "dd_denoise_forward": (c.c_int32, [cfgp, P, P, c.c_int32, c.c_int32, c.c_double, P,
                                                c.c_int64, P, c.c_size_t, P]),
+            "dd_attn_mask_build": (c.c_int32, [c.c_int32, c.c_int32, c.c_int32, c.POINTER(c.c_int32)]),
+            "dd_denoise_forward_ex": (c.c_int32, [cfgp, P, P, c.c_int32, c.c_int32, c.c_double, P, P,
+                                                  P, c.c_int64, P, c.c_size_t, P]),
             "dd_posterior_sample": (c.c_int32, [c.c_int32, P, c.c_int32, c.c_int64, c.c_int32,
                                                 c.c_int32, P, c.c_double, c.c_double, P,
                                                 c.c_uint64, c.c_uint32, c.c_uint32, P, P, P, P]),
@@ -122,7 +129,8 @@ def make_config(cfg):
                     int(cfg["d_mlp"]), int(cfg["vocab"]), int(cfg["max_len"]),
                     DD_PRIOR_MASK if cfg["prior"] == "mask" else DD_PRIOR_UNIFORM,
                     DD_BF16 if cfg["dtype"] == "bf16" else DD_FP32,
-                    1 if cfg.get("time_cond", True) else 0, float(cfg.get("norm_eps", 1e-5)))
+                    1 if cfg.get("time_cond", True) else 0, float(cfg.get("norm_eps", 1e-5)),
+                    int(cfg.get("lora_rank", 0) or 0), float(cfg.get("lora_alpha", 0.0) or 0.0))
 
 
 def prior_code(prior):
@@ -239,6 +247,29 @@ def denoise_forward(cfg, params, z_t, B, L, alpha_t, logits, ld, ws):
         _ptr(ws, workspace_bytes(cfg, B, L), "ws"), ws.numel() * ws.element_size(), _stream()))
 
 
+def attn_mask_build(pattern, L, block=0):
+    """Host int32 array [3, L] (pre, lo, hi) of a named pattern (see ATTN_PATTERNS)."""
+    out = np.zeros(3 * L, dtype=np.int32)
+    code = ATTN_PATTERNS[pattern] if isinstance(pattern, str) else int(pattern)
+    _check(lib().dd_attn_mask_build(code, int(L), int(block),
+                                    out.ctypes.data_as(ctypes.POINTER(ctypes.c_int32))))
+    return out.reshape(3, L)
+
+
+def denoise_forward_ex(cfg, params, z_t, B, L, alpha_t, logits, ld, ws, attn_mask=None, lora_gate=None):
+    """dd_denoise_forward_ex; attn_mask is a device int32 tensor of 3 L entries, lora_gate of L."""
+    torch = _torch()
+    es = 2 if cfg["dtype"] == "bf16" else 4
+    M = B * L
+    _check(lib().dd_denoise_forward_ex(
+        ctypes.byref(make_config(cfg)), _ptr(params, param_bytes(cfg), "params"),
+        _ptr(z_t, 4 * M, "z_t", torch.int32), B, L, float(alpha_t),
+        _ptr(attn_mask, 12 * L, "attn_mask", torch.int32) if attn_mask is not None else None,
+        _ptr(lora_gate, 4 * L, "lora_gate", torch.int32) if lora_gate is not None else None,
+        _ptr(logits, es * M * ld, "logits"), int(ld),
+        _ptr(ws, workspace_bytes(cfg, B, L), "ws"), ws.numel() * ws.element_size(), _stream()))
+
+
 def _posterior_args(prior, logits, logits_dtype, ld, rows, V, z_t, noise_words, z_s, probs, dev_err):
     torch = _torch()
     es = 2 if logits_dtype == "bf16" else 4
@@ -343,7 +374,8 @@ def read_device_error(err):
 
 PROFILE_CLASSES = ["time_embedding", "embed_layernorm", "layernorm", "gemm_qkv", "attention",
                    "gemm_attn_out", "gemm_mlp_up", "gemm_mlp_down", "gemm_vocab",
-                   "posterior_sample", "gaussian_latent", "init_params", "copy", "compact_masked"]
+                   "posterior_sample", "gaussian_latent", "init_params", "copy", "compact_masked",
+                   "gemm_lora_down"]
 
 
 def profile_begin(max_launches, classes=None):

@@ -70,7 +70,8 @@ dd_status launch_status(const char* what);
 // Profiling hooks around each launch (no-ops unless dd_profile_begin was called).
 enum KernelClass {
     KC_TEMB = 0, KC_EMBED_LN, KC_LN, KC_GEMM_QKV, KC_ATTN, KC_GEMM_O, KC_GEMM_MLP1,
-    KC_GEMM_MLP2, KC_GEMM_VOCAB, KC_POSTERIOR, KC_LATENT, KC_INIT, KC_COPY, KC_COMPACT, KC_COUNT
+    KC_GEMM_MLP2, KC_GEMM_VOCAB, KC_POSTERIOR, KC_LATENT, KC_INIT, KC_COPY, KC_COMPACT, KC_GEMM_LORA,
+    KC_COUNT
 };
 void prof_start(int cls, hipStream_t s);
 void prof_stop(int cls, hipStream_t s);

@@ -6,6 +6,7 @@
 #include <stdint.h>
 #include <string.h>
 
+#include <algorithm>
 #include <vector>
 
 #include "kernels.h"
@@ -49,7 +50,7 @@ dd_status launch_status(const char* what) {
 static const char* kClassNames[KC_COUNT] = {
     "time_embedding", "embed_layernorm", "layernorm", "gemm_qkv", "attention", "gemm_attn_out",
     "gemm_mlp_up", "gemm_mlp_down", "gemm_vocab", "posterior_sample", "gaussian_latent",
-    "init_params", "copy", "compact_masked"};
+    "init_params", "copy", "compact_masked", "gemm_lora_down"};
 
 struct Profiler {
     bool on = false;
@@ -101,27 +102,42 @@ static bool cfg_ok(const dd_config* c) {
     if (c->prior != DD_PRIOR_MASK && c->prior != DD_PRIOR_UNIFORM) { set_error("unknown prior"); return false; }
     if (c->dtype != DD_BF16 && c->dtype != DD_FP32) { set_error("unknown dtype"); return false; }
     if (!(c->norm_eps >= 0.f)) { set_error("norm_eps must be >= 0"); return false; }
+    if (c->lora_rank < 0 || c->lora_rank % 8 != 0) {
+        set_error("lora_rank must be a non-negative multiple of 8 (got %d)", c->lora_rank);
+        return false;
+    }
+    if (c->lora_rank > 0 && !(c->lora_alpha > 0.f && c->lora_alpha < INFINITY)) {
+        set_error("lora_alpha must be positive and finite");
+        return false;
+    }
     return true;
 }
 
 static int n_tok(const dd_config* c) { return c->prior == DD_PRIOR_MASK ? c->vocab + 1 : c->vocab; }
 
+// With adapters each projection row holds W[o][:] then B[o][:] (r more columns), so one GEMM over
+// K = in + r, with the gated down-projection written beside its input, applies W + g (alpha/r) B A.
 static std::vector<Tensor> tensor_list(const dd_config* c) {
-    const int64_t d = c->d_model, F = c->d_mlp, V = c->vocab;
+    const int64_t d = c->d_model, F = c->d_mlp, V = c->vocab, r = c->lora_rank;
     std::vector<std::pair<int64_t, int64_t>> shapes;
     shapes.push_back({n_tok(c), d});
     shapes.push_back({c->max_len, d});
     for (int l = 0; l < c->n_layers; ++l) {
-        shapes.push_back({1, d});      shapes.push_back({1, d});
-        shapes.push_back({3 * d, d});  shapes.push_back({1, 3 * d});
-        shapes.push_back({d, d});      shapes.push_back({1, d});
-        shapes.push_back({1, d});      shapes.push_back({1, d});
-        shapes.push_back({F, d});      shapes.push_back({1, F});
-        shapes.push_back({d, F});      shapes.push_back({1, d});
+        shapes.push_back({1, d});          shapes.push_back({1, d});
+        shapes.push_back({3 * d, d + r});  shapes.push_back({1, 3 * d});
+        shapes.push_back({d, d + r});      shapes.push_back({1, d});
+        shapes.push_back({1, d});          shapes.push_back({1, d});
+        shapes.push_back({F, d + r});      shapes.push_back({1, F});
+        shapes.push_back({d, F + r});      shapes.push_back({1, d});
     }
     shapes.push_back({1, d});
     shapes.push_back({1, d});
     shapes.push_back({V, d});
+    if (r > 0)
+        for (int l = 0; l < c->n_layers; ++l) {
+            shapes.push_back({r, d});  shapes.push_back({r, d});
+            shapes.push_back({r, d});  shapes.push_back({r, F});
+        }
     std::vector<Tensor> t;
     size_t off = 0;
     const size_t es = esize(c->dtype);
@@ -146,18 +162,20 @@ struct WsLayout {
     size_t err, temb, h, xln, qkv, att, mlp, logits, rows, count, total_fwd, total_loop;
 };
 
+// xln, att and mlp (the inputs of the projections) carry r more columns with adapters: the gated
+// down-projection g (alpha/r) A a of each row is written there.
 static WsLayout ws_layout(const dd_config* c, int64_t M) {
     const size_t es = esize(c->dtype);
-    const int64_t d = c->d_model, F = c->d_mlp;
+    const int64_t d = c->d_model, F = c->d_mlp, r = c->lora_rank;
     WsLayout w;
     size_t off = 0;
     w.err = off; off = align256(off + 4);
     w.temb = off; off = align256(off + (size_t)d * 4);
     w.h = off; off = align256(off + (size_t)(M * d) * 4);
-    w.xln = off; off = align256(off + (size_t)(M * d) * es);
+    w.xln = off; off = align256(off + (size_t)(M * (d + r)) * es);
     w.qkv = off; off = align256(off + (size_t)(M * 3 * d) * es);
-    w.att = off; off = align256(off + (size_t)(M * d) * es);
-    w.mlp = off; off = align256(off + (size_t)(M * F) * es);
+    w.att = off; off = align256(off + (size_t)(M * (d + r)) * es);
+    w.mlp = off; off = align256(off + (size_t)(M * (F + r)) * es);
     w.total_fwd = off;
     w.logits = off;
     const int64_t ld = (c->vocab + 63) / 64 * 64;
@@ -184,10 +202,13 @@ static bool forward_supported(const dd_config* c) {
 
 // vocab_rows / vocab_count (device, nullable): restrict the vocabulary projection to the listed
 // rows, written compacted (row j of `logits` belongs to token row vocab_rows[j]).
+// attn_mask (device [3L], nullable): visibility pattern; lora_gate (device [L], nullable): adapter
+// gate per position (all on when NULL).
 static dd_status run_forward(const dd_config* c, const void* params, const int32_t* z, int32_t B,
                              int32_t L, double alpha_t, void* logits, int64_t ld, char* ws,
                              hipStream_t s, const int32_t* vocab_rows = nullptr,
-                             const int32_t* vocab_count = nullptr) {
+                             const int32_t* vocab_count = nullptr,
+                             const int32_t* attn_mask = nullptr, const int32_t* lora_gate = nullptr) {
     const std::vector<Tensor> T = tensor_list(c);
     const WsLayout w = ws_layout(c, (int64_t)B * L);
     const char* P = (const char*)params;
@@ -204,34 +225,49 @@ static dd_status run_forward(const dd_config* c, const void* params, const int32
     void* att = ws + w.att;
     void* mlp = ws + w.mlp;
     const int lnf = 2 + 12 * nl;
+    const int r = c->lora_rank;
+    const int dr = d + r, Fr = F + r;     // row strides of the projection inputs
+    const float lscale = r > 0 ? c->lora_alpha / (float)r : 0.f;
+    // adapter down-projection of `in` (row stride ldin, width kin) by A (id a_id), gated and scaled,
+    // into the r columns after the input
+    auto lora_down = [&](void* in, int64_t ldin, int kin, int a_id) -> dd_status {
+        GemmArgs g = {in, ldin, tp(a_id), kin, nullptr, (char*)in + (size_t)kin * es, ldin, (int)M, r, kin,
+                      nullptr, nullptr, lora_gate, L, lscale};
+        return launch_gemm(dt, EPI_GATE, KC_GEMM_LORA, g, s);
+    };
 
     if (c->time_cond) DD_TRY(launch_temb(temb, d, 1000.0 * (1.0 - alpha_t), s));
     const int g0 = nl > 0 ? 2 : lnf;
     DD_TRY(launch_embed_ln(dt, z, M, L, n_tok(c), d, tp(0), tp(1), c->time_cond ? temb : nullptr,
-                           tp(g0), tp(g0 + 1), c->norm_eps, h, xln, err, s));
+                           tp(g0), tp(g0 + 1), c->norm_eps, h, xln, dr, err, s));
     for (int l = 0; l < nl; ++l) {
         const int b = 2 + 12 * l;
+        const int a0 = lnf + 3 + 4 * l;   // this layer's A matrices (adapters only)
         GemmArgs g;
-        g = {xln, d, tp(b + 2), d, tp(b + 3), qkv, 3 * d, (int)M, 3 * d, d, nullptr, nullptr};
+        if (r > 0) DD_TRY(lora_down(xln, dr, d, a0));
+        g = {xln, dr, tp(b + 2), dr, tp(b + 3), qkv, 3 * d, (int)M, 3 * d, dr, nullptr, nullptr};
         DD_TRY(launch_gemm(dt, EPI_BIAS, KC_GEMM_QKV, g, s));
-        AttnArgs aa = {qkv, 3 * d, att, d, B, L, H, d,
-                       (float)(1.4426950408889634 / sqrt((double)(d / H)))};
+        AttnArgs aa = {qkv, 3 * d, att, dr, B, L, H, d,
+                       (float)(1.4426950408889634 / sqrt((double)(d / H))), attn_mask, err};
         DD_TRY(launch_attn(dt, aa, s));
-        g = {att, d, tp(b + 4), d, tp(b + 5), h, d, (int)M, d, d, nullptr, nullptr};
+        if (r > 0) DD_TRY(lora_down(att, dr, d, a0 + 1));
+        g = {att, dr, tp(b + 4), dr, tp(b + 5), h, d, (int)M, d, dr, nullptr, nullptr};
         DD_TRY(launch_gemm(dt, EPI_BIAS_RESID, KC_GEMM_O, g, s));
-        DD_TRY(launch_ln(dt, h, M, d, tp(b + 6), tp(b + 7), c->norm_eps, xln, s));
-        g = {xln, d, tp(b + 8), d, tp(b + 9), mlp, F, (int)M, F, d, nullptr, nullptr};
+        DD_TRY(launch_ln(dt, h, M, d, tp(b + 6), tp(b + 7), c->norm_eps, xln, dr, s));
+        if (r > 0) DD_TRY(lora_down(xln, dr, d, a0 + 2));
+        g = {xln, dr, tp(b + 8), dr, tp(b + 9), mlp, Fr, (int)M, F, dr, nullptr, nullptr};
         DD_TRY(launch_gemm(dt, EPI_BIAS_GELU, KC_GEMM_MLP1, g, s));
-        g = {mlp, F, tp(b + 10), F, tp(b + 11), h, d, (int)M, d, F, nullptr, nullptr};
+        if (r > 0) DD_TRY(lora_down(mlp, Fr, F, a0 + 3));
+        g = {mlp, Fr, tp(b + 10), Fr, tp(b + 11), h, d, (int)M, d, Fr, nullptr, nullptr};
         DD_TRY(launch_gemm(dt, EPI_BIAS_RESID, KC_GEMM_MLP2, g, s));
         const int gn = (l + 1 < nl) ? b + 12 : lnf;
-        DD_TRY(launch_ln(dt, h, M, d, tp(gn), tp(gn + 1), c->norm_eps, xln, s));
+        DD_TRY(launch_ln(dt, h, M, d, tp(gn), tp(gn + 1), c->norm_eps, xln, dr, s));
     }
     if (vocab_rows) {   // only the listed rows (count on the device) get logits, compacted
-        GemmArgs g = {xln, d, tp(lnf + 2), d, nullptr, logits, ld, (int)M, V, d, vocab_rows, vocab_count};
+        GemmArgs g = {xln, dr, tp(lnf + 2), d, nullptr, logits, ld, (int)M, V, d, vocab_rows, vocab_count};
         DD_TRY(launch_gemm(dt, EPI_PLAIN, KC_GEMM_VOCAB, g, s));
     } else {
-        GemmArgs g = {xln, d, tp(lnf + 2), d, nullptr, logits, ld, (int)M, V, d, nullptr, nullptr};
+        GemmArgs g = {xln, dr, tp(lnf + 2), d, nullptr, logits, ld, (int)M, V, d, nullptr, nullptr};
         DD_TRY(launch_gemm(dt, EPI_PLAIN, KC_GEMM_VOCAB, g, s));
     }
     (void)es;
@@ -322,7 +358,7 @@ const char* dd_last_error(void) { return g_err; }
 
 int32_t dd_param_count(const dd_config* cfg) {
     if (!cfg_ok(cfg)) return 0;
-    return 2 + 12 * cfg->n_layers + 3;
+    return 2 + 12 * cfg->n_layers + 3 + (cfg->lora_rank > 0 ? 4 * cfg->n_layers : 0);
 }
 
 dd_status dd_param_tensor(const dd_config* cfg, int32_t id, size_t* offset_bytes, int64_t* rows,
@@ -395,6 +431,60 @@ dd_status dd_init_params(const dd_config* cfg, void* params, size_t params_bytes
                            is_gain(cfg, id) ? 1.0 : 0.0, cfg->dtype == DD_BF16, seed, s));
     }
     return DD_OK;
+}
+
+dd_status dd_attn_mask_build(int32_t pattern, int32_t L, int32_t block, int32_t* out) {
+    DD_CHECK(out, DD_E_ARG, "out is NULL");
+    DD_CHECK(L > 0, DD_E_ARG, "L must be positive");
+    DD_CHECK(pattern >= DD_ATTN_BIDIRECTIONAL && pattern <= DD_ATTN_DRAFT_TRAIN, DD_E_ARG,
+             "unknown attention pattern %d", pattern);
+    if (pattern == DD_ATTN_BLOCK_CAUSAL || pattern == DD_ATTN_DRAFT_TRAIN)
+        DD_CHECK(block >= 1, DD_E_ARG, "block must be >= 1");
+    if (pattern == DD_ATTN_DRAFT_TRAIN)
+        DD_CHECK(L % 2 == 0 && (L / 2) % block == 0, DD_E_SHAPE,
+                 "the [x, z_1] pattern needs L even and L/2 a multiple of block (L = %d, block = %d)", L, block);
+    int32_t* pre = out;
+    int32_t* lo = out + L;
+    int32_t* hi = out + 2 * (int64_t)L;
+    const int32_t n = L / 2;
+    for (int32_t i = 0; i < L; ++i) {
+        lo[i] = hi[i] = 0;
+        switch (pattern) {
+            case DD_ATTN_BIDIRECTIONAL: pre[i] = L; break;
+            case DD_ATTN_CAUSAL: pre[i] = i + 1; break;
+            case DD_ATTN_BLOCK_CAUSAL: pre[i] = (int32_t)std::min<int64_t>(L, ((int64_t)i / block + 1) * block); break;
+            default:
+                if (i < n) {             // clean token: causal within x
+                    pre[i] = i + 1;
+                } else {                 // token l of noisy block b: x^(<b), then its block up to itself
+                    const int32_t b = (i - n) / block;
+                    pre[i] = b * block;
+                    lo[i] = n + b * block;
+                    hi[i] = i + 1;
+                }
+        }
+    }
+    return DD_OK;
+}
+
+dd_status dd_denoise_forward_ex(const dd_config* cfg, const void* params, const int32_t* z_t,
+                                int32_t B, int32_t L, double alpha_t, const int32_t* attn_mask,
+                                const int32_t* lora_gate, void* logits, int64_t ld, void* ws,
+                                size_t ws_bytes, void* stream) {
+    DD_CHECK(cfg_ok(cfg), DD_E_ARG, "%s", g_err);
+    DD_CHECK(!lora_gate || cfg->lora_rank > 0, DD_E_ARG, "lora_gate given for a model without adapters");
+    DD_CHECK(params && z_t && logits && ws, DD_E_ARG, "NULL pointer argument");
+    DD_CHECK(B > 0 && L > 0, DD_E_ARG, "B and L must be positive");
+    DD_CHECK(L <= cfg->max_len, DD_E_SHAPE, "L = %d exceeds max_len = %d", L, cfg->max_len);
+    DD_CHECK(alpha_t >= 0.0 && alpha_t <= 1.0, DD_E_ARG, "alpha_t must lie in [0, 1]");
+    DD_CHECK(ld >= cfg->vocab && ld % 8 == 0, DD_E_SHAPE, "ld must be >= V and a multiple of 8");
+    DD_CHECK(((uintptr_t)logits & 15) == 0 && ((uintptr_t)ws & 255) == 0 && ((uintptr_t)params & 255) == 0,
+             DD_E_ARG, "logits must be 16-byte aligned, params and ws 256-byte aligned");
+    DD_CHECK(forward_supported(cfg), DD_E_UNSUPPORTED, "%s", g_err);
+    const size_t need = dd_workspace_bytes(cfg, B, L);
+    DD_CHECK(ws_bytes >= need, DD_E_WORKSPACE, "workspace has %zu bytes, needs %zu", ws_bytes, need);
+    return run_forward(cfg, params, z_t, B, L, alpha_t, logits, ld, (char*)ws, (hipStream_t)stream,
+                       nullptr, nullptr, attn_mask, lora_gate);
 }
 
 dd_status dd_denoise_forward(const dd_config* cfg, const void* params, const int32_t* z_t,

@@ -1,4 +1,7 @@
-// Non-causal multi-head attention softmax(q k^T / sqrt(dh)) v, flash style (no L x L tensor).
+// Multi-head attention softmax(q k^T / sqrt(dh)) v, flash style (no L x L tensor), over every key
+// or, with a visibility pattern, over the keys j of query i with j < pre_i or lo_i <= j < hi_i (a
+// prefix plus one window: bidirectional, causal, block-causal and the [x, z_1] block-diffusion
+// pattern all take this form).
 //
 // bf16 path (dh = 64): a workgroup of 4 wavefronts owns 128 queries of one (batch, head); each
 // wavefront owns 32 queries.  Key/value tiles of 64 tokens are staged in LDS (double-buffered,
@@ -12,7 +15,13 @@
 //   O^T += V^T P^T: the probabilities are rounded to bf16 and used directly as the second MFMA
 //         operand (no shuffles: the key order of V^T in LDS is permuted to match the accumulator
 //         layout of S^T), so each lane's output column is again its own query.
+// Patterns (MASKED instance): a workgroup visits only the key tiles that meet the union of its
+// queries' visible sets (the prefix tiles, then the window tiles); a wavefront whose queries see
+// nothing of a tile skips its arithmetic; a tile that every query of the wavefront sees whole takes
+// no per-element test.  Rows that have seen no visible key yet keep mref = -inf and use exponent
+// reference 0, so their probabilities are exactly 0 until their first visible key.
 // fp32 path (validation): one thread per (batch, head, query), fp32 online softmax.
+#include <limits.h>
 #include <math.h>
 
 #include "kernels.h"
@@ -33,9 +42,37 @@ constexpr int VSTR = AK + 8;
 // contiguously at positions 16s + 8g .. + 7 (key 16s + 4g + 8h + r at position 16s + 8g + 4h + r),
 // so each lane reads its operand with one 16-byte load.
 
+DD_DEV int wave_max_i(int v) {
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) v = max(v, __shfl_xor(v, o, 64));
+    return v;
+}
+DD_DEV int wave_min_i(int v) {
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) v = min(v, __shfl_xor(v, o, 64));
+    return v;
+}
+
+// The visible set of query qi (< L): (pre, lo, hi) read from the pattern, an invalid entry
+// reported and replaced by "every key".
+DD_DEV void query_window(const AttnArgs& a, int qi, int& pre, int& lo, int& hi) {
+    const int L = a.L;
+    pre = a.mask[qi];
+    lo = a.mask[L + qi];
+    hi = a.mask[2 * L + qi];
+    const bool ok = pre >= 0 && pre <= L && lo >= 0 && lo <= hi && hi <= L && (pre > 0 || hi > lo);
+    if (!ok) {
+        if (a.err) atomicOr(a.err, DD_DEVERR_MASK);
+        pre = L;
+        lo = hi = 0;
+    }
+}
+
+template <bool MASKED>
 __global__ __launch_bounds__(256) void attn_bf16_kernel(AttnArgs a) {
     __shared__ __attribute__((aligned(16))) bf16_t Ks[2][AK * KSTR];
     __shared__ __attribute__((aligned(16))) bf16_t Vt[2][DH * VSTR];
+    __shared__ int sh_rng[4][3];
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     // one-dimensional grid: the query blocks of one (batch, head) run on one XCD, one after another,
@@ -65,6 +102,46 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(AttnArgs a) {
 #pragma unroll
         for (int e = 0; e < 16; ++e) o[i][e] = 0.f;
     float mrow = -INFINITY, lpart = 0.f;
+
+    // Key tiles of this workgroup: 0 .. ntiles-1, or under a pattern the prefix tiles [0, tp) then
+    // the window tiles [tw0, tw1).  Per wavefront: the union bounds (pmax, wlo, whi) decide whether
+    // it has work in a tile; the intersection bounds (pmin, lomax, himin) whether the tile is whole.
+    int qpre = 0, qlo = 0, qhi = 0;
+    int tp = (L + AK - 1) / AK, tw0 = tp, tw1 = tp;
+    int pmax = L, wlo = 0, whi = 0, pmin = L, lomax = 0, himin = 0;
+    if constexpr (MASKED) {
+        if (qi < L) query_window(a, qi, qpre, qlo, qhi);
+        const bool win = qhi > qlo;
+        pmax = wave_max_i(qpre);
+        wlo = wave_min_i(win ? qlo : INT_MAX);
+        whi = wave_max_i(win ? qhi : 0);
+        // padded queries (qi >= L) see nothing and take no part in the intersection
+        pmin = wave_min_i(qi < L ? qpre : INT_MAX);
+        lomax = wave_max_i(qi < L ? qlo : INT_MIN);
+        himin = wave_min_i(qi < L ? qhi : INT_MAX);
+        if (lane == 0) {
+            sh_rng[wave][0] = pmax;
+            sh_rng[wave][1] = wlo;
+            sh_rng[wave][2] = whi;
+        }
+        __syncthreads();
+        int gp = 0, glo = INT_MAX, ghi = 0;
+#pragma unroll
+        for (int w = 0; w < 4; ++w) {
+            gp = max(gp, sh_rng[w][0]);
+            glo = min(glo, sh_rng[w][1]);
+            ghi = max(ghi, sh_rng[w][2]);
+        }
+        tp = (gp + AK - 1) / AK;
+        if (ghi > glo) {
+            tw0 = max(tp, glo / AK);
+            tw1 = max(tw0, (ghi + AK - 1) / AK);
+        } else {
+            tw0 = tw1 = tp;
+        }
+    }
+    const int ntiles = tp + (tw1 - tw0);
+    auto tile_of = [&](int k) { return k < tp ? k : tw0 + (k - tp); };
 
     // K tile: thread handles 16-byte chunks c = tid + 256 r (key c / 8, columns 8 (c % 8) ..).
     // V tile (stored transposed): thread handles dv chunk vc = tid / 32 and the pair of keys that
@@ -108,8 +185,8 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(AttnArgs a) {
     // RESCALE (base-2 units), so probabilities stay below 2^RESCALE and the O accumulators are
     // rescaled only on those rare steps (checked once per wavefront).
     constexpr float RESCALE = 8.0f;
-    auto tile = [&](int t) {
-        const int buf = t & 1, kb0 = t * AK;
+    auto tile = [&](int k) {
+        const int buf = k & 1, kb0 = tile_of(k) * AK;
         f32x16 sacc[2];
 #pragma unroll
         for (int kb = 0; kb < 2; ++kb) {
@@ -121,7 +198,19 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(AttnArgs a) {
                 sacc[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[kk], sacc[kb], 0, 0, 0);
             }
         }
-        if (kb0 + AK > L) {          // wave-uniform: only the last tile can run past L
+        if constexpr (MASKED) {
+            // whole tile visible to every query of the wavefront (then also inside L)?
+            const bool whole = kb0 + AK <= pmin || (kb0 >= lomax && kb0 + AK <= himin);
+            if (!whole) {
+#pragma unroll
+                for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+                    for (int j = 0; j < 16; ++j) {
+                        const int key = kb0 + kb * 32 + 8 * (j >> 2) + 4 * grp + (j & 3);
+                        if (!(key < qpre || (key >= qlo && key < qhi))) sacc[kb][j] = -INFINITY;
+                    }
+            }
+        } else if (kb0 + AK > L) {   // wave-uniform: only the last tile can run past L
 #pragma unroll
             for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
@@ -139,7 +228,8 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(AttnArgs a) {
         const bool raise = mloc > mrow + RESCALE;
         if (__any(raise)) {
             const float mnew = raise ? mloc : mrow;
-            const float corr = __builtin_amdgcn_exp2f(mrow - mnew);
+            // a row that has seen no visible key keeps mrow = -inf: its factor must be 1, not NaN
+            const float corr = MASKED && !raise ? 1.0f : __builtin_amdgcn_exp2f(mrow - mnew);
             lpart *= corr;
 #pragma unroll
             for (int i = 0; i < 2; ++i)
@@ -148,11 +238,12 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(AttnArgs a) {
             mrow = mnew;
         }
         float psum = 0.f;
+        const float negm = MASKED && mrow == -INFINITY ? 0.f : -mrow;
 #pragma unroll
         for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
             for (int j = 0; j < 16; ++j) {
-                const float p = __builtin_amdgcn_exp2f(fmaf(sacc[kb][j], a.scale_log2, -mrow));
+                const float p = __builtin_amdgcn_exp2f(fmaf(sacc[kb][j], a.scale_log2, negm));
                 sacc[kb][j] = p;
                 psum += p;
             }
@@ -169,14 +260,19 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(AttnArgs a) {
             }
         }
     };
-    const int ntiles = (L + AK - 1) / AK;
-    gload(0);
-    sstore(0);
+    // does any query of this wavefront see a key of the tile starting at kb0?
+    auto wave_needs = [&](int kb0) {
+        return !MASKED || kb0 < pmax || (kb0 < whi && kb0 + AK > wlo);
+    };
+    if (ntiles > 0) {
+        gload(tile_of(0) * AK);
+        sstore(0);
+    }
     __syncthreads();
-    for (int t = 0; t < ntiles; ++t) {
-        if (t + 1 < ntiles) gload((t + 1) * AK);
-        tile(t);
-        if (t + 1 < ntiles) sstore((t + 1) & 1);
+    for (int k = 0; k < ntiles; ++k) {
+        if (k + 1 < ntiles) gload(tile_of(k + 1) * AK);
+        if (wave_needs(tile_of(k) * AK)) tile(k);
+        if (k + 1 < ntiles) sstore((k + 1) & 1);
         __syncthreads();
     }
 
@@ -197,7 +293,7 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(AttnArgs a) {
     }
 }
 
-template <int D>
+template <int D, bool MASKED>
 __global__ __launch_bounds__(128) void attn_f32_kernel(AttnArgs a) {
     const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     const int L = a.L, H = a.H, d = a.d;
@@ -210,8 +306,11 @@ __global__ __launch_bounds__(128) void attn_f32_kernel(AttnArgs a) {
     float qv[D], acc[D];
 #pragma unroll
     for (int c = 0; c < D; ++c) { qv[c] = base[(int64_t)q * a.ld + h * D + c]; acc[c] = 0.f; }
+    int pre = L, lo = 0, hi = 0;
+    if (MASKED) query_window(a, q, pre, lo, hi);
     float m = -INFINITY, l = 0.f;
     for (int t = 0; t < L; ++t) {
+        if (MASKED && !(t < pre || (t >= lo && t < hi))) continue;
         const float* kr = base + (int64_t)t * a.ld + d + h * D;
         float sdot = 0.f;
 #pragma unroll
@@ -239,16 +338,22 @@ dd_status launch_attn(int dtype, const AttnArgs& a, hipStream_t s) {
     const int dh = a.d / a.H;
     ProfScope ps(KC_ATTN, s);
     if (dtype == DD_BF16) {
-        hipLaunchKernelGGL(attn_bf16_kernel, dim3((unsigned)(ceil_div(a.L, AQ) * a.H * a.B)), dim3(256), 0, s, a);
+        const dim3 grid((unsigned)(ceil_div(a.L, AQ) * a.H * a.B));
+        if (a.mask) hipLaunchKernelGGL(attn_bf16_kernel<true>, grid, dim3(256), 0, s, a);
+        else hipLaunchKernelGGL(attn_bf16_kernel<false>, grid, dim3(256), 0, s, a);
     } else {
         const int64_t n = (int64_t)a.B * a.H * a.L;
         const dim3 grid((unsigned)ceil_div(n, 128));
+#define DD_ATTN_F32(DV)                                                                         \
+    if (a.mask) hipLaunchKernelGGL((attn_f32_kernel<DV, true>), grid, dim3(128), 0, s, a);      \
+    else hipLaunchKernelGGL((attn_f32_kernel<DV, false>), grid, dim3(128), 0, s, a);
         switch (dh) {
-            case 16: hipLaunchKernelGGL(attn_f32_kernel<16>, grid, dim3(128), 0, s, a); break;
-            case 32: hipLaunchKernelGGL(attn_f32_kernel<32>, grid, dim3(128), 0, s, a); break;
-            case 64: hipLaunchKernelGGL(attn_f32_kernel<64>, grid, dim3(128), 0, s, a); break;
-            default: hipLaunchKernelGGL(attn_f32_kernel<128>, grid, dim3(128), 0, s, a); break;
+            case 16: DD_ATTN_F32(16) break;
+            case 32: DD_ATTN_F32(32) break;
+            case 64: DD_ATTN_F32(64) break;
+            default: DD_ATTN_F32(128) break;
         }
+#undef DD_ATTN_F32
     }
     return launch_status("attention");
 }

@@ -13,7 +13,8 @@
 // tiles in that XCD's L2.
 //
 // Epilogues: bias -> bf16 (QKV), bias + GELU(tanh) -> bf16 (MLP up), bias + fp32 residual add in
-// place (attention output, MLP down), plain store (vocabulary projection).
+// place (attention output, MLP down), plain store (vocabulary projection), per-row gate x scale ->
+// bf16 (adapter down-projection of a gated LoRA).
 #include <math.h>
 #include <stdlib.h>
 
@@ -50,13 +51,21 @@ DD_DEV void map_tile(int bid, int nblocks, int tiles_m, int tiles_n, int& tm, in
 // ------------------------------------------------------------------------------ bf16 MFMA
 constexpr int BK = 64, LSTR = BK + 8;
 
+// EPI_GATE row factor of output row m (m % gate_period is in range for any m, clamped rows too)
+DD_DEV float gate_row_scale(const GemmArgs& g, int m) {
+    if (!g.gate) return g.gate_scale;
+    return g.gate[m % g.gate_period] != 0 ? g.gate_scale : 0.f;
+}
+
 template <int EPI>
 DD_DEV void epilogue_bf16(const GemmArgs& g, int m, int n, const float* v, const float* bias4) {
     float o[4];
+    const float rs = EPI == EPI_GATE ? gate_row_scale(g, m) : 1.f;
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
         float x = v[e] + bias4[e];
         if (EPI == EPI_BIAS_GELU) x = gelu_tanh(x);
+        if (EPI == EPI_GATE) x = v[e] * rs;
         o[e] = x;
     }
     if (EPI == EPI_BIAS_RESID) {
@@ -170,7 +179,7 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmArgs g, int tiles_m,
             const int n = n0 + wn * (TBN / 2) + nb * 32 + 8 * j4 + 4 * (lane >> 5);
             if (n >= g.N) continue;
             float b4[4] = {0.f, 0.f, 0.f, 0.f};
-            if (EPI != EPI_PLAIN)
+            if (EPI != EPI_PLAIN && EPI != EPI_GATE)
 #pragma unroll
                 for (int e = 0; e < 4; ++e)
                     if (n + e < g.N) b4[e] = bf16_to_f32(((const bf16_t*)g.bias)[n + e]);
@@ -377,7 +386,7 @@ __global__ __launch_bounds__(64 * WGM_ * WGN_, 1) void gemm_bf16_dl_kernel(GemmA
     auto bias4 = [&](int nb, int j4, float* b4) {
         uint2 r = make_uint2(0u, 0u);
         if constexpr (PREFETCH_BIAS) r = braw[nb][j4];
-        else if constexpr (EPI != EPI_PLAIN) r = load_bias4(nb, j4);
+        else if constexpr (EPI != EPI_PLAIN && EPI != EPI_GATE) r = load_bias4(nb, j4);
         b4[0] = bf16_lo(r.x); b4[1] = bf16_hi(r.x); b4[2] = bf16_lo(r.y); b4[3] = bf16_hi(r.y);
     };
 
@@ -413,6 +422,11 @@ __global__ __launch_bounds__(64 * WGM_ * WGN_, 1) void gemm_bf16_dl_kernel(GemmA
             // row, 5 rows per instruction (lanes 60..63 idle)
             constexpr int CPR = S::WN / 8;            // 16-byte chunks per staged row
             constexpr int RPI = 64 / CPR;             // rows per wave instruction
+            float rs[EPI == EPI_GATE ? MB : 1];       // gate factor of this lane's rows
+            if constexpr (EPI == EPI_GATE) {
+#pragma unroll
+                for (int mb = 0; mb < MB; ++mb) rs[mb] = gate_row_scale(g, mrow0 + mb * 32 + (lane & 31));
+            }
 #pragma unroll
             for (int half = 0; half < 2; ++half) {
 #pragma unroll
@@ -430,6 +444,7 @@ __global__ __launch_bounds__(64 * WGM_ * WGN_, 1) void gemm_bf16_dl_kernel(GemmA
                             for (int e = 0; e < 4; ++e) {
                                 float x = acc[nb][mb][4 * j4 + e] + b4[e];
                                 if (EPI == EPI_BIAS_GELU) x = gelu_tanh(x);
+                                if constexpr (EPI == EPI_GATE) x = acc[nb][mb][4 * j4 + e] * rs[mb];
                                 o[e] = x;
                             }
                             uint2 pk;
@@ -538,7 +553,8 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmArgs g, int tiles_m, 
             const int n = n0 + tx * 4 + j;
             if (n >= g.N) continue;
             float x = acc[i][j];
-            if (EPI != EPI_PLAIN) x += ((const float*)g.bias)[n];
+            if (EPI == EPI_GATE) x *= gate_row_scale(g, m);
+            else if (EPI != EPI_PLAIN) x += ((const float*)g.bias)[n];
             if (EPI == EPI_BIAS_GELU) x = 0.5f * x * (1.0f + tanhf(0.7978845608028654f * (x + 0.044715f * x * x * x)));
             float* c = (float*)g.C + (int64_t)m * g.ldc + n;
             if (EPI == EPI_BIAS_RESID) *c += x;
@@ -644,6 +660,7 @@ dd_status launch_gemm(int dtype, int epi, int cls, const GemmArgs& g, hipStream_
             if (cls == KC_GEMM_O) launch_epi<EPI_BIAS_RESID, KC_GEMM_O>(dtype, g, s);
             else launch_epi<EPI_BIAS_RESID, KC_GEMM_MLP2>(dtype, g, s);
             break;
+        case EPI_GATE: launch_epi<EPI_GATE, KC_GEMM_LORA>(dtype, g, s); break;
         default: launch_epi<EPI_PLAIN, KC_GEMM_VOCAB>(dtype, g, s); break;
     }
     return launch_status("gemm");

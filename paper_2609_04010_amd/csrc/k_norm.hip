@@ -55,7 +55,8 @@ template <typename W, int NPL>
 __global__ __launch_bounds__(256) void embed_ln_kernel(const int32_t* z, int64_t rows, int L,
                                                        int n_tok, const W* tok, const W* pos,
                                                        const float* temb, const W* g, const W* b,
-                                                       float eps, float* h, W* xln, int32_t* err) {
+                                                       float eps, float* h, W* xln, int64_t ldo,
+                                                       int32_t* err) {
     const int64_t row = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
     const int lane = threadIdx.x & 63;
     if (row >= rows) return;
@@ -75,12 +76,12 @@ __global__ __launch_bounds__(256) void embed_ln_kernel(const int32_t* z, int64_t
         x[k] = v;
         h[row * d + c] = v;
     }
-    ln_row<W, NPL>(x, lane, d, g, b, eps, xln + row * d);
+    ln_row<W, NPL>(x, lane, d, g, b, eps, xln + row * ldo);
 }
 
 template <typename W, int NPL>
 __global__ __launch_bounds__(256) void ln_kernel(const float* h, int64_t rows, const W* g,
-                                                 const W* b, float eps, W* out) {
+                                                 const W* b, float eps, W* out, int64_t ldo) {
     const int64_t row = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
     const int lane = threadIdx.x & 63;
     if (row >= rows) return;
@@ -88,7 +89,7 @@ __global__ __launch_bounds__(256) void ln_kernel(const float* h, int64_t rows, c
     float x[NPL];
 #pragma unroll
     for (int k = 0; k < NPL; ++k) x[k] = h[row * d + lane + 64 * k];
-    ln_row<W, NPL>(x, lane, d, g, b, eps, out + row * d);
+    ln_row<W, NPL>(x, lane, d, g, b, eps, out + row * ldo);
 }
 
 // bf16 output, d % 256 == 0: each lane holds NV = d / 256 groups of four consecutive features,
@@ -96,7 +97,7 @@ __global__ __launch_bounds__(256) void ln_kernel(const float* h, int64_t rows, c
 template <int NV>
 __global__ __launch_bounds__(256) void ln_bf16_v4_kernel(const float* h, int64_t rows,
                                                          const bf16_t* g, const bf16_t* b,
-                                                         float eps, bf16_t* out) {
+                                                         float eps, bf16_t* out, int64_t ldo) {
     const int64_t row = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
     const int lane = threadIdx.x & 63;
     if (row >= rows) return;
@@ -116,7 +117,7 @@ __global__ __launch_bounds__(256) void ln_bf16_v4_kernel(const float* h, int64_t
         q += (a0 * a0 + a1 * a1) + (a2 * a2 + a3 * a3);
     }
     const float rstd = 1.0f / sqrtf(wave_sum(q) / (float)d + eps);
-    uint2* orow = (uint2*)(out + row * d);
+    uint2* orow = (uint2*)(out + row * ldo);
     const uint2* gv = (const uint2*)g;
     const uint2* bv = (const uint2*)b;
 #pragma unroll
@@ -137,7 +138,7 @@ __global__ __launch_bounds__(256) void ln_bf16_v4_kernel(const float* h, int64_t
 template <typename W>
 dd_status launch_embed_ln_t(const int32_t* z, int64_t rows, int L, int n_tok, int d, const void* tok,
                             const void* pos, const float* temb, const void* g, const void* b,
-                            float eps, float* h, void* xln, int32_t* err, hipStream_t s) {
+                            float eps, float* h, void* xln, int64_t ldo, int32_t* err, hipStream_t s) {
     const dim3 grid((unsigned)ceil_div(rows, 4)), blk(256);
     ProfScope ps(KC_EMBED_LN, s);
     switch (d / 64) {
@@ -145,7 +146,7 @@ dd_status launch_embed_ln_t(const int32_t* z, int64_t rows, int L, int n_tok, in
     case n:                                                                                      \
         hipLaunchKernelGGL((embed_ln_kernel<W, n>), grid, blk, 0, s, z, rows, L, n_tok,          \
                            (const W*)tok, (const W*)pos, temb, (const W*)g, (const W*)b, eps, h,  \
-                           (W*)xln, err);                                                        \
+                           (W*)xln, ldo, err);                                                   \
         break;
         DD_NPL_CASES(X)
 #undef X
@@ -156,23 +157,23 @@ dd_status launch_embed_ln_t(const int32_t* z, int64_t rows, int L, int n_tok, in
 
 dd_status launch_embed_ln(int dtype, const int32_t* z, int64_t rows, int L, int n_tok, int d,
                           const void* tok, const void* pos, const float* temb, const void* g,
-                          const void* b, float eps, float* h, void* xln, int32_t* err,
+                          const void* b, float eps, float* h, void* xln, int64_t ldo, int32_t* err,
                           hipStream_t s) {
     if (dtype == DD_BF16)
-        return launch_embed_ln_t<bf16_t>(z, rows, L, n_tok, d, tok, pos, temb, g, b, eps, h, xln, err, s);
-    return launch_embed_ln_t<float>(z, rows, L, n_tok, d, tok, pos, temb, g, b, eps, h, xln, err, s);
+        return launch_embed_ln_t<bf16_t>(z, rows, L, n_tok, d, tok, pos, temb, g, b, eps, h, xln, ldo, err, s);
+    return launch_embed_ln_t<float>(z, rows, L, n_tok, d, tok, pos, temb, g, b, eps, h, xln, ldo, err, s);
 }
 
 template <typename W>
 dd_status launch_ln_t(const float* h, int64_t rows, int d, const void* g, const void* b, float eps,
-                      void* out, hipStream_t s) {
+                      void* out, int64_t ldo, hipStream_t s) {
     const dim3 grid((unsigned)ceil_div(rows, 4)), blk(256);
     ProfScope ps(KC_LN, s);
     switch (d / 64) {
 #define X(n)                                                                                     \
     case n:                                                                                      \
         hipLaunchKernelGGL((ln_kernel<W, n>), grid, blk, 0, s, h, rows, (const W*)g,            \
-                           (const W*)b, eps, (W*)out);                                           \
+                           (const W*)b, eps, (W*)out, ldo);                                      \
         break;
         DD_NPL_CASES(X)
 #undef X
@@ -182,20 +183,20 @@ dd_status launch_ln_t(const float* h, int64_t rows, int d, const void* g, const 
 }
 
 dd_status launch_ln(int dtype, const float* h, int64_t rows, int d, const void* g, const void* b,
-                    float eps, void* out, hipStream_t s) {
-    if (dtype == DD_BF16 && (d == 768 || d == 1024 || d == 2048)) {
+                    float eps, void* out, int64_t ldo, hipStream_t s) {
+    if (dtype == DD_BF16 && (d == 768 || d == 1024 || d == 2048) && ldo % 4 == 0) {
         const dim3 grid((unsigned)ceil_div(rows, 4)), blk(256);
         ProfScope ps(KC_LN, s);
         const bf16_t* gg = (const bf16_t*)g;
         const bf16_t* bb = (const bf16_t*)b;
         bf16_t* o = (bf16_t*)out;
-        if (d == 768) hipLaunchKernelGGL(ln_bf16_v4_kernel<3>, grid, blk, 0, s, h, rows, gg, bb, eps, o);
-        else if (d == 1024) hipLaunchKernelGGL(ln_bf16_v4_kernel<4>, grid, blk, 0, s, h, rows, gg, bb, eps, o);
-        else hipLaunchKernelGGL(ln_bf16_v4_kernel<8>, grid, blk, 0, s, h, rows, gg, bb, eps, o);
+        if (d == 768) hipLaunchKernelGGL(ln_bf16_v4_kernel<3>, grid, blk, 0, s, h, rows, gg, bb, eps, o, ldo);
+        else if (d == 1024) hipLaunchKernelGGL(ln_bf16_v4_kernel<4>, grid, blk, 0, s, h, rows, gg, bb, eps, o, ldo);
+        else hipLaunchKernelGGL(ln_bf16_v4_kernel<8>, grid, blk, 0, s, h, rows, gg, bb, eps, o, ldo);
         return launch_status("layernorm");
     }
-    if (dtype == DD_BF16) return launch_ln_t<bf16_t>(h, rows, d, g, b, eps, out, s);
-    return launch_ln_t<float>(h, rows, d, g, b, eps, out, s);
+    if (dtype == DD_BF16) return launch_ln_t<bf16_t>(h, rows, d, g, b, eps, out, ldo, s);
+    return launch_ln_t<float>(h, rows, d, g, b, eps, out, ldo, s);
 }
 
 bool ln_supported(int d) {

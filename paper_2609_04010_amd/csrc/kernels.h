@@ -31,7 +31,9 @@ struct PostArgs {
     const int32_t* count;
 };
 
-enum Epi { EPI_BIAS = 0, EPI_BIAS_GELU = 1, EPI_BIAS_RESID = 2, EPI_PLAIN = 3 };
+// EPI_GATE: C = bf16(acc * s_m), s_m = gate_scale if gate is NULL or gate[m % gate_period] != 0,
+// else 0 (the adapter down-projection of a gated LoRA, written beside its input)
+enum Epi { EPI_BIAS = 0, EPI_BIAS_GELU = 1, EPI_BIAS_RESID = 2, EPI_PLAIN = 3, EPI_GATE = 4 };
 
 struct GemmArgs {
     const void* A;   // [M][K], row stride lda
@@ -45,6 +47,10 @@ struct GemmArgs {
     // optional row gather (bf16 path, K % 64 == 0): output row m < *m_count takes A row a_rows[m]
     const int32_t* a_rows;
     const int32_t* m_count;
+    // EPI_GATE only: per-row gate, read at m % gate_period, and the scale of open rows
+    const int32_t* gate;
+    int gate_period;
+    float gate_scale;
 };
 
 struct AttnArgs {
@@ -54,6 +60,11 @@ struct AttnArgs {
     int64_t ldo;
     int B, L, H, d;
     float scale_log2;  // log2(e) / sqrt(dh)
+    // visibility (NULL: every key): key j is visible to query i iff j < pre[i] or lo[i] <= j < hi[i],
+    // with pre = mask[0..L), lo = mask[L..2L), hi = mask[2L..3L); an entry outside 0 <= pre <= L,
+    // 0 <= lo <= hi <= L, or with no visible key, sets DD_DEVERR_MASK in *err and sees every key
+    const int32_t* mask;
+    int32_t* err;
 };
 
 dd_status launch_posterior(const PostArgs& a, int logits_dtype, hipStream_t s);
@@ -85,10 +96,11 @@ dd_status launch_init(void* dst, int64_t count, uint32_t id, double shift, int i
 dd_status launch_temb(float* temb, int d, double tau, hipStream_t s);
 dd_status launch_embed_ln(int dtype, const int32_t* z, int64_t rows, int L, int n_tok, int d,
                           const void* tok, const void* pos, const float* temb, const void* g,
-                          const void* b, float eps, float* h, void* xln, int32_t* err,
+                          const void* b, float eps, float* h, void* xln, int64_t ldo, int32_t* err,
                           hipStream_t s);
+// out rows have stride ldo (elements) >= d
 dd_status launch_ln(int dtype, const float* h, int64_t rows, int d, const void* g, const void* b,
-                    float eps, void* out, hipStream_t s);
+                    float eps, void* out, int64_t ldo, hipStream_t s);
 bool ln_supported(int d);
 dd_status launch_gemm(int dtype, int epi, int cls, const GemmArgs& g, hipStream_t s);
 dd_status launch_attn(int dtype, const AttnArgs& a, hipStream_t s);

@@ -185,3 +185,77 @@ def test_spec_verify_validation_and_sizes():
     assert dd.spec_verify_workspace_bytes(4, 3) == 256 and dd.spec_verify_workspace_bytes(100, 8) == 6144
     for B, V in ((1, 32), (4, 300), (16, 50257)):
         assert dd.spec_verify_noise_width(B, V) == overify.noise_width(B, V)
+
+
+@pytest.mark.parametrize("pattern,L,block", [("bidirectional", 7, 0), ("causal", 9, 0), ("block_causal", 10, 3),
+                                             ("block_causal", 8, 8), ("draft_train", 12, 3),
+                                             ("draft_train", 2, 1), ("draft_train", 16, 8)])
+def test_attn_mask_build_matches_oracle_patterns(pattern, L, block):
+    """The library's (pre, lo, hi) form, expanded, is the oracle's visibility matrix, bit for bit."""
+    from oracle import masks
+    m = dd.attn_mask_build(pattern, L, block)
+    pre, lo, hi = m[0][:, None], m[1][:, None], m[2][:, None]
+    j = np.arange(L)[None, :]
+    vis = (j < pre) | ((j >= lo) & (j < hi))
+    want = {"bidirectional": lambda: masks.bidirectional(L), "causal": lambda: masks.causal(L),
+            "block_causal": lambda: masks.block_causal(L, block),
+            "draft_train": lambda: masks.draft_training(L // 2 // block, block)}[pattern]()
+    assert np.array_equal(vis, want)
+    assert ((0 <= m[0]) & (m[0] <= L) & (0 <= m[1]) & (m[1] <= m[2]) & (m[2] <= L)).all()
+
+
+def test_attn_mask_build_validation():
+    L = dd.lib()
+    out = (ctypes.c_int32 * 64)()
+    assert L.dd_attn_mask_build(1, 8, 0, None) == 1
+    assert L.dd_attn_mask_build(9, 8, 0, out) == 1
+    assert L.dd_attn_mask_build(1, 0, 0, out) == 1
+    assert L.dd_attn_mask_build(2, 8, 0, out) == 1
+    assert L.dd_attn_mask_build(3, 9, 1, out) == 2      # L odd
+    assert L.dd_attn_mask_build(3, 12, 4, out) == 2     # L/2 = 6 not a multiple of 4
+    assert L.dd_attn_mask_build(3, 12, 3, out) == 0
+
+
+def _lora_cfg(**over):
+    return {**workloads.model_cfg(1, n_layers=2), "lora_rank": 16, "lora_alpha": 32.0, **over}
+
+
+def test_lora_param_layout_matches_oracle_storage():
+    cfg = _lora_cfg()
+    specs = oparams.specs(cfg)
+    assert dd.param_count(cfg) == len(specs) == 2 + 12 * 2 + 3 + 4 * 2
+    es = 2 if cfg["dtype"] == "bf16" else 4
+    end = 0
+    for tid, (name, shape, _) in enumerate(specs):
+        off, r, cc = dd.param_tensor(cfg, tid)
+        assert (r, cc) == (tuple(shape) if len(shape) == 2 else (1, shape[0])), name
+        assert off % 256 == 0 and off >= end
+        end = off + int(np.prod(shape)) * es
+    assert dd.param_bytes(cfg) >= end
+    P = oparams.init_params(cfg, 4)
+    blob = dd.pack_params(cfg, oparams.storage_tensors(cfg, P))
+    assert blob.size == dd.param_bytes(cfg)
+
+
+def test_lora_workspace_and_validation():
+    base = workloads.model_cfg(1, n_layers=2)
+    cfg = _lora_cfg()
+    B, Lq = 2, 64
+    d, F, r = cfg["d_model"], cfg["d_mlp"], cfg["lora_rank"]
+    grow = dd.workspace_bytes(cfg, B, Lq) - dd.workspace_bytes(base, B, Lq)
+    es = 2 if cfg["dtype"] == "bf16" else 4
+    assert 3 * B * Lq * r * es <= grow <= 3 * B * Lq * r * es + 3 * 256
+    L = dd.lib()
+    for bad in (dict(lora_rank=12), dict(lora_rank=-8), dict(lora_alpha=0.0), dict(lora_alpha=float("inf"))):
+        c = dd.make_config(_lora_cfg(**bad))
+        assert L.dd_param_count(ctypes.byref(c)) == 0
+        assert L.dd_denoise_forward_ex(ctypes.byref(c), FAKE, FAKE, 1, 8, 0.5, None, None, FAKE, 64, FAKE,
+                                       1 << 30, None) == 1
+    # a gate for a model without adapters is an argument error, found before any launch
+    c = dd.make_config(base)
+    assert L.dd_denoise_forward_ex(ctypes.byref(c), FAKE, FAKE, 1, 8, 0.5, None, FAKE, FAKE, 64, FAKE,
+                                   1 << 30, None) == 1
+    assert b"adapters" in L.dd_last_error()
+    c = dd.make_config(cfg)
+    assert L.dd_denoise_forward_ex(ctypes.byref(c), FAKE, FAKE, 1, 8, 0.5, None, FAKE, FAKE, 64, FAKE,
+                                   16, None) == 4

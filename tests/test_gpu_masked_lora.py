@@ -1,0 +1,193 @@
+"""GPU parity of the denoiser under attention patterns and with gated LoRA adapters, through
+dd_denoise_forward_ex, against the float64 oracle on the same seeded inputs.
+
+Patterns: causal (AR pathway, drafting pass), block-causal, the [x, z_1] block-diffusion pattern;
+lengths that span several 128-query workgroups and 64-key tiles with a ragged tail, block sizes
+aligned and not aligned to the tiles.  Adapters: the paper's rank 128 / alpha 256 on the bf16
+GPT-2-small shape, a rank whose K = in + r misses the 128 multiple (fallback GEMM), the fp32 build,
+mixed per-position gates, and the teacher property of the [x, z_1] pass.
+"""
+import numpy as np
+import pytest
+
+import workloads
+from oracle import forward as oforward, masks as omasks, params as oparams
+from paper_2609_04010_amd import _lib as dd
+from tests.gpu_util import dev_i32, say, torch_or_skip
+
+pytestmark = pytest.mark.gpu
+
+LOGIT_TOL = {"bf16": 5e-2, "fp32": 1e-4}
+
+
+def _vis(pattern, L, block):
+    return {"bidirectional": lambda: omasks.bidirectional(L), "causal": lambda: omasks.causal(L),
+            "block_causal": lambda: omasks.block_causal(L, block),
+            "draft_train": lambda: omasks.draft_training(L // 2 // block, block)}[pattern]()
+
+
+def _params(torch, cfg, seed, src):
+    if src == "seeded":
+        buf = torch.zeros(dd.param_bytes(cfg), dtype=torch.uint8, device="cuda")
+        dd.init_params(cfg, buf, seed=seed)
+        return oparams.init_params(cfg, seed), buf
+    P = oparams.split_storage(cfg, workloads.host_params(cfg, seed, oparams.specs(cfg)))
+    blob = dd.pack_params(cfg, oparams.storage_tensors(cfg, P))
+    buf = torch.zeros(blob.size, dtype=torch.uint8, device="cuda")
+    dd.init_params(cfg, buf, host_blob=blob)
+    return P, buf
+
+
+def _forward_ex(torch, cfg, buf, z, at, mask=None, gate=None):
+    B, L = z.shape
+    V = cfg["vocab"]
+    ld = int(dd.logits_ld(V))
+    tdt = torch.bfloat16 if cfg["dtype"] == "bf16" else torch.float32
+    logits = torch.zeros((B * L, ld), dtype=tdt, device="cuda")
+    ws = torch.zeros(dd.workspace_bytes(cfg, B, L), dtype=torch.uint8, device="cuda")
+    dmask = dev_i32(torch, np.asarray(mask).reshape(-1)) if mask is not None else None
+    dgate = dev_i32(torch, gate) if gate is not None else None
+    dd.denoise_forward_ex(cfg, buf, dev_i32(torch, z), B, L, at, logits, ld, ws, attn_mask=dmask, lora_gate=dgate)
+    err = dd.read_device_error(ws[:4].view(torch.int32))
+    return logits[:, :V].float().cpu().numpy().astype(np.float64).reshape(B, L, V), err
+
+
+def _tokens(cfg, c, B, L, mf=0.5):
+    V = cfg["vocab"]
+    if cfg["prior"] == "mask":
+        return workloads.masked_state(workloads.seeds(c)["data"], B, L, V, mf)
+    return workloads.uniform_state(workloads.seeds(c)["data"], B, L, V)
+
+
+MASK_CASES = [
+    # workload, overrides, B, L, pattern, block, alpha_t
+    (1, {}, 3, 32, "causal", 0, 0.5),
+    (1, {"max_len": 64}, 2, 60, "draft_train", 5, 0.3),
+    (2, {"n_layers": 2}, 2, 300, "causal", 0, 0.5),
+    (2, {"n_layers": 2}, 2, 300, "block_causal", 100, 0.4),
+    (2, {"n_layers": 2}, 2, 256, "block_causal", 64, 0.6),
+    (2, {"n_layers": 2}, 2, 320, "draft_train", 16, 1.0),
+    (2, {"n_layers": 2}, 1, 264, "draft_train", 33, 0.8),
+    (2, {"n_layers": 2}, 2, 200, "bidirectional", 0, 0.5),
+]
+
+
+@pytest.mark.parametrize("case", MASK_CASES, ids=lambda c: f"w{c[0]}-L{c[3]}-{c[4]}{c[5] or ''}")
+def test_masked_forward_parity(case):
+    torch = torch_or_skip()
+    c, over, B, L, pattern, block, at = case
+    say("masked forward", case)
+    cfg = workloads.model_cfg(c, **over)
+    P, buf = _params(torch, cfg, workloads.seeds(c)["param"], "seeded" if c == 1 else "host")
+    z = _tokens(cfg, c, B, L)
+    mask = dd.attn_mask_build(pattern, L, block)
+    got, err = _forward_ex(torch, cfg, buf, z, at, mask)
+    assert err == 0
+    ref = oforward.forward(cfg, P, z, at, _vis(pattern, L, block))
+    e = float(np.abs(got - ref).max())
+    say(f"max |dlogit| = {e:.3e} (logit std {ref.std():.3f})")
+    assert e <= LOGIT_TOL[cfg["dtype"]]
+
+
+def test_full_pattern_equals_unmasked_kernel():
+    """The pattern kernel with every key visible reproduces the unmasked kernel."""
+    torch = torch_or_skip()
+    cfg = workloads.model_cfg(2, n_layers=2)
+    P, buf = _params(torch, cfg, 5, "host")
+    z = _tokens(cfg, 2, 2, 200)
+    a, _ = _forward_ex(torch, cfg, buf, z, 0.5)
+    b, err = _forward_ex(torch, cfg, buf, z, 0.5, dd.attn_mask_build("bidirectional", 200))
+    d = float(np.abs(a - b).max())
+    say(f"full pattern vs unmasked: max diff {d:.3e}, identical {np.array_equal(a, b)}")
+    assert err == 0 and d <= 1e-3
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "fp32"])
+def test_invalid_pattern_entry_is_reported_and_sees_every_key(dtype):
+    torch = torch_or_skip()
+    over = {"n_layers": 2} if dtype == "bf16" else {}
+    c = 2 if dtype == "bf16" else 1
+    cfg = workloads.model_cfg(c, **over)
+    P, buf = _params(torch, cfg, 7, "host" if dtype == "bf16" else "seeded")
+    L = 96 if dtype == "bf16" else 32
+    z = _tokens(cfg, c, 1, L)
+    mask = dd.attn_mask_build("causal", L)
+    mask[0, 5] = L + 3                    # pre > L
+    mask[1, 9], mask[2, 9] = 4, 2         # lo > hi
+    got, err = _forward_ex(torch, cfg, buf, z, 0.5, mask)
+    assert err == dd.DD_DEVERR_MASK
+    vis = omasks.causal(L)
+    vis[5, :] = True
+    vis[9, :] = True
+    ref = oforward.forward(cfg, P, z, 0.5, vis)
+    e = float(np.abs(got - ref).max())
+    say(f"invalid entries: max |dlogit| = {e:.3e}")
+    assert e <= LOGIT_TOL[dtype]
+
+
+# ---------------------------------------------------------------- gated adapters
+
+LORA_CASES = [
+    # workload, overrides (rank, alpha, ...), B, L, pattern, block, gate kind, params source
+    (1, {"lora_rank": 8, "lora_alpha": 16.0}, 4, 32, "causal", 0, "mixed", "seeded"),
+    (1, {"lora_rank": 16, "lora_alpha": 32.0}, 2, 32, None, 0, None, "seeded"),
+    (2, {"n_layers": 2, "lora_rank": 128, "lora_alpha": 256.0}, 2, 192, "draft_train", 8, "noisy", "seeded"),
+    (2, {"n_layers": 2, "lora_rank": 128, "lora_alpha": 256.0}, 2, 300, None, 0, None, "host"),
+    (2, {"n_layers": 2, "lora_rank": 16, "lora_alpha": 64.0}, 2, 200, "causal", 0, "mixed", "host"),
+]
+
+
+def _gate(kind, L):
+    if kind is None:
+        return None
+    if kind == "noisy":              # adapters on the second half ([x, z_1]: z_1 only)
+        return (np.arange(L) >= L // 2).astype(np.int32)
+    return (np.arange(L) % 3 != 1).astype(np.int32)
+
+
+@pytest.mark.parametrize("case", LORA_CASES, ids=lambda c: f"w{c[0]}-r{c[1]['lora_rank']}-L{c[3]}-{c[4]}-{c[6]}")
+def test_gated_lora_forward_parity(case):
+    torch = torch_or_skip()
+    c, over, B, L, pattern, block, gk, src = case
+    say("gated lora forward", case)
+    cfg = workloads.model_cfg(c, **over)
+    P, buf = _params(torch, cfg, workloads.seeds(c)["param"] + 17, src)
+    z = _tokens(cfg, c, B, L)
+    mask = dd.attn_mask_build(pattern, L, block) if pattern else None
+    gate = _gate(gk, L)
+    got, err = _forward_ex(torch, cfg, buf, z, 0.5, mask, gate)
+    assert err == 0
+    ref = oforward.forward(cfg, P, z, 0.5, _vis(pattern, L, block) if pattern else None,
+                           None if gate is None else gate.astype(np.float64))
+    base_cfg = dict(cfg, lora_rank=0)
+    base = oforward.forward(base_cfg, {k: v for k, v in P.items() if "lora_" not in k}, z, 0.5,
+                            _vis(pattern, L, block) if pattern else None)
+    e = float(np.abs(got - ref).max())
+    say(f"max |dlogit| = {e:.3e}; adapter effect max {np.abs(ref - base).max():.3e} (logit std {ref.std():.3f})")
+    assert np.abs(ref - base).max() > 5 * LOGIT_TOL[cfg["dtype"]]   # the adapters matter here
+    assert e <= LOGIT_TOL[cfg["dtype"]]
+
+
+def test_teacher_logits_in_one_pass_match_base_model_on_gpu():
+    """Sec. 3.2 on the GPU: [x, z_1] with adapters on z_1 only gives, at x, the base model's causal
+    logits of x alone (run by the same library on a base-layout copy of the weights)."""
+    torch = torch_or_skip()
+    over = {"n_layers": 2, "lora_rank": 128, "lora_alpha": 256.0}
+    cfg = workloads.model_cfg(2, **over)
+    P, buf = _params(torch, cfg, 31, "host")
+    n, bs = 96, 8
+    x = workloads.clean_tokens(41, 2, n, cfg["vocab"])
+    seq = np.concatenate([x, np.full((2, n), cfg["vocab"])], axis=1)
+    gate = (np.arange(2 * n) >= n).astype(np.int32)
+    got, err = _forward_ex(torch, cfg, buf, seq, 1.0, dd.attn_mask_build("draft_train", 2 * n, bs), gate)
+    assert err == 0
+    base_cfg = dict(cfg, lora_rank=0)
+    Pb = {k: v for k, v in P.items() if "lora_" not in k}
+    blob = dd.pack_params(base_cfg, oparams.storage_tensors(base_cfg, Pb))
+    bbuf = torch.zeros(blob.size, dtype=torch.uint8, device="cuda")
+    dd.init_params(base_cfg, bbuf, host_blob=blob)
+    teach, err2 = _forward_ex(torch, base_cfg, bbuf, x, 1.0, dd.attn_mask_build("causal", n))
+    assert err2 == 0
+    d = float(np.abs(got[:, :n] - teach).max())
+    say(f"teacher logits: max diff {d:.3e}, identical {np.array_equal(got[:, :n], teach)}")
+    assert d <= 1e-3
