@@ -9,6 +9,12 @@ timed region.  Prints ONE JSON line.
   python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload 2] [--no-cpu-baseline]
   python bench.py --traffic-probe     (for rocprofv3 --pmc FETCH_SIZE / WRITE_SIZE runs: one 256 MiB
                                        device copy for calibration, then one forward pass; no output)
+  python bench.py --forward PATTERN[:BLOCK] [--lora-rank R --lora-alpha A --gate all|half]
+                                      (PATTERN: none, bidirectional, causal, block_causal, draft_train)
+                                      (forward passes only, dd_denoise_forward_ex on the workload's
+                                       B x L with an attention pattern and gated adapters: one JSON
+                                       line with ms per forward and per kernel class; not the
+                                       benchmark line)
 """
 import hashlib
 import argparse
@@ -116,6 +122,69 @@ def traffic_probe(c):
     torch.cuda.synchronize()
 
 
+def forward_bench(args):
+    """Time dd_denoise_forward_ex on the workload shape with a pattern and (optionally) adapters."""
+    import torch
+    import workloads
+    from paper_2609_04010_amd import _lib as dd
+    c = args.workload
+    w = workloads.CONFIGS[c]
+    over = {}
+    if args.lora_rank:
+        over = dict(lora_rank=args.lora_rank, lora_alpha=args.lora_alpha)
+    cfg = workloads.model_cfg(c, **over)
+    B, L, V = w["B"], w["L"], w["vocab"]
+    M, d, F, r = B * L, cfg["d_model"], cfg["d_mlp"], args.lora_rank
+    name, _, blk = args.forward.partition(":")
+    if name == "none":                   # no pattern: the unmasked attention kernel
+        mask, vis_pairs = None, L * L
+    else:
+        mask = dd.attn_mask_build(name, L, int(blk or 0))
+        j = np.arange(L)[None, :]
+        vis_pairs = int(((j < mask[0][:, None]) | ((j >= mask[1][:, None]) & (j < mask[2][:, None]))).sum())
+    dev = torch.device("cuda:0")
+    params = torch.zeros(dd.param_bytes(cfg), dtype=torch.uint8, device=dev)
+    dd.init_params(cfg, params, seed=workloads.seeds(c)["param"])
+    ld = int(dd.logits_ld(V))
+    logits = torch.empty((M, ld), dtype=torch.bfloat16, device=dev)
+    ws = torch.zeros(dd.workspace_bytes(cfg, B, L), dtype=torch.uint8, device=dev)
+    z = torch.from_numpy(workloads.masked_state(workloads.seeds(c)["data"], B, L, V, 0.5).reshape(-1)).to(dev)
+    dmask = torch.from_numpy(mask.reshape(-1).copy()).to(dev) if mask is not None else None
+    gate = None
+    if r and args.gate == "half":        # adapters on the second half of each sequence
+        gate = torch.from_numpy((np.arange(L) >= L // 2).astype(np.int32)).to(dev)
+    run = lambda: dd.denoise_forward_ex(cfg, params, z, B, L, 0.5, logits, ld, ws, attn_mask=dmask, lora_gate=gate)
+    for _ in range(max(1, args.warmup)):
+        run()
+    torch.cuda.synchronize()
+    per = 8 * cfg["n_layers"] + 8 + (4 * cfg["n_layers"] if r else 0)
+    dd.profile_begin(args.steps * per)
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        run()
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    dd.profile_end()
+    prof = dd.profile_read()
+    assert dd.read_device_error(ws[:4].view(torch.int32)) == 0
+    classes = {k: {"launches": n, "avg_ms": ms / n} for k, (n, ms) in prof.items()}
+    att = classes.get("attention")
+    out = {"mode": "forward", "workload": w["name"], "B": B, "L": L, "pattern": args.forward,
+           "visible_pairs": vis_pairs, "lora_rank": r, "lora_alpha": args.lora_alpha if r else None,
+           "gate": args.gate if r else None, "forwards": args.steps,
+           "ms_per_forward": elapsed / args.steps * 1e3, "classes": classes}
+    if att:   # 4 B d flops per visible (query, key) pair: Q K^T and P V
+        out["attention_tflops"] = 4.0 * B * d * vis_pairs / (att["avg_ms"] * 1e-3) / 1e12
+    if r and "gemm_lora_down" in classes:
+        nl = cfg["n_layers"]
+        down = 2.0 * M * r * (3 * d + F) * nl                # the four A projections of every layer
+        extra = 2.0 * M * r * (3 * d + d + F + d) * nl      # the r more K columns of the main GEMMs
+        out["lora_flops_per_forward"] = down + extra
+        lc = classes["gemm_lora_down"]
+        out["lora_down_tflops"] = down / (lc["launches"] / args.steps * lc["avg_ms"] * 1e-3) / 1e12
+    print(json.dumps(out), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -124,9 +193,16 @@ def main():
     ap.add_argument("--workload", type=int, default=2)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--traffic-probe", action="store_true")
+    ap.add_argument("--forward", default=None, help="attention pattern[:block] for forward-only timing")
+    ap.add_argument("--lora-rank", type=int, default=0)
+    ap.add_argument("--lora-alpha", type=float, default=256.0)
+    ap.add_argument("--gate", choices=["all", "half"], default="all")
     args = ap.parse_args()
     if args.traffic_probe:
         traffic_probe(args.workload)
+        return
+    if args.forward:
+        forward_bench(args)
         return
     if args.gpus != 1:
         log(f"bench.py measures one GPU only (asked for {args.gpus}); the sampling loop shards "

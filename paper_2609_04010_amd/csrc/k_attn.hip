@@ -24,6 +24,8 @@
 #include <limits.h>
 #include <math.h>
 
+#include <algorithm>
+
 #include "kernels.h"
 
 namespace dd {
@@ -79,7 +81,22 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(AttnArgs a) {
     // so that head's K and V are fetched into that XCD's L2 once and then re-read from it
     const int nqb = (a.L + AQ - 1) / AQ;
     const int work = xcd_linear(blockIdx.x, gridDim.x);
-    const int qb = work % nqb, bh = work / nqb;
+    int qb, bh;
+    if constexpr (MASKED) {
+        // Under a pattern the query blocks differ in work (causal: block qb sees qb + 1 blocks of
+        // keys).  The (batch, head) pairs go in groups of hgroup, about one XCD's worth of resident
+        // workgroups; inside a group the heaviest query blocks are dispatched first, so the long
+        // ones do not start last and form the tail.  K and V of a group stay within one XCD's L2.
+        const int nbh = a.H * a.B;
+        const int gsz = a.hgroup * nqb;
+        const int g = work / gsz, r = work - g * gsz;
+        const int gn = min(a.hgroup, nbh - g * a.hgroup);
+        qb = nqb - 1 - r / gn;
+        bh = g * a.hgroup + r % gn;
+    } else {
+        qb = work % nqb;
+        bh = work / nqb;
+    }
     const int h = bh % a.H, b = bh / a.H;
     const int L = a.L, d = a.d;
     const bf16_t* base = (const bf16_t*)a.qkv + (int64_t)b * L * a.ld;
@@ -334,11 +351,26 @@ bool attn_supported(int dtype, int dh) {
     return dh == 16 || dh == 32 || dh == 64 || dh == 128;
 }
 
-dd_status launch_attn(int dtype, const AttnArgs& a, hipStream_t s) {
-    const int dh = a.d / a.H;
+static int num_cus_attn() {
+    static int n = 0;
+    if (n == 0) {
+        int dev = 0, v = 0;
+        (void)hipGetDevice(&dev);
+        n = (hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess && v > 0) ? v : 256;
+    }
+    return n;
+}
+
+dd_status launch_attn(int dtype, const AttnArgs& a0, hipStream_t s) {
+    const int dh = a0.d / a0.H;
     ProfScope ps(KC_ATTN, s);
+    AttnArgs a = a0;
+    // resident workgroups per XCD (three per CU at the pattern kernel's register count), shared by
+    // the query blocks of hgroup (batch, head) pairs
+    const int nqb = ceil_div(a.L, AQ);
+    a.hgroup = std::max(1, (num_cus_attn() / 8) * 3 / nqb);
     if (dtype == DD_BF16) {
-        const dim3 grid((unsigned)(ceil_div(a.L, AQ) * a.H * a.B));
+        const dim3 grid((unsigned)(nqb * a.H * a.B));
         if (a.mask) hipLaunchKernelGGL(attn_bf16_kernel<true>, grid, dim3(256), 0, s, a);
         else hipLaunchKernelGGL(attn_bf16_kernel<false>, grid, dim3(256), 0, s, a);
     } else {

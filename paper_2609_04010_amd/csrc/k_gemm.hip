@@ -211,9 +211,12 @@ __global__ __launch_bounds__(256) void gemm_bf16_kernel(GemmArgs g, int tiles_m,
 // The 192-wide variant exists for tile quantisation: with d = 768 it divides N = 768, 2304 and
 // 3072 into whole rounds of 256 CUs.  Requires K % 128 == 0; rows past M or N are clamped (their
 // results are never stored).
-constexpr int DM = 256;                       // tile rows (M)
-// WGM x WGN wavefronts, each owning a WM x WN sub-tile of MB x NB 32x32 MFMA blocks.
-template <int TBN_, int WGM_, int WGN_> struct DLShape {
+constexpr int DM = 256;                       // tile rows (M) of the wide tiles
+// DM_ x TBN_ tiles over WGM x WGN wavefronts, each owning a WM x WN sub-tile of MB x NB 32x32 MFMA
+// blocks.  The 64-row form (64 x 128, four wavefronts side by side) serves skinny products: every
+// CU streams one 64-row strip of A while all of them share the small W through L2.
+template <int TBN_, int WGM_, int WGN_, int DM_ = DM> struct DLShape {
+    static constexpr int DM = DM_;                            // tile rows (M)
     static constexpr int TBN = TBN_;                          // tile columns (N)
     static constexpr int WGM = WGM_, WGN = WGN_, NW = WGM * WGN;
     static constexpr int THREADS = 64 * NW;
@@ -238,9 +241,10 @@ typedef __attribute__((address_space(1))) const void gbl_void;
 // Persistent: workgroup b takes tiles b, b + G, b + 2G, ... (G = grid size).  The number of K-tiles
 // is even, so the loads of the next tile's first K-tile go out during the last K-tile of the
 // current one into stage 0, which the staged epilogue leaves alone: they land while it runs.
-template <int EPI, int ROLE, int TBN_, int WGM_, int WGN_>
+template <int EPI, int ROLE, int TBN_, int WGM_, int WGN_, int DM_>
 __global__ __launch_bounds__(64 * WGM_ * WGN_, 1) void gemm_bf16_dl_kernel(GemmArgs g, int tiles_m, int tiles_n) {
-    using S = DLShape<TBN_, WGM_, WGN_>;
+    using S = DLShape<TBN_, WGM_, WGN_, DM_>;
+    constexpr int DM = S::DM;
     constexpr int MB = S::MB, NB = S::NB, NA = S::ALOADS, NWL = S::WLOADS;
     constexpr int AROWS = DM / S::NW, WROWS = S::TBN / S::NW;   // operand rows each wave loads
     extern __shared__ __attribute__((aligned(1024))) bf16_t smem[];
@@ -580,8 +584,11 @@ static void launch_tile(const GemmArgs& g, hipStream_t s) {
 // counting whole rounds of workgroups over the CUs (a round of 192-wide tiles takes about 0.85 of a
 // round of 256-wide ones on MI355X), in the 8-wavefront form (two wavefronts per SIMD, measured 2-6%
 // faster than four wavefronts of twice the sub-tile).  K % 128 != 0 falls back to the 128 x 128
-// register-staged kernel.  DD_GEMM_TILE (0..7) forces a variant for tuning and tests
-// (4: 256 x 256 / 4 waves, 5: 256 x 192 / 4 waves, 6: 256 x 256 / 8 waves, 7: 256 x 192 / 8 waves).
+// register-staged kernel.  Skinny products (N <= 128, e.g. an adapter down-projection to rank r)
+// take 64 x 128 register-staged tiles: the 256-row tiles would leave most CUs idle (M / 256
+// workgroups): direct-to-LDS when K % 128 == 0, else register-staged.  DD_GEMM_TILE (0..9) forces a
+// variant for tuning and tests (4: 256 x 256 / 4 waves, 5: 256 x 192 / 4 waves, 6: 256 x 256 /
+// 8 waves, 7: 256 x 192 / 8 waves, 8: 64 x 128 register-staged, 9: 64 x 128 direct-to-LDS).
 static int num_cus() {
     static int n = 0;
     if (n == 0) {
@@ -595,8 +602,9 @@ static int num_cus() {
 static int pick_tile(const GemmArgs& g) {
     const char* e = getenv("DD_GEMM_TILE");
     const int forced = e ? atoi(e) : -1;
-    if (forced >= 4 && forced <= 7 && g.K % (2 * BK) != 0) return 0;
-    if (forced >= 0 && forced <= 7 && !(g.a_rows && forced < 4)) return forced;
+    if (((forced >= 4 && forced <= 7) || forced == 9) && g.K % (2 * BK) != 0) return 0;
+    if (forced >= 0 && forced <= 9 && !(g.a_rows && (forced < 4 || forced == 8))) return forced;
+    if (g.N <= 128) return g.K % (2 * BK) == 0 ? 9 : (g.a_rows ? 0 : 8);
     if (g.K % (2 * BK) != 0) return 0;
     const int64_t ncu = num_cus();
     const int64_t tm = (g.M + DM - 1) / DM;
@@ -605,20 +613,20 @@ static int pick_tile(const GemmArgs& g) {
     return (17 * r192 < 20 * r256) ? 7 : 6;
 }
 
-template <int EPI, int ROLE, int TBN, int WGM, int WGN>
+template <int EPI, int ROLE, int TBN, int WGM, int WGN, int DMR = DM>
 static void launch_dl(const GemmArgs& g, hipStream_t s) {
-    using S = DLShape<TBN, WGM, WGN>;
-    const int tm = (g.M + DM - 1) / DM, tn = (g.N + S::TBN - 1) / S::TBN;
+    using S = DLShape<TBN, WGM, WGN, DMR>;
+    const int tm = (g.M + S::DM - 1) / S::DM, tn = (g.N + S::TBN - 1) / S::TBN;
     static bool attr = false;
     if (!attr) {
-        (void)hipFuncSetAttribute((const void*)gemm_bf16_dl_kernel<EPI, ROLE, TBN, WGM, WGN>,
+        (void)hipFuncSetAttribute((const void*)gemm_bf16_dl_kernel<EPI, ROLE, TBN, WGM, WGN, DMR>,
                                   hipFuncAttributeMaxDynamicSharedMemorySize, (int)S::LDS);
         attr = true;
     }
-    // persistent: at most one workgroup per CU (the LDS footprint allows no second one)
+    // persistent: at most one workgroup per CU
     const int grid = (int)std::min<int64_t>((int64_t)tm * tn, num_cus());
-    hipLaunchKernelGGL((gemm_bf16_dl_kernel<EPI, ROLE, TBN, WGM, WGN>), dim3(grid), dim3(S::THREADS), S::LDS, s,
-                       g, tm, tn);
+    hipLaunchKernelGGL((gemm_bf16_dl_kernel<EPI, ROLE, TBN, WGM, WGN, DMR>), dim3(grid), dim3(S::THREADS), S::LDS,
+                       s, g, tm, tn);
 }
 
 template <int EPI, int ROLE>
@@ -629,6 +637,8 @@ static void launch_epi(int dtype, const GemmArgs& g, hipStream_t s) {
             case 6: launch_dl<EPI, ROLE, 256, 2, 4>(g, s); break;
             case 5: launch_dl<EPI, ROLE, 192, 2, 2>(g, s); break;
             case 4: launch_dl<EPI, ROLE, 256, 2, 2>(g, s); break;
+            case 9: launch_dl<EPI, ROLE, 128, 1, 4, 64>(g, s); break;
+            case 8: launch_tile<64, 128, EPI>(g, s); break;
             case 3: launch_tile<256, 256, EPI>(g, s); break;
             case 2: launch_tile<256, 128, EPI>(g, s); break;
             case 1: launch_tile<128, 256, EPI>(g, s); break;

@@ -65,6 +65,7 @@ struct AttnArgs {
     // 0 <= lo <= hi <= L, or with no visible key, sets DD_DEVERR_MASK in *err and sees every key
     const int32_t* mask;
     int32_t* err;
+    int hgroup;   // set by launch_attn: (batch, head) pairs per dispatch group of the pattern kernel
 };
 
 dd_status launch_posterior(const PostArgs& a, int logits_dtype, hipStream_t s);
