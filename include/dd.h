@@ -61,6 +61,9 @@ typedef enum { DD_PRIOR_MASK = 0, DD_PRIOR_UNIFORM = 1 } dd_prior;
 /* Device error word bits. */
 #define DD_DEVERR_TOKEN 1
 #define DD_DEVERR_MASK 2   /* an attention-pattern entry was invalid (see dd_denoise_forward_ex) */
+#define DD_DEVERR_LOGITS 4 /* a row's logits gave no valid draw (NaN or +inf, or no finite
+                              logit where one is needed); that row's output is a fallback:
+                              z_s = z_t (posterior), z = 0 (verification) */
 
 /*
  * Denoiser architecture.  Pre-LN transformer, bidirectional attention (other
@@ -215,9 +218,11 @@ dd_status dd_denoise_forward_ex(const dd_config* cfg, const void* params,
  * dd_posterior_sample - one reverse-posterior draw per row (App. A.1 / A.2 with
  * x = softmax(logits); App. A.4 eq. psi-sampler at kappa_t = 1).
  *   prior        dd_prior
- *   logits       device [rows][ld] of logits_dtype (bf16 or fp32), finite or -inf;
- *                ld >= V, ld % 8 == 0.  Under the masked prior only rows whose
- *                z_t is the mask id are read.
+ *   logits       device [rows][ld] of logits_dtype (bf16 or fp32), finite or -inf,
+ *                at least one finite per read row; ld >= V, ld % 8 == 0.  Under the
+ *                masked prior only rows whose z_t is the mask id are read.  A row
+ *                that breaks this (NaN, +inf, all -inf) keeps z_s = z_t and sets
+ *                DD_DEVERR_LOGITS in dev_err.
  *   z_t          device int32 [rows]; z_s device int32 [rows], may alias z_t
  *   alpha_t, alpha_s  schedule values with 0 <= alpha_t < alpha_s <= 1 (s < t)
  *   noise_words  NULL: Philox4x32-10 noise under key `seed`, counters
@@ -227,7 +232,8 @@ dd_status dd_denoise_forward_ex(const dd_config* cfg, const void* params,
  *                A word w stands for the uniform u = (w + 1/2) 2^-32.
  *   probs        NULL, or device fp32 [rows][K] that receives the posterior
  *                probabilities (debug; slow).
- *   dev_err      NULL or device int32 error word (DD_DEVERR_TOKEN is or-ed in).
+ *   dev_err      NULL or device int32 error word (DD_DEVERR_TOKEN and
+ *                DD_DEVERR_LOGITS are or-ed in).
  * Draw: level 1 picks group g by argmax of log M_g + Gumbel (M_g = posterior
  * mass of the group of DD_GUMBEL_GROUP consecutive classes; the mask class is a
  * group of its own), level 2 picks the class in g by argmax of log p_j + Gumbel;
@@ -325,7 +331,9 @@ dd_status dd_psi_sample_loop(const dd_config* cfg, const void* params, int32_t B
  *   ws           device scratch >= dd_spec_verify_workspace_bytes(S, B) (row
  *                log-sum-exps)
  *   dev_err      NULL or device int32 error word (DD_DEVERR_TOKEN for a draft
- *                token outside [0, V), which is clamped).
+ *                token outside [0, V), which is clamped; DD_DEVERR_LOGITS when
+ *                the drawn row's logits hold NaN / +inf or no finite value, and
+ *                then z_out = 0 for that sequence).
  * Arithmetic in fp32.  Each emitted token is distributed as the target (the
  * tokens per verification forward pass are (n + 1) / 2 with the block's
  * always-accepted first token counted, between 1 and (B + 1) / 2).

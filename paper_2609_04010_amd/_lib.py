@@ -21,6 +21,7 @@ DD_PRIOR_MASK, DD_PRIOR_UNIFORM = 0, 1
 DD_GUMBEL_GROUP = 256
 DD_DEVERR_TOKEN = 1
 DD_DEVERR_MASK = 2
+DD_DEVERR_LOGITS = 4
 ATTN_PATTERNS = {"bidirectional": 0, "causal": 1, "block_causal": 2, "draft_train": 3}
 STATUS = {0: "DD_OK", 1: "DD_E_ARG", 2: "DD_E_SHAPE", 3: "DD_E_DTYPE", 4: "DD_E_WORKSPACE",
           5: "DD_E_HIP", 6: "DD_E_UNSUPPORTED", 7: "DD_E_DEVICE"}

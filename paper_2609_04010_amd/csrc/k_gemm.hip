@@ -267,13 +267,18 @@ __global__ __launch_bounds__(64 * WGM_ * WGN_, 1) void gemm_bf16_dl_kernel(GemmA
     // this lane's source rows: wave w fills A rows AROWS w + 8 i + lane / 8 and W rows
     // WROWS w + 8 i + lane / 8; its 16-byte slot lane % 8 holds K-chunk (lane % 8) ^ ((row >> 1) & 7)
     auto lchunk = [&](int row) { return (lane & 7) ^ ((row >> 1) & 7); };
-    int m0 = 0, n0 = 0;
+    // K order of a tile: K-tile t reads K-slice (t + skew) mod nk.  For the vocabulary projection
+    // the workgroups that share an operand tile (the 8 M-tiles of a group share W, the N-tiles of
+    // one M-tile share A) start at different K-slices, so they do not request the same L2 lines
+    // at the same moment (measured 8 % on that GEMM; the accumulation order is all that changes).
+    int m0 = 0, n0 = 0, skew = 0;
     int64_t offA[NA], offW[NWL];
     auto setup_tile = [&](int tile) {
         int tm, tn;
         map_tile(tile, nblocks, tiles_m, tiles_n, tm, tn);
         m0 = tm * DM;
         n0 = tn * S::TBN;
+        if constexpr (EPI == EPI_PLAIN) skew = ((tm & 7) + 2 * tn) % nk;
 #pragma unroll
         for (int i = 0; i < NA; ++i) {
             const int rl = AROWS * wave + 8 * i + (lane >> 3);
@@ -397,24 +402,50 @@ __global__ __launch_bounds__(64 * WGM_ * WGN_, 1) void gemm_bf16_dl_kernel(GemmA
     // epilogue of the tile at (m0, n0); n0 and the bias are read through the lambdas above, so the
     // caller keeps them describing this tile until the epilogue is done
     auto epilogue = [&](const int tm0) {
-        if constexpr (EPI == EPI_BIAS_RESID) {   // fp32 read-modify-write of the residual stream
+        if constexpr (EPI == EPI_BIAS_RESID) {
+            // The accumulators started from the residual h (loaded with the tile's first K-tile),
+            // so the epilogue only stores h + A W^T + bias.  One 32 x 32 block at a time goes
+            // through this wave's 4 KB of LDS (above stage 0) so that eight lanes write one 128-byte
+            // row segment (an MFMA lane holds four columns of 32 different rows).  Chunk slots are
+            // XOR-swizzled by row like the operand tiles (slot = chunk ^ ((row >> 1) & 7)), which
+            // keeps the row-per-lane writes and the row-segment reads free of bank conflicts.
+            __syncthreads();                      // every wave is done with the operand stages
+            float* cst = (float*)(smem + S::STAGE) + wave * (32 * 32);
+            float* C = (float*)g.C;
+            const bf16_t* bias = (const bf16_t*)g.bias;
+            const int rr = lane >> 3, c4 = (lane & 7) * 4;    // read-back: row rr + 8 it, columns c4..
 #pragma unroll
-            for (int nb = 0; nb < NB; ++nb)
+            for (int b = 0; b < MB * NB; ++b) {
+                const int mb = b % MB, nb = b / MB;
+                const int wr = lane & 31;
 #pragma unroll
                 for (int j4 = 0; j4 < 4; ++j4) {
-                    const int n = n0 + wn * S::WN + nb * 32 + 8 * j4 + 4 * (lane >> 5);
-                    if (n >= g.N) continue;
-                    float b4[4];
-                    bias4(nb, j4, b4);
+                    const int slot = (2 * j4 + (lane >> 5)) ^ ((wr >> 1) & 7);
+                    *(float4*)&cst[wr * 32 + slot * 4] =
+                        make_float4(acc[nb][mb][4 * j4], acc[nb][mb][4 * j4 + 1], acc[nb][mb][4 * j4 + 2],
+                                    acc[nb][mb][4 * j4 + 3]);
+                }
+                const int n = n0 + wn * S::WN + nb * 32 + c4;
+                float bv[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-                    for (int mb = 0; mb < MB; ++mb) {
-                        const int m = tm0 + wm * S::WM + mb * 32 + (lane & 31);
-                        if (m >= M) continue;
-                        float v[4] = {acc[nb][mb][4 * j4], acc[nb][mb][4 * j4 + 1], acc[nb][mb][4 * j4 + 2],
-                                      acc[nb][mb][4 * j4 + 3]};
-                        epilogue_bf16<EPI>(g, m, n, v, b4);
+                for (int e = 0; e < 4; ++e)
+                    if (n + e < g.N) bv[e] = bf16_to_f32(bias[n + e]);
+#pragma unroll
+                for (int it = 0; it < 4; ++it) {
+                    const int r = rr + 8 * it;
+                    const float4 v = *(const float4*)&cst[r * 32 + (((c4 >> 2) ^ ((r >> 1) & 7)) * 4)];
+                    const int m = tm0 + wm * S::WM + mb * 32 + r;
+                    if (m >= M) continue;
+                    float* dst = C + (int64_t)m * g.ldc + n;
+                    if (n + 3 < g.N) {
+                        *(float4*)dst = make_float4(v.x + bv[0], v.y + bv[1], v.z + bv[2], v.w + bv[3]);
+                    } else {
+                        const float o[4] = {v.x + bv[0], v.y + bv[1], v.z + bv[2], v.w + bv[3]};
+                        for (int e = 0; e < 4; ++e)
+                            if (n + e < g.N) dst[e] = o[e];
                     }
                 }
+            }
         } else {
             // bf16 outputs: each wave stages half of its WM x WN sub-tile at a time in LDS (rows
             // padded by 16 B, above stage 0), then writes whole row segments with 16-byte stores.
@@ -478,14 +509,43 @@ __global__ __launch_bounds__(64 * WGM_ * WGN_, 1) void gemm_bf16_dl_kernel(GemmA
     setup_tile(L);
     prefetch_bias();
 #pragma unroll
-    for (int j = 0; j < NL; ++j) issue_one(0, 0, j);
+    for (int j = 0; j < NL; ++j) issue_one(skew * BK, 0, j);
     while (true) {
+        const int cskew = skew;
+        if constexpr (EPI == EPI_BIAS_RESID) {
+            // residual epilogue: start from h (this lane's MFMA output positions), fetched together
+            // with the tile's first K-tile instead of after the K loop
+            const float* C = (const float*)g.C;
 #pragma unroll
-        for (int i = 0; i < NB; ++i)
+            for (int i = 0; i < NB; ++i)
 #pragma unroll
-            for (int j = 0; j < MB; ++j)
+                for (int j = 0; j < MB; ++j)
 #pragma unroll
-                for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
+                    for (int j4 = 0; j4 < 4; ++j4) {
+                        const int m = m0 + wm * S::WM + j * 32 + (lane & 31);
+                        const int n = n0 + wn * S::WN + i * 32 + 8 * j4 + 4 * (lane >> 5);
+                        float4 h = make_float4(0.f, 0.f, 0.f, 0.f);
+                        if (m < M && n + 3 < g.N) {
+                            h = *(const float4*)(C + (int64_t)m * g.ldc + n);
+                        } else if (m < M) {
+                            float t[4] = {0.f, 0.f, 0.f, 0.f};
+                            for (int e = 0; e < 4; ++e)
+                                if (n + e < g.N) t[e] = C[(int64_t)m * g.ldc + n + e];
+                            h = make_float4(t[0], t[1], t[2], t[3]);
+                        }
+                        acc[i][j][4 * j4] = h.x;
+                        acc[i][j][4 * j4 + 1] = h.y;
+                        acc[i][j][4 * j4 + 2] = h.z;
+                        acc[i][j][4 * j4 + 3] = h.w;
+                    }
+        } else {
+#pragma unroll
+            for (int i = 0; i < NB; ++i)
+#pragma unroll
+                for (int j = 0; j < MB; ++j)
+#pragma unroll
+                    for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
+        }
         const int Ln = L + (int)gridDim.x;
         const bool next = Ln < nblocks;
         const int tm0 = m0;
@@ -495,9 +555,11 @@ __global__ __launch_bounds__(64 * WGM_ * WGN_, 1) void gemm_bf16_dl_kernel(GemmA
                 setup_tile(Ln);
                 n0 = tn0;                         // the epilogue still describes this tile
             }
-            // after the very last K-tile this re-fetches K-tile 0 into stage 0 (unused, in bounds):
-            // one call site keeps the MFMA sequence in one copy
-            ktile(t, t + 1 < nk ? (t + 1) * BK : 0, std::true_type{});
+            // the last K-tile fetches the next tile's first K-slice (after the very last tile it
+            // re-fetches slice 0 into stage 0: unused, in bounds; one call site keeps the MFMA
+            // sequence in one copy)
+            const int next_k0 = t + 1 < nk ? ((t + 1 + cskew) % nk) * BK : (next ? skew * BK : 0);
+            ktile(t, next_k0, std::true_type{});
         }
         epilogue(tm0);
         if (!next) break;

@@ -271,7 +271,11 @@ __global__ __launch_bounds__(PT) void posterior_kernel(PostArgs a) {
         const int gstar = wave_argmax(best, bi);
 
         int result = V;
-        if (!(mask_prior && gstar == ngroups)) {   // level 2 inside the chosen group
+        if (gstar >= a.ntop || !isfinite(lse)) {
+            // no group had a valid score (NaN or +inf logits, or no finite logit): the row keeps
+            // its token and the caller is told; gstar must not index anything
+            result = -1;
+        } else if (!(mask_prior && gstar == ngroups)) {   // level 2 inside the chosen group
             best = -INFINITY;
             bi = 0x7FFFFFFF;
             const int base = gstar * DD_GUMBEL_GROUP + 4 * lane;
@@ -301,6 +305,11 @@ __global__ __launch_bounds__(PT) void posterior_kernel(PostArgs a) {
                 }
             }
             result = wave_argmax(best, bi);
+            if (result >= V) result = -1;           // no class of the group had a valid score
+        }
+        if (result < 0) {
+            if (lane == 0 && a.err) atomicOr(a.err, DD_DEVERR_LOGITS);
+            result = zt;
         }
         if (lane == 0) a.z_s[row] = result;
     }

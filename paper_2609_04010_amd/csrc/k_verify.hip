@@ -5,6 +5,8 @@
 // u_i (word (STREAM_VERIFY, step, row0 + s, i)):
 //   n = first i with u_i > min(1, p_i(x_i) / q_i(x_i)), else B
 //   z ~ Norm([p_n - q_n]_+) if n < B, else z ~ p_B     (p_n itself if the residual has no mass)
+// Rows whose logits give no valid draw (NaN, +inf, no finite logit) set DD_DEVERR_LOGITS and
+// emit z = 0.
 // z is drawn with the two-level Gumbel-max of the posterior kernel (groups of DD_GUMBEL_GROUP
 // classes, no mask group): the draw is invariant to the normaliser, so group masses and class
 // scores use the unnormalised residual.
@@ -173,10 +175,13 @@ __global__ __launch_bounds__(VT) void verify_kernel(VerifyArgs a, const float* l
         bi = take ? i2 : bi;
     }
     const int gstar = bi;
+    // no group with a valid score (NaN or +inf logits): report, emit token 0, index nothing
+    const bool bad = gstar >= ngroups || !isfinite(lp0) || (resid && !use_p && !isfinite(lq0));
     best = -INFINITY;
     bi = 0x7FFFFFFF;
     const int ntop = ngroups;
-    for (int j = gstar * DD_GUMBEL_GROUP + lane; j < min(V, (gstar + 1) * DD_GUMBEL_GROUP); j += 64) {
+    const int jend = bad ? 0 : min(V, (gstar + 1) * DD_GUMBEL_GROUP);
+    for (int j = bad ? 0 : gstar * DD_GUMBEL_GROUP + lane; j < jend; j += 64) {
         const float lpv = Elem<T>::load1(pr, j);
         const float lqv = (resid && !use_p) ? Elem<T>::load1(qr, j) : 0.f;
         const float sc = logf(cls_mass(lpv, lqv, use_p)) +
@@ -193,9 +198,11 @@ __global__ __launch_bounds__(VT) void verify_kernel(VerifyArgs a, const float* l
         best = take ? s2 : best;
         bi = take ? i2 : bi;
     }
+    const bool bad_z = bad || bi >= V;
     if (lane == 0) {
+        if (bad_z && a.err) atomicOr(a.err, DD_DEVERR_LOGITS);
         a.n_out[s] = n;
-        a.z_out[s] = bi;
+        a.z_out[s] = bad_z ? 0 : bi;
     }
 }
 

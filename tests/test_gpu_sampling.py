@@ -282,3 +282,40 @@ def test_gaussian_latent_parity(V, R, at):
     got = z.cpu().numpy()
     say(f"latent agree={np.mean(got == ref):.6f} kept={np.mean(ref == x):.4f}")
     assert np.array_equal(got, ref)
+
+
+@pytest.mark.parametrize("prior,dt", [("mask", "bf16"), ("uniform", "bf16"), ("mask", "fp32"), ("uniform", "fp32")])
+def test_degenerate_logit_rows_are_reported_and_keep_their_token(prior, dt):
+    """Rows with NaN, +inf or (uniform prior) no finite logit: DD_DEVERR_LOGITS, z_s = z_t there,
+    every other row bit-identical to the same call without those rows."""
+    torch = torch_or_skip()
+    say("degenerate rows", prior, dt)
+    R, V = 64, 700
+    lv = round_to_dtype(workloads.synthetic_logits(21, R, V, scale=2.0), dt)
+    zt = (np.full(R, V) if prior == "mask" else workloads.uniform_state(22, 1, R, V).reshape(-1)).astype(np.int64)
+    bad = {3: np.nan, 17: np.inf, 40: "allneg"}
+    lb = lv.copy()
+    for r, v in bad.items():
+        if v == "allneg":
+            lb[r, :] = -np.inf
+        else:
+            lb[r, 123] = v
+    ld = int(dd.logits_ld(V))
+    outs = []
+    for vals in (lv, lb):
+        lg = logits_dev(torch, vals, dt, ld)
+        zt_d = dev_i32(torch, zt)
+        zs_d = torch.empty_like(zt_d)
+        err = torch.zeros(1, dtype=torch.int32, device="cuda")
+        dd.posterior_sample(prior, lg, dt, ld, R, V, zt_d, 0.3, 0.6, zs_d, seed=9, step=4, dev_err=err)
+        outs.append((zs_d.cpu().numpy(), dd.read_device_error(err)))
+    (clean, e0), (dirty, e1) = outs
+    assert e0 == 0
+    flagged = list(bad)
+    assert e1 == dd.DD_DEVERR_LOGITS
+    for r in range(R):
+        if r in flagged:
+            assert dirty[r] == zt[r], (r, dirty[r])
+        else:
+            assert dirty[r] == clean[r], r
+    assert ((dirty >= 0) & (dirty <= V)).all()

@@ -123,3 +123,32 @@ def test_spec_verify_is_lossless_chi2():
     pvalue = stats.chisquare(counts, _softmax(p1) * S).pvalue
     say(f"lossless chi2 p = {pvalue:.4f}; acceptance {np.mean(n > 1):.3f}")
     assert pvalue > 1e-3
+
+
+def test_spec_verify_degenerate_logits_are_reported():
+    """NaN in every target row of one sequence: DD_DEVERR_LOGITS and z = 0 there.  NaN in the draft
+    rows of another: its draw stays valid (the residual falls back to p).  Every other sequence is
+    bit-identical to the clean call."""
+    torch = torch_or_skip()
+    S, B, V, dt = 8, 4, 600, "bf16"
+    pl, ql, draft = _case(17, S, B, V, dt, 0.3)
+    pd, qd = pl.copy(), ql.copy()
+    pd[2, :, 5] = np.nan
+    qd[5, :, 7] = np.nan
+    ld = int(dd.logits_ld(V))
+    res = []
+    for p_, q_ in ((pl, ql), (pd, qd)):
+        p_d = logits_dev(torch, p_.reshape(S * B, V), dt, ld)
+        q_d = logits_dev(torch, q_.reshape(S * (B - 1), V), dt, ld)
+        n = torch.empty(S, dtype=torch.int32, device="cuda")
+        z = torch.empty_like(n)
+        ws = torch.zeros(dd.spec_verify_workspace_bytes(S, B), dtype=torch.uint8, device="cuda")
+        err = torch.zeros(1, dtype=torch.int32, device="cuda")
+        dd.spec_verify(p_d, q_d, dt, ld, S, B, V, dev_i32(torch, draft), n, z, ws, seed=3, step=1, dev_err=err)
+        res.append((n.cpu().numpy(), z.cpu().numpy(), dd.read_device_error(err)))
+    (n0, z0, e0), (n1, z1, e1) = res
+    say(f"clean err {e0}, dirty err {e1}; seq 2 -> ({n1[2]}, {z1[2]}), seq 5 -> ({n1[5]}, {z1[5]})")
+    assert e0 == 0 and e1 == dd.DD_DEVERR_LOGITS
+    assert z1[2] == 0 and 1 <= n1[5] <= B and 0 <= z1[5] < V
+    keep = [s for s in range(S) if s not in (2, 5)]
+    assert np.array_equal(n0[keep], n1[keep]) and np.array_equal(z0[keep], z1[keep])
