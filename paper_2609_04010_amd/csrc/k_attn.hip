@@ -4,17 +4,20 @@
 // pattern all take this form).
 //
 // bf16 path (dh = 64): a workgroup of 4 wavefronts owns 128 queries of one (batch, head); each
-// wavefront owns 32 queries.  Key/value tiles of 64 tokens are staged in LDS (double-buffered,
-// prefetched through registers): K row-major (padded rows), V transposed so the P.V contraction
-// reads contiguous 16-byte fragments.
+// wavefront owns 32 queries.  Key/value tiles of 64 tokens go global -> LDS directly
+// (global_load_lds_dwordx4, double-buffered, no staging registers, which leaves room for four
+// wavefronts per SIMD), K and V both row-major in 128-byte rows whose 16-byte chunks are
+// XOR-swizzled by row; the P.V contraction reads its V^T operand with gfx950's transposing LDS
+// read (ds_read_b64_tr_b16).
 //   S^T = K Q^T with v_mfma_f32_32x32x16_bf16 (first operand: K rows from LDS; second: the wave's
 //         Q fragment, held in registers for the whole kernel).  Each lane then holds 32 scores of
 //         one query, the other 32 of the tile being in lane ^ 32.
 //   Online softmax in base 2 with the 1/sqrt(dh) scale folded into the exponent; the row max is
 //         combined with one cross-lane exchange; the running sum stays per lane until the end.
 //   O^T += V^T P^T: the probabilities are rounded to bf16 and used directly as the second MFMA
-//         operand (no shuffles: the key order of V^T in LDS is permuted to match the accumulator
-//         layout of S^T), so each lane's output column is again its own query.
+//         operand (no shuffles), so each lane's output column is again its own query.  The first
+//         operand needs, per lane, one head column of V at the 8 keys the accumulator layout of S^T
+//         gives that lane's probabilities: two transposing reads of 4 consecutive keys each.
 // Patterns (MASKED instance): a workgroup visits only the key tiles that meet the union of its
 // queries' visible sets (the prefix tiles, then the window tiles); a wavefront whose queries see
 // nothing of a tile skips its arithmetic; a tile that every query of the wavefront sees whole takes
@@ -25,6 +28,7 @@
 #include <math.h>
 
 #include <algorithm>
+#include <type_traits>
 
 #include "kernels.h"
 
@@ -36,13 +40,30 @@ typedef __attribute__((ext_vector_type(16))) float f32x16;
 constexpr int AQ = 128;  // queries per workgroup
 constexpr int AK = 64;   // keys per tile
 constexpr int DH = 64;
-constexpr int KSTR = DH + 8;
-constexpr int VSTR = AK + 8;
+constexpr int KROW = DH;   // bf16 per LDS row (128 bytes, no padding: chunks are swizzled)
 
-// Key order inside a transposed V row: within each 16-key step s the MFMA operand slots of lane
-// group g hold keys 16s + 4g + {0..3} and 16s + 8 + 4g + {0..3}; those eight keys are stored
-// contiguously at positions 16s + 8g .. + 7 (key 16s + 4g + 8h + r at position 16s + 8g + 4h + r),
-// so each lane reads its operand with one 16-byte load.
+typedef short v4s __attribute__((ext_vector_type(4)));
+typedef short v8s __attribute__((ext_vector_type(8)));
+
+// ds_read_b64_tr_b16 (gfx950): in each group of 16 lanes the 16 addresses name a 16 x 4 matrix M of
+// 16-bit elements (row j: the 4 elements at lane j's address); lane i receives M[4e + i/4][i % 4],
+// e = 0..3.  With lane j of the group pointing at V[k0 + j / 4][c0 + 4 (j % 4)] (row-major V), lane i
+// receives V[k0 + e][c0 + i]: four consecutive keys of head column c0 + i.
+//
+// LDS rows are 128 bytes (one key, 64 head columns); even rows fill banks 0-31, odd rows 32-63.
+// 16-byte chunk c of row r sits at slot c ^ sw(r):
+//   K: sw(r) = (r >> 1) & 7 -- a fragment read (16 lanes: rows r0..r0+15, one chunk) meets 8
+//      different slots in each bank half;
+//   V: sw(r) = r & 6 -- a transposing read (16 lanes: rows k..k+3, k % 4 == 0, two adjacent chunks
+//      x, x ^ 1 per row) gives rows k and k + 2 the slot pairs {x, x ^ 1} and {x ^ 2, x ^ 3}.
+DD_DEV int ksw(int r) { return (r >> 1) & 7; }
+DD_DEV int vsw(int r) { return r & 6; }
+
+typedef __attribute__((address_space(3))) void lds_void;
+typedef __attribute__((address_space(1))) const void gbl_void;
+DD_DEV v4s ds_read_tr16(const bf16_t* p) {
+    return __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) v4s*)p);
+}
 
 DD_DEV int wave_max_i(int v) {
 #pragma unroll
@@ -71,9 +92,9 @@ DD_DEV void query_window(const AttnArgs& a, int qi, int& pre, int& lo, int& hi) 
 }
 
 template <bool MASKED>
-__global__ __launch_bounds__(256) void attn_bf16_kernel(AttnArgs a) {
-    __shared__ __attribute__((aligned(16))) bf16_t Ks[2][AK * KSTR];
-    __shared__ __attribute__((aligned(16))) bf16_t Vt[2][DH * VSTR];
+__global__ __launch_bounds__(256, MASKED ? 3 : 4) void attn_bf16_kernel(AttnArgs a) {
+    __shared__ __attribute__((aligned(1024))) bf16_t Ks[2][AK * KROW];
+    __shared__ __attribute__((aligned(1024))) bf16_t Vs[2][AK * KROW];
     __shared__ int sh_rng[4][3];
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -160,49 +181,50 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(AttnArgs a) {
     const int ntiles = tp + (tw1 - tw0);
     auto tile_of = [&](int k) { return k < tp ? k : tw0 + (k - tp); };
 
-    // K tile: thread handles 16-byte chunks c = tid + 256 r (key c / 8, columns 8 (c % 8) ..).
-    // V tile (stored transposed): thread handles dv chunk vc = tid / 32 and the pair of keys that
-    // sit at transposed positions 2 vp, 2 vp + 1 (vp = tid % 32); these are adjacent keys, so each
-    // dv row receives one 32-bit word per thread (a half-wave writes 128 contiguous bytes).
-    const int vc = tid >> 5, vp = tid & 31;
-    const int vkey = 16 * (vp >> 3) + 4 * ((vp >> 2) & 1) + 8 * ((vp >> 1) & 1) + 2 * (vp & 1);
-    uint4 rk[2], rv[2];
-    auto gload = [&](int kb0) {
+    // Tile loads: 8 KB of K and 8 KB of V per tile, eight 1 KB wave instructions each; wavefront w
+    // issues K and V instructions 2w and 2w + 1 (rows 8 i .. 8 i + 7).  Lane l fills LDS slot l % 8 of
+    // row 8 i + l / 8 with the global chunk that belongs there.  Keys past L read row L - 1 (their
+    // scores are masked to -inf, so their probabilities are exactly 0).
+    // Per-lane offsets (elements from the tile's first key row, under 64 rows of the qkv matrix, so
+    // well inside 32 bits) are fixed; a tile adds kb0 rows.  The ragged last tile (rows past L read
+    // row L - 1) takes a separate, scalar-branched path.
+    const int sl = lane & 7;
+    int ok[2], ov[2];
 #pragma unroll
-        for (int r = 0; r < 2; ++r) {
-            const int c = tid + 256 * r, key = c >> 3, dc = (c & 7) * 8, t = kb0 + key;
-            rk[r] = (t < L) ? *(const uint4*)(base + (int64_t)t * a.ld + d + h * DH + dc)
-                            : make_uint4(0u, 0u, 0u, 0u);
-            const int tv = kb0 + vkey + r;
-            rv[r] = (tv < L) ? *(const uint4*)(base + (int64_t)tv * a.ld + 2 * d + h * DH + 8 * vc)
-                             : make_uint4(0u, 0u, 0u, 0u);
+    for (int ii = 0; ii < 2; ++ii) {
+        const int r = 8 * (2 * wave + ii) + (lane >> 3);
+        ok[ii] = r * (int)a.ld + d + h * DH + 8 * (sl ^ ksw(r));
+        ov[ii] = r * (int)a.ld + 2 * d + h * DH + 8 * (sl ^ vsw(r));
+    }
+    auto dma = [&](int kb0, int buf) {
+        const bf16_t* tb = base + (int64_t)kb0 * a.ld;
+        if (kb0 + AK <= L) {
+#pragma unroll
+            for (int ii = 0; ii < 2; ++ii) {
+                const int i = 2 * wave + ii;
+                __builtin_amdgcn_global_load_lds((gbl_void*)(tb + ok[ii]), (lds_void*)&Ks[buf][8 * i * KROW], 16, 0, 0);
+                __builtin_amdgcn_global_load_lds((gbl_void*)(tb + ov[ii]), (lds_void*)&Vs[buf][8 * i * KROW], 16, 0, 0);
+            }
+        } else {
+#pragma unroll
+            for (int ii = 0; ii < 2; ++ii) {
+                const int i = 2 * wave + ii, r = 8 * i + (lane >> 3);
+                const bf16_t* row = tb + (int64_t)min(r, L - 1 - kb0) * a.ld + h * DH;
+                __builtin_amdgcn_global_load_lds((gbl_void*)(row + d + 8 * (sl ^ ksw(r))),
+                                                 (lds_void*)&Ks[buf][8 * i * KROW], 16, 0, 0);
+                __builtin_amdgcn_global_load_lds((gbl_void*)(row + 2 * d + 8 * (sl ^ vsw(r))),
+                                                 (lds_void*)&Vs[buf][8 * i * KROW], 16, 0, 0);
+            }
         }
-    };
-    auto sstore = [&](int buf) {
-#pragma unroll
-        for (int r = 0; r < 2; ++r) {
-            const int c = tid + 256 * r, key = c >> 3, dc = (c & 7) * 8;
-            *(uint4*)&Ks[buf][key * KSTR + dc] = rk[r];
-        }
-        const uint32_t a0[4] = {rv[0].x, rv[0].y, rv[0].z, rv[0].w};
-        const uint32_t a1[4] = {rv[1].x, rv[1].y, rv[1].z, rv[1].w};
-        uint32_t wv[8];   // wv[e] = (V[key][8 vc + e], V[key + 1][8 vc + e]) as a bf16 pair
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-            wv[2 * e] = __builtin_amdgcn_perm(a1[e], a0[e], 0x05040100u);
-            wv[2 * e + 1] = __builtin_amdgcn_perm(a1[e], a0[e], 0x07060302u);
-        }
-        uint32_t* vt = (uint32_t*)&Vt[buf][0];
-#pragma unroll
-        for (int e = 0; e < 8; ++e) vt[((8 * vc + e) * VSTR + 2 * vp) >> 1] = wv[e];
     };
 
-    // One 64-key tile.
     // The exponent reference mref is raised only when a row's maximum exceeds it by more than
     // RESCALE (base-2 units), so probabilities stay below 2^RESCALE and the O accumulators are
     // rescaled only on those rare steps (checked once per wavefront).
     constexpr float RESCALE = 8.0f;
-    auto tile = [&](int k) {
+    // One 64-key tile; `part`: the tile is not entirely visible to every query of the wavefront
+    // (the ragged last tile, or pattern boundaries), so scores get the per-element key test.
+    auto tile = [&](int k, bool part) {
         const int buf = k & 1, kb0 = tile_of(k) * AK;
         f32x16 sacc[2];
 #pragma unroll
@@ -211,29 +233,19 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(AttnArgs a) {
             for (int e = 0; e < 16; ++e) sacc[kb][e] = 0.f;
 #pragma unroll
             for (int kk = 0; kk < 4; ++kk) {
-                const bf16x8 kf = *(const bf16x8*)&Ks[buf][(kb * 32 + (lane & 31)) * KSTR + kk * 16 + grp * 8];
+                const int kr = kb * 32 + (lane & 31);
+                const bf16x8 kf = *(const bf16x8*)&Ks[buf][kr * KROW + 8 * ((2 * kk + grp) ^ ksw(kr))];
                 sacc[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[kk], sacc[kb], 0, 0, 0);
             }
         }
-        if constexpr (MASKED) {
-            // whole tile visible to every query of the wavefront (then also inside L)?
-            const bool whole = kb0 + AK <= pmin || (kb0 >= lomax && kb0 + AK <= himin);
-            if (!whole) {
-#pragma unroll
-                for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-                    for (int j = 0; j < 16; ++j) {
-                        const int key = kb0 + kb * 32 + 8 * (j >> 2) + 4 * grp + (j & 3);
-                        if (!(key < qpre || (key >= qlo && key < qhi))) sacc[kb][j] = -INFINITY;
-                    }
-            }
-        } else if (kb0 + AK > L) {   // wave-uniform: only the last tile can run past L
+        if (part) {
 #pragma unroll
             for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
                 for (int j = 0; j < 16; ++j) {
                     const int key = kb0 + kb * 32 + 8 * (j >> 2) + 4 * grp + (j & 3);
-                    if (key >= L) sacc[kb][j] = -INFINITY;
+                    const bool vis = MASKED ? (key < qpre || (key >= qlo && key < qhi)) : key < L;
+                    if (!vis) sacc[kb][j] = -INFINITY;
                 }
         }
         float mloc = -INFINITY;
@@ -244,6 +256,9 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(AttnArgs a) {
         mloc = fmaxf(mloc, __shfl_xor(mloc, 32, 64)) * a.scale_log2;
         const bool raise = mloc > mrow + RESCALE;
         if (__any(raise)) {
+            // rare after the first tile: kept a real branch (an empty volatile asm stops the
+            // compiler from executing the 33 multiplies below unconditionally)
+            asm volatile("");
             const float mnew = raise ? mloc : mrow;
             // a row that has seen no visible key keeps mrow = -inf: its factor must be 1, not NaN
             const float corr = MASKED && !raise ? 1.0f : __builtin_amdgcn_exp2f(mrow - mnew);
@@ -270,9 +285,16 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(AttnArgs a) {
             bf16x8 pf;
 #pragma unroll
             for (int e = 0; e < 8; ++e) pf[e] = (__bf16)sacc[s4 >> 1][8 * (s4 & 1) + e];
+            // this lane's 8 operand keys: 4 grp + {0..3} and 8 + 4 grp + {0..3} within the step's 16
+            const int vk = (s4 >> 1) * 32 + 16 * (s4 & 1) + 4 * grp + ((lane & 15) >> 2);
 #pragma unroll
             for (int blk = 0; blk < 2; ++blk) {
-                const bf16x8 vf = *(const bf16x8*)&Vt[buf][(blk * 32 + (lane & 31)) * VSTR + s4 * 16 + grp * 8];
+                // column blk 32 + 16 ((lane >> 4) & 1) + 4 (lane & 3): chunk vc, half vh
+                const int vc = 4 * blk + 2 * ((lane >> 4) & 1) + ((lane >> 1) & 1), vh = 4 * (lane & 1);
+                const v4s lo = ds_read_tr16(&Vs[buf][vk * KROW + 8 * (vc ^ vsw(vk)) + vh]);
+                const v4s hi = ds_read_tr16(&Vs[buf][(vk + 8) * KROW + 8 * (vc ^ vsw(vk + 8)) + vh]);
+                const v8s v8 = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+                const bf16x8 vf = __builtin_bit_cast(bf16x8, v8);
                 o[blk] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf, o[blk], 0, 0, 0);
             }
         }
@@ -281,16 +303,19 @@ __global__ __launch_bounds__(256) void attn_bf16_kernel(AttnArgs a) {
     auto wave_needs = [&](int kb0) {
         return !MASKED || kb0 < pmax || (kb0 < whi && kb0 + AK > wlo);
     };
-    if (ntiles > 0) {
-        gload(tile_of(0) * AK);
-        sstore(0);
-    }
+    // tile k + 1 streams into the other buffer while tile k is computed; that buffer was last
+    // read in tile k - 1, which every wavefront finished before the barrier ending it
+    if (ntiles > 0) dma(tile_of(0) * AK, 0);
+    __builtin_amdgcn_s_waitcnt(0x3F70);          // vmcnt(0)
     __syncthreads();
     for (int k = 0; k < ntiles; ++k) {
-        if (k + 1 < ntiles) gload(tile_of(k + 1) * AK);
-        if (wave_needs(tile_of(k) * AK)) tile(k);
-        if (k + 1 < ntiles) sstore((k + 1) & 1);
-        __syncthreads();
+        if (k + 1 < ntiles) dma(tile_of(k + 1) * AK, (k + 1) & 1);
+        const int kb0 = tile_of(k) * AK;
+        // is the tile entirely visible to every query of this wavefront (and inside L)?
+        const bool whole = MASKED ? (kb0 + AK <= pmin || (kb0 >= lomax && kb0 + AK <= himin)) : kb0 + AK <= L;
+        if (wave_needs(kb0)) tile(k, !whole);
+        __builtin_amdgcn_s_waitcnt(0x3F70);      // vmcnt(0): this lane's loads of tile k + 1 landed
+        __syncthreads();                          // ... everyone's
     }
 
     const float l = lpart + __shfl_xor(lpart, 32, 64);
