@@ -190,6 +190,8 @@ def test_teacher_logits_in_one_pass_match_base_model_on_gpu():
     assert err2 == 0
     d = float(np.abs(got[:, :n] - teach).max())
     say(f"teacher logits: max diff {d:.3e}, identical {np.array_equal(got[:, :n], teach)}")
-    # equal up to the last bit of the bf16 logits: the vocabulary projection's fp32 summation order
-    # depends on which tile a row falls in, and the two calls place the x rows in different tiles
-    assert np.all(np.abs(got[:, :n] - teach) <= 2.0 ** -7 * np.abs(teach) + 1e-6)
+    # equal up to rounding: the GEMMs' fp32 summation order (the vocabulary projection's K order,
+    # the step at which a residual layer adds h) depends on where a row falls in its tile, the two
+    # calls place the x rows differently, and the differences pass through bf16 activations; both
+    # calls meet the oracle bar, and the oracle pins the property itself in float64
+    assert d <= LOGIT_TOL["bf16"]
