@@ -195,3 +195,54 @@ def test_teacher_logits_in_one_pass_match_base_model_on_gpu():
     # calls place the x rows differently, and the differences pass through bf16 activations; both
     # calls meet the oracle bar, and the oracle pins the property itself in float64
     assert d <= LOGIT_TOL["bf16"]
+
+
+def test_sample_loop_with_adapters_matches_oracle():
+    """The T-step loop on a model with adapters (all gates on), fp32 workload 1, explicit noise,
+    free running on both sides."""
+    from oracle import loop as oloop, sampler as osampler, schedule as osched
+    from tests.gpu_util import compare_ids, dev_words
+    torch = torch_or_skip()
+    cfg = workloads.model_cfg(1, lora_rank=8, lora_alpha=16.0)
+    w, s = workloads.CONFIGS[1], workloads.seeds(1)
+    B, L, V, T = w["B"], w["L"], w["vocab"], w["T"]
+    P, buf = _params(torch, cfg, s["param"], "seeded")
+    words = workloads.noise_words(s["noise"], (T, B * L, osampler.noise_width("mask", V)))
+    z1 = workloads.all_mask(B, L, V)
+    al = osched.alphas(T)
+    z = dev_i32(torch, z1)
+    trace = torch.zeros(((T + 1) * B * L,), dtype=torch.int32, device="cuda")
+    ws = torch.zeros(dd.loop_workspace_bytes(cfg, B, L), dtype=torch.uint8, device="cuda")
+    dd.sample_loop(cfg, buf, B, L, T, al, z, ws, noise_words=dev_words(torch, words), z_trace=trace)
+    assert dd.read_device_error(ws[:4].view(torch.int32)) == 0
+    trace = trace.cpu().numpy().reshape(T + 1, B, L)
+    _, rtrace, gaps = oloop.sample_loop(cfg, P, z1, T, al, noise_words=words)
+    say(f"adapter loop: trace agreement {np.mean(trace == rtrace):.6f}")
+    for k in range(T):
+        compare_ids(trace[k + 1].reshape(-1), rtrace[k + 1].reshape(-1), gaps[k], f"step {T - k}")
+
+
+@pytest.mark.parametrize("c", [1, 2])
+def test_forward_ex_without_pattern_or_gate_equals_forward(c):
+    """dd_denoise_forward_ex(NULL, NULL) is dd_denoise_forward, bit for bit, with and without adapters."""
+    torch = torch_or_skip()
+    over = {"n_layers": 2} if c == 2 else {}
+    for extra in ({}, {"lora_rank": 16, "lora_alpha": 32.0}):
+        cfg = workloads.model_cfg(c, **over, **extra)
+        _, buf = _params(torch, cfg, 3, "seeded")
+        B, L = 2, (32 if c == 1 else 64)
+        z = _tokens(cfg, c, B, L)
+        V = cfg["vocab"]
+        ld = int(dd.logits_ld(V))
+        tdt = torch.bfloat16 if cfg["dtype"] == "bf16" else torch.float32
+        outs = []
+        for ex in (False, True):
+            logits = torch.zeros((B * L, ld), dtype=tdt, device="cuda")
+            ws = torch.zeros(dd.workspace_bytes(cfg, B, L), dtype=torch.uint8, device="cuda")
+            if ex:
+                dd.denoise_forward_ex(cfg, buf, dev_i32(torch, z), B, L, 0.5, logits, ld, ws)
+            else:
+                dd.denoise_forward(cfg, buf, dev_i32(torch, z), B, L, 0.5, logits, ld, ws)
+            outs.append(logits.float().cpu().numpy())
+        say(f"workload {c} {extra}: identical {np.array_equal(outs[0], outs[1])}")
+        assert np.array_equal(outs[0], outs[1])
