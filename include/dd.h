@@ -128,7 +128,8 @@ size_t dd_param_bytes(const dd_config* cfg);
 /* Workspace for dd_denoise_forward (activations; the device error word is its
  * first int32).  0 if the configuration is invalid. */
 size_t dd_workspace_bytes(const dd_config* cfg, int32_t B, int32_t L);
-/* Workspace for dd_sample_loop: the forward workspace plus one logit matrix. */
+/* Workspace for dd_sample_loop: the forward workspace plus one logit matrix,
+ * the compacted row list and the per-group log-sum-exps of every logit row. */
 size_t dd_loop_workspace_bytes(const dd_config* cfg, int32_t B, int32_t L);
 /* Recommended logit row stride (elements): V rounded up to a multiple of 64. */
 int64_t dd_logits_ld(int32_t V);
@@ -281,8 +282,12 @@ dd_status dd_psi_posterior_sample(int32_t prior, const void* logits, int32_t log
  *                each step.
  *   ws           device workspace >= dd_loop_workspace_bytes(cfg, B, L).
  * Masked prior (bf16): each step lists the still-masked rows and runs the vocabulary projection
- * and the draw on those rows only; carried-over rows need no logits.  The result is identical to
- * calling dd_denoise_forward and dd_posterior_sample on every row.
+ * and the draw on those rows only; carried-over rows need no logits.  bf16 with d_model % 128
+ * == 0: the vocabulary projection also writes, beside each logit row, the log-sum-exp of each
+ * group of DD_GUMBEL_GROUP classes (from the rounded logits it stores), and the draw reads those
+ * and one group of logits per row instead of the whole row.  The result equals calling
+ * dd_denoise_forward and dd_posterior_sample on every row, up to the summation order inside each
+ * group's log-sum-exp (a draw can differ only where two level-1 scores lie within a few ulps).
  */
 dd_status dd_sample_loop(const dd_config* cfg, const void* params, int32_t B, int32_t L,
                          int32_t T, const double* alphas, int32_t* z,

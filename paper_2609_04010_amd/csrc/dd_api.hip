@@ -3,6 +3,7 @@
 #include <math.h>
 #include <stdarg.h>
 #include <stdio.h>
+#include <stdlib.h>
 #include <stdint.h>
 #include <string.h>
 
@@ -159,7 +160,8 @@ static bool is_gain(const dd_config* c, int id) {
 }
 
 struct WsLayout {
-    size_t err, temb, h, xln, qkv, att, mlp, logits, rows, count, total_fwd, total_loop;
+    size_t err, temb, h, xln, qkv, att, mlp, logits, rows, count, glse, total_fwd, total_loop;
+    int64_t glse_ld;   // per-group log-sum-exps per logits row (a multiple of 4 floats)
 };
 
 // xln, att and mlp (the inputs of the projections) carry r more columns with adapters: the gated
@@ -182,6 +184,8 @@ static WsLayout ws_layout(const dd_config* c, int64_t M) {
     off = align256(off + (size_t)(M * ld) * es);
     w.rows = off; off = align256(off + (size_t)M * 4);
     w.count = off; off = align256(off + 4);
+    w.glse_ld = ((c->vocab + DD_GUMBEL_GROUP - 1) / DD_GUMBEL_GROUP + 3) / 4 * 4;
+    w.glse = off; off = align256(off + (size_t)(M * w.glse_ld) * 4);
     w.total_loop = off;
     return w;
 }
@@ -203,12 +207,15 @@ static bool forward_supported(const dd_config* c) {
 // vocab_rows / vocab_count (device, nullable): restrict the vocabulary projection to the listed
 // rows, written compacted (row j of `logits` belongs to token row vocab_rows[j]).
 // attn_mask (device [3L], nullable): visibility pattern; lora_gate (device [L], nullable): adapter
-// gate per position (all on when NULL).
+// gate per position (all on when NULL).  vocab_lse (device, nullable; bf16 with d % 128 == 0): the
+// vocabulary projection also writes each logits row's per-group log-sum-exps there, row stride
+// lse_ld.
 static dd_status run_forward(const dd_config* c, const void* params, const int32_t* z, int32_t B,
                              int32_t L, double alpha_t, void* logits, int64_t ld, char* ws,
                              hipStream_t s, const int32_t* vocab_rows = nullptr,
                              const int32_t* vocab_count = nullptr,
-                             const int32_t* attn_mask = nullptr, const int32_t* lora_gate = nullptr) {
+                             const int32_t* attn_mask = nullptr, const int32_t* lora_gate = nullptr,
+                             float* vocab_lse = nullptr, int64_t lse_ld = 0) {
     const std::vector<Tensor> T = tensor_list(c);
     const WsLayout w = ws_layout(c, (int64_t)B * L);
     const char* P = (const char*)params;
@@ -263,13 +270,11 @@ static dd_status run_forward(const dd_config* c, const void* params, const int32
         const int gn = (l + 1 < nl) ? b + 12 : lnf;
         DD_TRY(launch_ln(dt, h, M, d, tp(gn), tp(gn + 1), c->norm_eps, xln, dr, s));
     }
-    if (vocab_rows) {   // only the listed rows (count on the device) get logits, compacted
-        GemmArgs g = {xln, dr, tp(lnf + 2), d, nullptr, logits, ld, (int)M, V, d, vocab_rows, vocab_count};
-        DD_TRY(launch_gemm(dt, EPI_PLAIN, KC_GEMM_VOCAB, g, s));
-    } else {
-        GemmArgs g = {xln, dr, tp(lnf + 2), d, nullptr, logits, ld, (int)M, V, d, nullptr, nullptr};
-        DD_TRY(launch_gemm(dt, EPI_PLAIN, KC_GEMM_VOCAB, g, s));
-    }
+    // with vocab_rows only the listed rows (count on the device) get logits, compacted
+    GemmArgs g = {xln, dr, tp(lnf + 2), d, nullptr, logits, ld, (int)M, V, d, vocab_rows, vocab_count};
+    g.lse = vocab_lse;
+    g.lse_ld = lse_ld;
+    DD_TRY(launch_gemm(dt, vocab_lse ? EPI_LSE : EPI_PLAIN, KC_GEMM_VOCAB, g, s));
     (void)es;
     return DD_OK;
 }
@@ -571,11 +576,18 @@ dd_status dd_psi_sample_loop(const dd_config* cfg, const void* params, int32_t B
     const bool compact = cfg->prior == DD_PRIOR_MASK && gemm_gather_supported(cfg->dtype, cfg->d_model);
     int32_t* rows = (int32_t*)(wsc + w.rows);
     int32_t* count = (int32_t*)(wsc + w.count);
+    // bf16 path: the vocabulary projection also emits each row's per-group log-sum-exps, so the
+    // draw reads one group of logits per row instead of the whole row.  DD_POSTERIOR_PASS=1 keeps
+    // the posterior's own pass over the rows instead (for comparison and tuning).
+    const char* pass_env = getenv("DD_POSTERIOR_PASS");
+    const bool fused = gemm_lse_supported(cfg->dtype, cfg->d_model) && !(pass_env && atoi(pass_env) == 1);
+    float* glse = fused ? (float*)(wsc + w.glse) : nullptr;
     DD_TRY(trace_copy(0));
     for (int k = T; k >= 1; --k) {
         if (compact) DD_TRY(launch_compact(z, M, cfg->vocab, rows, count, s));
         DD_TRY(run_forward(cfg, params, z, B, L, alphas[k], logits, ld, wsc, s,
-                           compact ? rows : nullptr, compact ? count : nullptr));
+                           compact ? rows : nullptr, compact ? count : nullptr, nullptr, nullptr,
+                           glse, w.glse_ld));
         const uint32_t* nw = noise_words ? noise_words + (int64_t)(k - 1) * M * nu : nullptr;
         PostArgs a = make_post(cfg->prior, logits, ld, (int32_t)M, cfg->vocab, z, alphas[k],
                                alphas[k - 1], kappas ? kappas[k] : 1.0, nw, noise_seed, (uint32_t)k,
@@ -587,6 +599,8 @@ dd_status dd_psi_sample_loop(const dd_config* cfg, const void* params, int32_t B
             a.rows_idx = rows;
             a.count = count;
         }
+        a.glse = glse;
+        a.glse_ld = w.glse_ld;
         DD_TRY(launch_posterior(a, cfg->dtype, s));
         DD_TRY(trace_copy(T - k + 1));
     }

@@ -13,8 +13,9 @@
 // tiles in that XCD's L2.
 //
 // Epilogues: bias -> bf16 (QKV), bias + GELU(tanh) -> bf16 (MLP up), bias + fp32 residual add in
-// place (attention output, MLP down), plain store (vocabulary projection), per-row gate x scale ->
-// bf16 (adapter down-projection of a gated LoRA).
+// place (attention output, MLP down), plain store (vocabulary projection), plain store plus the
+// per-row log-sum-exp of each 256-column group (vocabulary projection feeding the sampler), per-row
+// gate x scale -> bf16 (adapter down-projection of a gated LoRA).
 #include <math.h>
 #include <stdlib.h>
 
@@ -50,6 +51,7 @@ DD_DEV void map_tile(int bid, int nblocks, int tiles_m, int tiles_n, int& tm, in
 
 // ------------------------------------------------------------------------------ bf16 MFMA
 constexpr int BK = 64, LSTR = BK + 8;
+constexpr float LOG2E_F = 1.4426950408889634f;
 
 // EPI_GATE row factor of output row m (m % gate_period is in range for any m, clamped rows too)
 DD_DEV float gate_row_scale(const GemmArgs& g, int m) {
@@ -234,6 +236,12 @@ template <int TBN_, int WGM_, int WGN_, int DM_ = DM> struct DLShape {
     static_assert(LDS <= 160 * 1024, "LDS");
 };
 
+// LDS of the direct-to-LDS kernel: the shape's stages and staging, plus for EPI_LSE the (max, sum)
+// partials of each tile row from each of the WGN wavefronts across it
+template <int EPI, class S> constexpr size_t dl_lds_bytes() {
+    return S::LDS + (EPI == EPI_LSE ? (size_t)S::DM * S::WGN * sizeof(float2) : 0);
+}
+
 typedef __attribute__((address_space(3))) void lds_void;
 typedef __attribute__((address_space(1))) const void gbl_void;
 
@@ -278,7 +286,7 @@ __global__ __launch_bounds__(64 * WGM_ * WGN_, 1) void gemm_bf16_dl_kernel(GemmA
         map_tile(tile, nblocks, tiles_m, tiles_n, tm, tn);
         m0 = tm * DM;
         n0 = tn * S::TBN;
-        if constexpr (EPI == EPI_PLAIN) skew = ((tm & 7) + 2 * tn) % nk;
+        if constexpr (EPI == EPI_PLAIN || EPI == EPI_LSE) skew = ((tm & 7) + 2 * tn) % nk;
 #pragma unroll
         for (int i = 0; i < NA; ++i) {
             const int rl = AROWS * wave + 8 * i + (lane >> 3);
@@ -395,7 +403,7 @@ __global__ __launch_bounds__(64 * WGM_ * WGN_, 1) void gemm_bf16_dl_kernel(GemmA
     auto bias4 = [&](int nb, int j4, float* b4) {
         uint2 r = make_uint2(0u, 0u);
         if constexpr (PREFETCH_BIAS) r = braw[nb][j4];
-        else if constexpr (EPI != EPI_PLAIN && EPI != EPI_GATE) r = load_bias4(nb, j4);
+        else if constexpr (EPI != EPI_PLAIN && EPI != EPI_GATE && EPI != EPI_LSE) r = load_bias4(nb, j4);
         b4[0] = bf16_lo(r.x); b4[1] = bf16_hi(r.x); b4[2] = bf16_lo(r.y); b4[3] = bf16_hi(r.y);
     };
 
@@ -501,6 +509,66 @@ __global__ __launch_bounds__(64 * WGM_ * WGN_, 1) void gemm_bf16_dl_kernel(GemmA
                         const uint32_t w[4] = {v.x, v.y, v.z, v.w};
                         for (int e = 0; n + e < g.N; ++e) dst[e] = (bf16_t)((w[e >> 1] >> (16 * (e & 1))) & 0xFFFFu);
                     }
+                }
+            }
+            if constexpr (EPI == EPI_LSE) {
+                // Log-sum-exp of each tile row over the tile's 256 columns (one sampling group), taken
+                // over the rounded values just stored.  Rounding is monotonic, so the row maximum is
+                // the rounded maximum of the accumulators.  A wave covers 64 columns of a row (lanes
+                // l and l ^ 32 hold 32 each); the WGN partial (max, sum) pairs of a row meet in LDS
+                // past the staging area.  Columns past N (clamped W rows) do not count.
+                static_assert(S::TBN == DD_GUMBEL_GROUP, "one tile column = one sampling group");
+                float2* part = (float2*)((char*)smem + S::LDS);
+                const int nl0 = ncol0 + 4 * (lane >> 5);
+                auto rows_partial = [&](auto ragged_c) {
+                    constexpr bool ragged = decltype(ragged_c)::value;
+#pragma unroll
+                    for (int mb = 0; mb < MB; ++mb) {
+                        float mx = -INFINITY;
+#pragma unroll
+                        for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+                            for (int j4 = 0; j4 < 4; ++j4)
+#pragma unroll
+                                for (int e = 0; e < 4; ++e)
+                                    if (!ragged || nl0 + nb * 32 + 8 * j4 + e < g.N)
+                                        mx = fmaxf(mx, acc[nb][mb][4 * j4 + e]);
+                        mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+                        const float mr = bf16_to_f32(f32_to_bf16(mx));
+                        const float moff = (mr == -INFINITY ? 0.f : mr) * -LOG2E_F;
+                        float sum = 0.f;
+#pragma unroll
+                        for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+                            for (int j4 = 0; j4 < 4; ++j4) {
+                                const uint32_t p0 = pack_bf16x2(acc[nb][mb][4 * j4], acc[nb][mb][4 * j4 + 1]);
+                                const uint32_t p1 = pack_bf16x2(acc[nb][mb][4 * j4 + 2], acc[nb][mb][4 * j4 + 3]);
+                                const float v[4] = {bf16_lo(p0), bf16_hi(p0), bf16_lo(p1), bf16_hi(p1)};
+#pragma unroll
+                                for (int e = 0; e < 4; ++e)
+                                    if (!ragged || nl0 + nb * 32 + 8 * j4 + e < g.N)
+                                        sum += __builtin_amdgcn_exp2f(fmaf(v[e], LOG2E_F, moff));
+                            }
+                        sum += __shfl_xor(sum, 32, 64);
+                        if (lane < 32) part[(wm * S::WM + mb * 32 + lane) * S::WGN + wn] = make_float2(mr, sum);
+                    }
+                };
+                if (n0 + S::TBN <= g.N) rows_partial(std::false_type{});
+                else rows_partial(std::true_type{});
+                __syncthreads();
+                if (tid < DM && tm0 + tid < M) {
+                    float2 p[S::WGN];
+                    float mm = -INFINITY;
+#pragma unroll
+                    for (int w = 0; w < S::WGN; ++w) {
+                        p[w] = part[tid * S::WGN + w];
+                        mm = fmaxf(mm, p[w].x);
+                    }
+                    const float mref = mm == -INFINITY ? 0.f : mm;
+                    float sum = 0.f;
+#pragma unroll
+                    for (int w = 0; w < S::WGN; ++w) sum += p[w].y * exp2f((p[w].x - mref) * LOG2E_F);
+                    g.lse[(int64_t)(tm0 + tid) * g.lse_ld + n0 / DD_GUMBEL_GROUP] = mref + logf(sum);
                 }
             }
         }
@@ -678,16 +746,18 @@ static int pick_tile(const GemmArgs& g) {
 template <int EPI, int ROLE, int TBN, int WGM, int WGN, int DMR = DM>
 static void launch_dl(const GemmArgs& g, hipStream_t s) {
     using S = DLShape<TBN, WGM, WGN, DMR>;
+    constexpr size_t lds = dl_lds_bytes<EPI, S>();
+    static_assert(lds <= 160 * 1024, "LDS");
     const int tm = (g.M + S::DM - 1) / S::DM, tn = (g.N + S::TBN - 1) / S::TBN;
     static bool attr = false;
     if (!attr) {
         (void)hipFuncSetAttribute((const void*)gemm_bf16_dl_kernel<EPI, ROLE, TBN, WGM, WGN, DMR>,
-                                  hipFuncAttributeMaxDynamicSharedMemorySize, (int)S::LDS);
+                                  hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
         attr = true;
     }
     // persistent: at most one workgroup per CU
     const int grid = (int)std::min<int64_t>((int64_t)tm * tn, num_cus());
-    hipLaunchKernelGGL((gemm_bf16_dl_kernel<EPI, ROLE, TBN, WGM, WGN, DMR>), dim3(grid), dim3(S::THREADS), S::LDS,
+    hipLaunchKernelGGL((gemm_bf16_dl_kernel<EPI, ROLE, TBN, WGM, WGN, DMR>), dim3(grid), dim3(S::THREADS), lds,
                        s, g, tm, tn);
 }
 
@@ -713,6 +783,7 @@ static void launch_epi(int dtype, const GemmArgs& g, hipStream_t s) {
 }
 
 bool gemm_gather_supported(int dtype, int K) { return dtype == DD_BF16 && K % (2 * BK) == 0; }
+bool gemm_lse_supported(int dtype, int K) { return dtype == DD_BF16 && K % (2 * BK) == 0; }
 
 dd_status launch_gemm(int dtype, int epi, int cls, const GemmArgs& g, hipStream_t s) {
     if (g.M == 0 || g.N == 0) return DD_OK;
@@ -724,6 +795,10 @@ dd_status launch_gemm(int dtype, int epi, int cls, const GemmArgs& g, hipStream_
         set_error("row-gathered GEMM needs the bf16 path and K %% 128 == 0");
         return DD_E_UNSUPPORTED;
     }
+    if (epi == EPI_LSE && (!gemm_lse_supported(dtype, g.K) || !g.lse || g.lse_ld < (g.N + 255) / 256)) {
+        set_error("group log-sum-exp epilogue needs the bf16 path, K %% 128 == 0 and an lse buffer");
+        return DD_E_UNSUPPORTED;
+    }
     ProfScope ps(cls, s);
     switch (epi) {
         case EPI_BIAS: launch_epi<EPI_BIAS, KC_GEMM_QKV>(dtype, g, s); break;
@@ -733,6 +808,8 @@ dd_status launch_gemm(int dtype, int epi, int cls, const GemmArgs& g, hipStream_
             else launch_epi<EPI_BIAS_RESID, KC_GEMM_MLP2>(dtype, g, s);
             break;
         case EPI_GATE: launch_epi<EPI_GATE, KC_GEMM_LORA>(dtype, g, s); break;
+        // one tile column per sampling group: always the 256-wide, 8-wavefront tile
+        case EPI_LSE: launch_dl<EPI_LSE, KC_GEMM_VOCAB, 256, 2, 4>(g, s); break;
         default: launch_epi<EPI_PLAIN, KC_GEMM_VOCAB>(dtype, g, s); break;
     }
     return launch_status("gemm");

@@ -10,6 +10,11 @@
 // optional full posterior row (a debug output) comes from a separate kernel in
 // float64.
 //
+// When the vocabulary projection has already produced the per-group
+// log-sum-exps (its epilogue computes them from the rounded logits it stores),
+// the pass over the row is skipped: one wavefront per row reads the group values
+// and the 256 logits of the chosen group only.
+//
 // The transition is the Psi sampler step (App. A.4, eq. psi-sampler) with correction strength
 // kappa; kappa = 1 is the ancestral posterior.  The host folds kappa into the coefficients.
 // Masked prior (App. A.1, eq. mdm-posterior; App. A.4, eq. psi-mdm), x = softmax(logits):
@@ -89,6 +94,137 @@ DD_DEV int32_t keep_or_remask(const PostArgs& a, int row, int zt) {
     return sm > sr ? a.V : zt;
 }
 
+// Level-1 and level-2 draws of one masked (or uniform-prior) row, by one wavefront, from the row's
+// per-group log-sum-exps glse[0 .. ngroups) (LDS or global memory) and its logits rowp (read only
+// at the chosen group and, uniform prior, at the current token zt).  Row log-sum-exp over the group
+// values, level 1 over the groups (4 per lane: one Philox block gives their 4 words) and level 2
+// over the 256 classes of the chosen group (4 per lane), all in fp32 with wavefront shuffles.
+template <typename T>
+DD_DEV void draw_row(const PostArgs& a, int row, int zt, const char* rowp, const float* glse, int lane) {
+    const int V = a.V;
+    const bool mask_prior = a.prior == DD_PRIOR_MASK;
+    const int ngroups = (V + DD_GUMBEL_GROUP - 1) / DD_GUMBEL_GROUP;
+    const uint32_t grow = a.row0 + (uint32_t)row;
+    float m = -INFINITY;
+    for (int g = lane; g < ngroups; g += 64) m = fmaxf(m, glse[g]);
+    m = wave_max(m);
+    const float mref = isinf(m) ? 0.f : m;
+    float sum = 0.f;
+    for (int g = lane; g < ngroups; g += 64) sum += expf(glse[g] - mref);
+    const float lse = mref + logf(wave_sum(sum));
+
+    float c_r = 0.f, Dn = 1.f, c_u = 0.f;
+    if (!mask_prior) {   // uniform prior: x_r enters the mass of the current token's class
+        const float xr = expf(Elem<T>::load1(rowp, zt) - lse);
+        c_r = (float)a.Ka_r * xr + (float)a.c_z;
+        Dn = (float)a.Ka_t * xr + (float)a.one_m_at;
+        c_u = (float)a.c_u + (float)a.u1 * Dn;
+    }
+    const float log_wx = (float)a.log_wx, log_wm = (float)a.log_wm;
+    const float c_x = (float)a.c_x, log_dn = logf(Dn);
+    const uint32_t k0 = (uint32_t)a.seed, k1 = (uint32_t)(a.seed >> 32);
+
+    // level 1: group g has log mass log w_x + lse_g - lse (mask prior; the mask class is group
+    // `ngroups`) or log((c_x X_g + n_g c_u + [r in g] c_r) / D) (uniform prior)
+    float best = -INFINITY;
+    int bi = 0x7FFFFFFF;
+    for (int gb = 0; gb < a.ntop; gb += 256) {
+        const int base = gb + 4 * lane;
+        if (base >= a.ntop) break;
+        uint32_t wd[4];
+        if (a.noise) {
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+                wd[i] = (base + i < a.ntop) ? a.noise[(int64_t)row * a.nu + base + i] : 0u;
+        } else {
+            const Words4 W = philox4x32_10((uint32_t)(base >> 2), grow, a.step, STREAM_TOP, k0, k1);
+#pragma unroll
+            for (int i = 0; i < 4; ++i) wd[i] = W.w[i];
+        }
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const int g = base + i;
+            if (g >= a.ntop) continue;
+            float logm;
+            if (mask_prior) {
+                logm = (g < ngroups) ? log_wx + (glse[g] - lse) : log_wm;
+            } else {
+                const int lo = g * DD_GUMBEL_GROUP;
+                const int n = min(DD_GUMBEL_GROUP, V - lo);
+                const float X = expf(glse[g] - lse);
+                logm = logf(c_x * X + (float)n * c_u + ((zt >= lo && zt < lo + n) ? c_r : 0.f)) - log_dn;
+            }
+            const float sc = logm + word_gumbel_f(wd[i]);
+            const bool take = sc > best || (sc == best && g < bi);
+            best = take ? sc : best;
+            bi = take ? g : bi;
+        }
+    }
+    const int gstar = wave_argmax(best, bi);
+
+    int result = V;
+    if (gstar >= a.ntop || !isfinite(lse)) {
+        // no group had a valid score (NaN or +inf logits, or no finite logit): the row keeps
+        // its token and the caller is told; gstar must not index anything
+        result = -1;
+    } else if (!(mask_prior && gstar == ngroups)) {   // level 2 inside the chosen group
+        best = -INFINITY;
+        bi = 0x7FFFFFFF;
+        const int base = gstar * DD_GUMBEL_GROUP + 4 * lane;
+        if (base < V) {
+            uint32_t wd[4];
+            if (a.noise) {
+#pragma unroll
+                for (int i = 0; i < 4; ++i)
+                    wd[i] = (base + i < V) ? a.noise[(int64_t)row * a.nu + a.ntop + base + i] : 0u;
+            } else {
+                const Words4 W = philox4x32_10((uint32_t)(base >> 2), grow, a.step, STREAM_CLASS, k0, k1);
+#pragma unroll
+                for (int i = 0; i < 4; ++i) wd[i] = W.w[i];
+            }
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const int j = base + i;
+                if (j >= V) continue;
+                const float l = Elem<T>::load1(rowp, j);
+                float logp;
+                if (mask_prior) logp = log_wx + (l - lse);
+                else logp = logf(c_x * expf(l - lse) + c_u + (j == zt ? c_r : 0.f)) - log_dn;
+                const float sc = logp + word_gumbel_f(wd[i]);
+                const bool take = sc > best || (sc == best && j < bi);
+                best = take ? sc : best;
+                bi = take ? j : bi;
+            }
+        }
+        result = wave_argmax(best, bi);
+        if (result >= V) result = -1;           // no class of the group had a valid score
+    }
+    if (result < 0) {
+        if (lane == 0 && a.err) atomicOr(a.err, DD_DEVERR_LOGITS);
+        result = zt;
+    }
+    if (lane == 0) a.z_s[row] = result;
+}
+
+// The row's current token into zt (an id outside the K classes is flagged and clamped).  Returns
+// false when the row is settled without its logits: masked prior, unmasked row (carry-over, or
+// keep/remask under kappa < 1), whose z_s the leader thread has written.
+DD_DEV bool row_needs_draw(const PostArgs& a, int row, bool leader, int& zt) {
+    const int V = a.V;
+    const bool mask_prior = a.prior == DD_PRIOR_MASK;
+    const int K = mask_prior ? V + 1 : V;
+    zt = a.z_t[row];
+    if (zt < 0 || zt >= K) {
+        if (leader && a.err) atomicOr(a.err, DD_DEVERR_TOKEN);
+        zt = zt < 0 ? 0 : K - 1;
+    }
+    if (mask_prior && zt != V) {
+        if (leader) a.z_s[row] = a.remask ? keep_or_remask(a, row, zt) : zt;
+        return false;
+    }
+    return true;
+}
+
 template <typename T>
 __global__ __launch_bounds__(PT) void posterior_kernel(PostArgs a) {
     extern __shared__ float s_lse[];  // one log-sum-exp per group
@@ -103,23 +239,11 @@ __global__ __launch_bounds__(PT) void posterior_kernel(PostArgs a) {
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int V = a.V;
-    const bool mask_prior = a.prior == DD_PRIOR_MASK;
-    const int K = mask_prior ? V + 1 : V;
-    const uint32_t grow = a.row0 + (uint32_t)row;
-
-    int zt = a.z_t[row];
-    if (zt < 0 || zt >= K) {
-        if (tid == 0 && a.err) atomicOr(a.err, DD_DEVERR_TOKEN);
-        zt = zt < 0 ? 0 : K - 1;
-    }
-    if (mask_prior && zt != V) {  // carry-over or keep/remask: the row's logits are never read
-        if (tid == 0) a.z_s[row] = a.remask ? keep_or_remask(a, row, zt) : zt;
-        return;
-    }
+    int zt;
+    if (!row_needs_draw(a, row, tid == 0, zt)) return;
 
     const char* rowp = (const char*)a.logits + (size_t)blockIdx.x * (size_t)a.ld * sizeof(T);
     const int nchunk = (V + E - 1) / E;
-    const int ngroups = (V + DD_GUMBEL_GROUP - 1) / DD_GUMBEL_GROUP;
 
     // ---- pass over the row: per-group log-sum-exp ---------------------------------------
     // Elements past V count as -inf: chunks past the row are filled with -inf bits, and the one
@@ -207,113 +331,29 @@ __global__ __launch_bounds__(PT) void posterior_kernel(PostArgs a) {
     }
     __syncthreads();
 
-    // ---- tail: one wavefront finishes the row (no further workgroup barrier) ---------------
-    // Row log-sum-exp over the group values, level 1 over the groups (4 per lane: one Philox block
-    // gives their 4 words) and level 2 over the 256 classes of the chosen group (4 per lane), all in
-    // fp32 with wavefront shuffles.  The other wavefronts leave unless the debug output is wanted.
+    // ---- tail: one wavefront finishes the row (no further workgroup barrier); the other
+    // wavefronts leave
     if ((tid >> 6) != 0) return;
-    {
-        float m = -INFINITY;
-        for (int g = lane; g < ngroups; g += 64) m = fmaxf(m, s_lse[g]);
-        m = wave_max(m);
-        const float mref = isinf(m) ? 0.f : m;
-        float sum = 0.f;
-        for (int g = lane; g < ngroups; g += 64) sum += expf(s_lse[g] - mref);
-        const float lse = mref + logf(wave_sum(sum));
+    draw_row<T>(a, row, zt, rowp, s_lse, lane);
+}
 
-        float c_r = 0.f, Dn = 1.f, c_u = 0.f;
-        if (!mask_prior) {   // uniform prior: x_r enters the mass of the current token's class
-            const float xr = expf(Elem<T>::load1(rowp, zt) - lse);
-            c_r = (float)a.Ka_r * xr + (float)a.c_z;
-            Dn = (float)a.Ka_t * xr + (float)a.one_m_at;
-            c_u = (float)a.c_u + (float)a.u1 * Dn;
-        }
-        const float log_wx = (float)a.log_wx, log_wm = (float)a.log_wm;
-        const float c_x = (float)a.c_x, log_dn = logf(Dn);
-        const uint32_t k0 = (uint32_t)a.seed, k1 = (uint32_t)(a.seed >> 32);
-
-        // level 1: group g has log mass log w_x + lse_g - lse (mask prior; the mask class is group
-        // `ngroups`) or log((c_x X_g + n_g c_u + [r in g] c_r) / D) (uniform prior)
-        float best = -INFINITY;
-        int bi = 0x7FFFFFFF;
-        for (int gb = 0; gb < a.ntop; gb += 256) {
-            const int base = gb + 4 * lane;
-            if (base >= a.ntop) break;
-            uint32_t wd[4];
-            if (a.noise) {
-#pragma unroll
-                for (int i = 0; i < 4; ++i)
-                    wd[i] = (base + i < a.ntop) ? a.noise[(int64_t)row * a.nu + base + i] : 0u;
-            } else {
-                const Words4 W = philox4x32_10((uint32_t)(base >> 2), grow, a.step, STREAM_TOP, k0, k1);
-#pragma unroll
-                for (int i = 0; i < 4; ++i) wd[i] = W.w[i];
-            }
-#pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                const int g = base + i;
-                if (g >= a.ntop) continue;
-                float logm;
-                if (mask_prior) {
-                    logm = (g < ngroups) ? log_wx + (s_lse[g] - lse) : log_wm;
-                } else {
-                    const int lo = g * DD_GUMBEL_GROUP;
-                    const int n = min(DD_GUMBEL_GROUP, V - lo);
-                    const float X = expf(s_lse[g] - lse);
-                    logm = logf(c_x * X + (float)n * c_u + ((zt >= lo && zt < lo + n) ? c_r : 0.f)) - log_dn;
-                }
-                const float sc = logm + word_gumbel_f(wd[i]);
-                const bool take = sc > best || (sc == best && g < bi);
-                best = take ? sc : best;
-                bi = take ? g : bi;
-            }
-        }
-        const int gstar = wave_argmax(best, bi);
-
-        int result = V;
-        if (gstar >= a.ntop || !isfinite(lse)) {
-            // no group had a valid score (NaN or +inf logits, or no finite logit): the row keeps
-            // its token and the caller is told; gstar must not index anything
-            result = -1;
-        } else if (!(mask_prior && gstar == ngroups)) {   // level 2 inside the chosen group
-            best = -INFINITY;
-            bi = 0x7FFFFFFF;
-            const int base = gstar * DD_GUMBEL_GROUP + 4 * lane;
-            if (base < V) {
-                uint32_t wd[4];
-                if (a.noise) {
-#pragma unroll
-                    for (int i = 0; i < 4; ++i)
-                        wd[i] = (base + i < V) ? a.noise[(int64_t)row * a.nu + a.ntop + base + i] : 0u;
-                } else {
-                    const Words4 W = philox4x32_10((uint32_t)(base >> 2), grow, a.step, STREAM_CLASS, k0, k1);
-#pragma unroll
-                    for (int i = 0; i < 4; ++i) wd[i] = W.w[i];
-                }
-#pragma unroll
-                for (int i = 0; i < 4; ++i) {
-                    const int j = base + i;
-                    if (j >= V) continue;
-                    const float l = Elem<T>::load1(rowp, j);
-                    float logp;
-                    if (mask_prior) logp = log_wx + (l - lse);
-                    else logp = logf(c_x * expf(l - lse) + c_u + (j == zt ? c_r : 0.f)) - log_dn;
-                    const float sc = logp + word_gumbel_f(wd[i]);
-                    const bool take = sc > best || (sc == best && j < bi);
-                    best = take ? sc : best;
-                    bi = take ? j : bi;
-                }
-            }
-            result = wave_argmax(best, bi);
-            if (result >= V) result = -1;           // no class of the group had a valid score
-        }
-        if (result < 0) {
-            if (lane == 0 && a.err) atomicOr(a.err, DD_DEVERR_LOGITS);
-            result = zt;
-        }
-        if (lane == 0) a.z_s[row] = result;
+// Rows whose per-group log-sum-exps came with the logits (the vocabulary projection's group
+// log-sum-exp epilogue): one wavefront per row, four rows per workgroup, and no pass over the row.
+template <typename T>
+__global__ __launch_bounds__(256) void posterior_grouped_kernel(PostArgs a) {
+    const int lane = threadIdx.x & 63;
+    const int j = (int)blockIdx.x * 4 + (int)(threadIdx.x >> 6);   // logits row
+    int row = j;
+    if (a.count) {
+        if (j >= *a.count) return;
+        row = a.rows_idx[j];
+    } else if (j >= a.rows) {
+        return;
     }
-
+    int zt;
+    if (!row_needs_draw(a, row, lane == 0, zt)) return;
+    const char* rowp = (const char*)a.logits + (size_t)j * (size_t)a.ld * sizeof(T);
+    draw_row<T>(a, row, zt, rowp, a.glse + (int64_t)j * a.glse_ld, lane);
 }
 
 // Debug output: the full posterior row in float64 arithmetic (two passes over the logits).
@@ -427,7 +467,12 @@ dd_status launch_posterior(const PostArgs& a, int logits_dtype, hipStream_t s) {
     const size_t shmem = (size_t)ngroups * sizeof(float);
     {
         ProfScope ps(KC_POSTERIOR, s);
-        if (logits_dtype == DD_BF16)
+        const dim3 g4((unsigned)((a.rows + 3) / 4));
+        if (a.glse && logits_dtype == DD_BF16)
+            hipLaunchKernelGGL(posterior_grouped_kernel<bf16_t>, g4, dim3(256), 0, s, a);
+        else if (a.glse)
+            hipLaunchKernelGGL(posterior_grouped_kernel<float>, g4, dim3(256), 0, s, a);
+        else if (logits_dtype == DD_BF16)
             hipLaunchKernelGGL(posterior_kernel<bf16_t>, dim3(a.rows), dim3(PT), shmem, s, a);
         else
             hipLaunchKernelGGL(posterior_kernel<float>, dim3(a.rows), dim3(PT), shmem, s, a);

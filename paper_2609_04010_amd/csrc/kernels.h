@@ -29,11 +29,18 @@ struct PostArgs {
     // compacted mode (masked prior): logits row j belongs to token row rows_idx[j], j < *count
     const int32_t* rows_idx;
     const int32_t* count;
+    // per-group log-sum-exps of the logits rows, [rows][glse_ld] (written by the vocabulary
+    // projection's EPI_LSE epilogue), or NULL: then the posterior kernel computes them itself
+    const float* glse;
+    int64_t glse_ld;
 };
 
 // EPI_GATE: C = bf16(acc * s_m), s_m = gate_scale if gate is NULL or gate[m % gate_period] != 0,
 // else 0 (the adapter down-projection of a gated LoRA, written beside its input)
-enum Epi { EPI_BIAS = 0, EPI_BIAS_GELU = 1, EPI_BIAS_RESID = 2, EPI_PLAIN = 3, EPI_GATE = 4 };
+// EPI_LSE: plain bf16 store, and per row the log-sum-exp of each DD_GUMBEL_GROUP-column group of
+// the stored (rounded) values into lse[m * lse_ld + n / DD_GUMBEL_GROUP] (vocabulary projection
+// feeding the sampler; bf16, K % 128 == 0, 256-column tiles)
+enum Epi { EPI_BIAS = 0, EPI_BIAS_GELU = 1, EPI_BIAS_RESID = 2, EPI_PLAIN = 3, EPI_GATE = 4, EPI_LSE = 5 };
 
 struct GemmArgs {
     const void* A;   // [M][K], row stride lda
@@ -51,6 +58,9 @@ struct GemmArgs {
     const int32_t* gate;
     int gate_period;
     float gate_scale;
+    // EPI_LSE only: group log-sum-exps [M][lse_ld]
+    float* lse;
+    int64_t lse_ld;
 };
 
 struct AttnArgs {
@@ -109,5 +119,7 @@ bool attn_supported(int dtype, int dh);
 dd_status launch_compact(const int32_t* z, int64_t M, int32_t mask_id, int32_t* idx, int32_t* count,
                          hipStream_t s);
 bool gemm_gather_supported(int dtype, int K);
+// the EPI_LSE epilogue (group log-sum-exps beside the logits) runs for this dtype and K
+bool gemm_lse_supported(int dtype, int K);
 
 }  // namespace dd

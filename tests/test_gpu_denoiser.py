@@ -176,7 +176,9 @@ def test_forward_parity_every_gemm_tile(tile, monkeypatch):
 @pytest.mark.parametrize("c,over,B,L,T", [(2, dict(n_layers=2), 2, 300, 6), (5, dict(n_layers=1), 1, 520, 4)])
 def test_compacted_loop_equals_full_path_loop(c, over, B, L, T):
     """dd_sample_loop (vocabulary projection and draw on the still-masked rows only) must give the
-    same trajectory as dd_denoise_forward + dd_posterior_sample applied to every row."""
+    same trajectory as dd_denoise_forward + dd_posterior_sample applied to every row.  (The loop's
+    group log-sum-exps come from the projection's epilogue, the entry point's from its own pass:
+    summation order only, which no draw at these seeds is close enough to feel.)"""
     torch = torch_or_skip()
     say("compacted loop", c, over, B, L, T)
     cfg = workloads.model_cfg(c, **over)
@@ -196,6 +198,40 @@ def test_compacted_loop_equals_full_path_loop(c, over, B, L, T):
         got = z.cpu().numpy().reshape(B, L)
         assert np.array_equal(got, trace[T - k + 1]), f"step {k}"
     say("masked per step", [(t == V).sum() for t in trace])
+
+
+@pytest.mark.parametrize("c,over,B,L,T", [
+    (2, dict(n_layers=2), 2, 300, 6),                 # 197 groups, the last one 81 classes wide
+    (2, dict(n_layers=1, vocab=1000), 3, 200, 6),     # 4 groups, the last one 232 wide
+    (2, dict(n_layers=1, vocab=300), 2, 256, 5),      # 2 groups, the last one 44 wide
+    (3, dict(n_layers=2), 2, 300, 4),                 # uniform prior: every row, no compaction
+])
+def test_loop_group_lse_epilogue_equals_posterior_pass(c, over, B, L, T, monkeypatch):
+    """The loop draws from the per-group log-sum-exps that the vocabulary projection's epilogue
+    computes from the logits it stores; the same loop with DD_POSTERIOR_PASS=1 draws from the
+    posterior kernel's own pass over those logits (the path the posterior parity tests cover).  The
+    two differ only in the summation order inside each group's log-sum-exp, which can decide a draw
+    only when two level-1 scores are within a few ulps; with these seeds the trajectories agree."""
+    torch = torch_or_skip()
+    say("group lse loop", c, over, B, L, T)
+    cfg = workloads.model_cfg(c, **over)
+    V = cfg["vocab"]
+    _, buf = _params_seeded(torch, cfg, 45)
+    if cfg["prior"] == "mask":
+        z1 = workloads.all_mask(B, L, V)
+    else:
+        z1 = np.random.default_rng(6).integers(0, V, size=(B, L)).astype(np.int32)
+    al = osched.alphas(T)
+    monkeypatch.delenv("DD_POSTERIOR_PASS", raising=False)
+    _, fused = _loop_gpu(torch, cfg, buf, z1, T, al, seed=91)
+    monkeypatch.setenv("DD_POSTERIOR_PASS", "1")
+    _, passed = _loop_gpu(torch, cfg, buf, z1, T, al, seed=91)
+    last = (V - 1) // 256 * 256
+    drawn_last = int(sum(((t >= last) & (t < V)).sum() for t in fused[1:]))
+    say(f"agreement {np.mean(fused == passed):.6f}; draws in the last (ragged) group {drawn_last}")
+    for k in range(1, T + 1):
+        assert np.array_equal(fused[k], passed[k]), f"step {T - k + 1}"
+    assert np.mean(fused[-1] != fused[0]) > 0.3       # the loop did draw
 
 
 # ---------------------------------------------------------------- Psi sampler loop (kappa < 1)
