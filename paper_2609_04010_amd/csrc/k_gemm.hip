@@ -53,6 +53,14 @@ DD_DEV void map_tile(int bid, int nblocks, int tiles_m, int tiles_n, int& tm, in
 constexpr int BK = 64, LSTR = BK + 8;
 constexpr float LOG2E_F = 1.4426950408889634f;
 
+// x rounded to bf16 (round to nearest even, like the stores), as an fp32 value: one conversion that
+// writes bf16(0) to the low and bf16(x) to the high half of the word
+DD_DEV float round_bf16(float x) {
+    uint32_t r;
+    asm("v_cvt_pk_bf16_f32 %0, 0, %1" : "=v"(r) : "v"(x));
+    return __uint_as_float(r);
+}
+
 // EPI_GATE row factor of output row m (m % gate_period is in range for any m, clamped rows too)
 DD_DEV float gate_row_scale(const GemmArgs& g, int m) {
     if (!g.gate) return g.gate_scale;
@@ -540,15 +548,13 @@ __global__ __launch_bounds__(64 * WGM_ * WGN_, 1) void gemm_bf16_dl_kernel(GemmA
 #pragma unroll
                         for (int nb = 0; nb < NB; ++nb)
 #pragma unroll
-                            for (int j4 = 0; j4 < 4; ++j4) {
-                                const uint32_t p0 = pack_bf16x2(acc[nb][mb][4 * j4], acc[nb][mb][4 * j4 + 1]);
-                                const uint32_t p1 = pack_bf16x2(acc[nb][mb][4 * j4 + 2], acc[nb][mb][4 * j4 + 3]);
-                                const float v[4] = {bf16_lo(p0), bf16_hi(p0), bf16_lo(p1), bf16_hi(p1)};
+                            for (int j4 = 0; j4 < 4; ++j4)
 #pragma unroll
-                                for (int e = 0; e < 4; ++e)
-                                    if (!ragged || nl0 + nb * 32 + 8 * j4 + e < g.N)
-                                        sum += __builtin_amdgcn_exp2f(fmaf(v[e], LOG2E_F, moff));
-                            }
+                                for (int e = 0; e < 4; ++e) {
+                                    float v = round_bf16(acc[nb][mb][4 * j4 + e]);
+                                    if (ragged && nl0 + nb * 32 + 8 * j4 + e >= g.N) v = -INFINITY;
+                                    sum += __builtin_amdgcn_exp2f(fmaf(v, LOG2E_F, moff));
+                                }
                         sum += __shfl_xor(sum, 32, 64);
                         if (lane < 32) part[(wm * S::WM + mb * 32 + lane) * S::WGN + wn] = make_float2(mr, sum);
                     }
