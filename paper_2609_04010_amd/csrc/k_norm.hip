@@ -92,6 +92,38 @@ __global__ __launch_bounds__(256) void ln_kernel(const float* h, int64_t rows, c
     ln_row<W, NPL>(x, lane, d, g, b, eps, out + row * ldo);
 }
 
+// LayerNorm of one row held as NV groups of four consecutive features per lane (group lane + 64 k),
+// written as 8-byte bf16 stores.
+template <int NV>
+DD_DEV void ln4_row(const float4 (&x)[NV], int lane, const bf16_t* g, const bf16_t* b, float eps, bf16_t* out) {
+    constexpr int d = NV * 256;
+    float s = 0.f;
+#pragma unroll
+    for (int k = 0; k < NV; ++k) s += (x[k].x + x[k].y) + (x[k].z + x[k].w);
+    const float mean = wave_sum(s) / (float)d;
+    float q = 0.f;
+#pragma unroll
+    for (int k = 0; k < NV; ++k) {
+        const float a0 = x[k].x - mean, a1 = x[k].y - mean, a2 = x[k].z - mean, a3 = x[k].w - mean;
+        q += (a0 * a0 + a1 * a1) + (a2 * a2 + a3 * a3);
+    }
+    const float rstd = 1.0f / sqrtf(wave_sum(q) / (float)d + eps);
+    uint2* orow = (uint2*)out;
+    const uint2* gv = (const uint2*)g;
+    const uint2* bv = (const uint2*)b;
+#pragma unroll
+    for (int k = 0; k < NV; ++k) {
+        const int c = lane + 64 * k;
+        const uint2 gg = gv[c], bb = bv[c];
+        uint2 o;
+        o.x = pack_bf16x2((x[k].x - mean) * rstd * bf16_lo(gg.x) + bf16_lo(bb.x),
+                          (x[k].y - mean) * rstd * bf16_hi(gg.x) + bf16_hi(bb.x));
+        o.y = pack_bf16x2((x[k].z - mean) * rstd * bf16_lo(gg.y) + bf16_lo(bb.y),
+                          (x[k].w - mean) * rstd * bf16_hi(gg.y) + bf16_hi(bb.y));
+        orow[c] = o;
+    }
+}
+
 // bf16 output, d % 256 == 0: each lane holds NV = d / 256 groups of four consecutive features,
 // read as one 16-byte fp32 load and written as one 8-byte bf16 store.
 template <int NV>
@@ -106,31 +138,46 @@ __global__ __launch_bounds__(256) void ln_bf16_v4_kernel(const float* h, int64_t
     const float4* hr = (const float4*)(h + row * d);
 #pragma unroll
     for (int k = 0; k < NV; ++k) x[k] = hr[lane + 64 * k];
-    float s = 0.f;
-#pragma unroll
-    for (int k = 0; k < NV; ++k) s += (x[k].x + x[k].y) + (x[k].z + x[k].w);
-    const float mean = wave_sum(s) / (float)d;
-    float q = 0.f;
-#pragma unroll
-    for (int k = 0; k < NV; ++k) {
-        const float a0 = x[k].x - mean, a1 = x[k].y - mean, a2 = x[k].z - mean, a3 = x[k].w - mean;
-        q += (a0 * a0 + a1 * a1) + (a2 * a2 + a3 * a3);
+    ln4_row<NV>(x, lane, g, b, eps, out + row * ldo);
+}
+
+// Embedding + first LayerNorm, bf16, d % 256 == 0: token and position rows read four features at a
+// time (8-byte loads), the residual row written with 16-byte stores.
+template <int NV>
+__global__ __launch_bounds__(256) void embed_ln_bf16_v4_kernel(const int32_t* z, int64_t rows, int L,
+                                                               int n_tok, const bf16_t* tok,
+                                                               const bf16_t* pos, const float* temb,
+                                                               const bf16_t* g, const bf16_t* b, float eps,
+                                                               float* h, bf16_t* xln, int64_t ldo,
+                                                               int32_t* err) {
+    const int64_t row = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+    const int lane = threadIdx.x & 63;
+    if (row >= rows) return;
+    constexpr int d = NV * 256;
+    int id = z[row];
+    if (id < 0 || id >= n_tok) {
+        if (lane == 0 && err) atomicOr(err, DD_DEVERR_TOKEN);
+        id = id < 0 ? 0 : n_tok - 1;
     }
-    const float rstd = 1.0f / sqrtf(wave_sum(q) / (float)d + eps);
-    uint2* orow = (uint2*)(out + row * ldo);
-    const uint2* gv = (const uint2*)g;
-    const uint2* bv = (const uint2*)b;
+    const int l = (int)(row % L);
+    const uint2* tv = (const uint2*)(tok + (int64_t)id * d);
+    const uint2* pv = (const uint2*)(pos + (int64_t)l * d);
+    float4* hr = (float4*)(h + row * d);
+    float4 x[NV];
 #pragma unroll
     for (int k = 0; k < NV; ++k) {
         const int c = lane + 64 * k;
-        const uint2 gg = gv[c], bb = bv[c];
-        uint2 o;
-        o.x = pack_bf16x2((x[k].x - mean) * rstd * bf16_lo(gg.x) + bf16_lo(bb.x),
-                          (x[k].y - mean) * rstd * bf16_hi(gg.x) + bf16_hi(bb.x));
-        o.y = pack_bf16x2((x[k].z - mean) * rstd * bf16_lo(gg.y) + bf16_lo(bb.y),
-                          (x[k].w - mean) * rstd * bf16_hi(gg.y) + bf16_hi(bb.y));
-        orow[c] = o;
+        const uint2 a = tv[c], p = pv[c];
+        float4 v = make_float4(bf16_lo(a.x) + bf16_lo(p.x), bf16_hi(a.x) + bf16_hi(p.x),
+                               bf16_lo(a.y) + bf16_lo(p.y), bf16_hi(a.y) + bf16_hi(p.y));
+        if (temb) {
+            const float4 t = ((const float4*)temb)[c];
+            v.x += t.x; v.y += t.y; v.z += t.z; v.w += t.w;
+        }
+        x[k] = v;
+        hr[c] = v;
     }
+    ln4_row<NV>(x, lane, g, b, eps, xln + row * ldo);
 }
 
 #define DD_NPL_CASES(X) X(1) X(2) X(4) X(8) X(12) X(16) X(24) X(32)
@@ -159,6 +206,19 @@ dd_status launch_embed_ln(int dtype, const int32_t* z, int64_t rows, int L, int 
                           const void* tok, const void* pos, const float* temb, const void* g,
                           const void* b, float eps, float* h, void* xln, int64_t ldo, int32_t* err,
                           hipStream_t s) {
+    if (dtype == DD_BF16 && (d == 768 || d == 1024 || d == 2048) && ldo % 4 == 0) {
+        const dim3 grid((unsigned)ceil_div(rows, 4)), blk(256);
+        ProfScope ps(KC_EMBED_LN, s);
+        const bf16_t *tk = (const bf16_t*)tok, *ps_ = (const bf16_t*)pos, *gg = (const bf16_t*)g, *bb = (const bf16_t*)b;
+        bf16_t* o = (bf16_t*)xln;
+        if (d == 768)
+            hipLaunchKernelGGL(embed_ln_bf16_v4_kernel<3>, grid, blk, 0, s, z, rows, L, n_tok, tk, ps_, temb, gg, bb, eps, h, o, ldo, err);
+        else if (d == 1024)
+            hipLaunchKernelGGL(embed_ln_bf16_v4_kernel<4>, grid, blk, 0, s, z, rows, L, n_tok, tk, ps_, temb, gg, bb, eps, h, o, ldo, err);
+        else
+            hipLaunchKernelGGL(embed_ln_bf16_v4_kernel<8>, grid, blk, 0, s, z, rows, L, n_tok, tk, ps_, temb, gg, bb, eps, h, o, ldo, err);
+        return launch_status("embed_ln");
+    }
     if (dtype == DD_BF16)
         return launch_embed_ln_t<bf16_t>(z, rows, L, n_tok, d, tok, pos, temb, g, b, eps, h, xln, ldo, err, s);
     return launch_embed_ln_t<float>(z, rows, L, n_tok, d, tok, pos, temb, g, b, eps, h, xln, ldo, err, s);

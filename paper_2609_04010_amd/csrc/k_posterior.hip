@@ -427,31 +427,53 @@ dd_status launch_remask(const PostArgs& a, hipStream_t s) {
     return launch_status("remask");
 }
 
-// Ascending list of the rows whose token is the mask id, and its length (one workgroup: each thread
-// counts a contiguous slice, a workgroup scan gives the slice offsets, then the slices are written).
+// Ascending list of the rows whose token is the mask id, and its length.  One workgroup walks the
+// tokens in blocks of 4 per thread (16-byte loads when z is 16-byte aligned): each thread counts its 4
+// flags, an inclusive shuffle scan gives the offsets inside the wavefront, the 16 wavefront totals go
+// through LDS, and every thread writes its rows after the rows of earlier threads and blocks.
 constexpr int CT = 1024;
 
 __global__ __launch_bounds__(CT) void compact_masked_kernel(const int32_t* z, int64_t M,
                                                             int32_t mask_id, int32_t* idx,
                                                             int32_t* count) {
-    __shared__ int sh[CT];
-    const int tid = threadIdx.x;
-    const int64_t per = (M + CT - 1) / CT;
-    const int64_t lo = (int64_t)tid * per, hi = lo + per < M ? lo + per : M;
-    int c = 0;
-    for (int64_t r = lo; r < hi; ++r) c += (z[r] == mask_id);
-    sh[tid] = c;
-    __syncthreads();
-    for (int off = 1; off < CT; off <<= 1) {
-        const int v = tid >= off ? sh[tid - off] : 0;
+    __shared__ int wsum[CT / 64];
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const bool vec = ((uintptr_t)z & 15) == 0;
+    int base = 0;   // rows listed by earlier blocks (the same in every thread)
+    for (int64_t b0 = 0; b0 < M; b0 += 4 * CT) {
+        const int64_t i0 = b0 + 4 * (int64_t)tid;
+        int f[4];
+        if (vec && i0 + 3 < M) {
+            const int4 v = *(const int4*)(z + i0);
+            f[0] = v.x == mask_id; f[1] = v.y == mask_id; f[2] = v.z == mask_id; f[3] = v.w == mask_id;
+        } else {
+#pragma unroll
+            for (int e = 0; e < 4; ++e) f[e] = (i0 + e < M) && z[i0 + e] == mask_id;
+        }
+        const int c = f[0] + f[1] + f[2] + f[3];
+        int incl = c;
+#pragma unroll
+        for (int o = 1; o < 64; o <<= 1) {
+            const int t = __shfl_up(incl, o, 64);
+            if (lane >= o) incl += t;
+        }
+        if (lane == 63) wsum[wave] = incl;
         __syncthreads();
-        sh[tid] += v;
-        __syncthreads();
+        int before = 0, total = 0;
+#pragma unroll
+        for (int w = 0; w < CT / 64; ++w) {
+            const int v = wsum[w];
+            before += w < wave ? v : 0;
+            total += v;
+        }
+        int pos = base + before + incl - c;
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+            if (f[e]) idx[pos++] = (int32_t)(i0 + e);
+        base += total;
+        __syncthreads();   // wsum is rewritten by the next block
     }
-    int pos = sh[tid] - c;
-    for (int64_t r = lo; r < hi; ++r)
-        if (z[r] == mask_id) idx[pos++] = (int32_t)r;
-    if (tid == CT - 1) *count = sh[CT - 1];
+    if (tid == 0) *count = base;
 }
 
 dd_status launch_compact(const int32_t* z, int64_t M, int32_t mask_id, int32_t* idx, int32_t* count,
