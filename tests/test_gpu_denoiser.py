@@ -234,6 +234,31 @@ def test_loop_group_lse_epilogue_equals_posterior_pass(c, over, B, L, T, monkeyp
     assert np.mean(fused[-1] != fused[0]) > 0.3       # the loop did draw
 
 
+def test_bf16_loop_without_compaction_equals_full_path():
+    """bf16 with d_model % 128 != 0 (d = 64): no row compaction and no group log-sum-exp epilogue, so
+    the loop runs the vocabulary projection on every row and the posterior's own pass; it must give
+    exactly the trajectory of dd_denoise_forward + dd_posterior_sample on every row."""
+    torch = torch_or_skip()
+    cfg = workloads.model_cfg(2, n_layers=2, d_model=64, n_heads=1, d_mlp=256, vocab=1000)
+    V = cfg["vocab"]
+    B, L, T = 2, 100, 5
+    say("bf16 loop without compaction", B, L, T)
+    _, buf = _params_seeded(torch, cfg, 47)
+    z1 = workloads.all_mask(B, L, V)
+    al = osched.alphas(T)
+    _, trace = _loop_gpu(torch, cfg, buf, z1, T, al, seed=93)
+    M = B * L
+    ld = int(dd.logits_ld(V))
+    logits = torch.zeros((M, ld), dtype=torch.bfloat16, device="cuda")
+    ws = torch.zeros(dd.workspace_bytes(cfg, B, L), dtype=torch.uint8, device="cuda")
+    z = dev_i32(torch, z1)
+    for k in range(T, 0, -1):
+        dd.denoise_forward(cfg, buf, z, B, L, al[k], logits, ld, ws)
+        dd.posterior_sample("mask", logits, "bf16", ld, M, V, z, al[k], al[k - 1], z, seed=93, step=k)
+        assert np.array_equal(z.cpu().numpy().reshape(B, L), trace[T - k + 1]), f"step {k}"
+    assert (trace[-1] != V).all() and (np.diff([(t == V).sum() for t in trace]) <= 0).all()
+
+
 # ---------------------------------------------------------------- Psi sampler loop (kappa < 1)
 
 def test_psi_loop_config1_free_running_matches_oracle():
