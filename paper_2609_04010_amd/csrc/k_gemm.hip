@@ -239,6 +239,9 @@ template <int TBN_, int WGM_, int WGN_, int DM_ = DM> struct DLShape {
     // two operand stages; the epilogue stages half a sub-tile per wave above stage 0
     static constexpr size_t STAGING = (size_t)STAGE * 2 + (size_t)NW * (WM / 2) * CSTR * 2;
     static constexpr size_t LDS = STAGING > (size_t)2 * STAGE * 2 ? STAGING : (size_t)2 * STAGE * 2;
+    // workgroups per CU the launcher allows: one for the wide tiles (persistent), several for the
+    // one-wavefront skinny tile, whose K loop is latency-bound
+    static constexpr int WG_PER_CU = NW >= 4 ? 1 : 8 / NW;
     static_assert(WM % 64 == 0 && WN % 32 == 0 && (MB * NB) % 2 == 0, "wave sub-tile (two row halves)");
     static_assert(DM % (8 * NW) == 0 && TBN % (8 * NW) == 0, "load split");
     static_assert(LDS <= 160 * 1024, "LDS");
@@ -721,10 +724,13 @@ static void launch_tile(const GemmArgs& g, hipStream_t s) {
 // round of 256-wide ones on MI355X), in the 8-wavefront form (two wavefronts per SIMD, measured 2-6%
 // faster than four wavefronts of twice the sub-tile).  K % 128 != 0 falls back to the 128 x 128
 // register-staged kernel.  Skinny products (N <= 128, e.g. an adapter down-projection to rank r)
-// take 64 x 128 register-staged tiles: the 256-row tiles would leave most CUs idle (M / 256
-// workgroups): direct-to-LDS when K % 128 == 0, else register-staged.  DD_GEMM_TILE (0..9) forces a
+// would leave most CUs idle with 256-row tiles (M / 256 workgroups): with K % 128 == 0 they take
+// 64 x 32 direct-to-LDS tiles of one wavefront, up to eight workgroups per CU (their K loop is
+// latency-bound, so more independent loops per CU pay: 12 % faster than one 64 x 128 workgroup of
+// four wavefronts per CU), else 64 x 128 register-staged tiles.  DD_GEMM_TILE (0..10) forces a
 // variant for tuning and tests (4: 256 x 256 / 4 waves, 5: 256 x 192 / 4 waves, 6: 256 x 256 /
-// 8 waves, 7: 256 x 192 / 8 waves, 8: 64 x 128 register-staged, 9: 64 x 128 direct-to-LDS).
+// 8 waves, 7: 256 x 192 / 8 waves, 8: 64 x 128 register-staged, 9: 64 x 128 direct-to-LDS,
+// 10: 64 x 32 direct-to-LDS / 1 wave).
 static int num_cus() {
     static int n = 0;
     if (n == 0) {
@@ -738,9 +744,9 @@ static int num_cus() {
 static int pick_tile(const GemmArgs& g) {
     const char* e = getenv("DD_GEMM_TILE");
     const int forced = e ? atoi(e) : -1;
-    if (((forced >= 4 && forced <= 7) || forced == 9) && g.K % (2 * BK) != 0) return 0;
-    if (forced >= 0 && forced <= 9 && !(g.a_rows && (forced < 4 || forced == 8))) return forced;
-    if (g.N <= 128) return g.K % (2 * BK) == 0 ? 9 : (g.a_rows ? 0 : 8);
+    if (((forced >= 4 && forced <= 7) || forced >= 9) && g.K % (2 * BK) != 0) return 0;
+    if (forced >= 0 && forced <= 10 && !(g.a_rows && (forced < 4 || forced == 8))) return forced;
+    if (g.N <= 128) return g.K % (2 * BK) == 0 ? 10 : (g.a_rows ? 0 : 8);
     if (g.K % (2 * BK) != 0) return 0;
     const int64_t ncu = num_cus();
     const int64_t tm = (g.M + DM - 1) / DM;
@@ -761,8 +767,8 @@ static void launch_dl(const GemmArgs& g, hipStream_t s) {
                                   hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
         attr = true;
     }
-    // persistent: at most one workgroup per CU
-    const int grid = (int)std::min<int64_t>((int64_t)tm * tn, num_cus());
+    // persistent: at most WG_PER_CU workgroups per CU
+    const int grid = (int)std::min<int64_t>((int64_t)tm * tn, (int64_t)num_cus() * S::WG_PER_CU);
     hipLaunchKernelGGL((gemm_bf16_dl_kernel<EPI, ROLE, TBN, WGM, WGN, DMR>), dim3(grid), dim3(S::THREADS), lds,
                        s, g, tm, tn);
 }
@@ -776,6 +782,7 @@ static void launch_epi(int dtype, const GemmArgs& g, hipStream_t s) {
             case 5: launch_dl<EPI, ROLE, 192, 2, 2>(g, s); break;
             case 4: launch_dl<EPI, ROLE, 256, 2, 2>(g, s); break;
             case 9: launch_dl<EPI, ROLE, 128, 1, 4, 64>(g, s); break;
+            case 10: launch_dl<EPI, ROLE, 32, 1, 1, 64>(g, s); break;
             case 8: launch_tile<64, 128, EPI>(g, s); break;
             case 3: launch_tile<256, 256, EPI>(g, s); break;
             case 2: launch_tile<256, 128, EPI>(g, s); break;

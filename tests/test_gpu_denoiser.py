@@ -156,10 +156,10 @@ def test_loop_uniform_prior_runs_in_range():
     assert np.mean(trace[-1] != trace[0]) > 0.5          # the uniform prior keeps revising tokens
 
 
-@pytest.mark.parametrize("tile", ["0", "1", "2", "3", "4", "5", "6", "7", "8", "9"])
+@pytest.mark.parametrize("tile", ["0", "1", "2", "3", "4", "5", "6", "7", "8", "9", "10"])
 def test_forward_parity_every_gemm_tile(tile, monkeypatch):
-    """Each GEMM tile variant (64/128/256 rows x 128/192/256 columns, 4 or 8 wavefronts) on ragged M
-    and N."""
+    """Each GEMM tile variant (64/128/256 rows x 32/128/192/256 columns, 1, 4 or 8 wavefronts) on
+    ragged M and N."""
     torch = torch_or_skip()
     monkeypatch.setenv("DD_GEMM_TILE", tile)
     say("gemm tile", tile)
