@@ -15,6 +15,9 @@ timed region.  Prints ONE JSON line.
                                        B x L with an attention pattern and gated adapters: one JSON
                                        line with ms per forward and per kernel class; not the
                                        benchmark line)
+  python bench.py --kernels           (Psi-Spec verification and Gaussian-latent argmax outside the
+                                       loop: one JSON line each with its roofline; not the
+                                       benchmark line)
 """
 import hashlib
 import argparse
@@ -185,6 +188,73 @@ def forward_bench(args):
     print(json.dumps(out), flush=True)
 
 
+# ALU roofline of the Gaussian-latent argmax, per Philox-4x32-10 block (4 classes): 10 rounds of two
+# 32x32 -> 64-bit multiplies (v_mad_u64_u32) and two xors, plus a compare, compare and select per class
+# for the running argmax: 52 VALU instructions.  Peak = 256 CUs x 64 lanes x 2.4 GHz / 52 with every
+# instruction at full rate (an upper bound; the 64-bit multiplies may issue slower).
+LATENT_VALU_PER_BLOCK = 52
+LATENT_PEAK_GBLOCKS = 256 * 64 * 2.4e9 / LATENT_VALU_PER_BLOCK / 1e9
+HBM_PEAK_GBS = 8000.0
+
+
+def kernels_bench(args):
+    """Time the sampler-side kernels outside the loop, one JSON line each: Psi-Spec verification of
+    S drafted blocks (Alg. 1, linear sampler; HBM-bound) and the Gaussian-latent argmax (App. A.5;
+    ALU-bound).  Inputs are synthetic and generated on the device."""
+    import torch
+    from paper_2609_04010_amd import _lib as dd
+    dev = torch.device("cuda:0")
+    g = torch.Generator(device=dev)
+    g.manual_seed(17)
+
+    def timed(fn):
+        for _ in range(max(1, args.warmup)):
+            fn()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(args.steps):
+            fn()
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / args.steps
+
+    # Alg. 1 verification: S sequences, block size B = 16 (the paper's largest), bf16 target and draft
+    # logits of the workload vocabulary; drafts drawn uniformly, so most blocks reject early
+    S, B, V = 256, 16, 50257
+    ld = int(dd.logits_ld(V))
+    p = (torch.randn((S * B, ld), generator=g, device=dev) * 3.0).to(torch.bfloat16)
+    q = (p[: S * (B - 1)].float() + torch.randn((S * (B - 1), ld), generator=g, device=dev)).to(torch.bfloat16)
+    draft = torch.randint(0, V, (S * (B - 1),), generator=g, device=dev, dtype=torch.int32)
+    n_out = torch.empty(S, dtype=torch.int32, device=dev)
+    z_out = torch.empty(S, dtype=torch.int32, device=dev)
+    ws = torch.empty(dd.spec_verify_workspace_bytes(S, B), dtype=torch.uint8, device=dev)
+    err = torch.zeros(1, dtype=torch.int32, device=dev)
+    ms = timed(lambda: dd.spec_verify(p, q, "bf16", ld, S, B, V, draft, n_out, z_out, ws, seed=5, step=1,
+                                      dev_err=err))
+    assert int(err.item()) == 0
+    nbytes = S * (2 * B + 1) * V * 2     # every p and q row once (log-sum-exps), the chosen pair again
+    gbs = nbytes / (ms * 1e-3) / 1e9
+    print(json.dumps({"mode": "kernel", "kernel": "spec_verify", "S": S, "B": B, "V": V, "dtype": "bf16",
+                      "calls": args.steps, "ms_per_call": ms, "accepted_mean": float(n_out.float().mean()) - 1,
+                      "roofline": {"bound": "hbm", "achieved": gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                                   "frac": gbs / HBM_PEAK_GBS, "bytes_per_call": nbytes}}), flush=True)
+
+    # Gaussian-latent argmax of the uniform sampler's start: B16 x L1024 rows, V classes
+    rows = 16 * 1024
+    x = torch.randint(0, V, (rows,), generator=g, device=dev, dtype=torch.int32)
+    z = torch.empty_like(x)
+    ms = timed(lambda: dd.gaussian_latent_argmax(x, rows, V, 0.0, 1.0, seed=9, step=0, z_out=z, dev_err=err))
+    assert int(err.item()) == 0
+    blocks = rows * ((V + 3) // 4)
+    gbl = blocks / (ms * 1e-3) / 1e9
+    print(json.dumps({"mode": "kernel", "kernel": "gaussian_latent_argmax", "rows": rows, "V": V,
+                      "calls": args.steps, "ms_per_call": ms,
+                      "roofline": {"bound": "alu", "achieved": gbl, "peak": LATENT_PEAK_GBLOCKS,
+                                   "unit": "G Philox blocks/s", "frac": gbl / LATENT_PEAK_GBLOCKS,
+                                   "blocks_per_call": blocks}}), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -197,12 +267,17 @@ def main():
     ap.add_argument("--lora-rank", type=int, default=0)
     ap.add_argument("--lora-alpha", type=float, default=256.0)
     ap.add_argument("--gate", choices=["all", "half"], default="all")
+    ap.add_argument("--kernels", action="store_true",
+                    help="time the verification and Gaussian-latent kernels (one JSON line each)")
     args = ap.parse_args()
     if args.traffic_probe:
         traffic_probe(args.workload)
         return
     if args.forward:
         forward_bench(args)
+        return
+    if args.kernels:
+        kernels_bench(args)
         return
     if args.gpus != 1:
         log(f"bench.py measures one GPU only (asked for {args.gpus}); the sampling loop shards "

@@ -29,14 +29,17 @@ __global__ __launch_bounds__(256) void latent_kernel(const int32_t* x, int32_t V
     const uint32_t k0 = (uint32_t)seed, k1 = (uint32_t)(seed >> 32);
     for (int b = tid; b < nblk; b += 256) {
         const Words4 W = philox4x32_10((uint32_t)b, grow, step, STREAM_LATENT, k0, k1);
+        // branch-free running argmax over v != x (selects; a thread's classes rise with b and e, so
+        // an equal word never displaces an earlier class); the word of class x is set aside
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
             const int v = 4 * b + e;
-            if (v < V) {
-                if (v == xr) sh_wx = W.w[e];
-                else if (W.w[e] > bw || (W.w[e] == bw && v < bi)) { bw = W.w[e]; bi = v; }
-            }
+            const uint32_t w = W.w[e];
+            const bool take = v < V && v != xr && (w > bw || (w == bw && v < bi));
+            bw = take ? w : bw;
+            bi = take ? v : bi;
         }
+        if ((xr >> 2) == b) sh_wx = W.w[xr & 3];
     }
 #pragma unroll
     for (int o = 32; o > 0; o >>= 1) {

@@ -26,46 +26,65 @@ namespace {
 
 constexpr int VT = 256;   // threads per workgroup
 
-DD_DEV float block_reduce(float v, bool is_max, float* sh) {
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    v = is_max ? wave_max(v) : wave_sum(v);
-    if (lane == 0) sh[wave] = v;
-    __syncthreads();
-    float r = sh[0];
-#pragma unroll
-    for (int w = 1; w < VT / 64; ++w) r = is_max ? fmaxf(r, sh[w]) : r + sh[w];
-    __syncthreads();
-    return r;
-}
-
-// Row r < S B is target row r; otherwise draft row r - S B.
+// Row r < S B is target row r; otherwise draft row r - S B.  One pass over the row: each thread keeps
+// a running maximum m and the sum of exp(l - m), rescaled when m rises; the workgroup then combines
+// the (m, sum) pairs.  NaN and +inf logits are only flagged, so the result is that of the two-pass
+// definition: NaN if a logit is NaN, else +inf if one is +inf, else -inf if none is finite.
 template <typename T>
 __global__ __launch_bounds__(VT) void row_lse_kernel(VerifyArgs a, float* lse) {
-    __shared__ float sh[VT / 64];
+    __shared__ float sh_m[VT / 64], sh_s[VT / 64];
+    __shared__ int sh_f[VT / 64];
     constexpr int E = Elem<T>::E;
-    const int r = blockIdx.x;
+    const int r = blockIdx.x, lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int np = a.S * a.B;
     const char* rowp = r < np ? (const char*)a.p + (size_t)r * a.ld * sizeof(T)
                               : (const char*)a.q + (size_t)(r - np) * a.ld * sizeof(T);
     const int V = a.V, nchunk = (V + E - 1) / E;
-    float m = -INFINITY;
+    float m = -INFINITY, sum = 0.f;
+    int flags = 0;   // 1: a NaN, 2: a +inf
     for (int c = threadIdx.x; c < nchunk; c += VT) {
         const uint4 x = *(const uint4*)(rowp + (size_t)c * 16);
+        float v[E];
+        float cm = -INFINITY;
 #pragma unroll
-        for (int e = 0; e < E; ++e)
-            if (c * E + e < V) m = fmaxf(m, Elem<T>::get(x, e));
-    }
-    m = block_reduce(m, true, sh);
-    const float mref = isinf(m) ? 0.f : m;
-    float sum = 0.f;
-    for (int c = threadIdx.x; c < nchunk; c += VT) {
-        const uint4 x = *(const uint4*)(rowp + (size_t)c * 16);
+        for (int e = 0; e < E; ++e) {
+            float t = c * E + e < V ? Elem<T>::get(x, e) : -INFINITY;
+            flags |= (t != t) ? 1 : 0;
+            flags |= (t == INFINITY) ? 2 : 0;
+            t = (t != t || t == INFINITY) ? -INFINITY : t;
+            v[e] = t;
+            cm = fmaxf(cm, t);
+        }
+        if (cm > m) {
+            sum *= __builtin_amdgcn_exp2f((m - cm) * LOG2E);   // m = -inf: sum is 0 already
+            m = cm;
+        }
+        const float mref = m == -INFINITY ? 0.f : m;
 #pragma unroll
-        for (int e = 0; e < E; ++e)
-            if (c * E + e < V) sum += __builtin_amdgcn_exp2f((Elem<T>::get(x, e) - mref) * LOG2E);
+        for (int e = 0; e < E; ++e) sum += __builtin_amdgcn_exp2f((v[e] - mref) * LOG2E);
     }
-    sum = block_reduce(sum, false, sh);
-    if (threadIdx.x == 0) lse[r] = mref + logf(sum);
+    // workgroup: maximum, then the sums rescaled to it, and the flags
+    float M = wave_max(m);
+    int fl = flags;
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) fl |= __shfl_xor(fl, o, 64);
+    if (lane == 0) { sh_m[wave] = M; sh_f[wave] = fl; }
+    __syncthreads();
+    M = sh_m[0];
+    fl = sh_f[0];
+#pragma unroll
+    for (int w = 1; w < VT / 64; ++w) { M = fmaxf(M, sh_m[w]); fl |= sh_f[w]; }
+    const float Mref = M == -INFINITY ? 0.f : M;
+    float part = m == -INFINITY ? 0.f : sum * __builtin_amdgcn_exp2f((m - Mref) * LOG2E);
+    part = wave_sum(part);
+    if (lane == 0) sh_s[wave] = part;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        float S = sh_s[0];
+#pragma unroll
+        for (int w = 1; w < VT / 64; ++w) S += sh_s[w];
+        lse[r] = (fl & 1) ? __int_as_float(0x7FC00000) : (fl & 2) ? INFINITY : Mref + logf(S);
+    }
 }
 
 DD_DEV uint32_t verify_word(const VerifyArgs& a, int s, uint32_t stream, int idx, int explicit_off) {
