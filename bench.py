@@ -113,7 +113,7 @@ def traffic_probe(c):
     torch.cuda.synchronize()
     dst.copy_(src)
     torch.cuda.synchronize()
-    cfg, w = workloads.model_cfg(c), workloads.CONFIGS[c]
+    cfg, w = workloads.model_cfg(c), workloads.WORKLOADS[c]
     B, L, V = w["B"], w["L"], w["vocab"]
     params = torch.zeros(dd.param_bytes(cfg), dtype=torch.uint8, device="cuda")
     dd.init_params(cfg, params, seed=workloads.seeds(c)["param"])
@@ -131,7 +131,7 @@ def forward_bench(args):
     import workloads
     from paper_2609_04010_amd import _lib as dd
     c = args.workload
-    w = workloads.CONFIGS[c]
+    w = workloads.WORKLOADS[c]
     over = {}
     if args.lora_rank:
         over = dict(lora_rank=args.lora_rank, lora_alpha=args.lora_alpha)
@@ -289,7 +289,7 @@ def main():
     from paper_2609_04010_amd import _lib as dd
 
     c = args.workload
-    w = workloads.CONFIGS[c]
+    w = workloads.WORKLOADS[c]
     cfg = workloads.model_cfg(c)
     s = workloads.seeds(c)
     B, L, T, V = w["B"], w["L"], w["T"], w["vocab"]

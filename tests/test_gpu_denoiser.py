@@ -107,7 +107,7 @@ def test_loop_config1_free_running_matches_oracle():
     """fp32 workload 1: the whole 8-step loop on explicit noise, free running on both sides."""
     torch = torch_or_skip()
     cfg = workloads.model_cfg(1)
-    w, s = workloads.CONFIGS[1], workloads.seeds(1)
+    w, s = workloads.WORKLOADS[1], workloads.seeds(1)
     B, L, V, T = w["B"], w["L"], w["vocab"], w["T"]
     P, buf = _params_seeded(torch, cfg, s["param"])
     words = workloads.noise_words(s["noise"], (T, B * L, osampler.noise_width("mask", V)))
@@ -266,7 +266,7 @@ def test_psi_loop_config1_free_running_matches_oracle():
     the whole loop on explicit noise, free running on both sides."""
     torch = torch_or_skip()
     cfg = workloads.model_cfg(1)
-    w, s = workloads.CONFIGS[1], workloads.seeds(1)
+    w, s = workloads.WORKLOADS[1], workloads.seeds(1)
     B, L, V, T = w["B"], w["L"], w["vocab"], w["T"]
     P, buf = _params_seeded(torch, cfg, s["param"])
     words = workloads.noise_words(s["noise"] + 1, (T, B * L, osampler.noise_width("mask", V)))

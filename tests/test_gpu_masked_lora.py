@@ -204,7 +204,7 @@ def test_sample_loop_with_adapters_matches_oracle():
     from tests.gpu_util import compare_ids, dev_words
     torch = torch_or_skip()
     cfg = workloads.model_cfg(1, lora_rank=8, lora_alpha=16.0)
-    w, s = workloads.CONFIGS[1], workloads.seeds(1)
+    w, s = workloads.WORKLOADS[1], workloads.seeds(1)
     B, L, V, T = w["B"], w["L"], w["vocab"], w["T"]
     P, buf = _params(torch, cfg, s["param"], "seeded")
     words = workloads.noise_words(s["noise"], (T, B * L, osampler.noise_width("mask", V)))

@@ -148,7 +148,7 @@ def _tiny_cfg():
 
 def test_loop_bookkeeping_masked_config1():
     cfg = _tiny_cfg()
-    w = workloads.CONFIGS[1]
+    w = workloads.WORKLOADS[1]
     P = params.init_params(cfg, workloads.seeds(1)["param"])
     B, L, V, T = w["B"], w["L"], w["vocab"], w["T"]
     words = workloads.noise_words(workloads.seeds(1)["noise"], (T, B * L, sampler.noise_width("mask", V)))

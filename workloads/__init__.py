@@ -23,7 +23,7 @@ Seeds for workload c: params 1000 + c, data 2000 + c, noise 3000 + c.
 """
 import numpy as np
 
-CONFIGS = {
+WORKLOADS = {
     1: dict(name="tiny-mask-fp32", n_layers=2, d_model=64, n_heads=2, d_mlp=256, vocab=32,
             prior="mask", B=4, L=32, T=8, dtype="fp32", noise="explicit"),
     2: dict(name="gpt2s-mask-bf16", n_layers=12, d_model=768, n_heads=12, d_mlp=3072, vocab=50257,
@@ -39,7 +39,7 @@ CONFIGS = {
 
 def model_cfg(c, **over):
     """Architecture dictionary for workload c (keys the oracle and binding read)."""
-    w = dict(CONFIGS[c])
+    w = dict(WORKLOADS[c])
     cfg = dict(n_layers=w["n_layers"], d_model=w["d_model"], n_heads=w["n_heads"],
                d_mlp=w["d_mlp"], vocab=w["vocab"], prior=w["prior"], dtype=w["dtype"],
                max_len=w["L"], time_cond=True, norm_eps=1e-5)
