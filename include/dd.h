@@ -288,6 +288,8 @@ dd_status dd_psi_posterior_sample(int32_t prior, const void* logits, int32_t log
  * and one group of logits per row instead of the whole row.  The result equals calling
  * dd_denoise_forward and dd_posterior_sample on every row, up to the summation order inside each
  * group's log-sum-exp (a draw can differ only where two level-1 scores lie within a few ulps).
+ * The environment variable DD_POSTERIOR_PASS=1 (read at each call) makes the draw take its own
+ * pass over the logit rows instead, as dd_posterior_sample does.
  */
 dd_status dd_sample_loop(const dd_config* cfg, const void* params, int32_t B, int32_t L,
                          int32_t T, const double* alphas, int32_t* z,
