@@ -1,0 +1,58 @@
+"""Host-side logic of bench.py (no GPU): the algorithmic work per kernel class that the roofline
+divides by, the counter records it attaches only while the kernel source is unchanged, and the
+refusal of more than one GPU."""
+import json
+import os
+import subprocess
+import sys
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+sys.path.insert(0, ROOT)
+import bench  # noqa: E402
+import workloads  # noqa: E402
+
+
+def test_algorithmic_flops_of_the_gpt2s_workload():
+    cfg, w = workloads.model_cfg(2), workloads.WORKLOADS[2]
+    B, L = w["B"], w["L"]
+    M = B * L
+    assert bench.algorithmic_units("gemm_mlp_down", cfg, B, L) == (2.0 * M * 3072 * 768, "TFLOP/s", "mfma")
+    assert bench.algorithmic_units("gemm_qkv", cfg, B, L)[0] == 2.0 * M * 768 * 2304
+    assert bench.algorithmic_units("attention", cfg, B, L)[0] == 4.0 * B * L * L * 768
+    # the vocabulary projection counts the rows it actually projects
+    assert bench.algorithmic_units("gemm_vocab", cfg, B, L)[0] == 2.0 * M * 768 * 50257
+    assert bench.algorithmic_units("gemm_vocab", cfg, B, L, vocab_rows=8192.5)[0] == 2.0 * 8192.5 * 768 * 50257
+    assert bench.algorithmic_units("layernorm", cfg, B, L) == (None, None, None)
+
+
+def _record(tmp_path, sha, cls="gemm_mlp_down"):
+    (tmp_path / "profiles").mkdir()
+    (tmp_path / "src.hip").write_bytes(b"kernel source\n")
+    rec = {"kernel_class": cls, "source": "src.hip", "source_sha256": sha, "traffic_bytes_per_launch": 123.0}
+    (tmp_path / "profiles" / "traffic_x.md").write_text("# t\n\ntraffic-json: " + json.dumps(rec) + "\n")
+
+
+def test_traffic_record_only_while_the_source_is_unchanged(tmp_path, monkeypatch):
+    import hashlib
+    good = hashlib.sha256(b"kernel source\n").hexdigest()
+    _record(tmp_path, good)
+    monkeypatch.setattr(bench, "ROOT", str(tmp_path))
+    assert bench.recorded_traffic("gemm_mlp_down") == 123.0
+    assert bench.recorded_traffic("gemm_mlp_up") is None
+    (tmp_path / "src.hip").write_bytes(b"kernel source, edited\n")
+    assert bench.recorded_traffic("gemm_mlp_down") is None
+
+
+def test_committed_traffic_records_parse():
+    for cls in ("gemm_mlp_down", "gemm_mlp_up"):
+        t = bench.recorded_traffic(cls)
+        assert t is None or 1e8 < t < 1e9, (cls, t)
+
+
+def test_more_than_one_gpu_is_refused():
+    r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--gpus", "2"], capture_output=True,
+                       text=True, timeout=120)
+    assert r.returncode == 2
+    assert "one GPU only" in (r.stdout + r.stderr)
