@@ -204,6 +204,8 @@ def test_compacted_loop_equals_full_path_loop(c, over, B, L, T):
     (2, dict(n_layers=2), 2, 300, 6),                 # 197 groups, the last one 81 classes wide
     (2, dict(n_layers=1, vocab=1000), 3, 200, 6),     # 4 groups, the last one 232 wide
     (2, dict(n_layers=1, vocab=300), 2, 256, 5),      # 2 groups, the last one 44 wide
+    (2, dict(n_layers=1, vocab=512), 2, 128, 4),      # 2 whole groups, no ragged one
+    (2, dict(n_layers=1, vocab=100), 2, 128, 4),      # a single group narrower than the tile
     (3, dict(n_layers=2), 2, 300, 4),                 # uniform prior: every row, no compaction
 ])
 def test_loop_group_lse_epilogue_equals_posterior_pass(c, over, B, L, T, monkeypatch):
@@ -232,6 +234,21 @@ def test_loop_group_lse_epilogue_equals_posterior_pass(c, over, B, L, T, monkeyp
     for k in range(1, T + 1):
         assert np.array_equal(fused[k], passed[k]), f"step {T - k + 1}"
     assert np.mean(fused[-1] != fused[0]) > 0.3       # the loop did draw
+
+
+def test_loop_from_a_decoded_state_leaves_it_unchanged():
+    """Masked prior, no mask token in z_1: every step's compacted list is empty, so the gathered
+    vocabulary projection and the grouped draw launch with no rows, and z stays as it was."""
+    torch = torch_or_skip()
+    cfg = workloads.model_cfg(2, n_layers=1)
+    V = cfg["vocab"]
+    B, L, T = 2, 128, 4
+    say("loop from a decoded state", B, L, T)
+    _, buf = _params_seeded(torch, cfg, 49)
+    z1 = np.random.default_rng(8).integers(0, V, size=(B, L)).astype(np.int32)
+    z0, trace = _loop_gpu(torch, cfg, buf, z1, T, osched.alphas(T), seed=95)
+    assert np.array_equal(z0, z1)
+    assert all(np.array_equal(t, z1) for t in trace)
 
 
 def test_bf16_loop_without_compaction_equals_full_path():
