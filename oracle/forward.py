@@ -30,9 +30,11 @@ Two extensions toward the paper's drafting pathway (Sec. 3.1 - 3.2, Sec. 4.1):
         noisy ones); gate None switches them on everywhere.  With g_l = 1 this
         is the merged weight W + (alpha/r) B A of App. "Varying LoRA alpha / r".
 
-Parity unpinned by the paper (the architecture is a convention): pinned by a
-second, independent scalar-loop implementation (forward_loops), by LayerNorm
-moments, by permutation equivariance with zero position embeddings and by
+The paper does not fix this architecture, so its pins come from elsewhere: a
+library implementation of the same pre-LN layer (torch.nn.TransformerEncoderLayer
+with norm_first and tanh GELU, in float64, with and without an attention
+pattern), a second, independent scalar-loop implementation (forward_loops),
+LayerNorm moments, permutation equivariance with zero position embeddings and
 non-causality.  The extensions are pinned by forward_loops under every
 pattern and gate, by the reach of a perturbation under each pattern (it
 changes exactly the positions that can see it), by the merged-weight identity
