@@ -236,6 +236,35 @@ def test_loop_group_lse_epilogue_equals_posterior_pass(c, over, B, L, T, monkeyp
     assert np.mean(fused[-1] != fused[0]) > 0.3       # the loop did draw
 
 
+def test_full_size_loop_sampled_sequence_matches_oracle():
+    """The benchmark's configuration (gpt2s, 12 layers, B 16 x L 1024, the compacted loop with the
+    group log-sum-exp draw): the first two reverse steps of the 128-step schedule on all 16
+    sequences; one sequence recomputed by the oracle (forward pass and draw with that sequence's
+    noise counters, each step from the GPU's state before it) gives the same ids under the gap
+    rule."""
+    torch = torch_or_skip()
+    c = 2
+    cfg = workloads.model_cfg(c)
+    w, s = workloads.WORKLOADS[c], workloads.seeds(c)
+    B, L, V, T = w["B"], w["L"], w["vocab"], w["T"]
+    say("full-size loop, sampled sequence", B, L, T)
+    P, buf = _params_host(torch, cfg, s["param"])
+    al = osched.alphas(T)[T - 2:]          # steps T and T - 1 of the schedule as a two-step loop
+    z1 = workloads.all_mask(B, L, V)
+    _, trace = _loop_gpu(torch, cfg, buf, z1, 2, al, seed=s["noise"])
+    b = 11
+    rows = np.arange(b * L, (b + 1) * L)
+    for k in (2, 1):
+        z = trace[2 - k][b:b + 1].astype(np.int64)
+        logits = oforward.forward(cfg, P, z, al[k]).reshape(L, V)
+        zs, gaps = osampler.posterior_sample("mask", logits, z.reshape(-1), al[k], al[k - 1],
+                                             osampler.PhiloxNoise(s["noise"], k), rows=rows)
+        compare_ids(trace[2 - k + 1][b], zs, gaps, f"sequence {b}, step {k}")
+    decoded = int((trace[-1] != V).sum())
+    say(f"decoded after two steps: {decoded} of {B * L}")
+    assert decoded > 0
+
+
 def test_loop_from_a_decoded_state_leaves_it_unchanged():
     """Masked prior, no mask token in z_1: every step's compacted list is empty, so the gathered
     vocabulary projection and the grouped draw launch with no rows, and z stays as it was."""
