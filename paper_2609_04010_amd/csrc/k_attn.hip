@@ -227,58 +227,80 @@ __global__ __launch_bounds__(256, MASKED ? 3 : 4) void attn_bf16_kernel(AttnArgs
     auto tile = [&](int k, bool part) {
         const int buf = k & 1, kb0 = tile_of(k) * AK;
         f32x16 sacc[2];
+        auto scores = [&]() {
 #pragma unroll
-        for (int kb = 0; kb < 2; ++kb) {
+            for (int kb = 0; kb < 2; ++kb) {
 #pragma unroll
-            for (int e = 0; e < 16; ++e) sacc[kb][e] = 0.f;
+                for (int e = 0; e < 16; ++e) sacc[kb][e] = 0.f;
 #pragma unroll
-            for (int kk = 0; kk < 4; ++kk) {
-                const int kr = kb * 32 + (lane & 31);
-                const bf16x8 kf = *(const bf16x8*)&Ks[buf][kr * KROW + 8 * ((2 * kk + grp) ^ ksw(kr))];
-                sacc[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[kk], sacc[kb], 0, 0, 0);
+                for (int kk = 0; kk < 4; ++kk) {
+                    const int kr = kb * 32 + (lane & 31);
+                    const bf16x8 kf = *(const bf16x8*)&Ks[buf][kr * KROW + 8 * ((2 * kk + grp) ^ ksw(kr))];
+                    sacc[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[kk], sacc[kb], 0, 0, 0);
+                }
             }
-        }
-        if (part) {
+            if (part) {
+#pragma unroll
+                for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+                    for (int j = 0; j < 16; ++j) {
+                        const int key = kb0 + kb * 32 + 8 * (j >> 2) + 4 * grp + (j & 3);
+                        const bool vis = MASKED ? (key < qpre || (key >= qlo && key < qhi)) : key < L;
+                        if (!vis) sacc[kb][j] = -INFINITY;
+                    }
+            }
+        };
+        auto exps = [&](float negm) {
+            float ps = 0.f;
 #pragma unroll
             for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
                 for (int j = 0; j < 16; ++j) {
-                    const int key = kb0 + kb * 32 + 8 * (j >> 2) + 4 * grp + (j & 3);
-                    const bool vis = MASKED ? (key < qpre || (key >= qlo && key < qhi)) : key < L;
-                    if (!vis) sacc[kb][j] = -INFINITY;
+                    const float p = __builtin_amdgcn_exp2f(fmaf(sacc[kb][j], a.scale_log2, negm));
+                    sacc[kb][j] = p;
+                    ps += p;
                 }
-        }
-        float mloc = -INFINITY;
-#pragma unroll
-        for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-            for (int j = 0; j < 16; ++j) mloc = fmaxf(mloc, sacc[kb][j]);
-        mloc = fmaxf(mloc, __shfl_xor(mloc, 32, 64)) * a.scale_log2;
-        const bool raise = mloc > mrow + RESCALE;
-        if (__any(raise)) {
-            // rare after the first tile: kept a real branch (an empty volatile asm stops the
-            // compiler from executing the 33 multiplies below unconditionally)
-            asm volatile("");
-            const float mnew = raise ? mloc : mrow;
-            // a row that has seen no visible key keeps mrow = -inf: its factor must be 1, not NaN
-            const float corr = MASKED && !raise ? 1.0f : __builtin_amdgcn_exp2f(mrow - mnew);
-            lpart *= corr;
-#pragma unroll
-            for (int i = 0; i < 2; ++i)
-#pragma unroll
-                for (int e = 0; e < 16; ++e) o[i][e] *= corr;
-            mrow = mnew;
-        }
+            return ps;
+        };
+        scores();
         float psum = 0.f;
-        const float negm = MASKED && mrow == -INFINITY ? 0.f : -mrow;
-#pragma unroll
-        for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-            for (int j = 0; j < 16; ++j) {
-                const float p = __builtin_amdgcn_exp2f(fmaf(sacc[kb][j], a.scale_log2, negm));
-                sacc[kb][j] = p;
-                psum += p;
+        bool done = false;
+        // Once every row of the wavefront has an exponent reference it usually stays where it is:
+        // probabilities up to 2^64 are harmless in fp32 and bf16, so the tile maximum is not needed
+        // unless a lane's sum exceeds that (or is not a number).  Then the scores are computed again
+        // and the tile takes the path below.
+        if (!__any(mrow == -INFINITY)) {
+            psum = exps(-mrow);
+            done = !__any(!(psum <= 0x1p64f));
+            if (!done) {
+                asm volatile("");
+                scores();
             }
+        }
+        if (!done) {
+            float mloc = -INFINITY;
+#pragma unroll
+            for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+                for (int j = 0; j < 16; ++j) mloc = fmaxf(mloc, sacc[kb][j]);
+            mloc = fmaxf(mloc, __shfl_xor(mloc, 32, 64)) * a.scale_log2;
+            const bool raise = mloc > mrow + RESCALE;
+            if (__any(raise)) {
+                // rare after the first tile: kept a real branch (an empty volatile asm stops the
+                // compiler from executing the 33 multiplies below unconditionally)
+                asm volatile("");
+                const float mnew = raise ? mloc : mrow;
+                // a row that has seen no visible key keeps mrow = -inf: its factor must be 1, not NaN
+                const float corr = MASKED && !raise ? 1.0f : __builtin_amdgcn_exp2f(mrow - mnew);
+                lpart *= corr;
+#pragma unroll
+                for (int i = 0; i < 2; ++i)
+#pragma unroll
+                    for (int e = 0; e < 16; ++e) o[i][e] *= corr;
+                mrow = mnew;
+            }
+            psum = exps(MASKED && mrow == -INFINITY ? 0.f : -mrow);
+        }
         lpart += psum;
 #pragma unroll
         for (int s4 = 0; s4 < 4; ++s4) {
