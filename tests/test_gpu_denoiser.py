@@ -76,6 +76,61 @@ def test_denoise_forward_parity(case):
     assert err <= LOGIT_TOL[cfg["dtype"]]
 
 
+def _far_first_tile_params(cfg, seed, f1=3, f2=17, c=72.0):
+    """Host parameters of a one-head model in which every query scores keys 0..63 far below the
+    others.  Features f1 and f2 (< d / 2, where the time embedding at alpha_t = 1 is 0) are equal in
+    every token embedding, in the LayerNorm gain and bias, and in the position embedding past 63,
+    so after LN1 they are equal there; positions 0..63 put +64 and -64 on them.  Key component 0 is
+    x[f2] - x[f1] (zero past 63, about -11.3 before) and query component 0 carries a bias c."""
+    specs = oparams.specs(cfg)
+    P = workloads.host_params(cfg, seed, specs)
+    P["tok_emb"][:, f2] = P["tok_emb"][:, f1]
+    P["l0.ln1_g"][f2] = P["l0.ln1_g"][f1]
+    P["l0.ln1_b"][f2] = P["l0.ln1_b"][f1]
+    pos = P["pos_emb"]
+    pos[:, f2] = pos[:, f1]
+    pos[:64, f1], pos[:64, f2] = 64.0, -64.0
+    d = cfg["d_model"]
+    wk = P["l0.w_qkv"][d]                 # key component 0
+    wk[:] = 0.0
+    wk[f1], wk[f2] = -1.0, 1.0
+    P["l0.b_qkv"][d] = 0.0
+    P["l0.b_qkv"][0] = c                  # query component 0
+    return P, specs
+
+
+@pytest.mark.parametrize("L", [200, 1024])
+def test_attention_raises_its_reference_after_the_first_tile(L):
+    """Keys 0..63 score about 150 (base 2) below the rest for every query, so the exponent reference
+    set by the first key tile is exceeded by more than 2^64 in the second: the attention kernel takes
+    its recompute-and-raise path there and the fast path afterwards.  The gap is past 128, so
+    exponentials taken against the first tile's reference would overflow fp32.  The forward pass
+    matches the oracle to the logit bar (L 200: ragged last tile)."""
+    torch = torch_or_skip()
+    cfg = workloads.model_cfg(2, n_layers=1, d_model=64, n_heads=1, d_mlp=256, vocab=1000)
+    P, specs = _far_first_tile_params(cfg, seed=23)
+    B, V = 2, cfg["vocab"]
+    z = workloads.masked_state(5, B, L, V, 0.5)
+    # the precondition, from the oracle's own pieces: scores (base 2) of keys past 63 exceed those
+    # of keys 0..63 by more than 128 for every query
+    h = P["tok_emb"][z] + P["pos_emb"][:L][None] + oforward.time_embedding(1.0, 64)[None, None]
+    x = oforward.layer_norm(h, P["l0.ln1_g"], P["l0.ln1_b"], cfg["norm_eps"])
+    qkv = x @ P["l0.w_qkv"].T + P["l0.b_qkv"]
+    q, k = qkv[..., :64], qkv[..., 64:128]
+    s2 = np.einsum("bid,bjd->bij", q, k) / 8.0 * np.log2(np.e)
+    gap = s2[:, :, 64:128].max(axis=2) - s2[:, :, :64].max(axis=2)
+    say(f"L {L}: smallest gap between the second and the first key tile {gap.min():.1f}")
+    assert gap.min() > 128 + 5
+    blob = dd.pack_params(cfg, [P[n] for n, _, _ in specs])
+    buf = torch.zeros(blob.size, dtype=torch.uint8, device="cuda")
+    dd.init_params(cfg, buf, host_blob=blob)
+    got = _forward_gpu(torch, cfg, buf, z, 1.0)
+    ref = oforward.forward(cfg, P, z, 1.0)
+    err = float(np.abs(got - ref).max())
+    say(f"max |dlogit| = {err:.3e} (logit std {ref.std():.3f})")
+    assert err <= LOGIT_TOL["bf16"]
+
+
 def test_forward_out_of_range_token_sets_error_word():
     torch = torch_or_skip()
     cfg = workloads.model_cfg(1)
