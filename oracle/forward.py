@@ -5,7 +5,7 @@ The paper (Background, Discrete Diffusion Language Models) defines the
 denoiser only as a map from (z_t, t) to per-position distributions over the
 vocabulary; its own model is a causal AR transformer (Sec. 3, Diffusion-
 augmented LLMs) which this path does not use.  The workloads fix a pre-LN,
-GPT-2-shaped, non-causal transformer.  This build's reading:
+GPT-2-shaped, non-causal transformer.  Reading adopted here:
 
   h   = tok_emb[z_t] + pos_emb[l] + temb(alpha_t)
   temb_j = sin(tau w_j) (j < d/2), cos(tau w_{j-d/2}) (j >= d/2),

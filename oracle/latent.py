@@ -11,7 +11,7 @@ eps_v = N(word(STREAM_LATENT, step, row, v)) (noise.normal_icdf); the lowest
 index wins a tie.
 
 The paper does not print the map between alpha_tilde and the discrete
-schedule alpha.  This build's reading: z = x exactly when every other latent
+schedule alpha.  Reading adopted here: z = x exactly when every other latent
 falls below alpha_tilde / sigma + eps_x, so
 
   P(z = x) = integral phi(u) Phi(u + alpha_tilde / sigma)**(K - 1) du,

@@ -2,7 +2,7 @@
 (test infrastructure only).
 
 The paper does not specify how uniforms, Gumbels or normals are produced; the
-definitions below are this build's reading, chosen so that every value is
+definitions below are the reading adopted here, chosen so that every value is
 exactly defined in float64:
 
   u(w)  = (w + 1/2) * 2**-32                 in (0, 1), exact in float64

@@ -21,7 +21,7 @@ w_out, per layer l at ids 2 + 12 L + 3 + 4 l + (0..3) for qkv, o, 1, 2
 (L = n_layers).  `init_params` splits each stored row into P['l.w_*'] and
 P['l.lora_b_*']; `storage_tensors` joins them again in id order.
 
-Initialisation (this build's reading of "weights ~ N(0, 0.02)"): element e of
+Initialisation (the reading adopted here of "weights ~ N(0, 0.02)"): element e of
 tensor `id` takes the Box-Muller normal of Philox block
 (e >> 1 low, e >> 1 high, id, STREAM_PARAM) under key `seed`, using words 0
 and 1 (cosine branch for even e, sine for odd e).  Matrices, embeddings,

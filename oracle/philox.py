@@ -7,7 +7,7 @@ constants, swaps the high/low halves into a new word order xored with the key,
 and bumps the key by the Weyl increments.  Ten rounds.
 
 The paper being reproduced (arXiv 2609.04010) does not say how its noise is
-drawn; the counter layout below is this build's reading (see `counter`).
+drawn; the counter layout below is the reading adopted here (see `counter`).
 
 Pinned by the Random123 known-answer vectors (tests/golden/philox_kat.txt) and
 by agreement of the two implementations here (scalar Python ints vs numpy).

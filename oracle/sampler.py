@@ -3,7 +3,7 @@
 The paper draws each token of z_s from its per-position categorical
 (App. A.4: the transition is applied token-wise; Sec. 4 linear sampler: each
 position is drawn independently) but does not say how a categorical draw is
-made.  This build's reading is a two-level Gumbel-max draw, exact for any
+made.  The reading adopted here is a two-level Gumbel-max draw, exact for any
 partition of the classes into groups:
 
   groups     real classes in contiguous groups of GROUP = 256

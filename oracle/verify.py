@@ -17,7 +17,7 @@ therefore always accepted).  Every emitted token is distributed as the target
 pin: chi-square of the first emitted token against p_1, and 1 <= TPF =
 (n + 1) / 2 <= (B + 1) / 2.
 
-Noise (this build's definition, like the posterior draw's): r_i is the word
+Noise (the definition adopted here, like the posterior draw's): r_i is the word
 (STREAM_VERIFY, step, seq, i) read as u = (w + 1/2) 2^-32; z is the two-level
 Gumbel-max draw of sampler.py over K = V classes (no mask group) with the level-1
 and level-2 words of row `seq`.  Explicit noise: per sequence B - 1 acceptance
