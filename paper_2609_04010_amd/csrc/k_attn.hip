@@ -12,8 +12,10 @@
 //   S^T = K Q^T with v_mfma_f32_32x32x16_bf16 (first operand: K rows from LDS; second: the wave's
 //         Q fragment, held in registers for the whole kernel).  Each lane then holds 32 scores of
 //         one query, the other 32 of the tile being in lane ^ 32.
-//   Online softmax in base 2 with the 1/sqrt(dh) scale folded into the exponent; the row max is
-//         combined with one cross-lane exchange; the running sum stays per lane until the end.
+//   Online softmax in base 2 with the 1/sqrt(dh) scale folded into the exponent.  The exponent
+//         reference is the row maximum of the first tile (one cross-lane exchange) and stays while
+//         the probabilities of later tiles remain below 2^64; only a tile that exceeds that takes
+//         its maximum again and raises the reference.  The running sum stays per lane until the end.
 //   O^T += V^T P^T: the probabilities are rounded to bf16 and used directly as the second MFMA
 //         operand (no shuffles), so each lane's output column is again its own query.  The first
 //         operand needs, per lane, one head column of V at the 8 keys the accumulator layout of S^T
