@@ -31,6 +31,11 @@
  *   - Out-of-range token ids met on the device set bit DD_DEVERR_TOKEN in a
  *     device error word (the id is clamped so memory stays in bounds); read it
  *     with dd_read_device_error.  No call aborts and no exception crosses the ABI.
+ *   - Tuning override: the environment variable DD_GEMM_TILE = 0..10, when set,
+ *     forces one tile variant of the bf16 projections (for tuning and for tests
+ *     that cover every variant).  It changes speed and, for the vocabulary
+ *     projection, the order in which K-slices are summed; never the operation.
+ *     Nothing else in the library reads the environment.
  */
 #ifndef DD_H
 #define DD_H
@@ -93,6 +98,9 @@ typedef struct {
     int32_t n_heads;
     int32_t d_mlp;
     int32_t vocab;      /* V */
+    int32_t mask_id;    /* id of the [MASK] token: V under DD_PRIOR_MASK (the K-th category,
+                           Background: Notation), -1 under DD_PRIOR_UNIFORM (no mask);
+                           any other value is DD_E_UNSUPPORTED */
     int32_t max_len;    /* rows of the position embedding; L <= max_len */
     int32_t prior;      /* dd_prior: selects tok_emb rows (V + 1 or V) */
     int32_t dtype;      /* dd_dtype of weights, activations and logits */
@@ -129,8 +137,35 @@ size_t dd_param_bytes(const dd_config* cfg);
  * first int32).  0 if the configuration is invalid. */
 size_t dd_workspace_bytes(const dd_config* cfg, int32_t B, int32_t L);
 /* Workspace for dd_sample_loop: the forward workspace plus one logit matrix,
- * the compacted row list and the per-group log-sum-exps of every logit row. */
+ * the compacted row list, the per-group log-sum-exps of every logit row and one
+ * row log-sum-exp per token row. */
 size_t dd_loop_workspace_bytes(const dd_config* cfg, int32_t B, int32_t L);
+
+/*
+ * Where dd_sample_loop / dd_psi_sample_loop keep the last reverse step's
+ * intermediate values inside their workspace (byte offsets from its start), so
+ * that a caller can inspect the arithmetic of a step: run a loop of one step
+ * and read these regions once the stream has reached the end of the call.
+ *   logits      [rows][logits_ld] of cfg->dtype: the vocabulary projection of the
+ *               step.  Compacted (masked prior, bf16, d_model % 128 == 0):
+ *               logits row j < *count belongs to token row rows[j]; otherwise
+ *               logits row m belongs to token row m.
+ *   rows, count int32 [B*L] and int32: the compacted list of the token rows that
+ *               were masked before the step (ascending) and its length; count is
+ *               -1 when the loop does not compact.
+ *   glse        fp32 [rows][glse_ld]: per-group log-sum-exps of each logits row
+ *               (groups of DD_GUMBEL_GROUP classes) when the vocabulary
+ *               projection wrote them (see dd_sample_loop), else unspecified.
+ *   row_lse     fp32 [B*L]: log-sum-exp over the V logits of every token row the
+ *               step drew, in the fp32 arithmetic the draw uses; rows the step
+ *               did not draw (carried over) are left as they were.
+ * Returns DD_E_ARG for an invalid configuration or B, L <= 0.
+ */
+typedef struct {
+    size_t err, logits, rows, count, glse, row_lse;
+    int64_t logits_ld, glse_ld;
+} dd_loop_ws_layout;
+dd_status dd_loop_workspace_layout(const dd_config* cfg, int32_t B, int32_t L, dd_loop_ws_layout* out);
 /* Recommended logit row stride (elements): V rounded up to a multiple of 64. */
 int64_t dd_logits_ld(int32_t V);
 /* Explicit-noise words per row: level-1 words (one per group, plus one for the
@@ -219,6 +254,8 @@ dd_status dd_denoise_forward_ex(const dd_config* cfg, const void* params,
  * dd_posterior_sample - one reverse-posterior draw per row (App. A.1 / A.2 with
  * x = softmax(logits); App. A.4 eq. psi-sampler at kappa_t = 1).
  *   prior        dd_prior
+ *   mask_id      V under DD_PRIOR_MASK (the mask is the K-th category), -1 under
+ *                DD_PRIOR_UNIFORM; any other value is DD_E_UNSUPPORTED
  *   logits       device [rows][ld] of logits_dtype (bf16 or fp32), finite or -inf,
  *                at least one finite per read row; ld >= V, ld % 8 == 0.  Under the
  *                masked prior only rows whose z_t is the mask id are read.  A row
@@ -231,8 +268,14 @@ dd_status dd_denoise_forward_ex(const dd_config* cfg, const void* params,
  *                and (class >> 2, row0 + row, step, 1) for the level-2 word of
  *                a class.  Otherwise device uint32 [rows][dd_noise_width] words.
  *                A word w stands for the uniform u = (w + 1/2) 2^-32.
+ *   row_lse      NULL, or device fp32 [rows]: for every row that draws (masked
+ *                rows under the masked prior, every row under the uniform prior)
+ *                the log-sum-exp of its V logits as the draw computes it (fp32,
+ *                from the per-group log-sum-exps), so that a caller can form the
+ *                draw's probabilities x_v = exp(l_v - row_lse); other rows are
+ *                left untouched.
  *   probs        NULL, or device fp32 [rows][K] that receives the posterior
- *                probabilities (debug; slow).
+ *                probabilities (debug; a separate float64 kernel; slow).
  *   dev_err      NULL or device int32 error word (DD_DEVERR_TOKEN and
  *                DD_DEVERR_LOGITS are or-ed in).
  * Draw: level 1 picks group g by argmax of log M_g + Gumbel (M_g = posterior
@@ -244,10 +287,11 @@ dd_status dd_denoise_forward_ex(const dd_config* cfg, const void* params,
  * debug probabilities in float64.
  */
 dd_status dd_posterior_sample(int32_t prior, const void* logits, int32_t logits_dtype,
-                              int64_t ld, int32_t rows, int32_t V, const int32_t* z_t,
-                              double alpha_t, double alpha_s, const uint32_t* noise_words,
-                              uint64_t seed, uint32_t step, uint32_t row0, int32_t* z_s,
-                              float* probs, int32_t* dev_err, void* stream);
+                              int64_t ld, int32_t rows, int32_t V, int32_t mask_id,
+                              const int32_t* z_t, double alpha_t, double alpha_s,
+                              const uint32_t* noise_words, uint64_t seed, uint32_t step,
+                              uint32_t row0, int32_t* z_s, float* row_lse, float* probs,
+                              int32_t* dev_err, void* stream);
 
 /*
  * dd_psi_posterior_sample - one Psi-sampler draw per row (App. A.4, eq. psi:
@@ -262,11 +306,11 @@ dd_status dd_posterior_sample(int32_t prior, const void* logits, int32_t logits_
  * prior: every class keeps non-zero probability for kappa < 1.
  */
 dd_status dd_psi_posterior_sample(int32_t prior, const void* logits, int32_t logits_dtype,
-                                  int64_t ld, int32_t rows, int32_t V, const int32_t* z_t,
-                                  double alpha_t, double alpha_s, double kappa,
-                                  const uint32_t* noise_words, uint64_t seed, uint32_t step,
-                                  uint32_t row0, int32_t* z_s, float* probs, int32_t* dev_err,
-                                  void* stream);
+                                  int64_t ld, int32_t rows, int32_t V, int32_t mask_id,
+                                  const int32_t* z_t, double alpha_t, double alpha_s,
+                                  double kappa, const uint32_t* noise_words, uint64_t seed,
+                                  uint32_t step, uint32_t row0, int32_t* z_s, float* row_lse,
+                                  float* probs, int32_t* dev_err, void* stream);
 
 /*
  * dd_sample_loop - T ancestral steps z_1 -> z_0 on the grid t_k = k/T.
@@ -287,14 +331,20 @@ dd_status dd_psi_posterior_sample(int32_t prior, const void* logits, int32_t log
  * group of DD_GUMBEL_GROUP classes (from the rounded logits it stores), and the draw reads those
  * and one group of logits per row instead of the whole row.  The result equals calling
  * dd_denoise_forward and dd_posterior_sample on every row, up to the summation order inside each
- * group's log-sum-exp (a draw can differ only where two level-1 scores lie within a few ulps).
- * The environment variable DD_POSTERIOR_PASS=1 (read at each call) makes the draw take its own
- * pass over the logit rows instead, as dd_posterior_sample does.
+ * group's log-sum-exp (a draw can differ only where two level-1 scores lie within a few ulps);
+ * dd_psi_sample_loop with DD_LOOP_POSTERIOR_PASS makes the draw take its own pass over the
+ * logit rows instead, as dd_posterior_sample does.  The mask id is cfg->mask_id.  The last
+ * step's logits and log-sum-exps stay in the workspace (dd_loop_workspace_layout).
  */
 dd_status dd_sample_loop(const dd_config* cfg, const void* params, int32_t B, int32_t L,
                          int32_t T, const double* alphas, int32_t* z,
                          const uint32_t* noise_words, uint64_t noise_seed,
                          int32_t* z_trace, void* ws, size_t ws_bytes, void* stream);
+
+/* dd_psi_sample_loop flags */
+#define DD_LOOP_POSTERIOR_PASS 1u /* draw from the posterior's own pass over each logits row
+                                     instead of the group log-sum-exps the vocabulary
+                                     projection writes (same draws up to summation order) */
 
 /*
  * dd_psi_sample_loop - dd_sample_loop with the Psi transition (App. A.4,
@@ -302,6 +352,7 @@ dd_status dd_sample_loop(const dd_config* cfg, const void* params, int32_t B, in
  * kappa = kappas[k].
  *   kappas       NULL (every kappa 1: exactly dd_sample_loop) or host double
  *                [T + 1], each used entry (k = 1..T) in [0, 1].
+ *   flags        0 or DD_LOOP_POSTERIOR_PASS (other bits: DD_E_ARG).
  * With kappa < 1 decoded tokens can be remasked and T may exceed the number of
  * positions (inference-time scaling, Sec. 4); a step with alpha_s = 1 (the
  * last one) still unmasks every position.  Masked prior (bf16): the rows
@@ -311,7 +362,8 @@ dd_status dd_sample_loop(const dd_config* cfg, const void* params, int32_t B, in
  * dd_psi_posterior_sample on every row.
  */
 dd_status dd_psi_sample_loop(const dd_config* cfg, const void* params, int32_t B, int32_t L,
-                             int32_t T, const double* alphas, const double* kappas, int32_t* z,
+                             int32_t T, const double* alphas, const double* kappas,
+                             uint32_t flags, int32_t* z,
                              const uint32_t* noise_words, uint64_t noise_seed,
                              int32_t* z_trace, void* ws, size_t ws_bytes, void* stream);
 
@@ -372,7 +424,9 @@ dd_status dd_gaussian_latent_argmax(const int32_t* x, int32_t rows, int32_t V,
  * Per-launch timing with HIP events recorded on the launching stream.  While
  * enabled, every launch of a kernel class whose bit is set in `class_mask`
  * (bit c = class c; 0 selects every class) is bracketed by an event pair.  At
- * most `max_launches` launches are recorded.  Not thread-safe; for benchmarks.
+ * most `max_launches` launches are recorded.  For benchmarks.  The recorder is
+ * the library's only process-wide mutable state; it is guarded by a mutex, and
+ * while it is off (the default) no launch touches it.
  * Classes: 0 time_embedding, 1 embed_layernorm, 2 layernorm, 3 gemm_qkv,
  * 4 attention, 5 gemm_attn_out, 6 gemm_mlp_up, 7 gemm_mlp_down, 8 gemm_vocab,
  * 9 posterior_sample, 10 gaussian_latent, 11 init_params, 12 copy, 13 compact_masked.

@@ -84,8 +84,9 @@ def projection(cfg, P, l, name, a, gate):
     return y
 
 
-def forward_hidden(cfg, P, z, alpha_t, vis=None, gate=None):
-    """Final-LN activations [B, L, d] for token ids z [B, L]."""
+def forward_hidden(cfg, P, z, alpha_t, vis=None, gate=None, on_layer=None):
+    """Final-LN activations [B, L, d] for token ids z [B, L].  on_layer: optional callable that is
+    given the index of each layer once it is done (progress reporting of long runs only)."""
     z = np.asarray(z)
     B, L = z.shape
     d, H = cfg["d_model"], cfg["n_heads"]
@@ -108,12 +109,14 @@ def forward_hidden(cfg, P, z, alpha_t, vis=None, gate=None):
         h = h + projection(cfg, P, l, "o", o, g)
         a = layer_norm(h, p("ln2_g"), p("ln2_b"), eps)
         h = h + projection(cfg, P, l, "2", gelu_tanh(projection(cfg, P, l, "1", a, g)), g)
+        if on_layer is not None:
+            on_layer(l)
     return layer_norm(h, P["lnf_g"], P["lnf_b"], eps)
 
 
-def forward(cfg, P, z, alpha_t, vis=None, gate=None):
+def forward(cfg, P, z, alpha_t, vis=None, gate=None, on_layer=None):
     """Logits [B, L, V] (float64) of the denoiser at noise level alpha_t."""
-    return forward_hidden(cfg, P, z, alpha_t, vis, gate) @ P["w_out"].T
+    return forward_hidden(cfg, P, z, alpha_t, vis, gate, on_layer) @ P["w_out"].T
 
 
 def x_theta(logits):

@@ -22,13 +22,15 @@ DD_GUMBEL_GROUP = 256
 DD_DEVERR_TOKEN = 1
 DD_DEVERR_MASK = 2
 DD_DEVERR_LOGITS = 4
+DD_LOOP_POSTERIOR_PASS = 1
 ATTN_PATTERNS = {"bidirectional": 0, "causal": 1, "block_causal": 2, "draft_train": 3}
 STATUS = {0: "DD_OK", 1: "DD_E_ARG", 2: "DD_E_SHAPE", 3: "DD_E_DTYPE", 4: "DD_E_WORKSPACE",
           5: "DD_E_HIP", 6: "DD_E_UNSUPPORTED", 7: "DD_E_DEVICE"}
 
 EXPORTED = [
     "dd_param_count", "dd_param_tensor", "dd_param_bytes", "dd_workspace_bytes",
-    "dd_loop_workspace_bytes", "dd_logits_ld", "dd_noise_width", "dd_status_str", "dd_last_error",
+    "dd_loop_workspace_bytes", "dd_loop_workspace_layout", "dd_logits_ld", "dd_noise_width",
+    "dd_status_str", "dd_last_error",
     "dd_workspace_reset", "dd_read_device_error", "dd_init_params", "dd_denoise_forward",
     "dd_attn_mask_build", "dd_denoise_forward_ex",
     "dd_posterior_sample", "dd_psi_posterior_sample", "dd_sample_loop", "dd_psi_sample_loop",
@@ -41,10 +43,16 @@ EXPORTED = [
 class DDConfig(ctypes.Structure):
     _fields_ = [("n_layers", ctypes.c_int32), ("d_model", ctypes.c_int32),
                 ("n_heads", ctypes.c_int32), ("d_mlp", ctypes.c_int32),
-                ("vocab", ctypes.c_int32), ("max_len", ctypes.c_int32),
+                ("vocab", ctypes.c_int32), ("mask_id", ctypes.c_int32), ("max_len", ctypes.c_int32),
                 ("prior", ctypes.c_int32), ("dtype", ctypes.c_int32),
                 ("time_cond", ctypes.c_int32), ("norm_eps", ctypes.c_float),
                 ("lora_rank", ctypes.c_int32), ("lora_alpha", ctypes.c_float)]
+
+
+class DDLoopWsLayout(ctypes.Structure):
+    _fields_ = [("err", ctypes.c_size_t), ("logits", ctypes.c_size_t), ("rows", ctypes.c_size_t),
+                ("count", ctypes.c_size_t), ("glse", ctypes.c_size_t), ("row_lse", ctypes.c_size_t),
+                ("logits_ld", ctypes.c_int64), ("glse_ld", ctypes.c_int64)]
 
 
 class DDError(RuntimeError):
@@ -72,6 +80,7 @@ def lib():
             "dd_param_bytes": (c.c_size_t, [cfgp]),
             "dd_workspace_bytes": (c.c_size_t, [cfgp, c.c_int32, c.c_int32]),
             "dd_loop_workspace_bytes": (c.c_size_t, [cfgp, c.c_int32, c.c_int32]),
+            "dd_loop_workspace_layout": (c.c_int32, [cfgp, c.c_int32, c.c_int32, c.POINTER(DDLoopWsLayout)]),
             "dd_logits_ld": (c.c_int64, [c.c_int32]),
             "dd_noise_width": (c.c_int32, [c.c_int32, c.c_int32]),
             "dd_status_str": (c.c_char_p, [c.c_int32]),
@@ -85,18 +94,18 @@ def lib():
             "dd_denoise_forward_ex": (c.c_int32, [cfgp, P, P, c.c_int32, c.c_int32, c.c_double, P, P,
                                                   P, c.c_int64, P, c.c_size_t, P]),
             "dd_posterior_sample": (c.c_int32, [c.c_int32, P, c.c_int32, c.c_int64, c.c_int32,
-                                                c.c_int32, P, c.c_double, c.c_double, P,
-                                                c.c_uint64, c.c_uint32, c.c_uint32, P, P, P, P]),
+                                                c.c_int32, c.c_int32, P, c.c_double, c.c_double, P,
+                                                c.c_uint64, c.c_uint32, c.c_uint32, P, P, P, P, P]),
             "dd_psi_posterior_sample": (c.c_int32, [c.c_int32, P, c.c_int32, c.c_int64, c.c_int32,
-                                                    c.c_int32, P, c.c_double, c.c_double, c.c_double,
-                                                    P, c.c_uint64, c.c_uint32, c.c_uint32, P, P, P,
-                                                    P]),
+                                                    c.c_int32, c.c_int32, P, c.c_double, c.c_double,
+                                                    c.c_double, P, c.c_uint64, c.c_uint32, c.c_uint32,
+                                                    P, P, P, P, P]),
             "dd_sample_loop": (c.c_int32, [cfgp, P, c.c_int32, c.c_int32, c.c_int32,
                                            c.POINTER(c.c_double), P, P, c.c_uint64, P, P,
                                            c.c_size_t, P]),
             "dd_psi_sample_loop": (c.c_int32, [cfgp, P, c.c_int32, c.c_int32, c.c_int32,
-                                               c.POINTER(c.c_double), c.POINTER(c.c_double), P, P,
-                                               c.c_uint64, P, P, c.c_size_t, P]),
+                                               c.POINTER(c.c_double), c.POINTER(c.c_double), c.c_uint32,
+                                               P, P, c.c_uint64, P, P, c.c_size_t, P]),
             "dd_gaussian_latent_argmax": (c.c_int32, [P, c.c_int32, c.c_int32, c.c_double,
                                                       c.c_double, c.c_uint64, c.c_uint32,
                                                       c.c_uint32, P, P, P]),
@@ -124,10 +133,16 @@ def _check(st):
         raise DDError(st, lib().dd_last_error().decode())
 
 
+def default_mask_id(prior, V):
+    """The mask id a prior takes: V (the K-th category) for the masked prior, -1 for the uniform."""
+    return int(V) if prior == "mask" else -1
+
+
 def make_config(cfg):
     """DDConfig from the architecture dictionary used by the workloads and the oracle."""
+    mid = cfg.get("mask_id", default_mask_id(cfg["prior"], cfg["vocab"]))
     return DDConfig(int(cfg["n_layers"]), int(cfg["d_model"]), int(cfg["n_heads"]),
-                    int(cfg["d_mlp"]), int(cfg["vocab"]), int(cfg["max_len"]),
+                    int(cfg["d_mlp"]), int(cfg["vocab"]), int(mid), int(cfg["max_len"]),
                     DD_PRIOR_MASK if cfg["prior"] == "mask" else DD_PRIOR_UNIFORM,
                     DD_BF16 if cfg["dtype"] == "bf16" else DD_FP32,
                     1 if cfg.get("time_cond", True) else 0, float(cfg.get("norm_eps", 1e-5)),
@@ -165,6 +180,13 @@ def workspace_bytes(cfg, B, L):
 
 def loop_workspace_bytes(cfg, B, L):
     return lib().dd_loop_workspace_bytes(ctypes.byref(make_config(cfg)), B, L)
+
+
+def loop_workspace_layout(cfg, B, L):
+    """dict of the loop workspace regions (byte offsets, row strides) of dd_loop_workspace_layout."""
+    out = DDLoopWsLayout()
+    _check(lib().dd_loop_workspace_layout(ctypes.byref(make_config(cfg)), int(B), int(L), ctypes.byref(out)))
+    return {n: getattr(out, n) for n, _ in DDLoopWsLayout._fields_}
 
 
 def logits_ld(V):
@@ -271,7 +293,8 @@ def denoise_forward_ex(cfg, params, z_t, B, L, alpha_t, logits, ld, ws, attn_mas
         _ptr(ws, workspace_bytes(cfg, B, L), "ws"), ws.numel() * ws.element_size(), _stream()))
 
 
-def _posterior_args(prior, logits, logits_dtype, ld, rows, V, z_t, noise_words, z_s, probs, dev_err):
+def _posterior_args(prior, logits, logits_dtype, ld, rows, V, z_t, noise_words, z_s, row_lse, probs,
+                    dev_err):
     torch = _torch()
     es = 2 if logits_dtype == "bf16" else 4
     K = V + 1 if prior == "mask" else V
@@ -280,32 +303,39 @@ def _posterior_args(prior, logits, logits_dtype, ld, rows, V, z_t, noise_words, 
     return (lg, _ptr(z_t, 4 * rows, "z_t", torch.int32),
             _ptr(noise_words, 4 * rows * nu, "noise_words", torch.int32) if noise_words is not None else None,
             _ptr(z_s, 4 * rows, "z_s", torch.int32),
+            _ptr(row_lse, 4 * rows, "row_lse", torch.float32) if row_lse is not None else None,
             _ptr(probs, 4 * rows * K, "probs", torch.float32) if probs is not None else None,
             _ptr(dev_err, 4, "dev_err", torch.int32) if dev_err is not None else None)
 
 
 def posterior_sample(prior, logits, logits_dtype, ld, rows, V, z_t, alpha_t, alpha_s, z_s,
-                     noise_words=None, seed=0, step=0, row0=0, probs=None, dev_err=None):
-    lg, zt, nw, zs, pr, er = _posterior_args(prior, logits, logits_dtype, ld, rows, V, z_t, noise_words,
-                                             z_s, probs, dev_err)
+                     noise_words=None, seed=0, step=0, row0=0, probs=None, dev_err=None, row_lse=None,
+                     mask_id=None):
+    """dd_posterior_sample; mask_id defaults to the prior's (V for "mask", -1 for "uniform")."""
+    lg, zt, nw, zs, rl, pr, er = _posterior_args(prior, logits, logits_dtype, ld, rows, V, z_t, noise_words,
+                                                 z_s, row_lse, probs, dev_err)
+    mid = default_mask_id(prior, V) if mask_id is None else int(mask_id)
     _check(lib().dd_posterior_sample(
-        prior_code(prior), lg, dtype_code(logits_dtype), int(ld), int(rows), int(V), zt, float(alpha_t),
-        float(alpha_s), nw, int(seed) & 0xFFFFFFFFFFFFFFFF, int(step), int(row0), zs, pr, er, _stream()))
+        prior_code(prior), lg, dtype_code(logits_dtype), int(ld), int(rows), int(V), mid, zt, float(alpha_t),
+        float(alpha_s), nw, int(seed) & 0xFFFFFFFFFFFFFFFF, int(step), int(row0), zs, rl, pr, er, _stream()))
 
 
 def psi_posterior_sample(prior, logits, logits_dtype, ld, rows, V, z_t, alpha_t, alpha_s, kappa, z_s,
-                         noise_words=None, seed=0, step=0, row0=0, probs=None, dev_err=None):
-    lg, zt, nw, zs, pr, er = _posterior_args(prior, logits, logits_dtype, ld, rows, V, z_t, noise_words,
-                                             z_s, probs, dev_err)
+                         noise_words=None, seed=0, step=0, row0=0, probs=None, dev_err=None, row_lse=None,
+                         mask_id=None):
+    lg, zt, nw, zs, rl, pr, er = _posterior_args(prior, logits, logits_dtype, ld, rows, V, z_t, noise_words,
+                                                 z_s, row_lse, probs, dev_err)
+    mid = default_mask_id(prior, V) if mask_id is None else int(mask_id)
     _check(lib().dd_psi_posterior_sample(
-        prior_code(prior), lg, dtype_code(logits_dtype), int(ld), int(rows), int(V), zt, float(alpha_t),
-        float(alpha_s), float(kappa), nw, int(seed) & 0xFFFFFFFFFFFFFFFF, int(step), int(row0), zs, pr, er,
+        prior_code(prior), lg, dtype_code(logits_dtype), int(ld), int(rows), int(V), mid, zt, float(alpha_t),
+        float(alpha_s), float(kappa), nw, int(seed) & 0xFFFFFFFFFFFFFFFF, int(step), int(row0), zs, rl, pr, er,
         _stream()))
 
 
 def sample_loop(cfg, params, B, L, T, alphas, z, ws, noise_words=None, noise_seed=0, z_trace=None,
-                kappas=None):
-    """dd_sample_loop, or dd_psi_sample_loop when kappas (T + 1 values) is given."""
+                kappas=None, posterior_pass=False):
+    """dd_sample_loop, or dd_psi_sample_loop when kappas (T + 1 values) is given or posterior_pass
+    (DD_LOOP_POSTERIOR_PASS) is set."""
     torch = _torch()
     M = B * L
     a = np.ascontiguousarray(alphas, dtype=np.float64)
@@ -319,13 +349,16 @@ def sample_loop(cfg, params, B, L, T, alphas, z, ws, noise_words=None, noise_see
             int(noise_seed) & 0xFFFFFFFFFFFFFFFF,
             _ptr(z_trace, 4 * (T + 1) * M, "z_trace", torch.int32) if z_trace is not None else None,
             _ptr(ws, loop_workspace_bytes(cfg, B, L), "ws"), ws.numel() * ws.element_size(), _stream())
-    if kappas is None:
+    if kappas is None and not posterior_pass:
         _check(lib().dd_sample_loop(*head, *tail))
     else:
-        k = np.ascontiguousarray(kappas, dtype=np.float64)
-        if k.shape != (T + 1,):
-            raise ValueError("kappas must hold T + 1 values")
-        _check(lib().dd_psi_sample_loop(*head, k.ctypes.data_as(dp), *tail))
+        k = None
+        if kappas is not None:
+            k = np.ascontiguousarray(kappas, dtype=np.float64)
+            if k.shape != (T + 1,):
+                raise ValueError("kappas must hold T + 1 values")
+        flags = DD_LOOP_POSTERIOR_PASS if posterior_pass else 0
+        _check(lib().dd_psi_sample_loop(*head, k.ctypes.data_as(dp) if k is not None else None, flags, *tail))
 
 
 def spec_verify_workspace_bytes(S, B):

@@ -8,6 +8,8 @@
 #include <string.h>
 
 #include <algorithm>
+#include <atomic>
+#include <mutex>
 #include <vector>
 
 #include "kernels.h"
@@ -53,8 +55,10 @@ static const char* kClassNames[KC_COUNT] = {
     "gemm_mlp_up", "gemm_mlp_down", "gemm_vocab", "posterior_sample", "gaussian_latent",
     "init_params", "copy", "compact_masked", "gemm_lora_down"};
 
+// The recorder is the library's only process-wide mutable state: guarded by g_prof_mu, and skipped
+// without taking the lock while it is off.
 struct Profiler {
-    bool on = false;
+    std::atomic<bool> on{false};
     int cap = 0;
     uint32_t mask = 0xFFFFFFFFu;
     std::vector<hipEvent_t> ev;   // 2 per launch
@@ -63,8 +67,11 @@ struct Profiler {
     int64_t dropped = 0;
 };
 static Profiler g_prof;
+static std::mutex g_prof_mu;
 
 void prof_start(int c, hipStream_t s) {
+    if (!g_prof.on.load(std::memory_order_relaxed)) return;
+    std::lock_guard<std::mutex> lk(g_prof_mu);
     if (!g_prof.on || !((g_prof.mask >> c) & 1u)) return;
     const int n = (int)g_prof.cls.size();
     if (n >= g_prof.cap) { g_prof.dropped++; g_prof.open = -1; return; }
@@ -74,6 +81,8 @@ void prof_start(int c, hipStream_t s) {
 }
 
 void prof_stop(int c, hipStream_t s) {
+    if (!g_prof.on.load(std::memory_order_relaxed)) return;
+    std::lock_guard<std::mutex> lk(g_prof_mu);
     if (!g_prof.on || g_prof.open < 0) return;
     (void)hipEventRecord(g_prof.ev[2 * g_prof.open + 1], s);
     (void)c;
@@ -89,30 +98,32 @@ struct Tensor {
 static size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 static size_t esize(int dtype) { return dtype == DD_BF16 ? 2 : 4; }
 
-static bool cfg_ok(const dd_config* c) {
-    if (!c) { set_error("config is NULL"); return false; }
-    if (c->n_layers < 0 || c->d_model <= 0 || c->n_heads <= 0 || c->d_mlp <= 0 || c->vocab <= 0 ||
-        c->max_len <= 0) {
-        set_error("config sizes must be positive");
-        return false;
-    }
-    if (c->d_model % c->n_heads != 0 || c->d_model % 2 != 0) {
-        set_error("d_model must be even and divisible by n_heads");
-        return false;
-    }
-    if (c->prior != DD_PRIOR_MASK && c->prior != DD_PRIOR_UNIFORM) { set_error("unknown prior"); return false; }
-    if (c->dtype != DD_BF16 && c->dtype != DD_FP32) { set_error("unknown dtype"); return false; }
-    if (!(c->norm_eps >= 0.f)) { set_error("norm_eps must be >= 0"); return false; }
-    if (c->lora_rank < 0 || c->lora_rank % 8 != 0) {
-        set_error("lora_rank must be a non-negative multiple of 8 (got %d)", c->lora_rank);
-        return false;
-    }
-    if (c->lora_rank > 0 && !(c->lora_alpha > 0.f && c->lora_alpha < INFINITY)) {
-        set_error("lora_alpha must be positive and finite");
-        return false;
-    }
-    return true;
+// The mask id a prior takes: V (the K-th category) under the masked prior, none (-1) under the
+// uniform prior.
+static dd_status check_mask_id(int prior, int V, int mask_id) {
+    const int want = prior == DD_PRIOR_MASK ? V : -1;
+    DD_CHECK(mask_id == want, DD_E_UNSUPPORTED, "mask_id %d unsupported for the %s prior (it must be %d)",
+             mask_id, prior == DD_PRIOR_MASK ? "masked" : "uniform", want);
+    return DD_OK;
 }
+
+// Validation of a configuration; sets the error message itself (callers return the status as is).
+static dd_status cfg_check(const dd_config* c) {
+    DD_CHECK(c, DD_E_ARG, "config is NULL");
+    DD_CHECK(c->n_layers >= 0 && c->d_model > 0 && c->n_heads > 0 && c->d_mlp > 0 && c->vocab > 0 &&
+                 c->max_len > 0, DD_E_ARG, "config sizes must be positive");
+    DD_CHECK(c->d_model % c->n_heads == 0 && c->d_model % 2 == 0, DD_E_ARG,
+             "d_model must be even and divisible by n_heads");
+    DD_CHECK(c->prior == DD_PRIOR_MASK || c->prior == DD_PRIOR_UNIFORM, DD_E_ARG, "unknown prior");
+    DD_CHECK(c->dtype == DD_BF16 || c->dtype == DD_FP32, DD_E_ARG, "unknown dtype");
+    DD_CHECK(c->norm_eps >= 0.f, DD_E_ARG, "norm_eps must be >= 0");
+    DD_CHECK(c->lora_rank >= 0 && c->lora_rank % 8 == 0, DD_E_ARG,
+             "lora_rank must be a non-negative multiple of 8 (got %d)", c->lora_rank);
+    DD_CHECK(c->lora_rank == 0 || (c->lora_alpha > 0.f && c->lora_alpha < INFINITY), DD_E_ARG,
+             "lora_alpha must be positive and finite");
+    return check_mask_id(c->prior, c->vocab, c->mask_id);
+}
+static bool cfg_ok(const dd_config* c) { return cfg_check(c) == DD_OK; }
 
 static int n_tok(const dd_config* c) { return c->prior == DD_PRIOR_MASK ? c->vocab + 1 : c->vocab; }
 
@@ -160,7 +171,7 @@ static bool is_gain(const dd_config* c, int id) {
 }
 
 struct WsLayout {
-    size_t err, temb, h, xln, qkv, att, mlp, logits, rows, count, glse, total_fwd, total_loop;
+    size_t err, temb, h, xln, qkv, att, mlp, logits, rows, count, glse, row_lse, total_fwd, total_loop;
     int64_t glse_ld;   // per-group log-sum-exps per logits row (a multiple of 4 floats)
 };
 
@@ -186,22 +197,19 @@ static WsLayout ws_layout(const dd_config* c, int64_t M) {
     w.count = off; off = align256(off + 4);
     w.glse_ld = ((c->vocab + DD_GUMBEL_GROUP - 1) / DD_GUMBEL_GROUP + 3) / 4 * 4;
     w.glse = off; off = align256(off + (size_t)(M * w.glse_ld) * 4);
+    w.row_lse = off; off = align256(off + (size_t)M * 4);
     w.total_loop = off;
     return w;
 }
 
-static bool forward_supported(const dd_config* c) {
+static dd_status forward_check(const dd_config* c) {
     const int dh = c->d_model / c->n_heads;
-    if (!ln_supported(c->d_model)) {
-        set_error("d_model %d: LayerNorm kernels need d_model %% 64 == 0 and d_model <= 2048", c->d_model);
-        return false;
-    }
-    if (!attn_supported(c->dtype, dh)) {
-        set_error("head dim %d unsupported for this dtype (bf16: 64; fp32: 16/32/64/128)", dh);
-        return false;
-    }
-    if (c->d_mlp % 8 != 0) { set_error("d_mlp must be a multiple of 8"); return false; }
-    return true;
+    DD_CHECK(ln_supported(c->d_model), DD_E_UNSUPPORTED,
+             "d_model %d: LayerNorm kernels need d_model %% 64 == 0 and d_model <= 2048", c->d_model);
+    DD_CHECK(attn_supported(c->dtype, dh), DD_E_UNSUPPORTED,
+             "head dim %d unsupported for this dtype (bf16: 64; fp32: 16/32/64/128)", dh);
+    DD_CHECK(c->d_mlp % 8 == 0, DD_E_UNSUPPORTED, "d_mlp must be a multiple of 8");
+    return DD_OK;
 }
 
 // vocab_rows / vocab_count (device, nullable): restrict the vocabulary projection to the listed
@@ -296,7 +304,7 @@ static int32_t ntop_of(int prior, int V) {
 static PostArgs make_post(int prior, const void* logits, int64_t ld, int32_t rows, int32_t V,
                           const int32_t* z_t, double at, double as, double kappa,
                           const uint32_t* noise, uint64_t seed, uint32_t step, uint32_t row0,
-                          int32_t* z_s, float* probs, int32_t* err) {
+                          int32_t* z_s, float* row_lse, float* probs, int32_t* err) {
     PostArgs a;
     memset(&a, 0, sizeof(a));
     a.logits = logits; a.ld = ld; a.rows = rows; a.V = V; a.prior = prior;
@@ -331,6 +339,7 @@ static PostArgs make_post(int prior, const void* logits, int64_t ld, int32_t row
     a.nu = a.ntop + V;
     a.seed = seed; a.step = step; a.row0 = row0;
     a.probs = probs; a.err = err;
+    a.row_lse = row_lse;
     return a;
 }
 
@@ -368,7 +377,7 @@ int32_t dd_param_count(const dd_config* cfg) {
 
 dd_status dd_param_tensor(const dd_config* cfg, int32_t id, size_t* offset_bytes, int64_t* rows,
                           int64_t* cols) {
-    DD_CHECK(cfg_ok(cfg), DD_E_ARG, "%s", g_err);
+    DD_TRY(cfg_check(cfg));
     DD_CHECK(offset_bytes && rows && cols, DD_E_ARG, "output pointers must not be NULL");
     const std::vector<Tensor> t = tensor_list(cfg);
     DD_CHECK(id >= 0 && id < (int32_t)t.size(), DD_E_ARG, "tensor id %d out of range", id);
@@ -419,7 +428,7 @@ dd_status dd_read_device_error(const int32_t* err_word, int32_t* code_out, void*
 
 dd_status dd_init_params(const dd_config* cfg, void* params, size_t params_bytes, uint64_t seed,
                          const void* host_src, void* stream) {
-    DD_CHECK(cfg_ok(cfg), DD_E_ARG, "%s", g_err);
+    DD_TRY(cfg_check(cfg));
     DD_CHECK(params, DD_E_ARG, "params is NULL");
     const size_t need = dd_param_bytes(cfg);
     DD_CHECK(params_bytes >= need, DD_E_WORKSPACE, "parameter buffer has %zu bytes, needs %zu",
@@ -476,7 +485,7 @@ dd_status dd_denoise_forward_ex(const dd_config* cfg, const void* params, const 
                                 int32_t B, int32_t L, double alpha_t, const int32_t* attn_mask,
                                 const int32_t* lora_gate, void* logits, int64_t ld, void* ws,
                                 size_t ws_bytes, void* stream) {
-    DD_CHECK(cfg_ok(cfg), DD_E_ARG, "%s", g_err);
+    DD_TRY(cfg_check(cfg));
     DD_CHECK(!lora_gate || cfg->lora_rank > 0, DD_E_ARG, "lora_gate given for a model without adapters");
     DD_CHECK(params && z_t && logits && ws, DD_E_ARG, "NULL pointer argument");
     DD_CHECK(B > 0 && L > 0, DD_E_ARG, "B and L must be positive");
@@ -485,7 +494,7 @@ dd_status dd_denoise_forward_ex(const dd_config* cfg, const void* params, const 
     DD_CHECK(ld >= cfg->vocab && ld % 8 == 0, DD_E_SHAPE, "ld must be >= V and a multiple of 8");
     DD_CHECK(((uintptr_t)logits & 15) == 0 && ((uintptr_t)ws & 255) == 0 && ((uintptr_t)params & 255) == 0,
              DD_E_ARG, "logits must be 16-byte aligned, params and ws 256-byte aligned");
-    DD_CHECK(forward_supported(cfg), DD_E_UNSUPPORTED, "%s", g_err);
+    DD_TRY(forward_check(cfg));
     const size_t need = dd_workspace_bytes(cfg, B, L);
     DD_CHECK(ws_bytes >= need, DD_E_WORKSPACE, "workspace has %zu bytes, needs %zu", ws_bytes, need);
     return run_forward(cfg, params, z_t, B, L, alpha_t, logits, ld, (char*)ws, (hipStream_t)stream,
@@ -495,7 +504,7 @@ dd_status dd_denoise_forward_ex(const dd_config* cfg, const void* params, const 
 dd_status dd_denoise_forward(const dd_config* cfg, const void* params, const int32_t* z_t,
                              int32_t B, int32_t L, double alpha_t, void* logits, int64_t ld,
                              void* ws, size_t ws_bytes, void* stream) {
-    DD_CHECK(cfg_ok(cfg), DD_E_ARG, "%s", g_err);
+    DD_TRY(cfg_check(cfg));
     DD_CHECK(params && z_t && logits && ws, DD_E_ARG, "NULL pointer argument");
     DD_CHECK(B > 0 && L > 0, DD_E_ARG, "B and L must be positive");
     DD_CHECK(L <= cfg->max_len, DD_E_SHAPE, "L = %d exceeds max_len = %d", L, cfg->max_len);
@@ -503,49 +512,67 @@ dd_status dd_denoise_forward(const dd_config* cfg, const void* params, const int
     DD_CHECK(ld >= cfg->vocab && ld % 8 == 0, DD_E_SHAPE, "ld must be >= V and a multiple of 8");
     DD_CHECK(((uintptr_t)logits & 15) == 0 && ((uintptr_t)ws & 255) == 0 && ((uintptr_t)params & 255) == 0,
              DD_E_ARG, "logits must be 16-byte aligned, params and ws 256-byte aligned");
-    DD_CHECK(forward_supported(cfg), DD_E_UNSUPPORTED, "%s", g_err);
+    DD_TRY(forward_check(cfg));
     const size_t need = dd_workspace_bytes(cfg, B, L);
     DD_CHECK(ws_bytes >= need, DD_E_WORKSPACE, "workspace has %zu bytes, needs %zu", ws_bytes, need);
     return run_forward(cfg, params, z_t, B, L, alpha_t, logits, ld, (char*)ws, (hipStream_t)stream);
 }
 
 dd_status dd_psi_posterior_sample(int32_t prior, const void* logits, int32_t logits_dtype, int64_t ld,
-                                  int32_t rows, int32_t V, const int32_t* z_t, double alpha_t,
-                                  double alpha_s, double kappa, const uint32_t* noise_words,
-                                  uint64_t seed, uint32_t step, uint32_t row0, int32_t* z_s,
-                                  float* probs, int32_t* dev_err, void* stream) {
+                                  int32_t rows, int32_t V, int32_t mask_id, const int32_t* z_t,
+                                  double alpha_t, double alpha_s, double kappa,
+                                  const uint32_t* noise_words, uint64_t seed, uint32_t step,
+                                  uint32_t row0, int32_t* z_s, float* row_lse, float* probs,
+                                  int32_t* dev_err, void* stream) {
     DD_CHECK(prior == DD_PRIOR_MASK || prior == DD_PRIOR_UNIFORM, DD_E_ARG, "unknown prior %d", prior);
     DD_CHECK(logits_dtype == DD_BF16 || logits_dtype == DD_FP32, DD_E_DTYPE, "unknown logits dtype");
     DD_CHECK(rows >= 0 && V > 0, DD_E_ARG, "rows must be >= 0 and V > 0");
     DD_CHECK(V <= (1 << 24), DD_E_UNSUPPORTED, "V > 2^24 unsupported");
+    DD_TRY(check_mask_id(prior, V, mask_id));
     DD_CHECK(ld >= V && ld % 8 == 0, DD_E_SHAPE, "ld must be >= V and a multiple of 8");
     DD_TRY(check_schedule(alpha_t, alpha_s));
     DD_CHECK(kappa >= 0.0 && kappa <= 1.0, DD_E_ARG, "kappa must lie in [0, 1] (got %.17g)", kappa);
     if (rows == 0) return DD_OK;
     DD_CHECK(logits && z_t && z_s, DD_E_ARG, "NULL pointer argument");
     const PostArgs a = make_post(prior, logits, ld, rows, V, z_t, alpha_t, alpha_s, kappa, noise_words,
-                                 seed, step, row0, z_s, probs, dev_err);
+                                 seed, step, row0, z_s, row_lse, probs, dev_err);
     return launch_posterior(a, logits_dtype, (hipStream_t)stream);
 }
 
 dd_status dd_posterior_sample(int32_t prior, const void* logits, int32_t logits_dtype, int64_t ld,
-                              int32_t rows, int32_t V, const int32_t* z_t, double alpha_t,
-                              double alpha_s, const uint32_t* noise_words, uint64_t seed,
-                              uint32_t step, uint32_t row0, int32_t* z_s, float* probs,
-                              int32_t* dev_err, void* stream) {
-    return dd_psi_posterior_sample(prior, logits, logits_dtype, ld, rows, V, z_t, alpha_t, alpha_s, 1.0,
-                                   noise_words, seed, step, row0, z_s, probs, dev_err, stream);
+                              int32_t rows, int32_t V, int32_t mask_id, const int32_t* z_t,
+                              double alpha_t, double alpha_s, const uint32_t* noise_words,
+                              uint64_t seed, uint32_t step, uint32_t row0, int32_t* z_s,
+                              float* row_lse, float* probs, int32_t* dev_err, void* stream) {
+    return dd_psi_posterior_sample(prior, logits, logits_dtype, ld, rows, V, mask_id, z_t, alpha_t, alpha_s,
+                                   1.0, noise_words, seed, step, row0, z_s, row_lse, probs, dev_err, stream);
+}
+
+dd_status dd_loop_workspace_layout(const dd_config* cfg, int32_t B, int32_t L, dd_loop_ws_layout* out) {
+    DD_TRY(cfg_check(cfg));
+    DD_CHECK(B > 0 && L > 0 && out, DD_E_ARG, "B and L must be positive and out non-NULL");
+    const WsLayout w = ws_layout(cfg, (int64_t)B * L);
+    out->err = w.err;
+    out->logits = w.logits;
+    out->rows = w.rows;
+    out->count = w.count;
+    out->glse = w.glse;
+    out->row_lse = w.row_lse;
+    out->logits_ld = dd_logits_ld(cfg->vocab);
+    out->glse_ld = w.glse_ld;
+    return DD_OK;
 }
 
 dd_status dd_psi_sample_loop(const dd_config* cfg, const void* params, int32_t B, int32_t L,
-                             int32_t T, const double* alphas, const double* kappas, int32_t* z,
-                             const uint32_t* noise_words, uint64_t noise_seed, int32_t* z_trace,
-                             void* ws, size_t ws_bytes, void* stream) {
-    DD_CHECK(cfg_ok(cfg), DD_E_ARG, "%s", g_err);
+                             int32_t T, const double* alphas, const double* kappas, uint32_t flags,
+                             int32_t* z, const uint32_t* noise_words, uint64_t noise_seed,
+                             int32_t* z_trace, void* ws, size_t ws_bytes, void* stream) {
+    DD_TRY(cfg_check(cfg));
+    DD_CHECK((flags & ~DD_LOOP_POSTERIOR_PASS) == 0, DD_E_ARG, "unknown loop flags 0x%x", flags);
     DD_CHECK(params && z && ws && alphas, DD_E_ARG, "NULL pointer argument");
     DD_CHECK(B > 0 && L > 0 && T > 0, DD_E_ARG, "B, L and T must be positive");
     DD_CHECK(L <= cfg->max_len, DD_E_SHAPE, "L = %d exceeds max_len = %d", L, cfg->max_len);
-    DD_CHECK(forward_supported(cfg), DD_E_UNSUPPORTED, "%s", g_err);
+    DD_TRY(forward_check(cfg));
     DD_CHECK(((uintptr_t)ws & 255) == 0 && ((uintptr_t)params & 255) == 0, DD_E_ARG,
              "params and ws must be 256-byte aligned");
     for (int k = 1; k <= T; ++k) DD_TRY(check_schedule(alphas[k], alphas[k - 1]));
@@ -576,22 +603,26 @@ dd_status dd_psi_sample_loop(const dd_config* cfg, const void* params, int32_t B
     const bool compact = cfg->prior == DD_PRIOR_MASK && gemm_gather_supported(cfg->dtype, cfg->d_model);
     int32_t* rows = (int32_t*)(wsc + w.rows);
     int32_t* count = (int32_t*)(wsc + w.count);
+    float* row_lse = (float*)(wsc + w.row_lse);
     // bf16 path: the vocabulary projection also emits each row's per-group log-sum-exps, so the
-    // draw reads one group of logits per row instead of the whole row.  DD_POSTERIOR_PASS=1 keeps
-    // the posterior's own pass over the rows instead (for comparison and tuning).
-    const char* pass_env = getenv("DD_POSTERIOR_PASS");
-    const bool fused = gemm_lse_supported(cfg->dtype, cfg->d_model) && !(pass_env && atoi(pass_env) == 1);
+    // draw reads one group of logits per row instead of the whole row.  DD_LOOP_POSTERIOR_PASS keeps
+    // the posterior's own pass over the rows instead.
+    const bool fused = gemm_lse_supported(cfg->dtype, cfg->d_model) && !(flags & DD_LOOP_POSTERIOR_PASS);
     float* glse = fused ? (float*)(wsc + w.glse) : nullptr;
+    if (!compact) {   // the layout query reports count = -1 for a loop that does not compact
+        hipLaunchKernelGGL(fill_i32_kernel, dim3(1), dim3(64), 0, s, count, -1, (int64_t)1);
+        DD_TRY(launch_status("loop count"));
+    }
     DD_TRY(trace_copy(0));
     for (int k = T; k >= 1; --k) {
-        if (compact) DD_TRY(launch_compact(z, M, cfg->vocab, rows, count, s));
+        if (compact) DD_TRY(launch_compact(z, M, cfg->mask_id, rows, count, s));
         DD_TRY(run_forward(cfg, params, z, B, L, alphas[k], logits, ld, wsc, s,
                            compact ? rows : nullptr, compact ? count : nullptr, nullptr, nullptr,
                            glse, w.glse_ld));
         const uint32_t* nw = noise_words ? noise_words + (int64_t)(k - 1) * M * nu : nullptr;
         PostArgs a = make_post(cfg->prior, logits, ld, (int32_t)M, cfg->vocab, z, alphas[k],
                                alphas[k - 1], kappas ? kappas[k] : 1.0, nw, noise_seed, (uint32_t)k,
-                               0u, z, nullptr, (int32_t*)(wsc + w.err));
+                               0u, z, row_lse, nullptr, (int32_t*)(wsc + w.err));
         if (compact) {
             // kappa < 1: the rows unmasked before this step keep or remask first (they read no
             // logits and are not in the compacted list, which was taken before the step)
@@ -611,8 +642,8 @@ dd_status dd_sample_loop(const dd_config* cfg, const void* params, int32_t B, in
                          int32_t T, const double* alphas, int32_t* z, const uint32_t* noise_words,
                          uint64_t noise_seed, int32_t* z_trace, void* ws, size_t ws_bytes,
                          void* stream) {
-    return dd_psi_sample_loop(cfg, params, B, L, T, alphas, nullptr, z, noise_words, noise_seed, z_trace,
-                              ws, ws_bytes, stream);
+    return dd_psi_sample_loop(cfg, params, B, L, T, alphas, nullptr, 0u, z, noise_words, noise_seed,
+                              z_trace, ws, ws_bytes, stream);
 }
 
 size_t dd_spec_verify_workspace_bytes(int32_t S, int32_t B) {
@@ -665,6 +696,7 @@ dd_status dd_gaussian_latent_argmax(const int32_t* x, int32_t rows, int32_t V, d
 
 dd_status dd_profile_begin(int32_t max_launches, uint32_t class_mask) {
     DD_CHECK(max_launches > 0, DD_E_ARG, "max_launches must be positive");
+    std::lock_guard<std::mutex> lk(g_prof_mu);
     if ((int)g_prof.ev.size() < 2 * max_launches) {
         for (auto e : g_prof.ev) (void)hipEventDestroy(e);
         g_prof.ev.assign(2 * max_launches, nullptr);
@@ -683,6 +715,7 @@ dd_status dd_profile_begin(int32_t max_launches, uint32_t class_mask) {
 }
 
 dd_status dd_profile_end(void) {
+    std::lock_guard<std::mutex> lk(g_prof_mu);
     g_prof.on = false;
     return DD_OK;
 }
@@ -692,6 +725,7 @@ int32_t dd_profile_num_classes(void) { return KC_COUNT; }
 dd_status dd_profile_read(int32_t cls, const char** name, int64_t* launches, double* total_ms) {
     DD_CHECK(cls >= 0 && cls < KC_COUNT, DD_E_ARG, "class %d out of range", cls);
     DD_CHECK(name && launches && total_ms, DD_E_ARG, "NULL pointer argument");
+    std::lock_guard<std::mutex> lk(g_prof_mu);
     *name = kClassNames[cls];
     int64_t n = 0;
     double tot = 0.0;

@@ -203,7 +203,10 @@ DD_DEV void draw_row(const PostArgs& a, int row, int zt, const char* rowp, const
         if (lane == 0 && a.err) atomicOr(a.err, DD_DEVERR_LOGITS);
         result = zt;
     }
-    if (lane == 0) a.z_s[row] = result;
+    if (lane == 0) {
+        a.z_s[row] = result;
+        if (a.row_lse) a.row_lse[row] = lse;
+    }
 }
 
 // The row's current token into zt (an id outside the K classes is flagged and clamped).  Returns

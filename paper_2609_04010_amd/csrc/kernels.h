@@ -33,6 +33,8 @@ struct PostArgs {
     // projection's EPI_LSE epilogue), or NULL: then the posterior kernel computes them itself
     const float* glse;
     int64_t glse_ld;
+    // per token row drawn: the log-sum-exp of its V logits as the draw computes it (or NULL)
+    float* row_lse;
 };
 
 // EPI_GATE: C = bf16(acc * s_m), s_m = gate_scale if gate is NULL or gate[m % gate_period] != 0,

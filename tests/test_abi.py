@@ -61,21 +61,31 @@ def test_sizes_and_noise_width():
 
 
 def _post(**kw):
-    a = dict(prior=0, logits=FAKE, dtype=0, ld=64, rows=4, V=32, z_t=FAKE, at=0.2, as_=0.5,
-             noise=None, seed=0, step=1, row0=0, z_s=FAKE, probs=None, err=None)
+    a = dict(prior=0, logits=FAKE, dtype=0, ld=64, rows=4, V=32, mask_id=None, z_t=FAKE, at=0.2, as_=0.5,
+             noise=None, seed=0, step=1, row0=0, z_s=FAKE, row_lse=None, probs=None, err=None)
     a.update(kw)
+    mid = a["mask_id"] if a["mask_id"] is not None else (a["V"] if a["prior"] == 0 else -1)
     return dd.lib().dd_posterior_sample(a["prior"], a["logits"], a["dtype"], a["ld"], a["rows"],
-                                        a["V"], a["z_t"], a["at"], a["as_"], a["noise"], a["seed"],
-                                        a["step"], a["row0"], a["z_s"], a["probs"], a["err"], None)
+                                        a["V"], mid, a["z_t"], a["at"], a["as_"], a["noise"], a["seed"],
+                                        a["step"], a["row0"], a["z_s"], a["row_lse"], a["probs"], a["err"],
+                                        None)
 
 
 @pytest.mark.parametrize("kw,status", [
     (dict(prior=7), 1), (dict(dtype=9), 3), (dict(V=0), 1), (dict(rows=-1), 1),
     (dict(ld=31), 2), (dict(ld=36), 2), (dict(at=0.5, as_=0.5), 1), (dict(at=0.6, as_=0.5), 1),
     (dict(at=-0.1), 1), (dict(as_=1.5), 1), (dict(logits=None), 1), (dict(z_s=None), 1),
+    (dict(mask_id=31), 6), (dict(mask_id=-1), 6), (dict(prior=1, mask_id=32), 6), (dict(prior=1, mask_id=0), 6),
 ])
 def test_posterior_validation(kw, status):
     assert _post(**kw) == status
+
+
+def test_posterior_mask_id_message():
+    """A mask id that does not fit the prior is refused with a reason naming the expected id."""
+    assert _post(mask_id=5) == 6
+    msg = dd.lib().dd_last_error()
+    assert b"mask_id 5" in msg and b"32" in msg
 
 
 def test_posterior_zero_rows_is_a_noop():
@@ -95,6 +105,8 @@ def _fwd(cfg, B=1, L=16, at=0.5, ld=50304, ws_bytes=1 << 40):
 
 def test_forward_validation():
     assert _fwd(_cfg_struct(), L=2048) == 2            # L > max_len
+    assert _fwd(_cfg_struct(mask_id=0)) == 6           # the masked prior's mask is id V
+    assert _fwd(_cfg_struct(prior="uniform", mask_id=50257)) == 6   # the uniform prior has none
     assert _fwd(_cfg_struct(), B=0) == 1
     assert _fwd(_cfg_struct(), at=1.5) == 1
     assert _fwd(_cfg_struct(), ld=50257) == 2          # not a multiple of 8
@@ -110,6 +122,22 @@ def test_forward_validation():
     assert _fwd(bad) == 1
 
 
+def test_config_errors_keep_their_message():
+    """A configuration refused by the shared check keeps the check's own message (it is not
+    formatted into itself)."""
+    L = dd.lib()
+    bad = _cfg_struct(d_model=770)
+    assert _fwd(bad) == 1
+    assert L.dd_last_error() == b"d_model must be even and divisible by n_heads"
+    bad = _cfg_struct(lora_rank=12)
+    assert L.dd_init_params(ctypes.byref(bad), FAKE, 1 << 40, 0, None, None) == 1
+    assert L.dd_last_error() == b"lora_rank must be a non-negative multiple of 8 (got 12)"
+    bad = _cfg_struct(n_heads=24)
+    assert _fwd(bad) == 6
+    assert L.dd_last_error().startswith(b"head dim 32 unsupported")
+    assert L.dd_param_bytes(ctypes.byref(_cfg_struct(mask_id=7))) == 0
+
+
 def test_loop_validation():
     cfg = _cfg_struct()
     al = (ctypes.c_double * 3)(1.0, 0.5, 0.5)         # not strictly decreasing
@@ -120,6 +148,28 @@ def test_loop_validation():
                                    10, None) == 4
     assert dd.lib().dd_sample_loop(ctypes.byref(cfg), FAKE, 1, 16, 0, al, FAKE, None, 0, None, FAKE,
                                    1 << 40, None) == 1
+    # unknown loop flags
+    assert dd.lib().dd_psi_sample_loop(ctypes.byref(cfg), FAKE, 1, 16, 2, al, None, 2, FAKE, None, 0, None,
+                                       FAKE, 1 << 40, None) == 1
+    assert b"flags" in dd.lib().dd_last_error()
+
+
+def test_loop_workspace_layout():
+    """The inspection regions lie inside the loop workspace, aligned and without overlap."""
+    for c, B, L in ((1, 4, 32), (2, 2, 128), (3, 1, 64)):
+        cfg = workloads.model_cfg(c)
+        lay = dd.loop_workspace_layout(cfg, B, L)
+        M, V = B * L, cfg["vocab"]
+        es = 2 if cfg["dtype"] == "bf16" else 4
+        regions = sorted([(lay["err"], 4), (lay["logits"], M * lay["logits_ld"] * es), (lay["rows"], 4 * M),
+                          (lay["count"], 4), (lay["glse"], 4 * M * lay["glse_ld"]), (lay["row_lse"], 4 * M)])
+        assert lay["logits_ld"] == dd.logits_ld(V) and lay["glse_ld"] >= (V + 255) // 256
+        assert lay["logits"] >= dd.workspace_bytes(cfg, B, L)
+        for (o1, n1), (o2, _) in zip(regions, regions[1:]):
+            assert o1 % 256 == 0 and o1 + n1 <= o2
+        assert regions[-1][0] + regions[-1][1] <= dd.loop_workspace_bytes(cfg, B, L)
+    with pytest.raises(dd.DDError):
+        dd.loop_workspace_layout(workloads.model_cfg(2), 0, 16)
 
 
 def test_latent_and_init_validation():
@@ -155,14 +205,14 @@ def test_psi_entry_points_validate_kappa():
     """kappa outside [0, 1] is rejected before anything reaches the GPU."""
     L = dd.lib()
     for kappa, status in ((-0.1, 1), (1.5, 1), (float("nan"), 1)):
-        assert L.dd_psi_posterior_sample(0, FAKE, 0, 64, 4, 32, FAKE, 0.2, 0.5, kappa, None, 0, 1, 0, FAKE,
-                                         None, None, None) == status
-    assert L.dd_psi_posterior_sample(0, None, 0, 64, 0, 32, None, 0.2, 0.5, 0.5, None, 0, 1, 0, None,
-                                     None, None, None) == 0      # zero rows: nothing to do
+        assert L.dd_psi_posterior_sample(0, FAKE, 0, 64, 4, 32, 32, FAKE, 0.2, 0.5, kappa, None, 0, 1, 0, FAKE,
+                                         None, None, None, None) == status
+    assert L.dd_psi_posterior_sample(0, None, 0, 64, 0, 32, 32, None, 0.2, 0.5, 0.5, None, 0, 1, 0, None,
+                                     None, None, None, None) == 0      # zero rows: nothing to do
     cfg = _cfg_struct()
     al = (ctypes.c_double * 3)(1.0, 0.5, 0.0)
     bad = (ctypes.c_double * 3)(1.0, 0.5, 2.0)
-    assert L.dd_psi_sample_loop(ctypes.byref(cfg), FAKE, 1, 16, 2, al, bad, FAKE, None, 0, None, FAKE,
+    assert L.dd_psi_sample_loop(ctypes.byref(cfg), FAKE, 1, 16, 2, al, bad, 0, FAKE, None, 0, None, FAKE,
                                 1 << 40, None) == 1
 
 

@@ -146,14 +146,14 @@ def test_forward_out_of_range_token_sets_error_word():
     assert dd.read_device_error(ws[:4].view(torch.int32)) == 0
 
 
-def _loop_gpu(torch, cfg, buf, z1, T, alphas, words=None, seed=0, kappas=None):
+def _loop_gpu(torch, cfg, buf, z1, T, alphas, words=None, seed=0, kappas=None, posterior_pass=False):
     B, L = z1.shape
     z = dev_i32(torch, z1)
     trace = torch.zeros(((T + 1) * B * L,), dtype=torch.int32, device="cuda")
     ws = torch.zeros(dd.loop_workspace_bytes(cfg, B, L), dtype=torch.uint8, device="cuda")
     dd.sample_loop(cfg, buf, B, L, T, alphas, z, ws,
                    noise_words=dev_words(torch, words) if words is not None else None,
-                   noise_seed=seed, z_trace=trace, kappas=kappas)
+                   noise_seed=seed, z_trace=trace, kappas=kappas, posterior_pass=posterior_pass)
     assert dd.read_device_error(ws[:4].view(torch.int32)) == 0
     return z.cpu().numpy().reshape(B, L), trace.cpu().numpy().reshape(T + 1, B, L)
 
@@ -263,9 +263,9 @@ def test_compacted_loop_equals_full_path_loop(c, over, B, L, T):
     (2, dict(n_layers=1, vocab=100), 2, 128, 4),      # a single group narrower than the tile
     (3, dict(n_layers=2), 2, 300, 4),                 # uniform prior: every row, no compaction
 ])
-def test_loop_group_lse_epilogue_equals_posterior_pass(c, over, B, L, T, monkeypatch):
+def test_loop_group_lse_epilogue_equals_posterior_pass(c, over, B, L, T):
     """The loop draws from the per-group log-sum-exps that the vocabulary projection's epilogue
-    computes from the logits it stores; the same loop with DD_POSTERIOR_PASS=1 draws from the
+    computes from the logits it stores; the same loop with DD_LOOP_POSTERIOR_PASS draws from the
     posterior kernel's own pass over those logits (the path the posterior parity tests cover).  The
     two differ only in the summation order inside each group's log-sum-exp, which can decide a draw
     only when two level-1 scores are within a few ulps; with these seeds the trajectories agree."""
@@ -279,45 +279,14 @@ def test_loop_group_lse_epilogue_equals_posterior_pass(c, over, B, L, T, monkeyp
     else:
         z1 = np.random.default_rng(6).integers(0, V, size=(B, L)).astype(np.int32)
     al = osched.alphas(T)
-    monkeypatch.delenv("DD_POSTERIOR_PASS", raising=False)
     _, fused = _loop_gpu(torch, cfg, buf, z1, T, al, seed=91)
-    monkeypatch.setenv("DD_POSTERIOR_PASS", "1")
-    _, passed = _loop_gpu(torch, cfg, buf, z1, T, al, seed=91)
+    _, passed = _loop_gpu(torch, cfg, buf, z1, T, al, seed=91, posterior_pass=True)
     last = (V - 1) // 256 * 256
     drawn_last = int(sum(((t >= last) & (t < V)).sum() for t in fused[1:]))
     say(f"agreement {np.mean(fused == passed):.6f}; draws in the last (ragged) group {drawn_last}")
     for k in range(1, T + 1):
         assert np.array_equal(fused[k], passed[k]), f"step {T - k + 1}"
     assert np.mean(fused[-1] != fused[0]) > 0.3       # the loop did draw
-
-
-def test_full_size_loop_sampled_sequence_matches_oracle():
-    """The benchmark's configuration (gpt2s, 12 layers, B 16 x L 1024, the compacted loop with the
-    group log-sum-exp draw): the first two reverse steps of the 128-step schedule on all 16
-    sequences; one sequence recomputed by the oracle (forward pass and draw with that sequence's
-    noise counters, each step from the GPU's state before it) gives the same ids under the gap
-    rule."""
-    torch = torch_or_skip()
-    c = 2
-    cfg = workloads.model_cfg(c)
-    w, s = workloads.WORKLOADS[c], workloads.seeds(c)
-    B, L, V, T = w["B"], w["L"], w["vocab"], w["T"]
-    say("full-size loop, sampled sequence", B, L, T)
-    P, buf = _params_host(torch, cfg, s["param"])
-    al = osched.alphas(T)[T - 2:]          # steps T and T - 1 of the schedule as a two-step loop
-    z1 = workloads.all_mask(B, L, V)
-    _, trace = _loop_gpu(torch, cfg, buf, z1, 2, al, seed=s["noise"])
-    b = 11
-    rows = np.arange(b * L, (b + 1) * L)
-    for k in (2, 1):
-        z = trace[2 - k][b:b + 1].astype(np.int64)
-        logits = oforward.forward(cfg, P, z, al[k]).reshape(L, V)
-        zs, gaps = osampler.posterior_sample("mask", logits, z.reshape(-1), al[k], al[k - 1],
-                                             osampler.PhiloxNoise(s["noise"], k), rows=rows)
-        compare_ids(trace[2 - k + 1][b], zs, gaps, f"sequence {b}, step {k}")
-    decoded = int((trace[-1] != V).sum())
-    say(f"decoded after two steps: {decoded} of {B * L}")
-    assert decoded > 0
 
 
 def test_loop_from_a_decoded_state_leaves_it_unchanged():

@@ -4,7 +4,8 @@ import numpy as np
 import pytest
 
 import workloads
-from oracle import latent as olatent, params as oparams, philox as ophilox, sampler as osampler
+from oracle import latent as olatent, params as oparams, philox as ophilox, posterior as oposterior, \
+    sampler as osampler
 from paper_2609_04010_amd import _lib as dd
 from tests.gpu_util import (PROB_TOL, compare_ids, dev_i32, dev_words, logits_dev, round_to_dtype,
                             say, torch_or_skip)
@@ -91,6 +92,7 @@ def _run_posterior(torch, prior, V, R, dt, noise, t, s, mf, scale, spikes, seed=
     zs_d = torch.empty_like(zt_d)
     K = V + 1 if prior == "mask" else V
     probs = torch.zeros((R, K), dtype=torch.float32, device="cuda") if want_probs else None
+    rlse = torch.full((R,), float("nan"), dtype=torch.float32, device="cuda")
     ntop = osampler.n_top(prior, V)
     if noise == "explicit":
         words = workloads.noise_words(seed + 2, (R, osampler.noise_width(prior, V)))
@@ -102,15 +104,19 @@ def _run_posterior(torch, prior, V, R, dt, noise, t, s, mf, scale, spikes, seed=
     rows = np.arange(R) + row0
     if kappa is None:
         dd.posterior_sample(prior, lg, dt, ld, R, V, zt_d, at, as_, zs_d, noise_words=wd, seed=seed + 3,
-                            step=step, row0=row0, probs=probs)
+                            step=step, row0=row0, probs=probs, row_lse=rlse)
         ref, gaps, rprobs = osampler.posterior_sample(prior, lv, zt, at, as_, nz, rows=rows,
                                                       return_probs=True)
     else:
         dd.psi_posterior_sample(prior, lg, dt, ld, R, V, zt_d, at, as_, kappa, zs_d, noise_words=wd,
-                                seed=seed + 3, step=step, row0=row0, probs=probs)
+                                seed=seed + 3, step=step, row0=row0, probs=probs, row_lse=rlse)
         ref, gaps, rprobs = osampler.psi_sample(prior, lv, zt, at, as_, kappa, nz, rows=rows,
                                                 return_probs=True)
+    _last_row_lse[:] = [lv, rlse.cpu().numpy()]
     return zt, zs_d.cpu().numpy(), ref, gaps, rprobs, (probs.cpu().numpy() if want_probs else None)
+
+
+_last_row_lse = [None, None]   # (logits, row_lse output) of the latest _run_posterior call
 
 
 @pytest.mark.parametrize("case", POST_CASES, ids=lambda c: f"{c[0]}-V{c[1]}-{c[3]}-{c[4]}-t{c[5]:.3f}")
@@ -123,6 +129,20 @@ def test_posterior_parity(case):
     perr = float(np.abs(gprobs - rprobs).max())
     say(f"max |dp| = {perr:.3e}")
     assert perr <= PROB_TOL
+    # the draw's own fp32 row log-sum-exp: drawn rows get it, carried-over rows are left untouched;
+    # the probabilities it implies meet the same bar
+    lv, rl = _last_row_lse
+    drawn = (zt == V) if prior == "mask" else np.ones(zt.size, bool)
+    assert np.isnan(rl[~drawn]).all() and np.isfinite(rl[drawn]).all()
+    m = lv.max(axis=1)
+    lse = m + np.log(np.exp(lv - m[:, None]).sum(axis=1))
+    at, as_ = 1.0 - case[5], 1.0 - case[6]
+    dpl = 0.0
+    for r in np.nonzero(drawn)[0]:
+        p = oposterior.posterior(prior, np.exp(lv[r] - float(rl[r])), int(zt[r]), at, as_)
+        dpl = max(dpl, float(np.abs(p - rprobs[r]).max()))
+    say(f"row lse: max |d| = {np.abs(rl[drawn] - lse[drawn]).max():.3e}; implied max |dp| = {dpl:.3e}")
+    assert dpl <= PROB_TOL
     if prior == "mask":
         keep = zt != V
         assert np.array_equal(got[keep], zt[keep])          # carry-over, bit exact
