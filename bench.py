@@ -15,9 +15,9 @@ timed region.  Prints ONE JSON line.
                                        B x L with an attention pattern and gated adapters: one JSON
                                        line with ms per forward and per kernel class; not the
                                        benchmark line)
-  python bench.py --kernels           (Psi-Spec verification and Gaussian-latent argmax outside the
-                                       loop: one JSON line each with its roofline; not the
-                                       benchmark line)
+  python bench.py --kernels           (the fused posterior entry point, Psi-Spec verification and the
+                                       Gaussian-latent argmax outside the loop: one JSON line each
+                                       with its roofline; not the benchmark line)
 """
 import hashlib
 import argparse
@@ -58,15 +58,24 @@ def algorithmic_units(cls, cfg, B, L, vocab_rows=None):
     return None, None, None
 
 
+def cpu_model():
+    """The host CPU's model name (first 'model name' line of /proc/cpuinfo), or None."""
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return None
+
+
 def cpu_baseline(c, cfg, w):
-    """The float64 oracle on a bounded sample: one reverse step for ONE sequence."""
+    """The float64 oracle on a bounded sample: one reverse step for ONE sequence, with the BLAS
+    thread pool at its default size and again limited to one thread."""
     import workloads
     from oracle import forward as ofw, params as opar, sampler as osm, schedule as osch
-    try:
-        from threadpoolctl import threadpool_info
-        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
-    except Exception:
-        threads = os.cpu_count()
+    from threadpoolctl import threadpool_info, threadpool_limits
+    threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
     L, V, T = w["L"], w["vocab"], w["T"]
     P = workloads.host_params(cfg, workloads.seeds(c)["param"], opar.specs(cfg))
     k = T // 2
@@ -75,15 +84,24 @@ def cpu_baseline(c, cfg, w):
         z = workloads.masked_state(workloads.seeds(c)["data"], 1, L, V, k / T)
     else:
         z = workloads.uniform_state(workloads.seeds(c)["data"], 1, L, V)
-    t0 = time.perf_counter()
-    logits = ofw.forward(cfg, P, z, al[k]).reshape(L, V)
-    osm.posterior_sample(cfg["prior"], logits, z.reshape(-1), al[k], al[k - 1],
-                         osm.PhiloxNoise(workloads.seeds(c)["noise"], k))
-    dt = time.perf_counter() - t0
+
+    def one_step():
+        t0 = time.perf_counter()
+        logits = ofw.forward(cfg, P, z, al[k]).reshape(L, V)
+        osm.posterior_sample(cfg["prior"], logits, z.reshape(-1), al[k], al[k - 1],
+                             osm.PhiloxNoise(workloads.seeds(c)["noise"], k))
+        return time.perf_counter() - t0
+
+    dt = one_step()
+    with threadpool_limits(limits=1):
+        dt1 = one_step()
     # the oracle would need T such steps per sequence: generated tokens/s = L / (T dt)
     return {"value": L / (T * dt), "unit": "tokens/s", "cores": int(threads), "kind": "oracle",
+            "cpu_model": cpu_model(), "os_cpu_count": os.cpu_count(),
+            "one_thread": {"value": L / (T * dt1), "unit": "tokens/s", "seconds_per_step": dt1},
             "sample": f"one reverse step (forward + posterior + draw) of 1 of {w['B']} sequences, "
-                      f"L={L}, step {k}/{T}: {dt:.2f} s; extrapolated x{T} steps"}
+                      f"L={L}, step {k}/{T}: {dt:.2f} s with {threads} BLAS threads, {dt1:.2f} s with 1; "
+                      f"extrapolated x{T} steps (tokens/s = L / (T x step time))"}
 
 
 def recorded_traffic(cls):
@@ -199,9 +217,10 @@ HBM_PEAK_GBS = 8000.0
 
 
 def kernels_bench(args):
-    """Time the sampler-side kernels outside the loop, one JSON line each: Psi-Spec verification of
-    S drafted blocks (Alg. 1, linear sampler; HBM-bound) and the Gaussian-latent argmax (App. A.5;
-    ALU-bound).  Inputs are synthetic and generated on the device."""
+    """Time the sampler-side kernels outside the loop, one JSON line each: the fused posterior entry
+    point (App. A.1; HBM-bound), Psi-Spec verification of S drafted blocks (Alg. 1, linear sampler;
+    HBM-bound) and the Gaussian-latent argmax (App. A.5; ALU-bound).  Inputs are synthetic and
+    generated on the device."""
     import torch
     from paper_2609_04010_amd import _lib as dd
     dev = torch.device("cuda:0")
@@ -219,6 +238,26 @@ def kernels_bench(args):
         e1.record()
         torch.cuda.synchronize()
         return e0.elapsed_time(e1) / args.steps
+
+    # Fused posterior + draw (App. A.1 eq. mdm-posterior), the entry point's own pass over each row:
+    # 8192 masked rows (the average still-masked rows per reverse step of the B 16 x L 1024 loop) of
+    # bf16 logits over the V = 50257 vocabulary; algorithmic bytes = the logits once + 8 B per row
+    R, V = 8192, 50257
+    ld = int(dd.logits_ld(V))
+    lg = (torch.randn((R, ld), generator=g, device=dev) * 2.0).to(torch.bfloat16)
+    zt = torch.full((R,), V, dtype=torch.int32, device=dev)
+    zs = torch.empty_like(zt)
+    err = torch.zeros(1, dtype=torch.int32, device=dev)
+    ms = timed(lambda: dd.posterior_sample("mask", lg, "bf16", ld, R, V, zt, 0.25, 0.5, zs, seed=3, step=7,
+                                           dev_err=err))
+    assert int(err.item()) == 0
+    nbytes = R * V * 2 + 8 * R
+    gbs = nbytes / (ms * 1e-3) / 1e9
+    print(json.dumps({"mode": "kernel", "kernel": "posterior_sample", "rows": R, "V": V, "dtype": "bf16",
+                      "calls": args.steps, "ms_per_call": ms,
+                      "roofline": {"bound": "hbm", "achieved": gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                                   "frac": gbs / HBM_PEAK_GBS, "bytes_per_call": nbytes}}), flush=True)
+    del lg
 
     # Alg. 1 verification: S sequences, block size B = 16 (the paper's largest), bf16 target and draft
     # logits of the workload vocabulary; drafts drawn uniformly, so most blocks reject early
@@ -358,7 +397,7 @@ def main():
     peak = PEAK_BF16_TFLOPS if cfg["dtype"] == "bf16" else PEAK_FP32_TFLOPS
     tokens = args.steps * M
     out = {
-        "metric": "generated tokens/sec at L=1024,B=16,T=128 on 1 GPU; ms per reverse step",
+        "metric": f"generated tokens/sec at L={L},B={B},T={T} on 1 GPU; ms per reverse step",
         "value": tokens / elapsed,
         "unit": "tokens/s",
         "n_gpus": 1,

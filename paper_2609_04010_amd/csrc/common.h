@@ -47,6 +47,24 @@ DD_DEV float wave_sum(float v) {
     for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
     return v;
 }
+// Wavefront sum with DPP lane moves (VALU latency, no LDS round trips): two quad permutations and
+// the half-row and row mirrors leave every lane of a 16-lane row with that row's sum; the row
+// broadcasts of lanes 15 and 31 then add rows 0 and 2 into rows 1 and 3 and rows 0-1 into rows 2-3
+// (lanes outside a move's row mask add 0), so lane 63 ends with the total, which every lane gets.
+template <int CTRL, int ROW_MASK>
+DD_DEV float dpp_add(float v) {
+    const int m = __builtin_amdgcn_update_dpp(0, __float_as_int(v), CTRL, ROW_MASK, 0xF, false);
+    return v + __int_as_float(m);
+}
+DD_DEV float wave_sum_dpp(float v) {
+    v = dpp_add<0xB1, 0xF>(v);    // quad_perm [1, 0, 3, 2]
+    v = dpp_add<0x4E, 0xF>(v);    // quad_perm [2, 3, 0, 1]
+    v = dpp_add<0x141, 0xF>(v);   // row_half_mirror
+    v = dpp_add<0x140, 0xF>(v);   // row_mirror
+    v = dpp_add<0x142, 0xA>(v);   // row_bcast15 into rows 1 and 3
+    v = dpp_add<0x143, 0xC>(v);   // row_bcast31 into rows 2 and 3
+    return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 63));
+}
 DD_DEV float wave_max(float v) {
 #pragma unroll
     for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, 64));

@@ -93,52 +93,74 @@ __global__ __launch_bounds__(256) void ln_kernel(const float* h, int64_t rows, c
 }
 
 // LayerNorm of one row held as NV groups of four consecutive features per lane (group lane + 64 k),
-// written as 8-byte bf16 stores.
+// written as 8-byte bf16 stores; gg / bb hold the gain and shift of those features.  Both
+// statistics are wavefront sums by DPP lane moves.
 template <int NV>
-DD_DEV void ln4_row(const float4 (&x)[NV], int lane, const bf16_t* g, const bf16_t* b, float eps, bf16_t* out) {
+DD_DEV void ln4_row(const float4 (&x)[NV], int lane, const uint2 (&gg)[NV], const uint2 (&bb)[NV], float eps,
+                    bf16_t* out) {
     constexpr int d = NV * 256;
     float s = 0.f;
 #pragma unroll
     for (int k = 0; k < NV; ++k) s += (x[k].x + x[k].y) + (x[k].z + x[k].w);
-    const float mean = wave_sum(s) / (float)d;
+    const float mean = wave_sum_dpp(s) / (float)d;
     float q = 0.f;
 #pragma unroll
     for (int k = 0; k < NV; ++k) {
         const float a0 = x[k].x - mean, a1 = x[k].y - mean, a2 = x[k].z - mean, a3 = x[k].w - mean;
         q += (a0 * a0 + a1 * a1) + (a2 * a2 + a3 * a3);
     }
-    const float rstd = 1.0f / sqrtf(wave_sum(q) / (float)d + eps);
+    const float rstd = 1.0f / sqrtf(wave_sum_dpp(q) / (float)d + eps);
     uint2* orow = (uint2*)out;
-    const uint2* gv = (const uint2*)g;
-    const uint2* bv = (const uint2*)b;
 #pragma unroll
     for (int k = 0; k < NV; ++k) {
         const int c = lane + 64 * k;
-        const uint2 gg = gv[c], bb = bv[c];
         uint2 o;
-        o.x = pack_bf16x2((x[k].x - mean) * rstd * bf16_lo(gg.x) + bf16_lo(bb.x),
-                          (x[k].y - mean) * rstd * bf16_hi(gg.x) + bf16_hi(bb.x));
-        o.y = pack_bf16x2((x[k].z - mean) * rstd * bf16_lo(gg.y) + bf16_lo(bb.y),
-                          (x[k].w - mean) * rstd * bf16_hi(gg.y) + bf16_hi(bb.y));
+        o.x = pack_bf16x2((x[k].x - mean) * rstd * bf16_lo(gg[k].x) + bf16_lo(bb[k].x),
+                          (x[k].y - mean) * rstd * bf16_hi(gg[k].x) + bf16_hi(bb[k].x));
+        o.y = pack_bf16x2((x[k].z - mean) * rstd * bf16_lo(gg[k].y) + bf16_lo(bb[k].y),
+                          (x[k].w - mean) * rstd * bf16_hi(gg[k].y) + bf16_hi(bb[k].y));
         orow[c] = o;
     }
 }
 
+template <int NV>
+DD_DEV void load_gain_shift(const bf16_t* g, const bf16_t* b, int lane, uint2 (&gg)[NV], uint2 (&bb)[NV]) {
+#pragma unroll
+    for (int k = 0; k < NV; ++k) {
+        gg[k] = ((const uint2*)g)[lane + 64 * k];
+        bb[k] = ((const uint2*)b)[lane + 64 * k];
+    }
+}
+
 // bf16 output, d % 256 == 0: each lane holds NV = d / 256 groups of four consecutive features,
-// read as one 16-byte fp32 load and written as one 8-byte bf16 store.
+// read as one 16-byte fp32 load and written as one 8-byte bf16 store.  A wavefront normalises
+// LN_RPW consecutive rows and issues the loads of all of them before the first reduction, so
+// LN_RPW rows per wavefront are in flight (the kernel is bound by HBM latency per wavefront
+// otherwise).
+constexpr int LN_RPW = 2;
 template <int NV>
 __global__ __launch_bounds__(256) void ln_bf16_v4_kernel(const float* h, int64_t rows,
                                                          const bf16_t* g, const bf16_t* b,
                                                          float eps, bf16_t* out, int64_t ldo) {
-    const int64_t row = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+    const int64_t row0 = ((int64_t)blockIdx.x * 4 + (threadIdx.x >> 6)) * LN_RPW;
     const int lane = threadIdx.x & 63;
-    if (row >= rows) return;
+    if (row0 >= rows) return;
     constexpr int d = NV * 256;
-    float4 x[NV];
-    const float4* hr = (const float4*)(h + row * d);
+    float4 x[LN_RPW][NV];
 #pragma unroll
-    for (int k = 0; k < NV; ++k) x[k] = hr[lane + 64 * k];
-    ln4_row<NV>(x, lane, g, b, eps, out + row * ldo);
+    for (int r = 0; r < LN_RPW; ++r) {
+        if (row0 + r >= rows) break;
+        const float4* hr = (const float4*)(h + (row0 + r) * d);
+#pragma unroll
+        for (int k = 0; k < NV; ++k) x[r][k] = hr[lane + 64 * k];
+    }
+    uint2 gg[NV], bb[NV];
+    load_gain_shift<NV>(g, b, lane, gg, bb);
+#pragma unroll
+    for (int r = 0; r < LN_RPW; ++r) {
+        if (row0 + r >= rows) break;
+        ln4_row<NV>(x[r], lane, gg, bb, eps, out + (row0 + r) * ldo);
+    }
 }
 
 // Embedding + first LayerNorm, bf16, d % 256 == 0: token and position rows read four features at a
@@ -177,7 +199,9 @@ __global__ __launch_bounds__(256) void embed_ln_bf16_v4_kernel(const int32_t* z,
         x[k] = v;
         hr[c] = v;
     }
-    ln4_row<NV>(x, lane, g, b, eps, xln + row * ldo);
+    uint2 gg[NV], bb[NV];
+    load_gain_shift<NV>(g, b, lane, gg, bb);
+    ln4_row<NV>(x, lane, gg, bb, eps, xln + row * ldo);
 }
 
 #define DD_NPL_CASES(X) X(1) X(2) X(4) X(8) X(12) X(16) X(24) X(32)
@@ -245,7 +269,7 @@ dd_status launch_ln_t(const float* h, int64_t rows, int d, const void* g, const 
 dd_status launch_ln(int dtype, const float* h, int64_t rows, int d, const void* g, const void* b,
                     float eps, void* out, int64_t ldo, hipStream_t s) {
     if (dtype == DD_BF16 && (d == 768 || d == 1024 || d == 2048) && ldo % 4 == 0) {
-        const dim3 grid((unsigned)ceil_div(rows, 4)), blk(256);
+        const dim3 grid((unsigned)ceil_div(rows, 4 * LN_RPW)), blk(256);
         ProfScope ps(KC_LN, s);
         const bf16_t* gg = (const bf16_t*)g;
         const bf16_t* bb = (const bf16_t*)b;

@@ -19,8 +19,8 @@ sequence is then checked against the float64 oracle, one stage at a time:
 Stage 1 compares two forward passes; stages 2-3 never compare a GPU draw with an oracle draw made
 from the oracle's own logits (their difference, up to the logit bar, is far above the 1e-3 gap).
 Workload 4 checks sequence 127 of 128, whose logit rows start past 2^31 elements of the logit
-matrix; workload 5 runs the 24-layer d 1024 model at L 4096 (its second step checks stages 2-4
-only: a second float64 forward pass of that size takes minutes).
+matrix; workload 5 runs the 24-layer d 1024 model at L 4096 (its float64 forward pass takes about a
+minute on the host, and prints its progress per layer).
 """
 import time
 
@@ -39,7 +39,7 @@ pytestmark = [pytest.mark.gpu, pytest.mark.timeout(1200)]
 LOGIT_TOL = 5e-2
 
 # workload, the sequence checked, number of reverse steps, steps whose logits the oracle recomputes
-FULL_CASES = [(2, 11, 2, 2), (3, 5, 2, 2), (4, 127, 2, 2), (5, 7, 2, 1)]
+FULL_CASES = [(2, 11, 2, 2), (3, 5, 2, 2), (4, 127, 2, 2), (5, 7, 2, 2)]
 
 
 def _host_params(torch, cfg, seed):

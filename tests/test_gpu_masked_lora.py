@@ -168,10 +168,33 @@ def test_gated_lora_forward_parity(case):
     assert e <= LOGIT_TOL[cfg["dtype"]]
 
 
-def test_teacher_logits_in_one_pass_match_base_model_on_gpu():
+def _bf16_ulp(v):
+    """Spacing of bf16 values at |v| (8 significant bits)."""
+    e = np.floor(np.log2(np.maximum(np.abs(v), 2.0 ** -126)))
+    return 2.0 ** (e - 7)
+
+
+@pytest.mark.parametrize("tile", [None, "0"])
+def test_teacher_logits_in_one_pass_match_base_model_on_gpu(tile, monkeypatch):
     """Sec. 3.2 on the GPU: [x, z_1] with adapters on z_1 only gives, at x, the base model's causal
-    logits of x alone (run by the same library on a base-layout copy of the weights)."""
+    logits of x alone (run by the same library on a base-layout copy of the weights).
+
+    Every layer computes the x rows identically in the two calls: the adapter columns of those rows
+    are exact zeros (gate off), the K loops of the body GEMMs run in the same order wherever a row
+    sits, and each 32-query wavefront of the attention holds the same x queries and visits the same
+    key tiles (keys a query cannot see contribute exact zeros in both).  The one difference is the
+    vocabulary projection, which starts the K loop of M-tile tm, N-tile tn at K-slice
+    ((tm mod 8) + 2 tn) mod nk to spread L2 requests: sequence 1's x rows sit in M-tiles 0 and 1 of
+    the [x, z_1] call but all in M-tile 0 of the call on x alone, so their fp32 sums are taken in
+    another order and a logit can round to the neighbouring bf16 value.  Hence: at most one bf16
+    ulp of the logit with the default tiles (2^-6 = 1.6e-2 for |logit| in [2, 4)), and bit-identical
+    logits with the register-staged 128 x 128 tile (DD_GEMM_TILE=0), whose K loop always starts at
+    slice 0."""
     torch = torch_or_skip()
+    if tile is None:
+        monkeypatch.delenv("DD_GEMM_TILE", raising=False)
+    else:
+        monkeypatch.setenv("DD_GEMM_TILE", tile)
     over = {"n_layers": 2, "lora_rank": 128, "lora_alpha": 256.0}
     cfg = workloads.model_cfg(2, **over)
     P, buf = _params(torch, cfg, 31, "host")
@@ -188,13 +211,16 @@ def test_teacher_logits_in_one_pass_match_base_model_on_gpu():
     dd.init_params(base_cfg, bbuf, host_blob=blob)
     teach, err2 = _forward_ex(torch, base_cfg, bbuf, x, 1.0, dd.attn_mask_build("causal", n))
     assert err2 == 0
-    d = float(np.abs(got[:, :n] - teach).max())
-    say(f"teacher logits: max diff {d:.3e}, identical {np.array_equal(got[:, :n], teach)}")
-    # equal up to rounding: the GEMMs' fp32 summation order (the vocabulary projection's K order,
-    # the step at which a residual layer adds h) depends on where a row falls in its tile, the two
-    # calls place the x rows differently, and the differences pass through bf16 activations; both
-    # calls meet the oracle bar, and the oracle pins the property itself in float64
-    assert d <= LOGIT_TOL["bf16"]
+    diff = np.abs(got[:, :n] - teach)
+    nd = int((diff > 0).sum())
+    say(f"tile {tile}: teacher logits max diff {diff.max():.3e}, {nd} of {diff.size} differ "
+        f"(sequence 0: {int((diff[0] > 0).sum())}, sequence 1: {int((diff[1] > 0).sum())}); "
+        f"max diff / bf16 ulp {np.max(diff / _bf16_ulp(teach)):.3f}")
+    if tile is None:
+        assert np.all(diff <= _bf16_ulp(teach))
+        assert (diff[0] == 0).all()          # sequence 0's rows sit in M-tile 0 in both calls
+    else:
+        assert nd == 0
 
 
 def test_sample_loop_with_adapters_matches_oracle():
