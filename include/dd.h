@@ -406,6 +406,26 @@ dd_status dd_spec_verify(const void* p_logits, const void* q_logits, int32_t log
                          size_t ws_bytes, int32_t* dev_err, void* stream);
 
 /*
+ * dd_spec_verify_noalloc - dd_spec_verify for callers that cannot allocate device
+ * memory: code under HIP graph capture, tight serving loops, harnesses that forbid
+ * hipMalloc.  Same arguments and results as dd_spec_verify, without the
+ * workspace: the row log-sum-exps go to a library-held device array of
+ * DD_SPEC_VERIFY_NOALLOC_ROWS floats (1 MiB), one per device, which each device
+ * the library runs on holds until the process ends.  S (2B - 1) above
+ * DD_SPEC_VERIFY_NOALLOC_ROWS is DD_E_WORKSPACE, before any launch.  The call
+ * allocates nothing; its first call on a device looks up that device's array
+ * (with the device current).  Every call on a device shares the device's array:
+ * calls that can overlap on one device (several streams or host threads) race,
+ * and the caller must order them.
+ */
+#define DD_SPEC_VERIFY_NOALLOC_ROWS (1 << 18)
+dd_status dd_spec_verify_noalloc(const void* p_logits, const void* q_logits, int32_t logits_dtype,
+                                 int64_t ld, int32_t S, int32_t B, int32_t V, const int32_t* draft,
+                                 const uint32_t* noise_words, uint64_t seed, uint32_t step,
+                                 uint32_t row0, int32_t* n_out, int32_t* z_out, int32_t* dev_err,
+                                 void* stream);
+
+/*
  * dd_gaussian_latent_argmax - z = argmax_v (alpha_tilde [v == x] + sigma eps_v)
  * per row (App. A.5: uniform-state diffusion is the argmax projection of a
  * Gaussian diffusion on one-hot vectors).  eps_v = Phi^-1(u) of the Philox word

@@ -35,7 +35,7 @@ EXPORTED = [
     "dd_attn_mask_build", "dd_denoise_forward_ex",
     "dd_posterior_sample", "dd_psi_posterior_sample", "dd_sample_loop", "dd_psi_sample_loop",
     "dd_gaussian_latent_argmax", "dd_spec_verify_workspace_bytes", "dd_spec_verify_noise_width",
-    "dd_spec_verify", "dd_profile_begin",
+    "dd_spec_verify", "dd_spec_verify_noalloc", "dd_profile_begin",
     "dd_profile_end", "dd_profile_num_classes", "dd_profile_read",
 ]
 
@@ -114,6 +114,8 @@ def lib():
             "dd_spec_verify": (c.c_int32, [P, P, c.c_int32, c.c_int64, c.c_int32, c.c_int32, c.c_int32, P,
                                            P, c.c_uint64, c.c_uint32, c.c_uint32, P, P, P, c.c_size_t, P,
                                            P]),
+            "dd_spec_verify_noalloc": (c.c_int32, [P, P, c.c_int32, c.c_int64, c.c_int32, c.c_int32, c.c_int32,
+                                                   P, P, c.c_uint64, c.c_uint32, c.c_uint32, P, P, P, P]),
             "dd_profile_begin": (c.c_int32, [c.c_int32, c.c_uint32]),
             "dd_profile_end": (c.c_int32, []),
             "dd_profile_num_classes": (c.c_int32, []),
@@ -384,6 +386,26 @@ def spec_verify(p_logits, q_logits, logits_dtype, ld, S, B, V, draft, n_out, z_o
         _ptr(z_out, 4 * S, "z_out", torch.int32), _ptr(ws, spec_verify_workspace_bytes(S, B), "ws"),
         ws.numel() * ws.element_size(), _ptr(dev_err, 4, "dev_err", torch.int32) if dev_err is not None else None,
         _stream()))
+
+
+SPEC_VERIFY_NOALLOC_ROWS = 1 << 18
+
+
+def spec_verify_noalloc(p_logits, q_logits, logits_dtype, ld, S, B, V, draft, n_out, z_out, noise_words=None,
+                        seed=0, step=0, row0=0, dev_err=None):
+    """dd_spec_verify_noalloc: dd_spec_verify without a workspace (library-held device array)."""
+    torch = _torch()
+    es = 2 if logits_dtype == "bf16" else 4
+    nu = spec_verify_noise_width(B, V)
+    _check(lib().dd_spec_verify_noalloc(
+        _ptr(p_logits, es * S * B * ld, "p_logits"),
+        _ptr(q_logits, es * S * (B - 1) * ld, "q_logits") if B > 1 else None, dtype_code(logits_dtype),
+        int(ld), int(S), int(B), int(V),
+        _ptr(draft, 4 * S * (B - 1), "draft", torch.int32) if B > 1 else None,
+        _ptr(noise_words, 4 * S * nu, "noise_words", torch.int32) if noise_words is not None else None,
+        int(seed) & 0xFFFFFFFFFFFFFFFF, int(step), int(row0), _ptr(n_out, 4 * S, "n_out", torch.int32),
+        _ptr(z_out, 4 * S, "z_out", torch.int32),
+        _ptr(dev_err, 4, "dev_err", torch.int32) if dev_err is not None else None, _stream()))
 
 
 def gaussian_latent_argmax(x, rows, V, alpha_tilde, sigma, seed, step, z_out, row0=0, dev_err=None):

@@ -655,21 +655,24 @@ int32_t dd_spec_verify_noise_width(int32_t B, int32_t V) {
     return (B - 1) + ntop_of(DD_PRIOR_UNIFORM, V) + V;
 }
 
-dd_status dd_spec_verify(const void* p_logits, const void* q_logits, int32_t logits_dtype, int64_t ld,
-                         int32_t S, int32_t B, int32_t V, const int32_t* draft,
-                         const uint32_t* noise_words, uint64_t seed, uint32_t step, uint32_t row0,
-                         int32_t* n_out, int32_t* z_out, void* ws, size_t ws_bytes, int32_t* dev_err,
-                         void* stream) {
+// Validation shared by dd_spec_verify and dd_spec_verify_noalloc (everything but the workspace).
+static dd_status verify_check(const void* p_logits, const void* q_logits, int32_t logits_dtype, int64_t ld,
+                              int32_t S, int32_t B, int32_t V, const int32_t* draft, int32_t* n_out,
+                              int32_t* z_out) {
     DD_CHECK(logits_dtype == DD_BF16 || logits_dtype == DD_FP32, DD_E_DTYPE, "unknown logits dtype");
     DD_CHECK(S >= 0 && B >= 1 && V > 0, DD_E_ARG, "need S >= 0, B >= 1 and V > 0");
     DD_CHECK(V <= (1 << 24), DD_E_UNSUPPORTED, "V > 2^24 unsupported");
     DD_CHECK((int64_t)S * (2 * (int64_t)B - 1) <= INT32_MAX, DD_E_UNSUPPORTED, "too many rows");
     DD_CHECK(ld >= V && ld % 8 == 0, DD_E_SHAPE, "ld must be >= V and a multiple of 8");
     if (S == 0) return DD_OK;
-    DD_CHECK(p_logits && n_out && z_out && ws, DD_E_ARG, "NULL pointer argument");
+    DD_CHECK(p_logits && n_out && z_out, DD_E_ARG, "NULL pointer argument");
     DD_CHECK(B == 1 || (q_logits && draft), DD_E_ARG, "B > 1 needs draft logits and tokens");
-    const size_t need = dd_spec_verify_workspace_bytes(S, B);
-    DD_CHECK(ws_bytes >= need, DD_E_WORKSPACE, "workspace has %zu bytes, needs %zu", ws_bytes, need);
+    return DD_OK;
+}
+
+static VerifyArgs make_verify(const void* p_logits, const void* q_logits, int64_t ld, int32_t S, int32_t B,
+                              int32_t V, const int32_t* draft, const uint32_t* noise_words, uint64_t seed,
+                              uint32_t step, uint32_t row0, int32_t* n_out, int32_t* z_out, int32_t* dev_err) {
     VerifyArgs a;
     memset(&a, 0, sizeof(a));
     a.p = p_logits; a.q = q_logits; a.ld = ld;
@@ -679,7 +682,40 @@ dd_status dd_spec_verify(const void* p_logits, const void* q_logits, int32_t log
     a.nu = dd_spec_verify_noise_width(B, V);
     a.seed = seed; a.step = step; a.row0 = row0;
     a.n_out = n_out; a.z_out = z_out; a.err = dev_err;
+    return a;
+}
+
+dd_status dd_spec_verify(const void* p_logits, const void* q_logits, int32_t logits_dtype, int64_t ld,
+                         int32_t S, int32_t B, int32_t V, const int32_t* draft,
+                         const uint32_t* noise_words, uint64_t seed, uint32_t step, uint32_t row0,
+                         int32_t* n_out, int32_t* z_out, void* ws, size_t ws_bytes, int32_t* dev_err,
+                         void* stream) {
+    DD_TRY(verify_check(p_logits, q_logits, logits_dtype, ld, S, B, V, draft, n_out, z_out));
+    if (S == 0) return DD_OK;
+    DD_CHECK(ws, DD_E_ARG, "NULL pointer argument");
+    const size_t need = dd_spec_verify_workspace_bytes(S, B);
+    DD_CHECK(ws_bytes >= need, DD_E_WORKSPACE, "workspace has %zu bytes, needs %zu", ws_bytes, need);
+    const VerifyArgs a = make_verify(p_logits, q_logits, ld, S, B, V, draft, noise_words, seed, step, row0,
+                                     n_out, z_out, dev_err);
     return launch_verify(a, logits_dtype, (float*)ws, (hipStream_t)stream);
+}
+
+dd_status dd_spec_verify_noalloc(const void* p_logits, const void* q_logits, int32_t logits_dtype,
+                                 int64_t ld, int32_t S, int32_t B, int32_t V, const int32_t* draft,
+                                 const uint32_t* noise_words, uint64_t seed, uint32_t step,
+                                 uint32_t row0, int32_t* n_out, int32_t* z_out, int32_t* dev_err,
+                                 void* stream) {
+    DD_TRY(verify_check(p_logits, q_logits, logits_dtype, ld, S, B, V, draft, n_out, z_out));
+    if (S == 0) return DD_OK;
+    const int64_t rows = (int64_t)S * (2 * (int64_t)B - 1);
+    DD_CHECK(rows <= DD_SPEC_VERIFY_NOALLOC_ROWS, DD_E_WORKSPACE,
+             "S (2B - 1) = %lld logit rows exceed the %d row log-sum-exps the library holds per device",
+             (long long)rows, DD_SPEC_VERIFY_NOALLOC_ROWS);
+    float* lse = nullptr;
+    DD_TRY(verify_noalloc_scratch(&lse));
+    const VerifyArgs a = make_verify(p_logits, q_logits, ld, S, B, V, draft, noise_words, seed, step, row0,
+                                     n_out, z_out, dev_err);
+    return launch_verify(a, logits_dtype, lse, (hipStream_t)stream);
 }
 
 dd_status dd_gaussian_latent_argmax(const int32_t* x, int32_t rows, int32_t V, double alpha_tilde,

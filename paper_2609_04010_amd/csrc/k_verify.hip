@@ -16,6 +16,8 @@
 // chosen row pair for the group masses and the two-level draw.
 #include <math.h>
 
+#include <mutex>
+
 #include "elem.h"
 #include "kernels.h"
 #include "rng.h"
@@ -226,6 +228,41 @@ __global__ __launch_bounds__(VT) void verify_kernel(VerifyArgs a, const float* l
 }
 
 }  // namespace
+
+// Row log-sum-exps of dd_spec_verify_noalloc: a file-scope device array instead of a caller
+// workspace, one copy per device, held until the process ends.  In host code `scratch` names a
+// host-side stand-in, not device memory: the host takes each device's address from
+// hipGetSymbolAddress (once per device, with that device current) and passes that address on.
+static __device__ __align__(256) float scratch[DD_SPEC_VERIFY_NOALLOC_ROWS];
+
+constexpr int kMaxDevices = 64;
+static std::mutex g_scratch_mu;
+static float* g_scratch_dev[kMaxDevices] = {};
+
+dd_status verify_noalloc_scratch(float** out) {
+    int dev = -1;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) {
+        set_error("spec_verify_noalloc: hipGetDevice: %s", hipGetErrorString(e));
+        return DD_E_HIP;
+    }
+    if (dev < 0 || dev >= kMaxDevices) {
+        set_error("spec_verify_noalloc: device %d beyond the %d this library tracks", dev, kMaxDevices);
+        return DD_E_UNSUPPORTED;
+    }
+    std::lock_guard<std::mutex> lk(g_scratch_mu);
+    if (!g_scratch_dev[dev]) {
+        void* p = nullptr;
+        e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess || !p) {
+            set_error("spec_verify_noalloc: hipGetSymbolAddress: %s", hipGetErrorString(e));
+            return DD_E_HIP;
+        }
+        g_scratch_dev[dev] = (float*)p;
+    }
+    *out = g_scratch_dev[dev];
+    return DD_OK;
+}
 
 dd_status launch_verify(const VerifyArgs& a, int logits_dtype, float* lse, hipStream_t s) {
     if (a.S == 0) return DD_OK;

@@ -101,6 +101,9 @@ struct VerifyArgs {
     int32_t* err;
 };
 dd_status launch_verify(const VerifyArgs& a, int logits_dtype, float* lse, hipStream_t s);
+// Device address of the current device's DD_SPEC_VERIFY_NOALLOC_ROWS-float array of
+// dd_spec_verify_noalloc (looked up on the first call on each device).
+dd_status verify_noalloc_scratch(float** out);
 dd_status launch_latent(const int32_t* x, int32_t rows, int32_t V, double at, double sigma,
                         uint64_t seed, uint32_t step, uint32_t row0, int32_t* z, int32_t* err,
                         hipStream_t s);

@@ -233,6 +233,14 @@ def test_spec_verify_validation_and_sizes():
     assert call(q=None) == 1                       # B > 1 needs draft logits
     assert call(S=0, p=None, n=None, z=None, ws=None) == 0
     assert dd.spec_verify_workspace_bytes(4, 3) == 256 and dd.spec_verify_workspace_bytes(100, 8) == 6144
+    # the allocation-free form validates the same way and refuses more rows than its array holds
+    nv = lambda **k: (lambda a: L.dd_spec_verify_noalloc(a["p"], a["q"], a["dt"], a["ld"], a["S"], a["B"], a["V"],
+                                                         a["draft"], a["noise"], a["seed"], a["step"], a["row0"],
+                                                         a["n"], a["z"], a["err"], None))(args(**k))
+    assert nv(dt=7) == 3 and nv(B=0) == 1 and nv(ld=30) == 2 and nv(q=None) == 1
+    assert nv(S=0, p=None, n=None, z=None) == 0
+    assert nv(S=dd.SPEC_VERIFY_NOALLOC_ROWS // 5 + 1) == 4         # S (2B - 1) = 5 S rows
+    assert b"exceed" in L.dd_last_error()
     for B, V in ((1, 32), (4, 300), (16, 50257)):
         assert dd.spec_verify_noise_width(B, V) == overify.noise_width(B, V)
 
