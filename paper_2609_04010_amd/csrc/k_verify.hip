@@ -30,62 +30,99 @@ constexpr int VT = 256;   // threads per workgroup
 
 // Row r < S B is target row r; otherwise draft row r - S B.  One pass over the row: each thread keeps
 // a running maximum m and the sum of exp(l - m), rescaled when m rises; the workgroup then combines
-// the (m, sum) pairs.  NaN and +inf logits are only flagged, so the result is that of the two-pass
-// definition: NaN if a logit is NaN, else +inf if one is +inf, else -inf if none is finite.
+// the (m, sum) pairs.  The result is that of the two-pass definition: NaN if a logit is NaN, else
+// +inf if one is +inf, else -inf if none is finite.
+// The pass is bound by VALU work per logit, so the hot loop spends four full-rate operations and one
+// exp2 per logit: a thread takes VU chunks at a time (loaded together, the next VU loaded while these
+// are reduced), takes their maximum with fmax (which passes over NaN), rescales its sum when the
+// maximum rises, and adds exp2(l log2 e - m log2 e).  A NaN or +inf logit makes that sum NaN
+// (exp2 of NaN, or of inf - inf), so such rows are told apart afterwards by a second scan that
+// only they take.
+constexpr int VU = 4;
 template <typename T>
 __global__ __launch_bounds__(VT) void row_lse_kernel(VerifyArgs a, float* lse) {
     __shared__ float sh_m[VT / 64], sh_s[VT / 64];
     __shared__ int sh_f[VT / 64];
     constexpr int E = Elem<T>::E;
-    const int r = blockIdx.x, lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int r = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int np = a.S * a.B;
     const char* rowp = r < np ? (const char*)a.p + (size_t)r * a.ld * sizeof(T)
                               : (const char*)a.q + (size_t)(r - np) * a.ld * sizeof(T);
     const int V = a.V, nchunk = (V + E - 1) / E;
     float m = -INFINITY, sum = 0.f;
-    int flags = 0;   // 1: a NaN, 2: a +inf
-    for (int c = threadIdx.x; c < nchunk; c += VT) {
-        const uint4 x = *(const uint4*)(rowp + (size_t)c * 16);
-        float v[E];
+    constexpr int TS = VU * VT;   // chunks per tile
+    // chunks c0 + u VT + tid, u < VU; chunks past the row read as -inf, and so does the part of the
+    // last chunk past V
+    auto load = [&](uint4 (&x)[VU], int c0) {
+#pragma unroll
+        for (int u = 0; u < VU; ++u) {
+            const int c = c0 + u * VT + tid;
+            x[u] = c < nchunk ? *(const uint4*)(rowp + (size_t)c * 16) : Elem<T>::NEG_INF4;
+            if (V % E != 0 && c == nchunk - 1) Elem<T>::clip(x[u], V % E);
+        }
+    };
+    auto absorb = [&](const uint4 (&x)[VU]) {
         float cm = -INFINITY;
 #pragma unroll
-        for (int e = 0; e < E; ++e) {
-            float t = c * E + e < V ? Elem<T>::get(x, e) : -INFINITY;
-            flags |= (t != t) ? 1 : 0;
-            flags |= (t == INFINITY) ? 2 : 0;
-            t = (t != t || t == INFINITY) ? -INFINITY : t;
-            v[e] = t;
-            cm = fmaxf(cm, t);
-        }
+        for (int u = 0; u < VU; ++u)
+#pragma unroll
+            for (int e = 0; e < E; ++e) cm = fmaxf(cm, Elem<T>::get(x[u], e));
         if (cm > m) {
             sum *= __builtin_amdgcn_exp2f((m - cm) * LOG2E);   // m = -inf: sum is 0 already
             m = cm;
         }
-        const float mref = m == -INFINITY ? 0.f : m;
+        const float moff = m == -INFINITY ? 0.f : -m * LOG2E;
 #pragma unroll
-        for (int e = 0; e < E; ++e) sum += __builtin_amdgcn_exp2f((v[e] - mref) * LOG2E);
+        for (int u = 0; u < VU; ++u)
+#pragma unroll
+            for (int e = 0; e < E; ++e) sum += __builtin_amdgcn_exp2f(fmaf(Elem<T>::get(x[u], e), LOG2E, moff));
+    };
+    uint4 xa[VU], xb[VU];
+    load(xa, 0);
+    for (int c0 = 0; c0 < nchunk; c0 += 2 * TS) {
+        const bool more = c0 + TS < nchunk;
+        if (more) load(xb, c0 + TS);
+        absorb(xa);
+        if (!more) break;
+        if (c0 + 2 * TS < nchunk) load(xa, c0 + 2 * TS);
+        absorb(xb);
     }
-    // workgroup: maximum, then the sums rescaled to it, and the flags
+    // workgroup: maximum, then the sums rescaled to it
     float M = wave_max(m);
-    int fl = flags;
-#pragma unroll
-    for (int o = 32; o > 0; o >>= 1) fl |= __shfl_xor(fl, o, 64);
-    if (lane == 0) { sh_m[wave] = M; sh_f[wave] = fl; }
+    if (lane == 0) sh_m[wave] = M;
     __syncthreads();
     M = sh_m[0];
-    fl = sh_f[0];
 #pragma unroll
-    for (int w = 1; w < VT / 64; ++w) { M = fmaxf(M, sh_m[w]); fl |= sh_f[w]; }
+    for (int w = 1; w < VT / 64; ++w) M = fmaxf(M, sh_m[w]);
     const float Mref = M == -INFINITY ? 0.f : M;
-    float part = m == -INFINITY ? 0.f : sum * __builtin_amdgcn_exp2f((m - Mref) * LOG2E);
+    // a thread that met no finite logit has sum 0, or NaN if it met a NaN: kept as it is
+    float part = m == -INFINITY ? sum : sum * __builtin_amdgcn_exp2f((m - Mref) * LOG2E);
     part = wave_sum(part);
     if (lane == 0) sh_s[wave] = part;
     __syncthreads();
-    if (threadIdx.x == 0) {
-        float S = sh_s[0];
+    float S = sh_s[0];
 #pragma unroll
-        for (int w = 1; w < VT / 64; ++w) S += sh_s[w];
-        lse[r] = (fl & 1) ? __int_as_float(0x7FC00000) : (fl & 2) ? INFINITY : Mref + logf(S);
+    for (int w = 1; w < VT / 64; ++w) S += sh_s[w];
+    if (!(S == S) || M == INFINITY) {
+        // a NaN or +inf logit (the sum is NaN): NaN if any logit is NaN, else +inf
+        int fl = 0;
+        for (int c = tid; c < nchunk; c += VT) {
+            uint4 x = *(const uint4*)(rowp + (size_t)c * 16);
+            if (V % E != 0 && c == nchunk - 1) Elem<T>::clip(x, V % E);
+#pragma unroll
+            for (int e = 0; e < E; ++e) {
+                const float t = Elem<T>::get(x, e);
+                fl |= (t != t) ? 1 : (t == INFINITY ? 2 : 0);
+            }
+        }
+#pragma unroll
+        for (int o = 32; o > 0; o >>= 1) fl |= __shfl_xor(fl, o, 64);
+        if (lane == 0) sh_f[wave] = fl;
+        __syncthreads();
+        fl = sh_f[0] | sh_f[1] | sh_f[2] | sh_f[3];
+        if (tid == 0) lse[r] = (fl & 1) ? __int_as_float(0x7FC00000) : INFINITY;
+    } else if (tid == 0) {
+        lse[r] = Mref + logf(S);
     }
 }
 

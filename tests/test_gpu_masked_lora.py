@@ -213,12 +213,19 @@ def test_teacher_logits_in_one_pass_match_base_model_on_gpu(tile, monkeypatch):
     assert err2 == 0
     diff = np.abs(got[:, :n] - teach)
     nd = int((diff > 0).sum())
-    say(f"tile {tile}: teacher logits max diff {diff.max():.3e}, {nd} of {diff.size} differ "
-        f"(sequence 0: {int((diff[0] > 0).sum())}, sequence 1: {int((diff[1] > 0).sum())}); "
-        f"max diff / bf16 ulp {np.max(diff / _bf16_ulp(teach)):.3f}")
+    rows = np.nonzero(diff.max(axis=2) > 0)
+    say(f"tile {tile}: teacher logits max diff {diff.max():.3e}, {nd} of {diff.size} differ, in rows "
+        f"{sorted(set(zip(rows[0].tolist(), rows[1].tolist())))[:3]} .. (sequence, position)")
     if tile is None:
-        assert np.all(diff <= _bf16_ulp(teach))
-        assert (diff[0] == 0).all()          # sequence 0's rows sit in M-tile 0 in both calls
+        # rows whose vocabulary M-tile is the same in both calls: sequence 0, and positions 0..63 of
+        # sequence 1 (rows 192..255 of the [x, z_1] call, 96..159 of the call on x alone)
+        assert (diff[0] == 0).all() and (diff[1, :64] == 0).all()
+        # positions 64..95 of sequence 1 (rows 256..287: M-tile 1, against M-tile 0): the same fp32
+        # products summed in another order, rounded to bf16.  Bound: one bf16 ulp of the larger value
+        # plus the fp32 summation error of a 768-term dot product (about 1e-6 here; it dominates only
+        # for logits near zero, where the terms cancel)
+        ulp = np.maximum(_bf16_ulp(teach[1, 64:]), _bf16_ulp(got[1, 64:n]))
+        assert np.all(diff[1, 64:] <= ulp + 4e-6)
     else:
         assert nd == 0
 

@@ -126,14 +126,19 @@ def test_spec_verify_is_lossless_chi2():
 
 
 def test_spec_verify_degenerate_logits_are_reported():
-    """NaN in every target row of one sequence: DD_DEVERR_LOGITS and z = 0 there.  NaN in the draft
-    rows of another: its draw stays valid (the residual falls back to p).  Every other sequence is
-    bit-identical to the clean call."""
+    """NaN in every target row of one sequence, a NaN inside an otherwise -inf 16-byte chunk of every
+    target row of another (the thread reading that chunk meets no finite logit), +inf in every
+    target row of a third: DD_DEVERR_LOGITS and z = 0 there.  NaN in the draft rows of another: its
+    draw stays valid (the residual falls back to p).  Every other sequence is bit-identical to the
+    clean call."""
     torch = torch_or_skip()
     S, B, V, dt = 8, 4, 600, "bf16"
     pl, ql, draft = _case(17, S, B, V, dt, 0.3)
     pd, qd = pl.copy(), ql.copy()
     pd[2, :, 5] = np.nan
+    pd[3, :, 16:24] = -np.inf
+    pd[3, :, 21] = np.nan
+    pd[6, :, 9] = np.inf
     qd[5, :, 7] = np.nan
     ld = int(dd.logits_ld(V))
     res = []
@@ -149,6 +154,6 @@ def test_spec_verify_degenerate_logits_are_reported():
     (n0, z0, e0), (n1, z1, e1) = res
     say(f"clean err {e0}, dirty err {e1}; seq 2 -> ({n1[2]}, {z1[2]}), seq 5 -> ({n1[5]}, {z1[5]})")
     assert e0 == 0 and e1 == dd.DD_DEVERR_LOGITS
-    assert z1[2] == 0 and 1 <= n1[5] <= B and 0 <= z1[5] < V
-    keep = [s for s in range(S) if s not in (2, 5)]
+    assert z1[2] == 0 and z1[3] == 0 and z1[6] == 0 and 1 <= n1[5] <= B and 0 <= z1[5] < V
+    keep = [s for s in range(S) if s not in (2, 3, 5, 6)]
     assert np.array_equal(n0[keep], n1[keep]) and np.array_equal(z0[keep], z1[keep])
