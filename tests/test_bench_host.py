@@ -30,7 +30,8 @@ def test_algorithmic_flops_of_the_gpt2s_workload():
 def _record(tmp_path, sha, cls="gemm_mlp_down"):
     (tmp_path / "profiles").mkdir()
     (tmp_path / "src.hip").write_bytes(b"kernel source\n")
-    rec = {"kernel_class": cls, "source": "src.hip", "source_sha256": sha, "traffic_bytes_per_launch": 123.0}
+    rec = {"kernel_class": cls, "workload": "gpt2s-mask-bf16", "source": "src.hip", "source_sha256": sha,
+           "traffic_bytes_per_launch": 123.0}
     (tmp_path / "profiles" / "traffic_x.md").write_text("# t\n\ntraffic-json: " + json.dumps(rec) + "\n")
 
 
@@ -39,15 +40,17 @@ def test_traffic_record_only_while_the_source_is_unchanged(tmp_path, monkeypatch
     good = hashlib.sha256(b"kernel source\n").hexdigest()
     _record(tmp_path, good)
     monkeypatch.setattr(bench, "ROOT", str(tmp_path))
-    assert bench.recorded_traffic("gemm_mlp_down") == 123.0
-    assert bench.recorded_traffic("gemm_mlp_up") is None
+    assert bench.recorded_traffic("gemm_mlp_down", "gpt2s-mask-bf16") == 123.0
+    assert bench.recorded_traffic("gemm_mlp_up", "gpt2s-mask-bf16") is None
+    # a record taken on one workload says nothing about another workload's launches
+    assert bench.recorded_traffic("gemm_mlp_down", "gpt2s-mask-b128-bf16") is None
     (tmp_path / "src.hip").write_bytes(b"kernel source, edited\n")
-    assert bench.recorded_traffic("gemm_mlp_down") is None
+    assert bench.recorded_traffic("gemm_mlp_down", "gpt2s-mask-bf16") is None
 
 
 def test_committed_traffic_records_parse():
     for cls in ("gemm_mlp_down", "gemm_mlp_up"):
-        t = bench.recorded_traffic(cls)
+        t = bench.recorded_traffic(cls, "gpt2s-mask-bf16")
         assert t is None or 1e8 < t < 1e9, (cls, t)
 
 
