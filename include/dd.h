@@ -60,6 +60,7 @@ typedef enum {
 
 typedef enum { DD_BF16 = 0, DD_FP32 = 1 } dd_dtype;
 typedef enum { DD_PRIOR_MASK = 0, DD_PRIOR_UNIFORM = 1 } dd_prior;
+typedef enum { DD_NORM_LAYER = 0, DD_NORM_RMS = 1 } dd_norm;
 
 /* Classes per level-1 group of the two-level Gumbel-max draw. */
 #define DD_GUMBEL_GROUP 256
@@ -76,11 +77,17 @@ typedef enum { DD_PRIOR_MASK = 0, DD_PRIOR_UNIFORM = 1 } dd_prior;
  *   h = tok_emb[z] + pos_emb[l] + temb(alpha_t)       (temb only if time_cond)
  *   temb_j = sin(tau w_j) (j < d/2), cos(tau w_{j-d/2}) (j >= d/2),
  *   w_i = 10000^(-i/(d/2)), tau = 1000 (1 - alpha_t)
- *   per layer: h += W_o attn(LN1(h)) + b_o ; h += W_2 gelu_tanh(W_1 LN2(h) + b_1) + b_2
- *   logits = W_out LN_f(h)                              (V columns, no bias)
+ *   per layer: h += W_o attn(N1(h)) + b_o ; h += W_2 gelu_tanh(W_1 N2(h) + b_1) + b_2
+ *   logits = W_out N_f(h)                               (V columns, no bias)
+ * The normalisations N (per token row of d features, gain g and shift b from the
+ * parameter blob) follow `norm`:
+ *   DD_NORM_LAYER  (x - mean) / sqrt(var + eps) g + b, var the biased variance
+ *   DD_NORM_RMS    x / sqrt(mean(x^2) + eps) g: RMSNorm over the whole row (the
+ *                  paper's own model, Sec. 5.1, uses RMSNorm); the shift vectors
+ *                  keep their place in the blob and are not read
  * d_model even, d_model % n_heads == 0.  dtype DD_BF16: bf16 weights and
- * activations, fp32 accumulation, fp32 residual stream, LayerNorm and softmax;
- * DD_FP32: everything fp32 (validation build).
+ * activations, fp32 accumulation, fp32 residual stream, normalisation statistics
+ * and softmax; DD_FP32: everything fp32 (validation build).
  *
  * Adapters (lora_rank = r > 0; the diffusion weights of Sec. 3.1, a LoRA
  * adapter on every projection W_qkv, W_o, W_1, W_2): at sequence position l
@@ -105,7 +112,8 @@ typedef struct {
     int32_t prior;      /* dd_prior: selects tok_emb rows (V + 1 or V) */
     int32_t dtype;      /* dd_dtype of weights, activations and logits */
     int32_t time_cond;  /* 1: add the sinusoidal time embedding */
-    float norm_eps;     /* LayerNorm epsilon (biased variance) */
+    int32_t norm;       /* dd_norm: DD_NORM_LAYER or DD_NORM_RMS (other values: DD_E_ARG) */
+    float norm_eps;     /* epsilon of the normalisations */
     int32_t lora_rank;  /* r: adapter rank, 0 = no adapters */
     float lora_alpha;   /* adapter scale numerator: scale = lora_alpha / r */
 } dd_config;

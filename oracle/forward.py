@@ -15,7 +15,11 @@ GPT-2-shaped, non-causal transformer.  Reading adopted here:
               a = LN2(h); h += gelu_tanh(a W_1^T + b_1) W_2^T + b_2
   logits = LN_f(h) W_out^T                        (V columns, no bias)
 
-LayerNorm uses the biased variance and eps = cfg['norm_eps'].  x_theta is the
+LN is cfg['norm']: "layer" (the default) is LayerNorm with the biased variance,
+(x - mean) / sqrt(var + eps) g + b; "rms" is RMSNorm, x / sqrt(mean(x^2) + eps) g,
+over the whole row with no shift (the paper's own model, Sec. 5.1, names a
+grouped RMSNorm without giving the groups; the reading here is one group, the
+row), eps = cfg['norm_eps'] in both.  x_theta is the
 softmax of the logits over the V real tokens (the mask class gets zero mass,
 App. A.1: clean data contains no mask token).
 
@@ -58,6 +62,21 @@ def layer_norm(x, g, b, eps):
     return (x - mu) / np.sqrt(var + eps) * g + b
 
 
+def rms_norm(x, g, eps):
+    ms = (x ** 2).mean(axis=-1, keepdims=True)
+    return x / np.sqrt(ms + eps) * g
+
+
+def normalise(cfg, x, g, b):
+    """The normalisation cfg['norm'] selects ("layer" or "rms"; the shift b is unused by RMSNorm)."""
+    norm = cfg.get("norm", "layer")
+    if norm == "rms":
+        return rms_norm(x, g, cfg["norm_eps"])
+    if norm != "layer":
+        raise ValueError(f"unknown norm {norm!r}")
+    return layer_norm(x, g, b, cfg["norm_eps"])
+
+
 def gelu_tanh(x):
     return 0.5 * x * (1.0 + np.tanh(np.sqrt(2.0 / np.pi) * (x + 0.044715 * x ** 3)))
 
@@ -91,14 +110,13 @@ def forward_hidden(cfg, P, z, alpha_t, vis=None, gate=None, on_layer=None):
     B, L = z.shape
     d, H = cfg["d_model"], cfg["n_heads"]
     dh = d // H
-    eps = cfg["norm_eps"]
     g = np.ones(L) if gate is None else np.asarray(gate, dtype=np.float64)
     h = P["tok_emb"][z] + P["pos_emb"][:L][None]
     if cfg.get("time_cond", True):
         h = h + time_embedding(alpha_t, d)[None, None]
     for l in range(cfg["n_layers"]):
         p = lambda n: P[f"l{l}.{n}"]
-        a = layer_norm(h, p("ln1_g"), p("ln1_b"), eps)
+        a = normalise(cfg, h, p("ln1_g"), p("ln1_b"))
         qkv = projection(cfg, P, l, "qkv", a, g)
         q, k, v = qkv[..., :d], qkv[..., d:2 * d], qkv[..., 2 * d:]
         o = np.empty_like(q)
@@ -107,11 +125,11 @@ def forward_hidden(cfg, P, z, alpha_t, vis=None, gate=None, on_layer=None):
                 cs = slice(hh * dh, (hh + 1) * dh)
                 o[b, :, cs] = attention(q[b, :, cs], k[b, :, cs], v[b, :, cs], vis)
         h = h + projection(cfg, P, l, "o", o, g)
-        a = layer_norm(h, p("ln2_g"), p("ln2_b"), eps)
+        a = normalise(cfg, h, p("ln2_g"), p("ln2_b"))
         h = h + projection(cfg, P, l, "2", gelu_tanh(projection(cfg, P, l, "1", a, g)), g)
         if on_layer is not None:
             on_layer(l)
-    return layer_norm(h, P["lnf_g"], P["lnf_b"], eps)
+    return normalise(cfg, h, P["lnf_g"], P["lnf_b"])
 
 
 def forward(cfg, P, z, alpha_t, vis=None, gate=None, on_layer=None):

@@ -17,6 +17,13 @@ def _ln(vec, g, b, eps):
     return [(vec[i] - mu) * inv * g[i] + b[i] for i in range(n)]
 
 
+def _rms(vec, g, eps):
+    n = len(vec)
+    ms = sum(x * x for x in vec) / n
+    inv = 1.0 / math.sqrt(ms + eps)
+    return [vec[i] * inv * g[i] for i in range(n)]
+
+
 def _linear(vec, W, bias):
     """W is a nested list [out][in]; returns W vec + bias."""
     out = []
@@ -45,6 +52,8 @@ def forward_loops(cfg, P, z, alpha_t, vis=None, gate=None):
     scale = float(cfg["lora_alpha"]) / r if r else 0.0
     dh = d // H
     eps = cfg["norm_eps"]
+    rms = cfg.get("norm", "layer") == "rms"
+    norm = (lambda vec, g, b: _rms(vec, g, eps)) if rms else (lambda vec, g, b: _ln(vec, g, b, eps))
     tok, pos = tl(P["tok_emb"]), tl(P["pos_emb"])
     half = d // 2
     tau = 1000.0 * (1.0 - alpha_t)
@@ -74,7 +83,7 @@ def forward_loops(cfg, P, z, alpha_t, vis=None, gate=None):
                     y = [y[o] + scale * t[o] for o in range(len(y))]
                 return y
 
-            qkv = [lin("qkv", _ln(hs[l], ln1g, ln1b, eps), l) for l in range(L)]
+            qkv = [lin("qkv", norm(hs[l], ln1g, ln1b), l) for l in range(L)]
             att = [[0.0] * d for _ in range(L)]
             for hh in range(H):
                 off = hh * dh
@@ -97,9 +106,9 @@ def forward_loops(cfg, P, z, alpha_t, vis=None, gate=None):
             for l in range(L):
                 o = lin("o", att[l], l)
                 hs[l] = [hs[l][j] + o[j] for j in range(d)]
-                u = [_gelu(x) for x in lin("1", _ln(hs[l], ln2g, ln2b, eps), l)]
+                u = [_gelu(x) for x in lin("1", norm(hs[l], ln2g, ln2b), l)]
                 m = lin("2", u, l)
                 hs[l] = [hs[l][j] + m[j] for j in range(d)]
         lnfg, lnfb, wout = tl(P["lnf_g"]), tl(P["lnf_b"]), tl(P["w_out"])
-        out.append([_linear(_ln(hs[l], lnfg, lnfb, eps), wout, None) for l in range(L)])
+        out.append([_linear(norm(hs[l], lnfg, lnfb), wout, None) for l in range(L)])
     return out

@@ -18,6 +18,7 @@ LIB_PATH = os.path.join(_HERE, "libdd.so")
 
 DD_BF16, DD_FP32 = 0, 1
 DD_PRIOR_MASK, DD_PRIOR_UNIFORM = 0, 1
+DD_NORM_LAYER, DD_NORM_RMS = 0, 1
 DD_GUMBEL_GROUP = 256
 DD_DEVERR_TOKEN = 1
 DD_DEVERR_MASK = 2
@@ -45,7 +46,7 @@ class DDConfig(ctypes.Structure):
                 ("n_heads", ctypes.c_int32), ("d_mlp", ctypes.c_int32),
                 ("vocab", ctypes.c_int32), ("mask_id", ctypes.c_int32), ("max_len", ctypes.c_int32),
                 ("prior", ctypes.c_int32), ("dtype", ctypes.c_int32),
-                ("time_cond", ctypes.c_int32), ("norm_eps", ctypes.c_float),
+                ("time_cond", ctypes.c_int32), ("norm", ctypes.c_int32), ("norm_eps", ctypes.c_float),
                 ("lora_rank", ctypes.c_int32), ("lora_alpha", ctypes.c_float)]
 
 
@@ -147,8 +148,16 @@ def make_config(cfg):
                     int(cfg["d_mlp"]), int(cfg["vocab"]), int(mid), int(cfg["max_len"]),
                     DD_PRIOR_MASK if cfg["prior"] == "mask" else DD_PRIOR_UNIFORM,
                     DD_BF16 if cfg["dtype"] == "bf16" else DD_FP32,
-                    1 if cfg.get("time_cond", True) else 0, float(cfg.get("norm_eps", 1e-5)),
+                    1 if cfg.get("time_cond", True) else 0, norm_code(cfg.get("norm", "layer")),
+                    float(cfg.get("norm_eps", 1e-5)),
                     int(cfg.get("lora_rank", 0) or 0), float(cfg.get("lora_alpha", 0.0) or 0.0))
+
+
+def norm_code(norm):
+    """dd_norm of a normalisation name: "layer" (LayerNorm) or "rms" (RMSNorm)."""
+    if norm not in ("layer", "rms"):
+        raise ValueError(f"unknown norm {norm!r}")
+    return DD_NORM_RMS if norm == "rms" else DD_NORM_LAYER
 
 
 def prior_code(prior):

@@ -116,6 +116,7 @@ static dd_status cfg_check(const dd_config* c) {
              "d_model must be even and divisible by n_heads");
     DD_CHECK(c->prior == DD_PRIOR_MASK || c->prior == DD_PRIOR_UNIFORM, DD_E_ARG, "unknown prior");
     DD_CHECK(c->dtype == DD_BF16 || c->dtype == DD_FP32, DD_E_ARG, "unknown dtype");
+    DD_CHECK(c->norm == DD_NORM_LAYER || c->norm == DD_NORM_RMS, DD_E_ARG, "unknown norm %d", c->norm);
     DD_CHECK(c->norm_eps >= 0.f, DD_E_ARG, "norm_eps must be >= 0");
     DD_CHECK(c->lora_rank >= 0 && c->lora_rank % 8 == 0, DD_E_ARG,
              "lora_rank must be a non-negative multiple of 8 (got %d)", c->lora_rank);
@@ -253,7 +254,7 @@ static dd_status run_forward(const dd_config* c, const void* params, const int32
 
     if (c->time_cond) DD_TRY(launch_temb(temb, d, 1000.0 * (1.0 - alpha_t), s));
     const int g0 = nl > 0 ? 2 : lnf;
-    DD_TRY(launch_embed_ln(dt, z, M, L, n_tok(c), d, tp(0), tp(1), c->time_cond ? temb : nullptr,
+    DD_TRY(launch_embed_ln(dt, c->norm, z, M, L, n_tok(c), d, tp(0), tp(1), c->time_cond ? temb : nullptr,
                            tp(g0), tp(g0 + 1), c->norm_eps, h, xln, dr, err, s));
     for (int l = 0; l < nl; ++l) {
         const int b = 2 + 12 * l;
@@ -268,7 +269,7 @@ static dd_status run_forward(const dd_config* c, const void* params, const int32
         if (r > 0) DD_TRY(lora_down(att, dr, d, a0 + 1));
         g = {att, dr, tp(b + 4), dr, tp(b + 5), h, d, (int)M, d, dr, nullptr, nullptr};
         DD_TRY(launch_gemm(dt, EPI_BIAS_RESID, KC_GEMM_O, g, s));
-        DD_TRY(launch_ln(dt, h, M, d, tp(b + 6), tp(b + 7), c->norm_eps, xln, dr, s));
+        DD_TRY(launch_ln(dt, c->norm, h, M, d, tp(b + 6), tp(b + 7), c->norm_eps, xln, dr, s));
         if (r > 0) DD_TRY(lora_down(xln, dr, d, a0 + 2));
         g = {xln, dr, tp(b + 8), dr, tp(b + 9), mlp, Fr, (int)M, F, dr, nullptr, nullptr};
         DD_TRY(launch_gemm(dt, EPI_BIAS_GELU, KC_GEMM_MLP1, g, s));
@@ -276,7 +277,7 @@ static dd_status run_forward(const dd_config* c, const void* params, const int32
         g = {mlp, Fr, tp(b + 10), Fr, tp(b + 11), h, d, (int)M, d, Fr, nullptr, nullptr};
         DD_TRY(launch_gemm(dt, EPI_BIAS_RESID, KC_GEMM_MLP2, g, s));
         const int gn = (l + 1 < nl) ? b + 12 : lnf;
-        DD_TRY(launch_ln(dt, h, M, d, tp(gn), tp(gn + 1), c->norm_eps, xln, dr, s));
+        DD_TRY(launch_ln(dt, c->norm, h, M, d, tp(gn), tp(gn + 1), c->norm_eps, xln, dr, s));
     }
     // with vocab_rows only the listed rows (count on the device) get logits, compacted
     GemmArgs g = {xln, dr, tp(lnf + 2), d, nullptr, logits, ld, (int)M, V, d, vocab_rows, vocab_count};

@@ -1,7 +1,9 @@
-// Time embedding, token/position embedding + first LayerNorm, and LayerNorm.
+// Time embedding, token/position embedding + first normalisation, and normalisation (LayerNorm or
+// RMSNorm, a template parameter of every kernel).
 //
-// One wavefront per token row; statistics are reduced with cross-lane shuffles in
-// fp32 (mean first, then the biased variance of the centred values, from registers).
+// One wavefront per token row; statistics are reduced across the lanes in fp32 from registers.
+// LayerNorm: the mean first, then the biased variance of the centred values; y = (x - mean) rstd g + b.
+// RMSNorm: the mean square; y = x rstd g, rstd = 1 / sqrt(mean square + eps) (no shift is read).
 #include <math.h>
 
 #include "kernels.h"
@@ -33,13 +35,16 @@ template <> DD_DEV void stw<bf16_t>(bf16_t* p, int64_t i, float v) { p[i] = f32_
 template <> DD_DEV void stw<float>(float* p, int64_t i, float v) { p[i] = v; }
 
 // NPL = d / 64 elements per lane (d % 64 == 0).
-template <typename W, int NPL>
+template <typename W, int NPL, bool RMS>
 DD_DEV void ln_row(const float (&x)[NPL], int lane, int d, const W* g, const W* b, float eps,
                    W* out) {
-    float s = 0.f;
+    float mean = 0.f;
+    if constexpr (!RMS) {
+        float s = 0.f;
 #pragma unroll
-    for (int k = 0; k < NPL; ++k) s += x[k];
-    const float mean = wave_sum(s) / (float)d;
+        for (int k = 0; k < NPL; ++k) s += x[k];
+        mean = wave_sum(s) / (float)d;
+    }
     float q = 0.f;
 #pragma unroll
     for (int k = 0; k < NPL; ++k) { const float c = x[k] - mean; q += c * c; }
@@ -47,11 +52,12 @@ DD_DEV void ln_row(const float (&x)[NPL], int lane, int d, const W* g, const W* 
 #pragma unroll
     for (int k = 0; k < NPL; ++k) {
         const int c = lane + 64 * k;
-        stw<W>(out, c, (x[k] - mean) * rstd * ldw<W>(g, c) + ldw<W>(b, c));
+        if constexpr (RMS) stw<W>(out, c, x[k] * rstd * ldw<W>(g, c));
+        else stw<W>(out, c, (x[k] - mean) * rstd * ldw<W>(g, c) + ldw<W>(b, c));
     }
 }
 
-template <typename W, int NPL>
+template <typename W, int NPL, bool RMS>
 __global__ __launch_bounds__(256) void embed_ln_kernel(const int32_t* z, int64_t rows, int L,
                                                        int n_tok, const W* tok, const W* pos,
                                                        const float* temb, const W* g, const W* b,
@@ -76,10 +82,10 @@ __global__ __launch_bounds__(256) void embed_ln_kernel(const int32_t* z, int64_t
         x[k] = v;
         h[row * d + c] = v;
     }
-    ln_row<W, NPL>(x, lane, d, g, b, eps, xln + row * ldo);
+    ln_row<W, NPL, RMS>(x, lane, d, g, b, eps, xln + row * ldo);
 }
 
-template <typename W, int NPL>
+template <typename W, int NPL, bool RMS>
 __global__ __launch_bounds__(256) void ln_kernel(const float* h, int64_t rows, const W* g,
                                                  const W* b, float eps, W* out, int64_t ldo) {
     const int64_t row = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
@@ -89,20 +95,23 @@ __global__ __launch_bounds__(256) void ln_kernel(const float* h, int64_t rows, c
     float x[NPL];
 #pragma unroll
     for (int k = 0; k < NPL; ++k) x[k] = h[row * d + lane + 64 * k];
-    ln_row<W, NPL>(x, lane, d, g, b, eps, out + row * ldo);
+    ln_row<W, NPL, RMS>(x, lane, d, g, b, eps, out + row * ldo);
 }
 
-// LayerNorm of one row held as NV groups of four consecutive features per lane (group lane + 64 k),
-// written as 8-byte bf16 stores; gg / bb hold the gain and shift of those features.  Both
-// statistics are wavefront sums by DPP lane moves.
-template <int NV>
+// Normalisation of one row held as NV groups of four consecutive features per lane (group
+// lane + 64 k), written as 8-byte bf16 stores; gg / bb hold the gain and shift of those features
+// (bb unused under RMS).  The statistics are wavefront sums by DPP lane moves.
+template <int NV, bool RMS>
 DD_DEV void ln4_row(const float4 (&x)[NV], int lane, const uint2 (&gg)[NV], const uint2 (&bb)[NV], float eps,
                     bf16_t* out) {
     constexpr int d = NV * 256;
-    float s = 0.f;
+    float mean = 0.f;
+    if constexpr (!RMS) {
+        float s = 0.f;
 #pragma unroll
-    for (int k = 0; k < NV; ++k) s += (x[k].x + x[k].y) + (x[k].z + x[k].w);
-    const float mean = wave_sum_dpp(s) / (float)d;
+        for (int k = 0; k < NV; ++k) s += (x[k].x + x[k].y) + (x[k].z + x[k].w);
+        mean = wave_sum_dpp(s) / (float)d;
+    }
     float q = 0.f;
 #pragma unroll
     for (int k = 0; k < NV; ++k) {
@@ -115,6 +124,12 @@ DD_DEV void ln4_row(const float4 (&x)[NV], int lane, const uint2 (&gg)[NV], cons
     for (int k = 0; k < NV; ++k) {
         const int c = lane + 64 * k;
         uint2 o;
+        if constexpr (RMS) {
+            o.x = pack_bf16x2(x[k].x * rstd * bf16_lo(gg[k].x), x[k].y * rstd * bf16_hi(gg[k].x));
+            o.y = pack_bf16x2(x[k].z * rstd * bf16_lo(gg[k].y), x[k].w * rstd * bf16_hi(gg[k].y));
+            orow[c] = o;
+            continue;
+        }
         o.x = pack_bf16x2((x[k].x - mean) * rstd * bf16_lo(gg[k].x) + bf16_lo(bb[k].x),
                           (x[k].y - mean) * rstd * bf16_hi(gg[k].x) + bf16_hi(bb[k].x));
         o.y = pack_bf16x2((x[k].z - mean) * rstd * bf16_lo(gg[k].y) + bf16_lo(bb[k].y),
@@ -123,12 +138,13 @@ DD_DEV void ln4_row(const float4 (&x)[NV], int lane, const uint2 (&gg)[NV], cons
     }
 }
 
-template <int NV>
+template <int NV, bool RMS>
 DD_DEV void load_gain_shift(const bf16_t* g, const bf16_t* b, int lane, uint2 (&gg)[NV], uint2 (&bb)[NV]) {
 #pragma unroll
     for (int k = 0; k < NV; ++k) {
         gg[k] = ((const uint2*)g)[lane + 64 * k];
-        bb[k] = ((const uint2*)b)[lane + 64 * k];
+        if constexpr (!RMS) bb[k] = ((const uint2*)b)[lane + 64 * k];
+        else bb[k] = make_uint2(0u, 0u);
     }
 }
 
@@ -138,7 +154,7 @@ DD_DEV void load_gain_shift(const bf16_t* g, const bf16_t* b, int lane, uint2 (&
 // LN_RPW rows per wavefront are in flight (the kernel is bound by HBM latency per wavefront
 // otherwise).
 constexpr int LN_RPW = 2;
-template <int NV>
+template <int NV, bool RMS>
 __global__ __launch_bounds__(256) void ln_bf16_v4_kernel(const float* h, int64_t rows,
                                                          const bf16_t* g, const bf16_t* b,
                                                          float eps, bf16_t* out, int64_t ldo) {
@@ -155,17 +171,17 @@ __global__ __launch_bounds__(256) void ln_bf16_v4_kernel(const float* h, int64_t
         for (int k = 0; k < NV; ++k) x[r][k] = hr[lane + 64 * k];
     }
     uint2 gg[NV], bb[NV];
-    load_gain_shift<NV>(g, b, lane, gg, bb);
+    load_gain_shift<NV, RMS>(g, b, lane, gg, bb);
 #pragma unroll
     for (int r = 0; r < LN_RPW; ++r) {
         if (row0 + r >= rows) break;
-        ln4_row<NV>(x[r], lane, gg, bb, eps, out + (row0 + r) * ldo);
+        ln4_row<NV, RMS>(x[r], lane, gg, bb, eps, out + (row0 + r) * ldo);
     }
 }
 
 // Embedding + first LayerNorm, bf16, d % 256 == 0: token and position rows read four features at a
 // time (8-byte loads), the residual row written with 16-byte stores.
-template <int NV>
+template <int NV, bool RMS>
 __global__ __launch_bounds__(256) void embed_ln_bf16_v4_kernel(const int32_t* z, int64_t rows, int L,
                                                                int n_tok, const bf16_t* tok,
                                                                const bf16_t* pos, const float* temb,
@@ -200,87 +216,110 @@ __global__ __launch_bounds__(256) void embed_ln_bf16_v4_kernel(const int32_t* z,
         hr[c] = v;
     }
     uint2 gg[NV], bb[NV];
-    load_gain_shift<NV>(g, b, lane, gg, bb);
-    ln4_row<NV>(x, lane, gg, bb, eps, xln + row * ldo);
+    load_gain_shift<NV, RMS>(g, b, lane, gg, bb);
+    ln4_row<NV, RMS>(x, lane, gg, bb, eps, xln + row * ldo);
 }
 
 #define DD_NPL_CASES(X) X(1) X(2) X(4) X(8) X(12) X(16) X(24) X(32)
 
-template <typename W>
+template <typename W, bool RMS>
 dd_status launch_embed_ln_t(const int32_t* z, int64_t rows, int L, int n_tok, int d, const void* tok,
                             const void* pos, const float* temb, const void* g, const void* b,
                             float eps, float* h, void* xln, int64_t ldo, int32_t* err, hipStream_t s) {
     const dim3 grid((unsigned)ceil_div(rows, 4)), blk(256);
-    ProfScope ps(KC_EMBED_LN, s);
     switch (d / 64) {
 #define X(n)                                                                                     \
     case n:                                                                                      \
-        hipLaunchKernelGGL((embed_ln_kernel<W, n>), grid, blk, 0, s, z, rows, L, n_tok,          \
+        hipLaunchKernelGGL((embed_ln_kernel<W, n, RMS>), grid, blk, 0, s, z, rows, L, n_tok,     \
                            (const W*)tok, (const W*)pos, temb, (const W*)g, (const W*)b, eps, h,  \
                            (W*)xln, ldo, err);                                                   \
         break;
         DD_NPL_CASES(X)
 #undef X
-        default: set_error("d_model %d unsupported by the LayerNorm kernels", d); return DD_E_UNSUPPORTED;
+        default: set_error("d_model %d unsupported by the normalisation kernels", d); return DD_E_UNSUPPORTED;
     }
     return launch_status("embed_ln");
 }
 
-dd_status launch_embed_ln(int dtype, const int32_t* z, int64_t rows, int L, int n_tok, int d,
+template <bool RMS>
+void launch_embed_ln_v4(int d, dim3 grid, const int32_t* z, int64_t rows, int L, int n_tok,
+                        const bf16_t* tk, const bf16_t* ps, const float* temb, const bf16_t* g,
+                        const bf16_t* b, float eps, float* h, bf16_t* o, int64_t ldo, int32_t* err,
+                        hipStream_t s) {
+    const dim3 blk(256);
+    if (d == 768)
+        hipLaunchKernelGGL((embed_ln_bf16_v4_kernel<3, RMS>), grid, blk, 0, s, z, rows, L, n_tok, tk, ps, temb, g, b, eps, h, o, ldo, err);
+    else if (d == 1024)
+        hipLaunchKernelGGL((embed_ln_bf16_v4_kernel<4, RMS>), grid, blk, 0, s, z, rows, L, n_tok, tk, ps, temb, g, b, eps, h, o, ldo, err);
+    else
+        hipLaunchKernelGGL((embed_ln_bf16_v4_kernel<8, RMS>), grid, blk, 0, s, z, rows, L, n_tok, tk, ps, temb, g, b, eps, h, o, ldo, err);
+}
+
+dd_status launch_embed_ln(int dtype, int norm, const int32_t* z, int64_t rows, int L, int n_tok, int d,
                           const void* tok, const void* pos, const float* temb, const void* g,
                           const void* b, float eps, float* h, void* xln, int64_t ldo, int32_t* err,
                           hipStream_t s) {
+    const bool rms = norm == DD_NORM_RMS;
+    ProfScope ps(KC_EMBED_LN, s);
     if (dtype == DD_BF16 && (d == 768 || d == 1024 || d == 2048) && ldo % 4 == 0) {
-        const dim3 grid((unsigned)ceil_div(rows, 4)), blk(256);
-        ProfScope ps(KC_EMBED_LN, s);
+        const dim3 grid((unsigned)ceil_div(rows, 4));
         const bf16_t *tk = (const bf16_t*)tok, *ps_ = (const bf16_t*)pos, *gg = (const bf16_t*)g, *bb = (const bf16_t*)b;
         bf16_t* o = (bf16_t*)xln;
-        if (d == 768)
-            hipLaunchKernelGGL(embed_ln_bf16_v4_kernel<3>, grid, blk, 0, s, z, rows, L, n_tok, tk, ps_, temb, gg, bb, eps, h, o, ldo, err);
-        else if (d == 1024)
-            hipLaunchKernelGGL(embed_ln_bf16_v4_kernel<4>, grid, blk, 0, s, z, rows, L, n_tok, tk, ps_, temb, gg, bb, eps, h, o, ldo, err);
-        else
-            hipLaunchKernelGGL(embed_ln_bf16_v4_kernel<8>, grid, blk, 0, s, z, rows, L, n_tok, tk, ps_, temb, gg, bb, eps, h, o, ldo, err);
+        if (rms) launch_embed_ln_v4<true>(d, grid, z, rows, L, n_tok, tk, ps_, temb, gg, bb, eps, h, o, ldo, err, s);
+        else launch_embed_ln_v4<false>(d, grid, z, rows, L, n_tok, tk, ps_, temb, gg, bb, eps, h, o, ldo, err, s);
         return launch_status("embed_ln");
     }
     if (dtype == DD_BF16)
-        return launch_embed_ln_t<bf16_t>(z, rows, L, n_tok, d, tok, pos, temb, g, b, eps, h, xln, ldo, err, s);
-    return launch_embed_ln_t<float>(z, rows, L, n_tok, d, tok, pos, temb, g, b, eps, h, xln, ldo, err, s);
+        return rms ? launch_embed_ln_t<bf16_t, true>(z, rows, L, n_tok, d, tok, pos, temb, g, b, eps, h, xln, ldo, err, s)
+                   : launch_embed_ln_t<bf16_t, false>(z, rows, L, n_tok, d, tok, pos, temb, g, b, eps, h, xln, ldo, err, s);
+    return rms ? launch_embed_ln_t<float, true>(z, rows, L, n_tok, d, tok, pos, temb, g, b, eps, h, xln, ldo, err, s)
+               : launch_embed_ln_t<float, false>(z, rows, L, n_tok, d, tok, pos, temb, g, b, eps, h, xln, ldo, err, s);
 }
 
-template <typename W>
+template <typename W, bool RMS>
 dd_status launch_ln_t(const float* h, int64_t rows, int d, const void* g, const void* b, float eps,
                       void* out, int64_t ldo, hipStream_t s) {
     const dim3 grid((unsigned)ceil_div(rows, 4)), blk(256);
-    ProfScope ps(KC_LN, s);
     switch (d / 64) {
 #define X(n)                                                                                     \
     case n:                                                                                      \
-        hipLaunchKernelGGL((ln_kernel<W, n>), grid, blk, 0, s, h, rows, (const W*)g,            \
+        hipLaunchKernelGGL((ln_kernel<W, n, RMS>), grid, blk, 0, s, h, rows, (const W*)g,       \
                            (const W*)b, eps, (W*)out, ldo);                                      \
         break;
         DD_NPL_CASES(X)
 #undef X
-        default: set_error("d_model %d unsupported by the LayerNorm kernels", d); return DD_E_UNSUPPORTED;
+        default: set_error("d_model %d unsupported by the normalisation kernels", d); return DD_E_UNSUPPORTED;
     }
     return launch_status("layernorm");
 }
 
-dd_status launch_ln(int dtype, const float* h, int64_t rows, int d, const void* g, const void* b,
+template <bool RMS>
+void launch_ln_v4(int d, dim3 grid, const float* h, int64_t rows, const bf16_t* g, const bf16_t* b,
+                  float eps, bf16_t* o, int64_t ldo, hipStream_t s) {
+    const dim3 blk(256);
+    if (d == 768) hipLaunchKernelGGL((ln_bf16_v4_kernel<3, RMS>), grid, blk, 0, s, h, rows, g, b, eps, o, ldo);
+    else if (d == 1024) hipLaunchKernelGGL((ln_bf16_v4_kernel<4, RMS>), grid, blk, 0, s, h, rows, g, b, eps, o, ldo);
+    else hipLaunchKernelGGL((ln_bf16_v4_kernel<8, RMS>), grid, blk, 0, s, h, rows, g, b, eps, o, ldo);
+}
+
+dd_status launch_ln(int dtype, int norm, const float* h, int64_t rows, int d, const void* g, const void* b,
                     float eps, void* out, int64_t ldo, hipStream_t s) {
+    const bool rms = norm == DD_NORM_RMS;
+    ProfScope ps(KC_LN, s);
     if (dtype == DD_BF16 && (d == 768 || d == 1024 || d == 2048) && ldo % 4 == 0) {
-        const dim3 grid((unsigned)ceil_div(rows, 4 * LN_RPW)), blk(256);
-        ProfScope ps(KC_LN, s);
+        const dim3 grid((unsigned)ceil_div(rows, 4 * LN_RPW));
         const bf16_t* gg = (const bf16_t*)g;
         const bf16_t* bb = (const bf16_t*)b;
         bf16_t* o = (bf16_t*)out;
-        if (d == 768) hipLaunchKernelGGL(ln_bf16_v4_kernel<3>, grid, blk, 0, s, h, rows, gg, bb, eps, o, ldo);
-        else if (d == 1024) hipLaunchKernelGGL(ln_bf16_v4_kernel<4>, grid, blk, 0, s, h, rows, gg, bb, eps, o, ldo);
-        else hipLaunchKernelGGL(ln_bf16_v4_kernel<8>, grid, blk, 0, s, h, rows, gg, bb, eps, o, ldo);
+        if (rms) launch_ln_v4<true>(d, grid, h, rows, gg, bb, eps, o, ldo, s);
+        else launch_ln_v4<false>(d, grid, h, rows, gg, bb, eps, o, ldo, s);
         return launch_status("layernorm");
     }
-    if (dtype == DD_BF16) return launch_ln_t<bf16_t>(h, rows, d, g, b, eps, out, ldo, s);
-    return launch_ln_t<float>(h, rows, d, g, b, eps, out, ldo, s);
+    if (dtype == DD_BF16)
+        return rms ? launch_ln_t<bf16_t, true>(h, rows, d, g, b, eps, out, ldo, s)
+                   : launch_ln_t<bf16_t, false>(h, rows, d, g, b, eps, out, ldo, s);
+    return rms ? launch_ln_t<float, true>(h, rows, d, g, b, eps, out, ldo, s)
+               : launch_ln_t<float, false>(h, rows, d, g, b, eps, out, ldo, s);
 }
 
 bool ln_supported(int d) {

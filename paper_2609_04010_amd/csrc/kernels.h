@@ -110,12 +110,13 @@ dd_status launch_latent(const int32_t* x, int32_t rows, int32_t V, double at, do
 dd_status launch_init(void* dst, int64_t count, uint32_t id, double shift, int is_bf16,
                       uint64_t seed, hipStream_t s);
 dd_status launch_temb(float* temb, int d, double tau, hipStream_t s);
-dd_status launch_embed_ln(int dtype, const int32_t* z, int64_t rows, int L, int n_tok, int d,
+// norm: dd_norm (LayerNorm or RMSNorm; b is not read under RMSNorm)
+dd_status launch_embed_ln(int dtype, int norm, const int32_t* z, int64_t rows, int L, int n_tok, int d,
                           const void* tok, const void* pos, const float* temb, const void* g,
                           const void* b, float eps, float* h, void* xln, int64_t ldo, int32_t* err,
                           hipStream_t s);
 // out rows have stride ldo (elements) >= d
-dd_status launch_ln(int dtype, const float* h, int64_t rows, int d, const void* g, const void* b,
+dd_status launch_ln(int dtype, int norm, const float* h, int64_t rows, int d, const void* g, const void* b,
                     float eps, void* out, int64_t ldo, hipStream_t s);
 bool ln_supported(int d);
 dd_status launch_gemm(int dtype, int epi, int cls, const GemmArgs& g, hipStream_t s);

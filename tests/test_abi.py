@@ -120,6 +120,14 @@ def test_forward_validation():
     bad = _cfg_struct()
     bad.dtype = 3
     assert _fwd(bad) == 1
+    bad = _cfg_struct()
+    bad.norm = 2
+    assert _fwd(bad) == 1
+    assert dd.lib().dd_last_error() == b"unknown norm 2"
+    assert dd.make_config(dict(workloads.model_cfg(2), norm="rms")).norm == dd.DD_NORM_RMS
+    assert dd.make_config(workloads.model_cfg(2)).norm == dd.DD_NORM_LAYER
+    with pytest.raises(ValueError):
+        dd.make_config(dict(workloads.model_cfg(2), norm="group"))
 
 
 def test_config_errors_keep_their_message():

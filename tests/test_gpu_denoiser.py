@@ -53,10 +53,20 @@ FWD_CASES = [
     (2, {}, 1, 1024, 0.25, 0.75, "host"),
     (3, {}, 2, 130, 0.4, 0.0, "host"),
     (5, {"max_len": 4096}, 1, 300, 0.7, 0.3, "host"),
+    # RMSNorm: fp32 (row-per-wavefront kernels), bf16 at d 64 (the same kernels in bf16) and bf16
+    # at d 768 / 1024 (the four-features-per-lane kernels)
+    (1, {"norm": "rms"}, 4, 32, 0.625, 0.375, "seeded"),
+    (1, {"norm": "rms", "dtype": "bf16", "n_heads": 1, "max_len": 96}, 2, 70, 0.5, 0.5, "host"),
+    (2, {"norm": "rms", "n_layers": 3}, 2, 200, 0.5, 0.5, "host"),
+    (5, {"norm": "rms", "n_layers": 2, "max_len": 4096}, 1, 300, 0.7, 0.3, "host"),
 ]
 
 
-@pytest.mark.parametrize("case", FWD_CASES, ids=lambda c: f"w{c[0]}-B{c[2]}-L{c[3]}-a{c[4]}")
+def _fwd_id(c):
+    return f"w{c[0]}-B{c[2]}-L{c[3]}-a{c[4]}" + ("-" + "-".join(f"{k}{v}" for k, v in c[1].items()) if c[1] else "")
+
+
+@pytest.mark.parametrize("case", FWD_CASES, ids=_fwd_id)
 def test_denoise_forward_parity(case):
     torch = torch_or_skip()
     c, over, B, L, at, mf, src = case

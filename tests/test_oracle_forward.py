@@ -41,6 +41,64 @@ def test_layer_norm_moments():
     assert np.allclose(y.mean(-1), 0, atol=1e-12) and np.allclose(y.var(-1), 1, atol=1e-12)
 
 
+def test_rms_norm_unit_mean_square_and_scale_invariance():
+    """With unit gain and eps = 0 every output row has mean square 1, and scaling a row by a > 0
+    leaves it unchanged (the defining properties of RMS normalisation)."""
+    x = np.random.default_rng(2).standard_normal((5, 64)) * 3 + 2
+    y = forward.rms_norm(x, np.ones(64), 0.0)
+    assert np.allclose((y ** 2).mean(-1), 1, atol=1e-12)
+    assert np.allclose(forward.rms_norm(7.5 * x, np.ones(64), 0.0), y, atol=1e-12)
+    # the mean is not removed: a row's sign pattern and the ratios of its entries survive
+    assert np.allclose(y / y[:, :1], x / x[:, :1], atol=1e-10)
+
+
+def test_rms_norm_closed_form_on_constant_rows():
+    g = np.linspace(0.5, 2.0, 8)
+    for c, eps in ((3.0, 0.0), (-0.25, 1e-2), (1e-3, 1e-5)):
+        y = forward.rms_norm(np.full((1, 8), c), g, eps)
+        assert np.allclose(y[0], c / np.sqrt(c * c + eps) * g, rtol=1e-14, atol=0)
+
+
+def test_rms_norm_equals_layer_norm_on_centred_rows():
+    """On rows of mean zero the mean square is the biased variance, so RMSNorm and LayerNorm with a
+    zero shift coincide (for any eps)."""
+    rng = np.random.default_rng(4)
+    x = rng.standard_normal((6, 32)) * 2.5
+    x -= x.mean(-1, keepdims=True)
+    g = rng.uniform(0.5, 1.5, 32)
+    for eps in (0.0, 1e-5, 0.3):
+        assert np.allclose(forward.rms_norm(x, g, eps), forward.layer_norm(x, g, np.zeros(32), eps),
+                           atol=1e-13)
+
+
+def test_rms_norm_equals_library():
+    torch = __import__("pytest").importorskip("torch")
+    rng = np.random.default_rng(5)
+    x, g = rng.standard_normal((4, 48)) * 3 + 1, rng.uniform(0.5, 1.5, 48)
+    ref = torch.nn.functional.rms_norm(torch.from_numpy(x), (48,), torch.from_numpy(g), eps=1e-5).numpy()
+    assert np.allclose(forward.rms_norm(x, g, 1e-5), ref, rtol=1e-13, atol=1e-13)
+
+
+def test_rms_forward_vectorised_equals_scalar_loops():
+    cfg = dict(CFG, norm="rms")
+    P = _P(cfg, scale=20.0)
+    z = _z()
+    a = forward.forward(cfg, P, z, 0.37)
+    b = np.array(forward_loops.forward_loops(cfg, P, z, 0.37))
+    assert np.abs(a - b).max() < 1e-10 * max(1.0, np.abs(a).max())
+    # and the shift vectors are not read: changing them changes nothing
+    P2 = {k: (v + 1.0 if k.endswith("_b") and "ln" in k else v) for k, v in P.items()}
+    assert np.array_equal(forward.forward(cfg, P2, z, 0.37), a)
+    # while under LayerNorm the same change moves the logits
+    assert np.abs(forward.forward(CFG, P2, z, 0.37) - forward.forward(CFG, P, z, 0.37)).max() > 1e-3
+
+
+def test_unknown_norm_is_refused():
+    import pytest
+    with pytest.raises(ValueError):
+        forward.forward(dict(CFG, norm="group"), _P(), _z(), 0.5)
+
+
 def test_permutation_equivariance_without_positions():
     P = _P(scale=10.0)
     P["pos_emb"] = np.zeros_like(P["pos_emb"])

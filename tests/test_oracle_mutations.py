@@ -81,6 +81,21 @@ def test_loop_pin_catches_swapped_time_embedding(monkeypatch):
     assert _forward_mismatch() > 1e-6
 
 
+def test_loop_pin_catches_centred_rms_norm(monkeypatch):
+    """RMSNorm that removes the mean first (i.e. a shift-free LayerNorm) is caught by the scalar
+    loops under norm = "rms"."""
+    def rms(x, g, eps):
+        c = x - x.mean(-1, keepdims=True)
+        return c / np.sqrt((c ** 2).mean(-1, keepdims=True) + eps) * g
+    monkeypatch.setattr(forward, "rms_norm", rms)
+    cfg = dict(CFG, norm="rms")
+    P = _P(cfg, scale=20.0)
+    z = _z()
+    a = forward.forward(cfg, P, z, 0.37)
+    b = np.array(forward_loops.forward_loops(cfg, P, z, 0.37))
+    assert np.abs(a - b).max() > 1e-6
+
+
 def test_loop_pin_catches_unbiased_variance(monkeypatch):
     def ln(x, g, b, eps):
         mu = x.mean(-1, keepdims=True)
