@@ -26,6 +26,7 @@ STREAM_CLASS = 1    # per-class Gumbels of the two-level sampler
 STREAM_LATENT = 2   # Gaussian latents (uniform-state start / probes)
 STREAM_PARAM = 3    # parameter initialisation
 STREAM_VERIFY = 4   # acceptance uniforms of speculative verification
+STREAM_GROUP_U = 5  # per-group uniforms of the inverse-CDF level 2 of the two-level sampler
 
 
 def philox_scalar(ctr, key, rounds=10):

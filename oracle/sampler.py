@@ -15,6 +15,19 @@ partition of the classes into groups:
              G_j = Gumbel of word (STREAM_CLASS, step, row, j).
   ties       the lowest index wins at both levels; log 0 = -inf.
 
+A second reading of level 2 (the "inverse-CDF" draw, used where a group's
+candidate must be fixed before the group is known to win, so that one uniform
+per group replaces one Gumbel per class):
+
+  level 2'   u_g = uniform of word (STREAM_GROUP_U, step, row, g) for every
+             group g; z_s = the first j of g* (in class order) with
+             sum_{i in g*, i <= j} p_i > u_{g*} M_{g*}  (if rounding leaves
+             none, the last j of g* with p_j > 0).
+
+Level 1 is the same in both readings (same words, same group).  Level 2' picks
+j with probability p_j / M_g because u is uniform on (0, 1) and independent of
+the level-1 noise, so the pair is again an exact draw from p.
+
 Exactness: the maximum over a group of log p_j + G_j is distributed as
 log M_g plus a standard Gumbel and is independent of the group's argmax, so
 level 1 picks group g with probability M_g and level 2 picks j with
@@ -76,6 +89,9 @@ class PhiloxNoise:
     def cls(self, row, idx):
         return _ph.counter_words(self.seed, _ph.STREAM_CLASS, self.step, row, np.asarray(idx))
 
+    def group_u(self, row, g):
+        return _ph.counter_words(self.seed, _ph.STREAM_GROUP_U, self.step, row, np.asarray(g))
+
 
 class ExplicitNoise:
     """Noise words read from a [rows, NU] uint32 array (level-1 words first)."""
@@ -120,19 +136,70 @@ def sample_from_probs(prior, p, row, noise):
     return a + j, gap1, gap2
 
 
+def inverse_cdf(w, word):
+    """Level 2' inside one group: the first index whose running sum of the weights w exceeds
+    u * sum(w), u = uniform(word) (the last index with w > 0 if rounding leaves none).
+
+    Returns (index, gap): gap = the distance of u * sum(w) to the nearest running-sum boundary
+    that separates two classes of non-zero weight, relative to sum(w) (inf with one such class)."""
+    w = np.asarray(w, dtype=np.float64)
+    S = w.sum()
+    t = float(_nz.uniform(word)) * S
+    c = np.cumsum(w)
+    above = np.nonzero(c > t)[0]
+    pos = np.nonzero(w > 0)[0]
+    j = int(above[0]) if above.size else int(pos[-1])
+    inner = c[pos[:-1]]                       # boundaries between consecutive classes of mass
+    gap = float(np.abs(inner - t).min() / S) if inner.size else np.inf
+    return j, gap
+
+
+def sample_from_probs_cdf(prior, p, row, noise):
+    """Two-level draw with the inverse-CDF level 2' (level 1 as sample_from_probs).
+
+    Returns (class id, level-1 gap, level-2 gap); the level-2 gap is relative mass (inverse_cdf)."""
+    V = p.shape[0] - (1 if prior == "mask" else 0)
+    bounds = group_bounds(prior, V)
+    with np.errstate(divide="ignore"):
+        logM = np.log(np.array([p[a:b].sum() for a, b in bounds]))
+        G = _nz.gumbel(noise.top(row, len(bounds)))
+    g, gap1 = _first_argmax_and_gap(logM + G)
+    a, b = bounds[g]
+    if prior == "mask" and a == V:
+        return V, gap1, np.inf
+    j, gap2 = inverse_cdf(p[a:b], noise.group_u(row, g))
+    return a + j, gap1, gap2
+
+
+def group_candidates(logits_row, row, noise, V):
+    """Level 2' of every real group of one row, each with its own uniform, from logits (the
+    within-group distribution of the masked prior's posterior is softmax of the group's logits).
+    Returns (candidates [n_groups], gaps [n_groups])."""
+    l = np.asarray(logits_row, dtype=np.float64)
+    out, gaps = [], []
+    for g, (a, b) in enumerate(group_bounds("uniform", V)):
+        w = np.exp(l[a:b] - l[a:b].max())
+        j, gp = inverse_cdf(w, noise.group_u(row, g))
+        out.append(a + j)
+        gaps.append(gp)
+    return np.array(out), np.array(gaps)
+
+
 def sample_flat(p, words):
     """Textbook one-Gumbel-per-class draw (used only to pin the two-level draw)."""
     with np.errstate(divide="ignore"):
         return int(np.argmax(np.log(p) + _nz.gumbel(words)))
 
 
-def posterior_sample(prior, logits, z_t, alpha_t, alpha_s, noise, rows=None, return_probs=False):
+def posterior_sample(prior, logits, z_t, alpha_t, alpha_s, noise, rows=None, return_probs=False,
+                     level2="gumbel"):
     """One reverse step on a [R, V] logit matrix.
 
     Masked prior: rows whose z_t is not the mask id V are carried over.
     Returns z_s [R] (int64), the per-row level gaps [R, 2] and, optionally,
-    the posterior probabilities [R, K].
+    the posterior probabilities [R, K].  level2: "gumbel" (level 2) or "cdf" (level 2').
     """
+    draw = _draw_fn(level2)
     logits = np.asarray(logits, dtype=np.float64)
     z_t = np.asarray(z_t)
     R, V = logits.shape
@@ -153,15 +220,17 @@ def posterior_sample(prior, logits, z_t, alpha_t, alpha_s, noise, rows=None, ret
         p = _post.posterior(prior, x, zt, alpha_t, alpha_s)
         if return_probs:
             probs[i] = p
-        out[i], gaps[i, 0], gaps[i, 1] = sample_from_probs(prior, p, int(rows[i]), noise)
+        out[i], gaps[i, 0], gaps[i, 1] = draw(prior, p, int(rows[i]), noise)
     return (out, gaps, probs) if return_probs else (out, gaps)
 
 
-def psi_sample(prior, logits, z_t, alpha_t, alpha_s, kappa, noise, rows=None, return_probs=False):
+def psi_sample(prior, logits, z_t, alpha_t, alpha_s, kappa, noise, rows=None, return_probs=False,
+               level2="gumbel"):
     """One Psi-sampler step (App. A.4, eq. (psi-sampler)) on a [R, V] logit matrix.
 
     Same outputs as posterior_sample; every row draws (masked prior: unmasked rows
     choose between keeping their token and the mask)."""
+    draw = _draw_fn(level2)
     logits = np.asarray(logits, dtype=np.float64)
     z_t = np.asarray(z_t)
     R, V = logits.shape
@@ -183,5 +252,13 @@ def psi_sample(prior, logits, z_t, alpha_t, alpha_s, kappa, noise, rows=None, re
             p = (_post.psi_mdm if prior == "mask" else _post.psi_usdm)(x, zt, alpha_t, alpha_s, kappa)
         if return_probs:
             probs[i] = p
-        out[i], gaps[i, 0], gaps[i, 1] = sample_from_probs(prior, p, int(rows[i]), noise)
+        out[i], gaps[i, 0], gaps[i, 1] = draw(prior, p, int(rows[i]), noise)
     return (out, gaps, probs) if return_probs else (out, gaps)
+
+
+def _draw_fn(level2):
+    if level2 == "gumbel":
+        return sample_from_probs
+    if level2 == "cdf":
+        return sample_from_probs_cdf
+    raise ValueError(f"unknown level-2 rule {level2!r}")

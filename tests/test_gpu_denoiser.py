@@ -4,8 +4,8 @@ import numpy as np
 import pytest
 
 import workloads
-from oracle import forward as oforward, loop as oloop, params as oparams, sampler as osampler, \
-    schedule as osched
+from oracle import forward as oforward, latent as olatent, loop as oloop, params as oparams, \
+    sampler as osampler, schedule as osched
 from paper_2609_04010_amd import _lib as dd
 from tests.gpu_util import compare_ids, dev_i32, dev_words, say, torch_or_skip
 
@@ -204,6 +204,41 @@ def test_loop_bookkeeping_masked(c, B, L, T):
     assert np.all((z0 >= 0) & (z0 < V))
     z0b, _ = _loop_gpu(torch, cfg, buf, z1, T, osched.alphas(T), seed=workloads.seeds(c)["noise"])
     assert np.array_equal(z0, z0b)                                   # deterministic
+
+
+@pytest.mark.parametrize("noise", ["words", "philox"])
+def test_loop_uniform_reduced_config3_free_running_matches_oracle(noise):
+    """The uniform-prior loop (App. A.2) from a Gaussian-latent start (App. A.5) in fp32 on a reduced
+    workload-3 model (2 layers, d 64, V 1000 in four groups, the last one ragged): every step's
+    state against the oracle's free-running loop on the same noise (explicit words or Philox), ids
+    by the gap rule, and z_0 identical."""
+    torch = torch_or_skip()
+    cfg = workloads.model_cfg(3, dtype="fp32", n_layers=2, d_model=64, n_heads=2, d_mlp=256,
+                              vocab=1000, max_len=64)
+    s = workloads.seeds(3)
+    B, L, V, T = 2, 48, cfg["vocab"], 6
+    say("uniform loop, reduced workload 3", B, L, V, T, noise)
+    P, buf = _params_seeded(torch, cfg, s["param"])
+    x = workloads.clean_tokens(s["data"], B, L, V)
+    z1d = torch.empty(B * L, dtype=torch.int32, device="cuda")
+    dd.gaussian_latent_argmax(dev_i32(torch, x), B * L, V, 0.0, 1.0, seed=s["noise"], step=0, z_out=z1d)
+    z1 = z1d.cpu().numpy().reshape(B, L)
+    assert np.array_equal(z1.reshape(-1), olatent.latent_argmax(x.reshape(-1), V, 0.0, 1.0, s["noise"], 0))
+    al = osched.alphas(T)
+    if noise == "words":
+        words = workloads.noise_words(s["noise"] + 2, (T, B * L, osampler.noise_width("uniform", V)))
+        z0, trace = _loop_gpu(torch, cfg, buf, z1, T, al, words=words)
+        rz0, rtrace, gaps = oloop.sample_loop(cfg, P, z1, T, al, noise_words=words)
+    else:
+        z0, trace = _loop_gpu(torch, cfg, buf, z1, T, al, seed=s["noise"])
+        rz0, rtrace, gaps = oloop.sample_loop(cfg, P, z1, T, al, noise_seed=s["noise"])
+    changed = float(np.mean(trace[-1] != trace[0]))
+    say(f"uniform loop: min gap {np.min(gaps):.3e}; agreement {np.mean(trace == rtrace):.6f}; "
+        f"changed since z_1 {changed:.3f}")
+    for k in range(T):
+        compare_ids(trace[k + 1].reshape(-1), rtrace[k + 1].reshape(-1), gaps[k], f"step {T - k}")
+    assert np.array_equal(z0, rz0)
+    assert changed > 0.5
 
 
 def test_loop_uniform_prior_runs_in_range():

@@ -181,3 +181,18 @@ def test_lora_pins_catch_gate_on_the_wrong_positions(monkeypatch):
     monkeypatch.setattr(forward, "projection", lambda cfg, P, l, name, a, gate: orig(cfg, P, l, name, a, gate[::-1]))
     with pytest.raises(AssertionError):
         t.test_teacher_logits_from_one_pass_over_x_and_z()
+
+
+def test_exact_pin_catches_reversed_inverse_cdf(monkeypatch):
+    """An inverse CDF that scans the group from its last class has the same distribution (chi-square
+    cannot see it) but a different map from the uniform to the class: the exact-rational pin fails."""
+    from tests.test_oracle_sampler import check_inverse_cdf_against_exact
+    orig = sampler.inverse_cdf
+
+    def reversed_cdf(w, word):
+        w = np.asarray(w, dtype=np.float64)
+        j, gap = orig(w[::-1], word)
+        return len(w) - 1 - j, gap
+    monkeypatch.setattr(sampler, "inverse_cdf", reversed_cdf)
+    assert check_inverse_cdf_against_exact(n=500) > 50
+

@@ -241,3 +241,111 @@ def test_psi_loop_bookkeeping_masked_config1():
         changed = a != b
         # a change is either mask -> token or token -> mask
         assert np.all((a[changed] == V) ^ (b[changed] == V))
+
+
+# ---------------------------------------------------------------- level 2' (inverse CDF in the group)
+
+def inverse_cdf_exact(w, word):
+    """The class u * sum(w) falls in, in exact rational arithmetic (u = (word + 1/2) 2^-32): the
+    first j with w_0 + .. + w_j > u * sum(w).  Integer weights only."""
+    from fractions import Fraction
+    S = sum(int(x) for x in w)
+    t = Fraction(2 * int(word) + 1, 2 ** 33) * S
+    c = 0
+    for j, x in enumerate(w):
+        c += int(x)
+        if c > t:
+            return j
+    raise AssertionError("u < 1 always falls inside")
+
+
+def check_inverse_cdf_against_exact(n=3000, seed=7):
+    """Number of random integer-weight groups (with zero weights mixed in) on which
+    sampler.inverse_cdf disagrees with the exact rational answer (away from boundaries)."""
+    r = np.random.default_rng(seed)
+    bad = 0
+    for _ in range(n):
+        k = int(r.integers(1, 12))
+        w = r.integers(0, 6, size=k)
+        if w.sum() == 0:
+            w[int(r.integers(0, k))] = 1
+        word = int(r.integers(0, 2 ** 32))
+        j, gap = sampler.inverse_cdf(w.astype(float), word)
+        if gap > 1e-12 and j != inverse_cdf_exact(w, word):
+            bad += 1
+    return bad
+
+
+def test_inverse_cdf_equals_exact_rational_answer():
+    assert check_inverse_cdf_against_exact() == 0
+    # fixed cases: u just below 1/2 and just above, on weights (1, 1, 2); a zero weight is skipped
+    assert sampler.inverse_cdf([1.0, 1.0, 2.0], 2 ** 31 - 1)[0] == 1
+    assert sampler.inverse_cdf([1.0, 1.0, 2.0], 2 ** 31)[0] == 2
+    assert sampler.inverse_cdf([0.0, 3.0, 0.0, 1.0], 0)[0] == 1
+    assert sampler.inverse_cdf([0.0, 3.0, 0.0, 1.0], 2 ** 32 - 1)[0] == 3
+
+
+def draw_many_cdf(prior, p, n, seed=13):
+    out = np.empty(n, dtype=np.int64)
+    for i in range(n):
+        out[i] = sampler.sample_from_probs_cdf(prior, p, 3, sampler.PhiloxNoise(seed, i))[0]
+    return out
+
+
+@pytest.mark.parametrize("prior", ["mask", "uniform"])
+def test_inverse_cdf_draws_match_posterior_chi2(prior):
+    V = 600                                    # three real groups (256, 256, 88)
+    p = _peaked_probs(prior, V, 3)
+    z = draw_many_cdf(prior, p, 20000)
+    counts = np.bincount(z, minlength=p.shape[0])
+    assert chi2_pvalue(counts, p) > 1e-3
+    gb = sampler.group_bounds(prior, V)
+    gc = np.array([counts[a:b].sum() for a, b in gb])
+    gp = np.array([p[a:b].sum() for a, b in gb])
+    assert chi2_pvalue(gc, gp) > 1e-3
+
+
+def test_inverse_cdf_and_gumbel_draws_pick_the_same_group():
+    """Level 1 is shared: on the same noise both readings choose the same group every time."""
+    V = 700
+    p = _peaked_probs("mask", V, 4)
+    bounds = sampler.group_bounds("mask", V)
+    grp = lambda z: next(i for i, (a, b) in enumerate(bounds) if a <= z < b)
+    for i in range(400):
+        nz = sampler.PhiloxNoise(21, i)
+        a = sampler.sample_from_probs("mask", p, 5, nz)[0]
+        b = sampler.sample_from_probs_cdf("mask", p, 5, nz)[0]
+        assert grp(a) == grp(b)
+
+
+def test_group_candidates_follow_the_group_softmax_chi2():
+    """Each group's candidate, over many rows (independent uniforms), is distributed as the
+    softmax of the group's logits; the last group is ragged."""
+    V = 300
+    l = 2.0 * np.random.default_rng(8).standard_normal(V)
+    n = 12000
+    cands = np.array([sampler.group_candidates(l, row, sampler.PhiloxNoise(17, 2), V)[0] for row in range(n)])
+    for g, (a, b) in enumerate(sampler.group_bounds("uniform", V)):
+        w = np.exp(l[a:b] - l[a:b].max())
+        counts = np.bincount(cands[:, g] - a, minlength=b - a)
+        assert chi2_pvalue(counts, w / w.sum()) > 1e-3
+
+
+def test_posterior_sample_cdf_masked_rows_and_carry_over():
+    """posterior_sample with level 2': unmasked rows carried over, masked rows drawn inside the
+    group level 1 picks, the draw equal to sample_from_probs_cdf on the row's posterior."""
+    V, R = 520, 40
+    r = np.random.default_rng(9)
+    logits = r.standard_normal((R, V)) * 2
+    z_t = np.where(r.random(R) < 0.6, V, r.integers(0, V, R))
+    nz = sampler.PhiloxNoise(33, 4)
+    zs, gaps = sampler.posterior_sample("mask", logits, z_t, 0.3, 0.6, nz, level2="cdf")
+    for i in range(R):
+        if z_t[i] != V:
+            assert zs[i] == z_t[i]
+            continue
+        x = np.exp(logits[i] - logits[i].max())
+        p = posterior.posterior("mask", x / x.sum(), V, 0.3, 0.6)
+        assert zs[i] == sampler.sample_from_probs_cdf("mask", p, i, nz)[0]
+    with pytest.raises(ValueError):
+        sampler.posterior_sample("mask", logits, z_t, 0.3, 0.6, nz, level2="flat")
