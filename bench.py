@@ -309,6 +309,8 @@ def main():
     ap.add_argument("--lora-rank", type=int, default=0)
     ap.add_argument("--lora-alpha", type=float, default=256.0)
     ap.add_argument("--gate", choices=["all", "half"], default="all")
+    ap.add_argument("--store-free", action="store_true",
+                    help="sampling loop with DD_LOOP_STORE_FREE (masked prior, bf16): no logits stored")
     ap.add_argument("--kernels", action="store_true",
                     help="time the verification and Gaussian-latent kernels (one JSON line each)")
     args = ap.parse_args()
@@ -355,7 +357,8 @@ def main():
             z.copy_(z0)
         else:   # z_1 = argmax of a pure-noise Gaussian latent (alpha_tilde = 0, sigma = 1)
             dd.gaussian_latent_argmax(z0, M, V, 0.0, 1.0, seed=s["noise"], step=0, z_out=z)
-        dd.sample_loop(cfg, params, B, L, T, alphas, z, ws, noise_seed=s["noise"], z_trace=trace)
+        dd.sample_loop(cfg, params, B, L, T, alphas, z, ws, noise_seed=s["noise"], z_trace=trace,
+                       store_free=args.store_free)
 
     # Masked prior on the bf16 path with d % 128 == 0: the loop projects only the still-masked rows,
     # so the first warm-up pass keeps the trajectory (the same in every pass: same inputs and noise)

@@ -164,13 +164,17 @@ size_t dd_loop_workspace_bytes(const dd_config* cfg, int32_t B, int32_t L);
  *   glse        fp32 [rows][glse_ld]: per-group log-sum-exps of each logits row
  *               (groups of DD_GUMBEL_GROUP classes) when the vocabulary
  *               projection wrote them (see dd_sample_loop), else unspecified.
+ *   cand        int32 [rows][glse_ld]: with DD_LOOP_STORE_FREE, each logits row's
+ *               per-group candidates (a class id, -1 for a group with no finite
+ *               logit); the region is the logits region, which that mode does not
+ *               otherwise write.
  *   row_lse     fp32 [B*L]: log-sum-exp over the V logits of every token row the
  *               step drew, in the fp32 arithmetic the draw uses; rows the step
  *               did not draw (carried over) are left as they were.
  * Returns DD_E_ARG for an invalid configuration or B, L <= 0.
  */
 typedef struct {
-    size_t err, logits, rows, count, glse, row_lse;
+    size_t err, logits, rows, count, glse, cand, row_lse;
     int64_t logits_ld, glse_ld;
 } dd_loop_ws_layout;
 dd_status dd_loop_workspace_layout(const dd_config* cfg, int32_t B, int32_t L, dd_loop_ws_layout* out);
@@ -353,6 +357,17 @@ dd_status dd_sample_loop(const dd_config* cfg, const void* params, int32_t B, in
 #define DD_LOOP_POSTERIOR_PASS 1u /* draw from the posterior's own pass over each logits row
                                      instead of the group log-sum-exps the vocabulary
                                      projection writes (same draws up to summation order) */
+#define DD_LOOP_STORE_FREE 2u     /* the store-free draw (masked prior, bf16, d_model % 128 == 0,
+                                     Philox noise only): no logits are written.  The vocabulary
+                                     projection's epilogue writes, per row and group of
+                                     DD_GUMBEL_GROUP classes, the group's log-sum-exp and its
+                                     candidate: the first class of the group whose running sum
+                                     of exp(logit) exceeds u times the group's sum, u the
+                                     uniform of the Philox word (g >> 2, row, step, 5), word
+                                     g & 3.  The draw then takes level 1 as always and the chosen
+                                     group's candidate as level 2: an exact draw from the same
+                                     posterior, with different noise at level 2 (one uniform per
+                                     group instead of one Gumbel per class) */
 
 /*
  * dd_psi_sample_loop - dd_sample_loop with the Psi transition (App. A.4,
@@ -360,7 +375,9 @@ dd_status dd_sample_loop(const dd_config* cfg, const void* params, int32_t B, in
  * kappa = kappas[k].
  *   kappas       NULL (every kappa 1: exactly dd_sample_loop) or host double
  *                [T + 1], each used entry (k = 1..T) in [0, 1].
- *   flags        0 or DD_LOOP_POSTERIOR_PASS (other bits: DD_E_ARG).
+ *   flags        0, DD_LOOP_POSTERIOR_PASS or DD_LOOP_STORE_FREE (both together or
+ *                other bits: DD_E_ARG; DD_LOOP_STORE_FREE outside its conditions or
+ *                with noise_words: DD_E_UNSUPPORTED).
  * With kappa < 1 decoded tokens can be remasked and T may exceed the number of
  * positions (inference-time scaling, Sec. 4); a step with alpha_s = 1 (the
  * last one) still unmasks every position.  Masked prior (bf16): the rows

@@ -24,6 +24,7 @@ DD_DEVERR_TOKEN = 1
 DD_DEVERR_MASK = 2
 DD_DEVERR_LOGITS = 4
 DD_LOOP_POSTERIOR_PASS = 1
+DD_LOOP_STORE_FREE = 2
 ATTN_PATTERNS = {"bidirectional": 0, "causal": 1, "block_causal": 2, "draft_train": 3}
 STATUS = {0: "DD_OK", 1: "DD_E_ARG", 2: "DD_E_SHAPE", 3: "DD_E_DTYPE", 4: "DD_E_WORKSPACE",
           5: "DD_E_HIP", 6: "DD_E_UNSUPPORTED", 7: "DD_E_DEVICE"}
@@ -52,7 +53,8 @@ class DDConfig(ctypes.Structure):
 
 class DDLoopWsLayout(ctypes.Structure):
     _fields_ = [("err", ctypes.c_size_t), ("logits", ctypes.c_size_t), ("rows", ctypes.c_size_t),
-                ("count", ctypes.c_size_t), ("glse", ctypes.c_size_t), ("row_lse", ctypes.c_size_t),
+                ("count", ctypes.c_size_t), ("glse", ctypes.c_size_t), ("cand", ctypes.c_size_t),
+                ("row_lse", ctypes.c_size_t),
                 ("logits_ld", ctypes.c_int64), ("glse_ld", ctypes.c_int64)]
 
 
@@ -344,9 +346,9 @@ def psi_posterior_sample(prior, logits, logits_dtype, ld, rows, V, z_t, alpha_t,
 
 
 def sample_loop(cfg, params, B, L, T, alphas, z, ws, noise_words=None, noise_seed=0, z_trace=None,
-                kappas=None, posterior_pass=False):
-    """dd_sample_loop, or dd_psi_sample_loop when kappas (T + 1 values) is given or posterior_pass
-    (DD_LOOP_POSTERIOR_PASS) is set."""
+                kappas=None, posterior_pass=False, store_free=False):
+    """dd_sample_loop, or dd_psi_sample_loop when kappas (T + 1 values) is given or a flag is set:
+    posterior_pass (DD_LOOP_POSTERIOR_PASS), store_free (DD_LOOP_STORE_FREE)."""
     torch = _torch()
     M = B * L
     a = np.ascontiguousarray(alphas, dtype=np.float64)
@@ -360,7 +362,7 @@ def sample_loop(cfg, params, B, L, T, alphas, z, ws, noise_words=None, noise_see
             int(noise_seed) & 0xFFFFFFFFFFFFFFFF,
             _ptr(z_trace, 4 * (T + 1) * M, "z_trace", torch.int32) if z_trace is not None else None,
             _ptr(ws, loop_workspace_bytes(cfg, B, L), "ws"), ws.numel() * ws.element_size(), _stream())
-    if kappas is None and not posterior_pass:
+    if kappas is None and not posterior_pass and not store_free:
         _check(lib().dd_sample_loop(*head, *tail))
     else:
         k = None
@@ -368,7 +370,7 @@ def sample_loop(cfg, params, B, L, T, alphas, z, ws, noise_words=None, noise_see
             k = np.ascontiguousarray(kappas, dtype=np.float64)
             if k.shape != (T + 1,):
                 raise ValueError("kappas must hold T + 1 values")
-        flags = DD_LOOP_POSTERIOR_PASS if posterior_pass else 0
+        flags = (DD_LOOP_POSTERIOR_PASS if posterior_pass else 0) | (DD_LOOP_STORE_FREE if store_free else 0)
         _check(lib().dd_psi_sample_loop(*head, k.ctypes.data_as(dp) if k is not None else None, flags, *tail))
 
 

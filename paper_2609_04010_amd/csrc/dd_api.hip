@@ -224,7 +224,9 @@ static dd_status run_forward(const dd_config* c, const void* params, const int32
                              hipStream_t s, const int32_t* vocab_rows = nullptr,
                              const int32_t* vocab_count = nullptr,
                              const int32_t* attn_mask = nullptr, const int32_t* lora_gate = nullptr,
-                             float* vocab_lse = nullptr, int64_t lse_ld = 0) {
+                             float* vocab_lse = nullptr, int64_t lse_ld = 0,
+                             int32_t* vocab_cand = nullptr, uint64_t cand_seed = 0,
+                             uint32_t cand_step = 0) {
     const std::vector<Tensor> T = tensor_list(c);
     const WsLayout w = ws_layout(c, (int64_t)B * L);
     const char* P = (const char*)params;
@@ -283,7 +285,12 @@ static dd_status run_forward(const dd_config* c, const void* params, const int32
     GemmArgs g = {xln, dr, tp(lnf + 2), d, nullptr, logits, ld, (int)M, V, d, vocab_rows, vocab_count};
     g.lse = vocab_lse;
     g.lse_ld = lse_ld;
-    DD_TRY(launch_gemm(dt, vocab_lse ? EPI_LSE : EPI_PLAIN, KC_GEMM_VOCAB, g, s));
+    g.cand = vocab_cand;
+    g.cand_ld = lse_ld;
+    g.seed = cand_seed;
+    g.step = cand_step;
+    g.row0 = 0;
+    DD_TRY(launch_gemm(dt, vocab_cand ? EPI_LSE_CDF : vocab_lse ? EPI_LSE : EPI_PLAIN, KC_GEMM_VOCAB, g, s));
     (void)es;
     return DD_OK;
 }
@@ -558,6 +565,7 @@ dd_status dd_loop_workspace_layout(const dd_config* cfg, int32_t B, int32_t L, d
     out->rows = w.rows;
     out->count = w.count;
     out->glse = w.glse;
+    out->cand = w.logits;
     out->row_lse = w.row_lse;
     out->logits_ld = dd_logits_ld(cfg->vocab);
     out->glse_ld = w.glse_ld;
@@ -569,7 +577,15 @@ dd_status dd_psi_sample_loop(const dd_config* cfg, const void* params, int32_t B
                              int32_t* z, const uint32_t* noise_words, uint64_t noise_seed,
                              int32_t* z_trace, void* ws, size_t ws_bytes, void* stream) {
     DD_TRY(cfg_check(cfg));
-    DD_CHECK((flags & ~DD_LOOP_POSTERIOR_PASS) == 0, DD_E_ARG, "unknown loop flags 0x%x", flags);
+    DD_CHECK((flags & ~(DD_LOOP_POSTERIOR_PASS | DD_LOOP_STORE_FREE)) == 0, DD_E_ARG, "unknown loop flags 0x%x",
+             flags);
+    const bool store_free = (flags & DD_LOOP_STORE_FREE) != 0;
+    DD_CHECK(!store_free || !(flags & DD_LOOP_POSTERIOR_PASS), DD_E_ARG,
+             "DD_LOOP_STORE_FREE and DD_LOOP_POSTERIOR_PASS exclude each other");
+    DD_CHECK(!store_free || (cfg->prior == DD_PRIOR_MASK && gemm_lse_supported(cfg->dtype, cfg->d_model) &&
+                             gemm_gather_supported(cfg->dtype, cfg->d_model)),
+             DD_E_UNSUPPORTED, "DD_LOOP_STORE_FREE needs the masked prior, bf16 and d_model %% 128 == 0");
+    DD_CHECK(!store_free || !noise_words, DD_E_UNSUPPORTED, "DD_LOOP_STORE_FREE draws Philox noise only");
     DD_CHECK(params && z && ws && alphas, DD_E_ARG, "NULL pointer argument");
     DD_CHECK(B > 0 && L > 0 && T > 0, DD_E_ARG, "B, L and T must be positive");
     DD_CHECK(L <= cfg->max_len, DD_E_SHAPE, "L = %d exceeds max_len = %d", L, cfg->max_len);
@@ -610,6 +626,8 @@ dd_status dd_psi_sample_loop(const dd_config* cfg, const void* params, int32_t B
     // the posterior's own pass over the rows instead.
     const bool fused = gemm_lse_supported(cfg->dtype, cfg->d_model) && !(flags & DD_LOOP_POSTERIOR_PASS);
     float* glse = fused ? (float*)(wsc + w.glse) : nullptr;
+    // store-free: the logits region holds the group candidates [rows][glse_ld] int32 instead
+    int32_t* cand = store_free ? (int32_t*)logits : nullptr;
     if (!compact) {   // the layout query reports count = -1 for a loop that does not compact
         hipLaunchKernelGGL(fill_i32_kernel, dim3(1), dim3(64), 0, s, count, -1, (int64_t)1);
         DD_TRY(launch_status("loop count"));
@@ -619,7 +637,7 @@ dd_status dd_psi_sample_loop(const dd_config* cfg, const void* params, int32_t B
         if (compact) DD_TRY(launch_compact(z, M, cfg->mask_id, rows, count, s));
         DD_TRY(run_forward(cfg, params, z, B, L, alphas[k], logits, ld, wsc, s,
                            compact ? rows : nullptr, compact ? count : nullptr, nullptr, nullptr,
-                           glse, w.glse_ld));
+                           glse, w.glse_ld, cand, noise_seed, (uint32_t)k));
         const uint32_t* nw = noise_words ? noise_words + (int64_t)(k - 1) * M * nu : nullptr;
         PostArgs a = make_post(cfg->prior, logits, ld, (int32_t)M, cfg->vocab, z, alphas[k],
                                alphas[k - 1], kappas ? kappas[k] : 1.0, nw, noise_seed, (uint32_t)k,
@@ -633,6 +651,8 @@ dd_status dd_psi_sample_loop(const dd_config* cfg, const void* params, int32_t B
         }
         a.glse = glse;
         a.glse_ld = w.glse_ld;
+        a.cand = cand;
+        a.cand_ld = w.glse_ld;
         DD_TRY(launch_posterior(a, cfg->dtype, s));
         DD_TRY(trace_copy(T - k + 1));
     }

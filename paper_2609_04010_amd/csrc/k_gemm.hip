@@ -27,6 +27,7 @@
 #include <type_traits>
 
 #include "kernels.h"
+#include "rng.h"
 
 namespace dd {
 
@@ -262,7 +263,8 @@ template <int TBN_, int WGM_, int WGN_, int DM_ = DM> struct DLShape {
 // LDS of the direct-to-LDS kernel: the shape's stages and staging, plus for EPI_LSE the (max, sum)
 // partials of each tile row from each of the WGN wavefronts across it
 template <int EPI, class S> constexpr size_t dl_lds_bytes() {
-    return S::LDS + (EPI == EPI_LSE ? (size_t)S::DM * S::WGN * sizeof(float2) : 0);
+    return S::LDS + (EPI == EPI_LSE || EPI == EPI_LSE_CDF ? (size_t)S::DM * S::WGN * sizeof(float2) : 0) +
+           (EPI == EPI_LSE_CDF ? (size_t)S::DM * sizeof(float2) : 0);
 }
 
 typedef __attribute__((address_space(3))) void lds_void;
@@ -277,7 +279,8 @@ __global__ __launch_bounds__(64 * WGM_ * WGN_, 1) void gemm_bf16_dl_kernel(GemmA
     using S = DLShape<TBN_, WGM_, WGN_, DM_>;
     constexpr int DM = S::DM;
     constexpr int MB = S::MB, NB = S::NB, NA = S::ALOADS, NWL = S::WLOADS;
-    constexpr int TILE_GM = (EPI == EPI_PLAIN || EPI == EPI_LSE) ? 8 : DD_GEMM_GM_BODY;
+    constexpr bool GROUP_EPI = EPI == EPI_LSE || EPI == EPI_LSE_CDF;
+    constexpr int TILE_GM = (EPI == EPI_PLAIN || GROUP_EPI) ? 8 : DD_GEMM_GM_BODY;
     constexpr int AROWS = DM / S::NW, WROWS = S::TBN / S::NW;   // operand rows each wave loads
     extern __shared__ __attribute__((aligned(1024))) bf16_t smem[];
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -310,7 +313,7 @@ __global__ __launch_bounds__(64 * WGM_ * WGN_, 1) void gemm_bf16_dl_kernel(GemmA
         map_tile<TILE_GM>(tile, nblocks, tiles_m, tiles_n, tm, tn);
         m0 = tm * DM;
         n0 = tn * S::TBN;
-        if constexpr (EPI == EPI_PLAIN || EPI == EPI_LSE) skew = ((tm & 7) + 2 * tn) % nk;
+        if constexpr (EPI == EPI_PLAIN || GROUP_EPI) skew = ((tm & 7) + 2 * tn) % nk;
 #pragma unroll
         for (int i = 0; i < NA; ++i) {
             const int rl = AROWS * wave + 8 * i + (lane >> 3);
@@ -427,7 +430,7 @@ __global__ __launch_bounds__(64 * WGM_ * WGN_, 1) void gemm_bf16_dl_kernel(GemmA
     auto bias4 = [&](int nb, int j4, float* b4) {
         uint2 r = make_uint2(0u, 0u);
         if constexpr (PREFETCH_BIAS) r = braw[nb][j4];
-        else if constexpr (EPI != EPI_PLAIN && EPI != EPI_GATE && EPI != EPI_LSE) r = load_bias4(nb, j4);
+        else if constexpr (EPI != EPI_PLAIN && EPI != EPI_GATE && !GROUP_EPI) r = load_bias4(nb, j4);
         b4[0] = bf16_lo(r.x); b4[1] = bf16_hi(r.x); b4[2] = bf16_lo(r.y); b4[3] = bf16_hi(r.y);
     };
 
@@ -497,6 +500,7 @@ __global__ __launch_bounds__(64 * WGM_ * WGN_, 1) void gemm_bf16_dl_kernel(GemmA
             }
 #pragma unroll
             for (int half = 0; half < 2; ++half) {
+                if constexpr (EPI == EPI_LSE_CDF) break;   // the store-free draw keeps no logits
 #pragma unroll
                 for (int nb = 0; nb < NB; ++nb)
 #pragma unroll
@@ -536,7 +540,7 @@ __global__ __launch_bounds__(64 * WGM_ * WGN_, 1) void gemm_bf16_dl_kernel(GemmA
                     }
                 }
             }
-            if constexpr (EPI == EPI_LSE) {
+            if constexpr (GROUP_EPI) {
                 // Log-sum-exp of each tile row over the tile's 256 columns (one sampling group), taken
                 // over the rounded values just stored.  Rounding is monotonic, so the row maximum is
                 // the rounded maximum of the accumulators.  A wave covers 64 columns of a row (lanes
@@ -545,6 +549,15 @@ __global__ __launch_bounds__(64 * WGM_ * WGN_, 1) void gemm_bf16_dl_kernel(GemmA
                 static_assert(S::TBN == DD_GUMBEL_GROUP, "one tile column = one sampling group");
                 float2* part = (float2*)((char*)smem + S::LDS);
                 const int nl0 = ncol0 + 4 * (lane >> 5);
+                // store-free draw: the chunk sums of every tile row, [DM][CHK_LD] floats with chunk
+                // c of row r at slot c ^ (r & 31), so that 32 rows written (or scanned) at once hit
+                // 32 banks, in operand stage 1: the last K-tile read it and the next tile's first
+                // K-tile loads go to stage 0
+                constexpr int CHK_LD = S::TBN / 4;
+                static_assert(EPI != EPI_LSE_CDF || (CHK_LD == 64 && (size_t)S::DM * CHK_LD * sizeof(float) <=
+                                                                      S::STAGE * sizeof(bf16_t)),
+                              "chunk sums fit in one operand stage");
+                float* chk = (float*)(smem + S::STAGE);
                 auto rows_partial = [&](auto ragged_c) {
                     constexpr bool ragged = decltype(ragged_c)::value;
 #pragma unroll
@@ -561,17 +574,25 @@ __global__ __launch_bounds__(64 * WGM_ * WGN_, 1) void gemm_bf16_dl_kernel(GemmA
                         mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
                         const float mr = bf16_to_f32(f32_to_bf16(mx));
                         const float moff = (mr == -INFINITY ? 0.f : mr) * -LOG2E_F;
+                        // sums over chunks of 4 consecutive classes first (lanes l and l ^ 32 hold
+                        // alternate chunks); the store-free draw keeps them in LDS for its scan
                         float sum = 0.f;
 #pragma unroll
                         for (int nb = 0; nb < NB; ++nb)
 #pragma unroll
-                            for (int j4 = 0; j4 < 4; ++j4)
+                            for (int j4 = 0; j4 < 4; ++j4) {
+                                float cs = 0.f;
 #pragma unroll
                                 for (int e = 0; e < 4; ++e) {
                                     float v = round_bf16(acc[nb][mb][4 * j4 + e]);
                                     if (ragged && nl0 + nb * 32 + 8 * j4 + e >= g.N) v = -INFINITY;
-                                    sum += __builtin_amdgcn_exp2f(fmaf(v, LOG2E_F, moff));
+                                    cs += __builtin_amdgcn_exp2f(fmaf(v, LOG2E_F, moff));
                                 }
+                                if constexpr (EPI == EPI_LSE_CDF)
+                                    chk[(wm * S::WM + mb * 32 + (lane & 31)) * CHK_LD +
+                                        ((wn * 16 + nb * 8 + 2 * j4 + (lane >> 5)) ^ (lane & 31))] = cs;
+                                sum += cs;
+                            }
                         sum += __shfl_xor(sum, 32, 64);
                         if (lane < 32) part[(wm * S::WM + mb * 32 + lane) * S::WGN + wn] = make_float2(mr, sum);
                     }
@@ -579,6 +600,10 @@ __global__ __launch_bounds__(64 * WGM_ * WGN_, 1) void gemm_bf16_dl_kernel(GemmA
                 if (n0 + S::TBN <= g.N) rows_partial(std::false_type{});
                 else rows_partial(std::true_type{});
                 __syncthreads();
+                // store-free draw: per tile row, the wave whose 64 columns hold the crossing of the
+                // running sum and the remaining target in that wave's own reference (wave -1: none)
+                float2* sel = part + DM * S::WGN;
+                const int grp = n0 / DD_GUMBEL_GROUP;
                 if (tid < DM && tm0 + tid < M) {
                     float2 p[S::WGN];
                     float mm = -INFINITY;
@@ -591,7 +616,92 @@ __global__ __launch_bounds__(64 * WGM_ * WGN_, 1) void gemm_bf16_dl_kernel(GemmA
                     float sum = 0.f;
 #pragma unroll
                     for (int w = 0; w < S::WGN; ++w) sum += p[w].y * exp2f((p[w].x - mref) * LOG2E_F);
-                    g.lse[(int64_t)(tm0 + tid) * g.lse_ld + n0 / DD_GUMBEL_GROUP] = mref + logf(sum);
+                    g.lse[(int64_t)(tm0 + tid) * g.lse_ld + grp] = mref + logf(sum);
+                    if constexpr (EPI == EPI_LSE_CDF) {
+                        // the row's target t = u S; the wave sums (scaled to the common reference)
+                        // in class order give the crossing wave, a scan of that wave's 16 chunk
+                        // sums the crossing chunk and the remaining target in the wave's reference
+                        const int m = tm0 + tid;
+                        const uint32_t grow = g.row0 + (uint32_t)(g.a_rows ? g.a_rows[m] : m);
+                        const uint32_t word = counter_word(g.seed, STREAM_GROUP_U, g.step, grow, (uint32_t)grp);
+                        const float t = (float)(((double)word + 0.5) * 0x1p-32 * (double)sum);
+                        const float* crow = chk + tid * CHK_LD;
+                        // the crossing wave from the wave sums, then its 16 chunks
+                        float cum = 0.f, tw = 0.f;
+                        int wsel = -1, wlast = -1;
+#pragma unroll
+                        for (int w = 0; w < S::WGN; ++w) {
+                            const float add = p[w].y * exp2f((p[w].x - mref) * LOG2E_F);
+                            if (add > 0.f) wlast = w;
+                            if (wsel < 0 && cum + add > t) {
+                                wsel = w;
+                                tw = (t - cum) / exp2f((p[w].x - mref) * LOG2E_F);
+                            }
+                            cum += add;
+                        }
+                        if (wsel < 0) {          // rounding left no crossing: the last wave with mass
+                            wsel = wlast;
+                            tw = INFINITY;
+                        }
+                        float tres = 0.f;
+                        int csel = -1, clast = -1;
+                        if (wsel >= 0) {
+                            float cc = 0.f;
+#pragma unroll 4
+                            for (int c = 0; c < 16; ++c) {
+                                const float cw = crow[(wsel * 16 + c) ^ (tid & 31)];
+                                if (cw > 0.f) clast = wsel * 16 + c;
+                                if (csel < 0 && cc + cw > tw) {
+                                    csel = wsel * 16 + c;
+                                    tres = tw - cc;
+                                }
+                                cc += cw;
+                            }
+                            if (csel < 0) {      // the wave's scan fell short of its sum: its last chunk
+                                csel = clast;
+                                tres = INFINITY;
+                            }
+                        }
+                        sel[tid] = make_float2(tres, __int_as_float(csel));
+                        if (csel < 0) g.cand[(int64_t)m * g.cand_ld + grp] = -1;   // no finite logit
+                    }
+                }
+                if constexpr (EPI == EPI_LSE_CDF) {
+                    // the lane holding the crossing chunk of a row scans its 4 classes, from its
+                    // accumulators and its wave's row maximum
+                    __syncthreads();
+                    const int myh = lane >> 5;
+#pragma unroll
+                    for (int mb = 0; mb < MB; ++mb) {
+                        const int rl = wm * S::WM + mb * 32 + (lane & 31);
+                        const float2 sl = sel[rl];
+                        const int c = __float_as_int(sl.y);
+                        if (tm0 + rl >= M || c < 0 || (c >> 4) != wn || (c & 1) != myh) continue;
+                        const int q = (c & 15) >> 1;      // nb * 4 + j4
+                        float a4[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+                        for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+                            for (int j4 = 0; j4 < 4; ++j4)
+#pragma unroll
+                                for (int e = 0; e < 4; ++e)
+                                    a4[e] = (nb * 4 + j4 == q) ? acc[nb][mb][4 * j4 + e] : a4[e];
+                        const float mr = part[rl * S::WGN + wn].x;
+                        const float moff = (mr == -INFINITY ? 0.f : mr) * -LOG2E_F;
+                        const int n0c = nl0 + 32 * (q >> 2) + 8 * (q & 3);   // class of a4[0]
+                        int ce = -1, le = -1;
+                        float c2 = 0.f;
+#pragma unroll
+                        for (int e = 0; e < 4; ++e) {
+                            const float v = n0c + e < g.N ? round_bf16(a4[e]) : -INFINITY;
+                            const float x = __builtin_amdgcn_exp2f(fmaf(v, LOG2E_F, moff));
+                            if (x > 0.f) le = e;
+                            if (ce < 0 && c2 + x > sl.x) ce = e;
+                            c2 += x;
+                        }
+                        if (ce < 0) ce = le;
+                        g.cand[(int64_t)(tm0 + rl) * g.cand_ld + grp] = ce < 0 ? -1 : n0c + ce;
+                    }
                 }
             }
         }
@@ -822,8 +932,13 @@ dd_status launch_gemm(int dtype, int epi, int cls, const GemmArgs& g, hipStream_
         set_error("row-gathered GEMM needs the bf16 path and K %% 128 == 0");
         return DD_E_UNSUPPORTED;
     }
-    if (epi == EPI_LSE && (!gemm_lse_supported(dtype, g.K) || !g.lse || g.lse_ld < (g.N + 255) / 256)) {
+    if ((epi == EPI_LSE || epi == EPI_LSE_CDF) &&
+        (!gemm_lse_supported(dtype, g.K) || !g.lse || g.lse_ld < (g.N + 255) / 256)) {
         set_error("group log-sum-exp epilogue needs the bf16 path, K %% 128 == 0 and an lse buffer");
+        return DD_E_UNSUPPORTED;
+    }
+    if (epi == EPI_LSE_CDF && (!g.cand || g.cand_ld < (g.N + 255) / 256)) {
+        set_error("store-free draw epilogue needs a candidate buffer");
         return DD_E_UNSUPPORTED;
     }
     ProfScope ps(cls, s);
@@ -837,6 +952,7 @@ dd_status launch_gemm(int dtype, int epi, int cls, const GemmArgs& g, hipStream_
         case EPI_GATE: launch_epi<EPI_GATE, KC_GEMM_LORA>(dtype, g, s); break;
         // one tile column per sampling group: always the 256-wide, 8-wavefront tile
         case EPI_LSE: launch_dl<EPI_LSE, KC_GEMM_VOCAB, 256, 2, 4>(g, s); break;
+        case EPI_LSE_CDF: launch_dl<EPI_LSE_CDF, KC_GEMM_VOCAB, 256, 2, 4>(g, s); break;
         default: launch_epi<EPI_PLAIN, KC_GEMM_VOCAB>(dtype, g, s); break;
     }
     return launch_status("gemm");

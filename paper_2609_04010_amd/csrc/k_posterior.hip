@@ -99,8 +99,11 @@ DD_DEV int32_t keep_or_remask(const PostArgs& a, int row, int zt) {
 // at the chosen group and, uniform prior, at the current token zt).  Row log-sum-exp over the group
 // values, level 1 over the groups (4 per lane: one Philox block gives their 4 words) and level 2
 // over the 256 classes of the chosen group (4 per lane), all in fp32 with wavefront shuffles.
+// With cand (masked prior; the store-free draw) level 2 is the chosen group's candidate, computed
+// by the vocabulary projection's epilogue, and the logits are not read.
 template <typename T>
-DD_DEV void draw_row(const PostArgs& a, int row, int zt, const char* rowp, const float* glse, int lane) {
+DD_DEV void draw_row(const PostArgs& a, int row, int zt, const char* rowp, const float* glse, int lane,
+                     const int32_t* cand = nullptr) {
     const int V = a.V;
     const bool mask_prior = a.prior == DD_PRIOR_MASK;
     const int ngroups = (V + DD_GUMBEL_GROUP - 1) / DD_GUMBEL_GROUP;
@@ -167,6 +170,9 @@ DD_DEV void draw_row(const PostArgs& a, int row, int zt, const char* rowp, const
         // no group had a valid score (NaN or +inf logits, or no finite logit): the row keeps
         // its token and the caller is told; gstar must not index anything
         result = -1;
+    } else if (cand && !(mask_prior && gstar == ngroups)) {   // level 2 by the group's candidate
+        const int c = cand[gstar], lo = gstar * DD_GUMBEL_GROUP;
+        result = (c >= lo && c < min(V, lo + DD_GUMBEL_GROUP)) ? c : -1;
     } else if (!(mask_prior && gstar == ngroups)) {   // level 2 inside the chosen group
         best = -INFINITY;
         bi = 0x7FFFFFFF;
@@ -355,8 +361,9 @@ __global__ __launch_bounds__(256) void posterior_grouped_kernel(PostArgs a) {
     }
     int zt;
     if (!row_needs_draw(a, row, lane == 0, zt)) return;
-    const char* rowp = (const char*)a.logits + (size_t)j * (size_t)a.ld * sizeof(T);
-    draw_row<T>(a, row, zt, rowp, a.glse + (int64_t)j * a.glse_ld, lane);
+    const char* rowp = a.logits ? (const char*)a.logits + (size_t)j * (size_t)a.ld * sizeof(T) : nullptr;
+    draw_row<T>(a, row, zt, rowp, a.glse + (int64_t)j * a.glse_ld, lane,
+                a.cand ? a.cand + (int64_t)j * a.cand_ld : nullptr);
 }
 
 // Debug output: the full posterior row in float64 arithmetic (two passes over the logits).

@@ -33,6 +33,10 @@ struct PostArgs {
     // projection's EPI_LSE epilogue), or NULL: then the posterior kernel computes them itself
     const float* glse;
     int64_t glse_ld;
+    // with glse: each row's per-group level-2 candidates [rows][cand_ld] (EPI_LSE_CDF), or NULL: then
+    // level 2 reads the chosen group's logits (masked prior only)
+    const int32_t* cand;
+    int64_t cand_ld;
     // per token row drawn: the log-sum-exp of its V logits as the draw computes it (or NULL)
     float* row_lse;
 };
@@ -42,7 +46,13 @@ struct PostArgs {
 // EPI_LSE: plain bf16 store, and per row the log-sum-exp of each DD_GUMBEL_GROUP-column group of
 // the stored (rounded) values into lse[m * lse_ld + n / DD_GUMBEL_GROUP] (vocabulary projection
 // feeding the sampler; bf16, K % 128 == 0, 256-column tiles)
-enum Epi { EPI_BIAS = 0, EPI_BIAS_GELU = 1, EPI_BIAS_RESID = 2, EPI_PLAIN = 3, EPI_GATE = 4, EPI_LSE = 5 };
+// EPI_LSE_CDF: EPI_LSE without storing the logits; instead, per row and group, the group's
+// inverse-CDF candidate: the first class whose running sum of exp(l - ref) over the group exceeds
+// u times the group's sum, u the Philox uniform of word (group, row0 + token row, step,
+// STREAM_GROUP_U), into cand[m * cand_ld + n / DD_GUMBEL_GROUP] (the level 2 of the store-free
+// two-level draw)
+enum Epi { EPI_BIAS = 0, EPI_BIAS_GELU = 1, EPI_BIAS_RESID = 2, EPI_PLAIN = 3, EPI_GATE = 4, EPI_LSE = 5,
+           EPI_LSE_CDF = 6 };
 
 struct GemmArgs {
     const void* A;   // [M][K], row stride lda
@@ -60,9 +70,15 @@ struct GemmArgs {
     const int32_t* gate;
     int gate_period;
     float gate_scale;
-    // EPI_LSE only: group log-sum-exps [M][lse_ld]
+    // EPI_LSE / EPI_LSE_CDF: group log-sum-exps [M][lse_ld]
     float* lse;
     int64_t lse_ld;
+    // EPI_LSE_CDF only: group candidates [M][cand_ld]; the noise key and counters (the token row of
+    // output row m is a_rows[m] when gathered, else m)
+    int32_t* cand;
+    int64_t cand_ld;
+    uint64_t seed;
+    uint32_t step, row0;
 };
 
 struct AttnArgs {

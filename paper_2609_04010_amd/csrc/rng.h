@@ -17,7 +17,8 @@
 
 namespace dd {
 
-enum Stream : uint32_t { STREAM_TOP = 0, STREAM_CLASS = 1, STREAM_LATENT = 2, STREAM_PARAM = 3, STREAM_VERIFY = 4 };
+enum Stream : uint32_t { STREAM_TOP = 0, STREAM_CLASS = 1, STREAM_LATENT = 2, STREAM_PARAM = 3, STREAM_VERIFY = 4,
+                         STREAM_GROUP_U = 5 };
 
 struct Words4 {
     uint32_t w[4];

@@ -157,9 +157,17 @@ def test_loop_validation():
     assert dd.lib().dd_sample_loop(ctypes.byref(cfg), FAKE, 1, 16, 0, al, FAKE, None, 0, None, FAKE,
                                    1 << 40, None) == 1
     # unknown loop flags
-    assert dd.lib().dd_psi_sample_loop(ctypes.byref(cfg), FAKE, 1, 16, 2, al, None, 2, FAKE, None, 0, None,
-                                       FAKE, 1 << 40, None) == 1
+    psi = lambda c, flags, words=None: dd.lib().dd_psi_sample_loop(ctypes.byref(c), FAKE, 1, 16, 2, al, None, flags,
+                                                                   FAKE, words, 0, None, FAKE, 1 << 40, None)
+    assert psi(cfg, 4) == 1
     assert b"flags" in dd.lib().dd_last_error()
+    # the store-free draw: not with the posterior pass, the uniform prior, fp32 or explicit noise
+    assert psi(cfg, dd.DD_LOOP_STORE_FREE | dd.DD_LOOP_POSTERIOR_PASS) == 1
+    assert psi(_cfg_struct(prior="uniform", mask_id=-1), dd.DD_LOOP_STORE_FREE) == 6
+    assert dd.lib().dd_last_error().startswith(b"DD_LOOP_STORE_FREE needs the masked prior")
+    assert psi(dd.make_config(workloads.model_cfg(1)), dd.DD_LOOP_STORE_FREE) == 6
+    assert psi(cfg, dd.DD_LOOP_STORE_FREE, words=FAKE) == 6
+    assert dd.lib().dd_last_error() == b"DD_LOOP_STORE_FREE draws Philox noise only"
 
 
 def test_loop_workspace_layout():
@@ -176,6 +184,8 @@ def test_loop_workspace_layout():
         for (o1, n1), (o2, _) in zip(regions, regions[1:]):
             assert o1 % 256 == 0 and o1 + n1 <= o2
         assert regions[-1][0] + regions[-1][1] <= dd.loop_workspace_bytes(cfg, B, L)
+        # the store-free candidates live in the logits region and fit there
+        assert lay["cand"] == lay["logits"] and 4 * M * lay["glse_ld"] <= M * lay["logits_ld"] * es
     with pytest.raises(dd.DDError):
         dd.loop_workspace_layout(workloads.model_cfg(2), 0, 16)
 
