@@ -63,7 +63,7 @@ def _one_step(torch, cfg, buf, B, L, z0, at, as_, seed, kappa, store_free, check
     return z.cpu().numpy(), count, rows, logits, glse, cand
 
 
-def _check(torch, cfg, B, L, frac, at, as_, kappa, seed, cand_rows=None):
+def _check(torch, cfg, B, L, frac, at, as_, kappa, seed, cand_rows=None, id_rows=None):
     V = cfg["vocab"]
     buf = _params(torch, cfg, seed)
     z0 = workloads.masked_state(seed + 1, B, L, V, frac).reshape(-1)
@@ -86,13 +86,16 @@ def _check(torch, cfg, B, L, frac, at, as_, kappa, seed, cand_rows=None):
         assert bad.size == 0, f"row {j} (token {rb[j]}): candidates {cand[j][bad]} vs {ref[bad]} in groups {bad}"
         mism += int((cand[j] != ref).sum())
     say(f"  candidates: {sel.size} rows x {cand.shape[1]} groups, {clear} clear, {mism} differ (all near a boundary)")
-    # the ids: the oracle's inverse-CDF two-level draw on the same logits and counters
-    tok = rb
+    # the ids: the oracle's inverse-CDF two-level draw on the same logits and counters (on the
+    # logits rows id_rows only, if given)
+    js = np.arange(cb) if id_rows is None else id_rows
+    tok = rb[js]
     if kappa is None:
-        zs, gaps = osampler.posterior_sample("mask", G, z0[tok], at, as_, nz, rows=tok, level2="cdf")
+        zs, gaps = osampler.posterior_sample("mask", G[js], z0[tok], at, as_, nz, rows=tok, level2="cdf")
     else:
-        zs, gaps = osampler.psi_sample("mask", G, z0[tok], at, as_, kappa, nz, rows=tok, level2="cdf")
+        zs, gaps = osampler.psi_sample("mask", G[js], z0[tok], at, as_, kappa, nz, rows=tok, level2="cdf")
     compare_ids(zb[tok], zs, gaps, "  store-free ids")
+    tok = rb
     # rows not in the list: carried over (kappa None) or kept / remasked exactly as the default mode
     rest = np.setdiff1d(np.arange(B * L), tok)
     if kappa is None:
@@ -133,6 +136,23 @@ def test_store_free_step_full_size_workload2():
     T = w["T"]
     say("store-free step, workload 2 full size")
     _check(torch, cfg, w["B"], w["L"], 1.0, 0.0, 1.0 / T, None, workloads.seeds(2)["param"], cand_rows=512)
+
+
+def test_store_free_step_full_size_workload4():
+    """B 128 x L 1024 (131072 rows, the largest batch): a mid-schedule step from a state with a
+    quarter of the rows masked; ids checked on the last sequence's rows (the end of the compacted
+    list), candidates on 256 rows spread over the list."""
+    torch = torch_or_skip()
+    cfg = workloads.model_cfg(4)
+    w = workloads.WORKLOADS[4]
+    B, L = w["B"], w["L"]
+    say("store-free step, workload 4 full size")
+    seed = workloads.seeds(4)["param"]
+    z0 = workloads.masked_state(seed + 1, B, L, cfg["vocab"], 0.25).reshape(-1)
+    last = np.nonzero(z0[(B - 1) * L:] == cfg["vocab"])[0].size
+    count = int((z0 == cfg["vocab"]).sum())
+    _check(torch, cfg, B, L, 0.25, 0.7, 0.75, None, seed, cand_rows=256,
+           id_rows=np.arange(count - last, count))
 
 
 def test_store_free_loop_bookkeeping_and_determinism():
