@@ -386,10 +386,9 @@ def main():
             dominant = next(k for k, _ in ranked if algorithmic_units(k, cfg, B, L, vocab_rows)[0] is not None)
     assert dd.read_device_error(ws[:4].view(torch.int32)) == 0
 
-    # The dominant class is timed live with HIP events on the library's stream, over the first
-    # PROFILED_LAUNCHES of its launches in the timed region: each event pair adds a few microseconds
-    # of stream time around the launch it brackets (about 11 us per MLP-down launch, 2.7 % of a
-    # reverse step if every launch were bracketed), so the rest of the region runs without them.
+    # The dominant class is timed live with HIP events on the library's stream (recorded by the
+    # dispatch of each launch: hipExtLaunchKernel), over the first PROFILED_LAUNCHES of its
+    # launches in the timed region; the rest of the region runs with the profiler off.
     dd.profile_begin(PROFILED_LAUNCHES, classes=[dominant])
     torch.cuda.synchronize()
     t0 = time.perf_counter()

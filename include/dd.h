@@ -466,9 +466,10 @@ dd_status dd_gaussian_latent_argmax(const int32_t* x, int32_t rows, int32_t V,
 /* ---------------------------------------------------------------- profiling */
 
 /*
- * Per-launch timing with HIP events recorded on the launching stream.  While
- * enabled, every launch of a kernel class whose bit is set in `class_mask`
- * (bit c = class c; 0 selects every class) is bracketed by an event pair.  At
+ * Per-launch timing with HIP events on the launching stream.  While enabled,
+ * every launch of a kernel class whose bit is set in `class_mask` (bit c =
+ * class c; 0 selects every class) gets an event pair: a kernel's pair is
+ * recorded by its dispatch (hipExtLaunchKernel), a copy's around the copy.  At
  * most `max_launches` launches are recorded.  For benchmarks.  The recorder is
  * the library's only process-wide mutable state; it is guarded by a mutex, and
  * while it is off (the default) no launch touches it.

@@ -1,8 +1,11 @@
 // Shared device/host helpers of the gfx950 reverse-step library.
 #pragma once
 
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 #include <stdint.h>
+
+#include <tuple>
 
 #include "dd.h"
 
@@ -91,15 +94,38 @@ enum KernelClass {
     KC_GEMM_MLP2, KC_GEMM_VOCAB, KC_POSTERIOR, KC_LATENT, KC_INIT, KC_COPY, KC_COMPACT, KC_GEMM_LORA,
     KC_COUNT
 };
-void prof_start(int cls, hipStream_t s);
+// A scope around one kernel launch (kernel = true) hands its event pair to that launch (launch_k),
+// which records them as part of the dispatch (hipExtLaunchKernel): no marker packets of their own
+// between the kernels.  Other scopes (a copy) record the events around their work.
+void prof_start(int cls, hipStream_t s, bool kernel);
 void prof_stop(int cls, hipStream_t s);
+// the event pair a kernel-launch scope opened on this host thread (once; false if none)
+bool prof_take(hipEvent_t* start, hipEvent_t* stop);
 
 struct ProfScope {
     int cls;
     hipStream_t s;
-    ProfScope(int c, hipStream_t st) : cls(c), s(st) { prof_start(cls, s); }
+    ProfScope(int c, hipStream_t st, bool kernel = true) : cls(c), s(st) { prof_start(cls, s, kernel); }
     ~ProfScope() { prof_stop(cls, s); }
 };
+
+// Launch of kernel k with its arguments converted to the kernel's parameter types; with the event
+// pair of an enclosing profiling scope, through hipExtLaunchKernel.
+template <typename... KP, typename... A>
+inline void launch_k(void (*k)(KP...), dim3 grid, dim3 block, uint32_t shmem, hipStream_t s, A... a) {
+    static_assert(sizeof...(KP) == sizeof...(A), "argument count");
+    std::tuple<KP...> args(static_cast<KP>(a)...);
+    std::apply(
+        [&](auto&... x) {
+            void* argv[] = {(void*)&x..., nullptr};
+            hipEvent_t e0, e1;
+            if (prof_take(&e0, &e1))
+                (void)hipExtLaunchKernel((const void*)k, grid, block, argv, shmem, s, e0, e1, 0);
+            else
+                (void)hipLaunchKernel((const void*)k, grid, block, argv, shmem, s);
+        },
+        args);
+}
 
 inline int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 

@@ -63,29 +63,60 @@ struct Profiler {
     uint32_t mask = 0xFFFFFFFFu;
     std::vector<hipEvent_t> ev;   // 2 per launch
     std::vector<int> cls;         // class per launch
-    int open = -1;                // index of the launch whose start was recorded
+    int open = -1;                // index of the open sample
+    bool open_kernel = false;     // its events go with a kernel dispatch (else recorded around)
     int64_t dropped = 0;
 };
 static Profiler g_prof;
 static std::mutex g_prof_mu;
 
-void prof_start(int c, hipStream_t s) {
+// The event pair a kernel-launch scope opened and its launch has not taken yet (per host thread).
+static thread_local hipEvent_t t_pend[2] = {nullptr, nullptr};
+
+void prof_start(int c, hipStream_t s, bool kernel) {
     if (!g_prof.on.load(std::memory_order_relaxed)) return;
     std::lock_guard<std::mutex> lk(g_prof_mu);
     if (!g_prof.on || !((g_prof.mask >> c) & 1u)) return;
     const int n = (int)g_prof.cls.size();
     if (n >= g_prof.cap) { g_prof.dropped++; g_prof.open = -1; return; }
-    (void)hipEventRecord(g_prof.ev[2 * n], s);
+    if (kernel) {
+        t_pend[0] = g_prof.ev[2 * n];
+        t_pend[1] = g_prof.ev[2 * n + 1];
+    } else {
+        (void)hipEventRecord(g_prof.ev[2 * n], s);
+    }
     g_prof.cls.push_back(c);
     g_prof.open = n;
+    g_prof.open_kernel = kernel;
+}
+
+bool prof_take(hipEvent_t* start, hipEvent_t* stop) {
+    if (!t_pend[0]) return false;
+    *start = t_pend[0];
+    *stop = t_pend[1];
+    t_pend[0] = t_pend[1] = nullptr;
+    return true;
 }
 
 void prof_stop(int c, hipStream_t s) {
-    if (!g_prof.on.load(std::memory_order_relaxed)) return;
-    std::lock_guard<std::mutex> lk(g_prof_mu);
-    if (!g_prof.on || g_prof.open < 0) return;
-    (void)hipEventRecord(g_prof.ev[2 * g_prof.open + 1], s);
     (void)c;
+    if (!g_prof.on.load(std::memory_order_relaxed)) {
+        t_pend[0] = t_pend[1] = nullptr;
+        return;
+    }
+    std::lock_guard<std::mutex> lk(g_prof_mu);
+    if (!g_prof.on || g_prof.open < 0) {
+        t_pend[0] = t_pend[1] = nullptr;
+        return;
+    }
+    if (g_prof.open_kernel) {
+        if (t_pend[0]) {        // the scope launched nothing (an early return): no sample
+            t_pend[0] = t_pend[1] = nullptr;
+            g_prof.cls.pop_back();
+        }                       // else the dispatch recorded both events
+    } else {
+        (void)hipEventRecord(g_prof.ev[2 * g_prof.open + 1], s);
+    }
     g_prof.open = -1;
 }
 
@@ -421,7 +452,7 @@ int32_t dd_noise_width(int32_t prior, int32_t V) {
 
 dd_status dd_workspace_reset(void* ws, void* stream) {
     DD_CHECK(ws, DD_E_ARG, "workspace is NULL");
-    hipLaunchKernelGGL(fill_i32_kernel, dim3(1), dim3(64), 0, (hipStream_t)stream, (int32_t*)ws, 0,
+    launch_k(fill_i32_kernel, dim3(1), dim3(64), 0, (hipStream_t)stream, (int32_t*)ws, 0,
                        (int64_t)1);
     return launch_status("workspace_reset");
 }
@@ -608,7 +639,7 @@ dd_status dd_psi_sample_loop(const dd_config* cfg, const void* params, int32_t B
     const int32_t nu = dd_noise_width(cfg->prior, cfg->vocab);
     auto trace_copy = [&](int slot) -> dd_status {
         if (!z_trace) return DD_OK;
-        ProfScope ps(KC_COPY, s);
+        ProfScope ps(KC_COPY, s, false);
         const hipError_t e = hipMemcpyAsync(z_trace + (int64_t)slot * M, z, M * sizeof(int32_t),
                                             hipMemcpyDeviceToDevice, s);
         DD_CHECK(e == hipSuccess, DD_E_HIP, "trace copy: %s", hipGetErrorString(e));
@@ -629,7 +660,7 @@ dd_status dd_psi_sample_loop(const dd_config* cfg, const void* params, int32_t B
     // store-free: the logits region holds the group candidates [rows][glse_ld] int32 instead
     int32_t* cand = store_free ? (int32_t*)logits : nullptr;
     if (!compact) {   // the layout query reports count = -1 for a loop that does not compact
-        hipLaunchKernelGGL(fill_i32_kernel, dim3(1), dim3(64), 0, s, count, -1, (int64_t)1);
+        launch_k(fill_i32_kernel, dim3(1), dim3(64), 0, s, count, -1, (int64_t)1);
         DD_TRY(launch_status("loop count"));
     }
     DD_TRY(trace_copy(0));

@@ -420,14 +420,14 @@ dd_status launch_attn(int dtype, const AttnArgs& a0, hipStream_t s) {
     a.hgroup = std::max(1, (num_cus_attn() / 8) * 3 / nqb);
     if (dtype == DD_BF16) {
         const dim3 grid((unsigned)(nqb * a.H * a.B));
-        if (a.mask) hipLaunchKernelGGL(attn_bf16_kernel<true>, grid, dim3(256), 0, s, a);
-        else hipLaunchKernelGGL(attn_bf16_kernel<false>, grid, dim3(256), 0, s, a);
+        if (a.mask) launch_k(attn_bf16_kernel<true>, grid, dim3(256), 0, s, a);
+        else launch_k(attn_bf16_kernel<false>, grid, dim3(256), 0, s, a);
     } else {
         const int64_t n = (int64_t)a.B * a.H * a.L;
         const dim3 grid((unsigned)ceil_div(n, 128));
 #define DD_ATTN_F32(DV)                                                                         \
-    if (a.mask) hipLaunchKernelGGL((attn_f32_kernel<DV, true>), grid, dim3(128), 0, s, a);      \
-    else hipLaunchKernelGGL((attn_f32_kernel<DV, false>), grid, dim3(128), 0, s, a);
+    if (a.mask) launch_k((attn_f32_kernel<DV, true>), grid, dim3(128), 0, s, a);      \
+    else launch_k((attn_f32_kernel<DV, false>), grid, dim3(128), 0, s, a);
         switch (dh) {
             case 16: DD_ATTN_F32(16) break;
             case 32: DD_ATTN_F32(32) break;

@@ -840,7 +840,7 @@ static void launch_tile(const GemmArgs& g, hipStream_t s) {
                                   hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
         attr = true;
     }
-    hipLaunchKernelGGL((gemm_bf16_kernel<TBM, TBN, EPI>), dim3(tm * tn), dim3(256), lds, s, g, tm, tn);
+    launch_k((gemm_bf16_kernel<TBM, TBN, EPI>), dim3(tm * tn), dim3(256), lds, s, g, tm, tn);
 }
 
 // Tile choice for the direct-to-LDS kernel: the N width (256 or 192) with the smaller estimated time,
@@ -893,7 +893,7 @@ static void launch_dl(const GemmArgs& g, hipStream_t s) {
     }
     // persistent: at most WG_PER_CU workgroups per CU
     const int grid = (int)std::min<int64_t>((int64_t)tm * tn, (int64_t)num_cus() * S::WG_PER_CU);
-    hipLaunchKernelGGL((gemm_bf16_dl_kernel<EPI, ROLE, TBN, WGM, WGN, DMR>), dim3(grid), dim3(S::THREADS), lds,
+    launch_k((gemm_bf16_dl_kernel<EPI, ROLE, TBN, WGM, WGN, DMR>), dim3(grid), dim3(S::THREADS), lds,
                        s, g, tm, tn);
 }
 
@@ -915,7 +915,7 @@ static void launch_epi(int dtype, const GemmArgs& g, hipStream_t s) {
         }
     } else {
         const int tm = (g.M + FT - 1) / FT, tn = (g.N + FT - 1) / FT;
-        hipLaunchKernelGGL(gemm_f32_kernel<EPI>, dim3(tm * tn), dim3(256), 0, s, g, tm, tn);
+        launch_k(gemm_f32_kernel<EPI>, dim3(tm * tn), dim3(256), 0, s, g, tm, tn);
     }
 }
 

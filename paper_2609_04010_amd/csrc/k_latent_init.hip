@@ -67,7 +67,7 @@ dd_status launch_latent(const int32_t* x, int32_t rows, int32_t V, double at, do
                         hipStream_t s) {
     if (rows == 0) return DD_OK;
     ProfScope ps(KC_LATENT, s);
-    hipLaunchKernelGGL(latent_kernel, dim3(rows), dim3(256), 0, s, x, V, at, sigma, seed, step, row0,
+    launch_k(latent_kernel, dim3(rows), dim3(256), 0, s, x, V, at, sigma, seed, step, row0,
                        z, err);
     return launch_status("gaussian_latent_argmax");
 }
@@ -95,7 +95,7 @@ dd_status launch_init(void* dst, int64_t count, uint32_t id, double shift, int i
                       uint64_t seed, hipStream_t s) {
     if (count == 0) return DD_OK;
     ProfScope ps(KC_INIT, s);
-    hipLaunchKernelGGL(init_kernel, dim3((unsigned)ceil_div(count, 256)), dim3(256), 0, s, dst,
+    launch_k(init_kernel, dim3((unsigned)ceil_div(count, 256)), dim3(256), 0, s, dst,
                        count, id, shift, is_bf16, seed);
     return launch_status("init_params");
 }

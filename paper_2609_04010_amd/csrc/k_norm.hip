@@ -23,7 +23,7 @@ __global__ void temb_kernel(float* temb, int d, double tau) {
 
 dd_status launch_temb(float* temb, int d, double tau, hipStream_t s) {
     ProfScope ps(KC_TEMB, s);
-    hipLaunchKernelGGL(temb_kernel, dim3((d + 255) / 256), dim3(256), 0, s, temb, d, tau);
+    launch_k(temb_kernel, dim3((d + 255) / 256), dim3(256), 0, s, temb, d, tau);
     return launch_status("time_embedding");
 }
 
@@ -230,7 +230,7 @@ dd_status launch_embed_ln_t(const int32_t* z, int64_t rows, int L, int n_tok, in
     switch (d / 64) {
 #define X(n)                                                                                     \
     case n:                                                                                      \
-        hipLaunchKernelGGL((embed_ln_kernel<W, n, RMS>), grid, blk, 0, s, z, rows, L, n_tok,     \
+        launch_k((embed_ln_kernel<W, n, RMS>), grid, blk, 0, s, z, rows, L, n_tok,     \
                            (const W*)tok, (const W*)pos, temb, (const W*)g, (const W*)b, eps, h,  \
                            (W*)xln, ldo, err);                                                   \
         break;
@@ -248,11 +248,11 @@ void launch_embed_ln_v4(int d, dim3 grid, const int32_t* z, int64_t rows, int L,
                         hipStream_t s) {
     const dim3 blk(256);
     if (d == 768)
-        hipLaunchKernelGGL((embed_ln_bf16_v4_kernel<3, RMS>), grid, blk, 0, s, z, rows, L, n_tok, tk, ps, temb, g, b, eps, h, o, ldo, err);
+        launch_k((embed_ln_bf16_v4_kernel<3, RMS>), grid, blk, 0, s, z, rows, L, n_tok, tk, ps, temb, g, b, eps, h, o, ldo, err);
     else if (d == 1024)
-        hipLaunchKernelGGL((embed_ln_bf16_v4_kernel<4, RMS>), grid, blk, 0, s, z, rows, L, n_tok, tk, ps, temb, g, b, eps, h, o, ldo, err);
+        launch_k((embed_ln_bf16_v4_kernel<4, RMS>), grid, blk, 0, s, z, rows, L, n_tok, tk, ps, temb, g, b, eps, h, o, ldo, err);
     else
-        hipLaunchKernelGGL((embed_ln_bf16_v4_kernel<8, RMS>), grid, blk, 0, s, z, rows, L, n_tok, tk, ps, temb, g, b, eps, h, o, ldo, err);
+        launch_k((embed_ln_bf16_v4_kernel<8, RMS>), grid, blk, 0, s, z, rows, L, n_tok, tk, ps, temb, g, b, eps, h, o, ldo, err);
 }
 
 dd_status launch_embed_ln(int dtype, int norm, const int32_t* z, int64_t rows, int L, int n_tok, int d,
@@ -283,7 +283,7 @@ dd_status launch_ln_t(const float* h, int64_t rows, int d, const void* g, const 
     switch (d / 64) {
 #define X(n)                                                                                     \
     case n:                                                                                      \
-        hipLaunchKernelGGL((ln_kernel<W, n, RMS>), grid, blk, 0, s, h, rows, (const W*)g,       \
+        launch_k((ln_kernel<W, n, RMS>), grid, blk, 0, s, h, rows, (const W*)g,       \
                            (const W*)b, eps, (W*)out, ldo);                                      \
         break;
         DD_NPL_CASES(X)
@@ -297,9 +297,9 @@ template <bool RMS>
 void launch_ln_v4(int d, dim3 grid, const float* h, int64_t rows, const bf16_t* g, const bf16_t* b,
                   float eps, bf16_t* o, int64_t ldo, hipStream_t s) {
     const dim3 blk(256);
-    if (d == 768) hipLaunchKernelGGL((ln_bf16_v4_kernel<3, RMS>), grid, blk, 0, s, h, rows, g, b, eps, o, ldo);
-    else if (d == 1024) hipLaunchKernelGGL((ln_bf16_v4_kernel<4, RMS>), grid, blk, 0, s, h, rows, g, b, eps, o, ldo);
-    else hipLaunchKernelGGL((ln_bf16_v4_kernel<8, RMS>), grid, blk, 0, s, h, rows, g, b, eps, o, ldo);
+    if (d == 768) launch_k((ln_bf16_v4_kernel<3, RMS>), grid, blk, 0, s, h, rows, g, b, eps, o, ldo);
+    else if (d == 1024) launch_k((ln_bf16_v4_kernel<4, RMS>), grid, blk, 0, s, h, rows, g, b, eps, o, ldo);
+    else launch_k((ln_bf16_v4_kernel<8, RMS>), grid, blk, 0, s, h, rows, g, b, eps, o, ldo);
 }
 
 dd_status launch_ln(int dtype, int norm, const float* h, int64_t rows, int d, const void* g, const void* b,

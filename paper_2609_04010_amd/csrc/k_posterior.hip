@@ -433,7 +433,7 @@ __global__ __launch_bounds__(256) void remask_kernel(PostArgs a) {
 dd_status launch_remask(const PostArgs& a, hipStream_t s) {
     if (a.rows == 0) return DD_OK;
     ProfScope ps(KC_POSTERIOR, s);
-    hipLaunchKernelGGL(remask_kernel, dim3((a.rows + 255) / 256), dim3(256), 0, s, a);
+    launch_k(remask_kernel, dim3((a.rows + 255) / 256), dim3(256), 0, s, a);
     return launch_status("remask");
 }
 
@@ -489,7 +489,7 @@ __global__ __launch_bounds__(CT) void compact_masked_kernel(const int32_t* z, in
 dd_status launch_compact(const int32_t* z, int64_t M, int32_t mask_id, int32_t* idx, int32_t* count,
                          hipStream_t s) {
     ProfScope ps(KC_COMPACT, s);
-    hipLaunchKernelGGL(compact_masked_kernel, dim3(1), dim3(CT), 0, s, z, M, mask_id, idx, count);
+    launch_k(compact_masked_kernel, dim3(1), dim3(CT), 0, s, z, M, mask_id, idx, count);
     return launch_status("compact_masked");
 }
 
@@ -501,19 +501,19 @@ dd_status launch_posterior(const PostArgs& a, int logits_dtype, hipStream_t s) {
         ProfScope ps(KC_POSTERIOR, s);
         const dim3 g4((unsigned)((a.rows + 3) / 4));
         if (a.glse && logits_dtype == DD_BF16)
-            hipLaunchKernelGGL(posterior_grouped_kernel<bf16_t>, g4, dim3(256), 0, s, a);
+            launch_k(posterior_grouped_kernel<bf16_t>, g4, dim3(256), 0, s, a);
         else if (a.glse)
-            hipLaunchKernelGGL(posterior_grouped_kernel<float>, g4, dim3(256), 0, s, a);
+            launch_k(posterior_grouped_kernel<float>, g4, dim3(256), 0, s, a);
         else if (logits_dtype == DD_BF16)
-            hipLaunchKernelGGL(posterior_kernel<bf16_t>, dim3(a.rows), dim3(PT), shmem, s, a);
+            launch_k(posterior_kernel<bf16_t>, dim3(a.rows), dim3(PT), shmem, s, a);
         else
-            hipLaunchKernelGGL(posterior_kernel<float>, dim3(a.rows), dim3(PT), shmem, s, a);
+            launch_k(posterior_kernel<float>, dim3(a.rows), dim3(PT), shmem, s, a);
     }
     if (a.probs && !a.count) {
         if (logits_dtype == DD_BF16)
-            hipLaunchKernelGGL(posterior_probs_kernel<bf16_t>, dim3(a.rows), dim3(PT), 0, s, a);
+            launch_k(posterior_probs_kernel<bf16_t>, dim3(a.rows), dim3(PT), 0, s, a);
         else
-            hipLaunchKernelGGL(posterior_probs_kernel<float>, dim3(a.rows), dim3(PT), 0, s, a);
+            launch_k(posterior_probs_kernel<float>, dim3(a.rows), dim3(PT), 0, s, a);
     }
     return launch_status("posterior");
 }

@@ -307,11 +307,11 @@ dd_status launch_verify(const VerifyArgs& a, int logits_dtype, float* lse, hipSt
     const int ngroups = (a.V + DD_GUMBEL_GROUP - 1) / DD_GUMBEL_GROUP;
     const size_t shmem = (size_t)ngroups * sizeof(float);
     if (logits_dtype == DD_BF16) {
-        hipLaunchKernelGGL(row_lse_kernel<bf16_t>, dim3(rows), dim3(VT), 0, s, a, lse);
-        hipLaunchKernelGGL(verify_kernel<bf16_t>, dim3(a.S), dim3(VT), shmem, s, a, (const float*)lse);
+        launch_k(row_lse_kernel<bf16_t>, dim3(rows), dim3(VT), 0, s, a, lse);
+        launch_k(verify_kernel<bf16_t>, dim3(a.S), dim3(VT), shmem, s, a, (const float*)lse);
     } else {
-        hipLaunchKernelGGL(row_lse_kernel<float>, dim3(rows), dim3(VT), 0, s, a, lse);
-        hipLaunchKernelGGL(verify_kernel<float>, dim3(a.S), dim3(VT), shmem, s, a, (const float*)lse);
+        launch_k(row_lse_kernel<float>, dim3(rows), dim3(VT), 0, s, a, lse);
+        launch_k(verify_kernel<float>, dim3(a.S), dim3(VT), shmem, s, a, (const float*)lse);
     }
     return launch_status("spec_verify");
 }
