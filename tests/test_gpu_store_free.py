@@ -115,6 +115,9 @@ CASES = [
     (2, dict(n_layers=1, vocab=512), 2, 130, 0.5, 0.3, 0.45, None),
     (2, dict(n_layers=1, vocab=700), 2, 256, 0.6, 0.4, 0.55, 0.5),
     (5, dict(n_layers=1, max_len=4096), 1, 520, 0.8, 0.6, 0.7, None),
+    # one ragged group only (V < 256), and a last group of a single class
+    (2, dict(n_layers=1, vocab=100), 2, 96, 1.0, 0.0, 0.25, None),
+    (2, dict(n_layers=1, vocab=257), 2, 96, 0.9, 0.2, 0.5, 0.3),
 ]
 
 
