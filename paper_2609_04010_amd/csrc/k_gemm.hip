@@ -260,9 +260,27 @@ template <int TBN_, int WGM_, int WGN_, int DM_ = DM> struct DLShape {
     static_assert(LDS <= 160 * 1024, "LDS");
 };
 
-// LDS of the direct-to-LDS kernel: the shape's stages and staging, plus for EPI_LSE the (max, sum)
-// partials of each tile row from each of the WGN wavefronts across it
+#ifndef DD_GEMM_RING
+#define DD_GEMM_RING 1
+#endif
+// Operand ring of the residual projections (attention output, MLP down) on the 256 x 192 tile
+// (eight wavefronts): A in three LDS stages and W in two, so that A's K-tile G + 2 and W's K-tile
+// G + 1 stream in while K-tile G is computed.  A is the operand that mostly comes from HBM (each A
+// strip is read by the four tiles across N = d, W by every tile of the XCD), and with one K-tile of
+// lead the loop waited for its loads.  The other projections (QKV, MLP up) gained nothing from it.
+template <int EPI, class S> constexpr bool dl_ring() {
+    return DD_GEMM_RING && S::TBN == 192 && S::DM == 256 && S::NW == 8 && EPI == EPI_BIAS_RESID;
+}
+// the ring's LDS: three A stages and two W stages (the residual epilogue stages in the A stage of
+// the last K-tile)
+template <class S> constexpr size_t dl_ring_lds() {
+    return ((size_t)3 * S::DM * BK + (size_t)2 * S::TBN * BK) * sizeof(bf16_t);
+}
+
+// LDS of the direct-to-LDS kernel: the shape's stages and staging (or the ring's), plus for EPI_LSE
+// the (max, sum) partials of each tile row from each of the WGN wavefronts across it
 template <int EPI, class S> constexpr size_t dl_lds_bytes() {
+    if constexpr (dl_ring<EPI, S>()) return dl_ring_lds<S>();
     return S::LDS + (EPI == EPI_LSE || EPI == EPI_LSE_CDF ? (size_t)S::DM * S::WGN * sizeof(float2) : 0) +
            (EPI == EPI_LSE_CDF ? (size_t)S::DM * sizeof(float2) : 0);
 }
@@ -282,7 +300,17 @@ __global__ __launch_bounds__(64 * WGM_ * WGN_, 1) void gemm_bf16_dl_kernel(GemmA
     constexpr bool GROUP_EPI = EPI == EPI_LSE || EPI == EPI_LSE_CDF;
     constexpr int TILE_GM = (EPI == EPI_PLAIN || GROUP_EPI) ? 8 : DD_GEMM_GM_BODY;
     constexpr int AROWS = DM / S::NW, WROWS = S::TBN / S::NW;   // operand rows each wave loads
+    constexpr bool RING = dl_ring<EPI, S>();
+    constexpr int AST = DM * BK, WST = S::TBN * BK;   // elements of one ring stage of A / W
+    static_assert(!RING || (NA < 16 && dl_ring_lds<S>() <= 160 * 1024 && S::NW * 32 * 32 * 2 <= AST),
+                  "ring: the wait counts A's loads, and one A stage holds the residual staging");
     extern __shared__ __attribute__((aligned(1024))) bf16_t smem[];
+    // the LDS of A's and W's K-tile G (G counts K-tiles over the workgroup's tiles; nk is even, so
+    // without the ring G & 1 is also the tile's own K-tile parity)
+    auto a_stage = [&](int G) -> bf16_t* { return RING ? smem + (G % 3) * AST : smem + (G & 1) * S::STAGE; };
+    auto w_stage = [&](int G) -> bf16_t* {
+        return RING ? smem + 3 * AST + (G & 1) * WST : smem + (G & 1) * S::STAGE + DM * BK;
+    };
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int wm = wave / S::WGN, wn = wave % S::WGN;
     // Gathered mode: only the first *m_count output rows exist; the tile grid is re-derived from
@@ -307,34 +335,59 @@ __global__ __launch_bounds__(64 * WGM_ * WGN_, 1) void gemm_bf16_dl_kernel(GemmA
     // one M-tile share A) start at different K-slices, so they do not request the same L2 lines
     // at the same moment (measured 8 % on that GEMM; the accumulation order is all that changes).
     int m0 = 0, n0 = 0, skew = 0;
-    int64_t offA[NA], offW[NWL];
+    // this tile's operand offsets, and (ring) the next tile's, which the last K-tiles fetch from
+    int64_t offA[NA], offW[NWL], offAn[RING ? NA : 1], offWn[RING ? NWL : 1];
+    auto a_offsets = [&](int tm0, int64_t* o) {
+#pragma unroll
+        for (int i = 0; i < NA; ++i) {
+            const int rl = AROWS * wave + 8 * i + (lane >> 3);
+            const int r = min(tm0 + rl, M - 1);
+            // (the ring reads the next tile's offsets inside the K loop, where a gathered row id
+            // would be a global load to wait for; its launcher never passes a_rows)
+            o[i] = (int64_t)(!RING && g.a_rows ? g.a_rows[r] : r) * g.lda + lchunk(rl) * 8;
+        }
+    };
+    auto w_offsets = [&](int tn0, int64_t* o) {
+#pragma unroll
+        for (int i = 0; i < NWL; ++i) {
+            const int rl = WROWS * wave + 8 * i + (lane >> 3);
+            o[i] = (int64_t)min(tn0 + rl, g.N - 1) * g.ldw + lchunk(rl) * 8;
+        }
+    };
+    auto set_offA = [&](int tm0) { a_offsets(tm0, offA); };
+    auto set_offW = [&](int tn0) { w_offsets(tn0, offW); };
+    // the ring switches A's and W's offsets to the next tile one K-tile apart
+    auto tile_origin = [&](int tile, int& tm0, int& tn0) {
+        int tm, tn;
+        map_tile<TILE_GM>(tile, nblocks, tiles_m, tiles_n, tm, tn);
+        tm0 = tm * DM;
+        tn0 = tn * S::TBN;
+    };
     auto setup_tile = [&](int tile) {
         int tm, tn;
         map_tile<TILE_GM>(tile, nblocks, tiles_m, tiles_n, tm, tn);
         m0 = tm * DM;
         n0 = tn * S::TBN;
         if constexpr (EPI == EPI_PLAIN || GROUP_EPI) skew = ((tm & 7) + 2 * tn) % nk;
-#pragma unroll
-        for (int i = 0; i < NA; ++i) {
-            const int rl = AROWS * wave + 8 * i + (lane >> 3);
-            const int r = min(m0 + rl, M - 1);
-            offA[i] = (int64_t)(g.a_rows ? g.a_rows[r] : r) * g.lda + lchunk(rl) * 8;
-        }
-#pragma unroll
-        for (int i = 0; i < NWL; ++i) {
-            const int rl = WROWS * wave + 8 * i + (lane >> 3);
-            offW[i] = (int64_t)min(n0 + rl, g.N - 1) * g.ldw + lchunk(rl) * 8;
-        }
+        set_offA(m0);
+        set_offW(n0);
     };
-    // load j of a stage: j < NA fills A rows AROWS w + 8 j.., otherwise W rows WROWS w + 8 (j - NA)..
-    auto issue_one = [&](int k0, int stage, int j) {
-        if (j < NA) {
-            bf16_t* sA = smem + stage * S::STAGE + (AROWS * wave) * BK;
-            __builtin_amdgcn_global_load_lds((gbl_void*)(A + offA[j] + k0), (lds_void*)(sA + 8 * j * BK), 16, 0, 0);
-        } else {
-            bf16_t* sW = smem + stage * S::STAGE + DM * BK + (WROWS * wave) * BK;
-            __builtin_amdgcn_global_load_lds((gbl_void*)(W + offW[j - NA] + k0), (lds_void*)(sW + 8 * (j - NA) * BK), 16, 0, 0);
-        }
+    // load j of A rows AROWS w + 8 j.. / of W rows WROWS w + 8 j.. at K offset k0 into stage st
+    // (nx: from the next tile, ring only; a uniform select, no branch inside the MFMA sequence)
+    auto issue_a = [&](int k0, bf16_t* st, int j, bool nx = false) {
+        int64_t o = offA[j];
+        if constexpr (RING) o = nx ? offAn[j] : o;
+        __builtin_amdgcn_global_load_lds((gbl_void*)(A + o + k0), (lds_void*)(st + (AROWS * wave + 8 * j) * BK), 16, 0, 0);
+    };
+    auto issue_w = [&](int k0, bf16_t* st, int j, bool nx = false) {
+        int64_t o = offW[j];
+        if constexpr (RING) o = nx ? offWn[j] : o;
+        __builtin_amdgcn_global_load_lds((gbl_void*)(W + o + k0), (lds_void*)(st + (WROWS * wave + 8 * j) * BK), 16, 0, 0);
+    };
+    // load j of K-tile G (both operands at k0): j < NA fills A, otherwise W
+    auto issue_one = [&](int k0, int G, int j) {
+        if (j < NA) issue_a(k0, a_stage(G), j);
+        else issue_w(k0, w_stage(G), j - NA);
     };
     constexpr int NL = NA + NWL;                       // load instructions per wave per stage
     constexpr int LD_STEPS = 3;                        // K steps over which they are spread
@@ -350,14 +403,26 @@ __global__ __launch_bounds__(64 * WGM_ * WGN_, 1) void gemm_bf16_dl_kernel(GemmA
         return *(const bf16x8*)&tile[(row0 + frow) * BK + slot * 8];
     };
 
-    // one K-tile; with_loads: also fetch K offset next_k0 (of the tile offA/offW describe) into the
-    // other stage; without, the load issue stays free of branches inside the MFMA sequence
-    auto ktile = [&](const int t, const int next_k0, auto with_loads) {
+    // K-tile G; with_loads: also fetch, from the tiles offA/offW describe, K-tile G + 1 of both
+    // operands at K offset k0a (two stages) or W's K-tile G + 1 at k0w and A's K-tile G + 2 at k0a
+    // (ring); without, the load issue stays free of branches inside the MFMA sequence
+    auto ktile = [&](const int G, const int k0a, const int k0w, auto with_loads, bool a_nx = false,
+                     bool w_nx = false, bool has_a1 = false, bool has_a2 = false, bool has_w1 = false) {
         constexpr bool more = decltype(with_loads)::value;
-        __builtin_amdgcn_s_waitcnt(0x3F70);      // vmcnt(0): this lane's loads of K-tile t landed
-        __syncthreads();                          // ... everyone's; and everyone left K-tile t-1
-        const bf16_t* sA = smem + (t & 1) * S::STAGE + (wm * S::WM) * BK;
-        const bf16_t* sW = smem + (t & 1) * S::STAGE + DM * BK + (wn * S::WN) * BK;
+        if constexpr (RING) {
+            // this lane's loads of K-tile G landed: only A's K-tile G + 1 (has_a1), issued after
+            // them, may still be in flight; then everyone's, and everyone left K-tile G - 1.  The
+            // barrier is a bare s_barrier with a memory clobber: __syncthreads would also wait for
+            // A's G + 1
+            if (has_a1) __builtin_amdgcn_s_waitcnt(0x3F70 | NA);
+            else __builtin_amdgcn_s_waitcnt(0x3F70);
+            asm volatile("s_barrier" ::: "memory");
+        } else {
+            __builtin_amdgcn_s_waitcnt(0x3F70);  // vmcnt(0): this lane's loads of K-tile G landed
+            __syncthreads();                      // ... everyone's; and everyone left K-tile G - 1
+        }
+        const bf16_t* sA = a_stage(G) + (wm * S::WM) * BK;
+        const bf16_t* sW = w_stage(G) + (wn * S::WN) * BK;
         bf16x8 af[2][MB], wf[2][NB];
 #pragma unroll
         for (int i = 0; i < MB; ++i) af[0][i] = frag(sA, 32 * i, 0);
@@ -398,7 +463,19 @@ __global__ __launch_bounds__(64 * WGM_ * WGN_, 1) void gemm_bf16_dl_kernel(GemmA
                     }
                 }
                 if constexpr (more)
-                    if (i < nload) issue_one(next_k0, (t + 1) & 1, kk * LPS + i);
+                    if (i < nload) {
+                        const int j = kk * LPS + i;
+                        if constexpr (RING) {
+                            // W first: see the wait above; past the last tile nothing is fetched
+                            if (j < NWL) {
+                                if (has_w1) issue_w(k0w, w_stage(G + 1), j, w_nx);
+                            } else if (has_a2) {
+                                issue_a(k0a, a_stage(G + 2), j - NWL, a_nx);
+                            }
+                        } else {
+                            issue_one(k0a, G + 1, j);
+                        }
+                    }
                 __builtin_amdgcn_sched_barrier(0);
             }
             if (kk + 1 < BK / 16) __builtin_amdgcn_s_waitcnt(0xC07F);   // lgkmcnt(0)
@@ -436,7 +513,7 @@ __global__ __launch_bounds__(64 * WGM_ * WGN_, 1) void gemm_bf16_dl_kernel(GemmA
 
     // epilogue of the tile at (m0, n0); n0 and the bias are read through the lambdas above, so the
     // caller keeps them describing this tile until the epilogue is done
-    auto epilogue = [&](const int tm0) {
+    auto epilogue = [&](const int tm0, const int Gl) {
         if constexpr (EPI == EPI_BIAS_RESID) {
             // The accumulators started from the residual h (loaded with the tile's first K-tile),
             // so the epilogue only stores h + A W^T + bias.  One 32 x 32 block at a time goes
@@ -445,7 +522,9 @@ __global__ __launch_bounds__(64 * WGM_ * WGN_, 1) void gemm_bf16_dl_kernel(GemmA
             // XOR-swizzled by row like the operand tiles (slot = chunk ^ ((row >> 1) & 7)), which
             // keeps the row-per-lane writes and the row-segment reads free of bank conflicts.
             __syncthreads();                      // every wave is done with the operand stages
-            float* cst = (float*)(smem + S::STAGE) + wave * (32 * 32);
+            // staging above stage 0 (two stages: the next tile's first K-tile streams into stage 0), or
+            // in the A stage of the last K-tile (ring: the next tile's loads go to the other stages)
+            float* cst = (RING ? (float*)a_stage(Gl) : (float*)(smem + S::STAGE)) + wave * (32 * 32);
             float* C = (float*)g.C;
             const bf16_t* bias = (const bf16_t*)g.bias;
             const int rr = lane >> 3, c4 = (lane & 7) * 4;    // read-back: row rr + 8 it, columns c4..
@@ -709,8 +788,19 @@ __global__ __launch_bounds__(64 * WGM_ * WGN_, 1) void gemm_bf16_dl_kernel(GemmA
 
     setup_tile(L);
     prefetch_bias();
+    if constexpr (RING) {
+        // W's K-tile 0, then A's K-tiles 0 and 1 (nk >= 2)
 #pragma unroll
-    for (int j = 0; j < NL; ++j) issue_one(skew * BK, 0, j);
+        for (int j = 0; j < NWL; ++j) issue_w(0, w_stage(0), j);
+#pragma unroll
+        for (int j = 0; j < NA; ++j) issue_a(0, a_stage(0), j);
+#pragma unroll
+        for (int j = 0; j < NA; ++j) issue_a(BK, a_stage(1), j);
+    } else {
+#pragma unroll
+        for (int j = 0; j < NL; ++j) issue_one(skew * BK, 0, j);
+    }
+    int G = 0;                                    // K-tiles begun by this workgroup
     while (true) {
         const int cskew = skew;
         if constexpr (EPI == EPI_BIAS_RESID) {
@@ -750,19 +840,42 @@ __global__ __launch_bounds__(64 * WGM_ * WGN_, 1) void gemm_bf16_dl_kernel(GemmA
         const int Ln = L + (int)gridDim.x;
         const bool next = Ln < nblocks;
         const int tm0 = m0;
-        for (int t = 0; t < nk; ++t) {
-            if (t == nk - 1 && next) {            // the last K-tile fetches the next tile's first one
-                const int tn0 = n0;
-                setup_tile(Ln);
-                n0 = tn0;                         // the epilogue still describes this tile
-            }
-            // the last K-tile fetches the next tile's first K-slice (after the very last tile it
-            // re-fetches slice 0 into stage 0: unused, in bounds; one call site keeps the MFMA
-            // sequence in one copy)
-            const int next_k0 = t + 1 < nk ? ((t + 1 + cskew) % nk) * BK : (next ? skew * BK : 0);
-            ktile(t, next_k0, std::true_type{});
+        if constexpr (RING) {
+            int tm_n = m0, tn_n = n0;
+            if (next) tile_origin(Ln, tm_n, tn_n);
+            a_offsets(tm_n, offAn);
+            w_offsets(tn_n, offWn);
         }
-        epilogue(tm0);
+        for (int t = 0; t < nk; ++t, ++G) {
+            if constexpr (RING) {
+                // A's loads move to the next tile one K-tile before W's: K-tile nk - 2 fetches A's
+                // first K-tile of the next tile, K-tile nk - 1 W's first and A's second (uniform
+                // branches around the loads; after the last tile nothing is fetched, so the
+                // epilogue's barrier has no load to wait for)
+                const int k0w = t + 1 < nk ? (t + 1) * BK : 0;
+                const int k0a = t + 2 < nk ? (t + 2) * BK : (t + 2 - nk) * BK;
+                ktile(G, k0a, k0w, std::true_type{}, t + 2 >= nk, t + 1 >= nk, t + 1 < nk || next,
+                      t + 2 < nk || next, t + 1 < nk || next);
+            } else {
+                if (t == nk - 1 && next) {        // the last K-tile fetches the next tile's first one
+                    const int tn0 = n0;
+                    setup_tile(Ln);
+                    n0 = tn0;                     // the epilogue still describes this tile
+                }
+                // the last K-tile fetches the next tile's first K-slice (after the very last tile it
+                // re-fetches slice 0 into stage 0: unused, in bounds; one call site keeps the MFMA
+                // sequence in one copy)
+                const int next_k0 = t + 1 < nk ? ((t + 1 + cskew) % nk) * BK : (next ? skew * BK : 0);
+                ktile(G, next_k0, 0, std::true_type{});
+            }
+        }
+        if constexpr (RING) {
+#pragma unroll
+            for (int i = 0; i < NA; ++i) offA[i] = offAn[i];
+#pragma unroll
+            for (int i = 0; i < NWL; ++i) offW[i] = offWn[i];
+        }
+        epilogue(tm0, G - 1);
         if (!next) break;
         int tm_n, tn_n;
         map_tile<TILE_GM>(Ln, nblocks, tiles_m, tiles_n, tm_n, tn_n);
@@ -900,7 +1013,10 @@ static void launch_dl(const GemmArgs& g, hipStream_t s) {
 template <int EPI, int ROLE>
 static void launch_epi(int dtype, const GemmArgs& g, hipStream_t s) {
     if (dtype == DD_BF16) {
-        switch (pick_tile(g)) {
+        int tile = pick_tile(g);
+        // the ring instance of the 256 x 192 tile takes no gathered rows: the four-wavefront form
+        if (tile == 7 && g.a_rows && dl_ring<EPI, DLShape<192, 4, 2>>()) tile = 5;
+        switch (tile) {
             case 7: launch_dl<EPI, ROLE, 192, 4, 2>(g, s); break;
             case 6: launch_dl<EPI, ROLE, 256, 2, 4>(g, s); break;
             case 5: launch_dl<EPI, ROLE, 192, 2, 2>(g, s); break;
