@@ -12,9 +12,10 @@
 // contiguous run of tile ids, walked in groups of 8 M-tiles so concurrent tiles share A and W
 // tiles in that XCD's L2.
 //
-// bf16 outputs are written with non-temporal stores: they are read by the next kernel, not by this
-// one, so they should not push the operand tiles other workgroups still reuse out of L2 (measured:
-// MLP up 91 -> 85 us at B16 L1024).  The fp32 residual row is stored normally (see its epilogue).
+// bf16 outputs other than QKV's are written with non-temporal stores: they are read by the next
+// kernel, not by this one, so they should not push the operand tiles other workgroups still reuse
+// out of L2 (measured: MLP up 91 -> 85 us at B16 L1024).  The QKV output and the fp32 residual row
+// are stored normally (see the epilogues).
 //
 // Epilogues: bias -> bf16 (QKV), bias + GELU(tanh) -> bf16 (MLP up), bias + fp32 residual add in
 // place (attention output, MLP down), plain store (vocabulary projection), plain store plus the
@@ -613,7 +614,10 @@ __global__ __launch_bounds__(64 * WGM_ * WGN_, 1) void gemm_bf16_dl_kernel(GemmA
                     const uint4 v = *(const uint4*)&cst[r * S::CSTR + c];
                     bf16_t* dst = C + (int64_t)m * g.ldc + n;
                     if (n + 7 < g.N) {
-                        __builtin_nontemporal_store(u32x4{v.x, v.y, v.z, v.w}, (u32x4*)dst);
+                        // the QKV output is stored normally: the attention reads it next, from the
+                        // Infinity Cache (attention 66.8-69.5 -> 63.5-67.4 us, QKV +0.4-0.9 us)
+                        if constexpr (EPI == EPI_BIAS) *(u32x4*)dst = u32x4{v.x, v.y, v.z, v.w};
+                        else __builtin_nontemporal_store(u32x4{v.x, v.y, v.z, v.w}, (u32x4*)dst);
                     } else {
                         const uint32_t w[4] = {v.x, v.y, v.z, v.w};
                         for (int e = 0; n + e < g.N; ++e) dst[e] = (bf16_t)((w[e >> 1] >> (16 * (e & 1))) & 0xFFFFu);
