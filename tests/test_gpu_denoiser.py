@@ -59,6 +59,9 @@ FWD_CASES = [
     (1, {"norm": "rms", "dtype": "bf16", "n_heads": 1, "max_len": 96}, 2, 70, 0.5, 0.5, "host"),
     (2, {"norm": "rms", "n_layers": 3}, 2, 200, 0.5, 0.5, "host"),
     (5, {"norm": "rms", "n_layers": 2, "max_len": 4096}, 1, 300, 0.7, 0.3, "host"),
+    # the residual projections' operand ring over two tiles per workgroup (33 x 990 rows: 512 tiles
+    # of 256 x 192 for 256 CUs, the last M-tile ragged) and with two K-tiles (d_mlp 128)
+    (2, {"n_layers": 1, "d_mlp": 128, "vocab": 300}, 33, 990, 0.5, 0.5, "host"),
 ]
 
 
