@@ -292,7 +292,9 @@ typedef __attribute__((address_space(1))) const void gbl_void;
 // ROLE (the profiler class of the layer) only separates the symbols of layers sharing an epilogue.
 // Persistent: workgroup b takes tiles b, b + G, b + 2G, ... (G = grid size).  The number of K-tiles
 // is even, so the loads of the next tile's first K-tile go out during the last K-tile of the
-// current one into stage 0, which the staged epilogue leaves alone: they land while it runs.
+// current one into stage 0, which the staged epilogue leaves alone: they land while it runs.  (The
+// operand ring of the residual projections fetches the next tile's first K-tiles the same way, into
+// the stages its epilogue does not use.)
 template <int EPI, int ROLE, int TBN_, int WGM_, int WGN_, int DM_>
 __global__ __launch_bounds__(64 * WGM_ * WGN_, 1) void gemm_bf16_dl_kernel(GemmArgs g, int tiles_m, int tiles_n) {
     using S = DLShape<TBN_, WGM_, WGN_, DM_>;
