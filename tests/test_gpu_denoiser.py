@@ -171,10 +171,12 @@ def _loop_gpu(torch, cfg, buf, z1, T, alphas, words=None, seed=0, kappas=None, p
     return z.cpu().numpy().reshape(B, L), trace.cpu().numpy().reshape(T + 1, B, L)
 
 
-def test_loop_config1_free_running_matches_oracle():
-    """fp32 workload 1: the whole 8-step loop on explicit noise, free running on both sides."""
+@pytest.mark.parametrize("norm", ["layer", "rms"])
+def test_loop_config1_free_running_matches_oracle(norm):
+    """fp32 workload 1: the whole 8-step loop on explicit noise, free running on both sides (with
+    LayerNorm, the workload's choice, and with RMSNorm)."""
     torch = torch_or_skip()
-    cfg = workloads.model_cfg(1)
+    cfg = workloads.model_cfg(1, norm=norm)
     w, s = workloads.WORKLOADS[1], workloads.seeds(1)
     B, L, V, T = w["B"], w["L"], w["vocab"], w["T"]
     P, buf = _params_seeded(torch, cfg, s["param"])
