@@ -45,9 +45,9 @@ DD_DEV float gelu_tanh(float x) {
     return x * __builtin_amdgcn_rcpf(1.0f + e);
 }
 
-// M-tiles per group of the tile order (map_tile): 4 for the body projections, 8 for the vocabulary
-// projection (measured: QKV 69.6 -> 66.0 us with 4 instead of 8, the others unchanged; the
-// vocabulary projection slower with 4)
+// M-tiles per group of the tile order (map_tile) of the body projections other than QKV (4; QKV
+// takes 2, the vocabulary projection 8: see the kernel).  Measured: QKV 69.6 -> 66.0 us with 4
+// instead of 8, the others unchanged; the vocabulary projection slower with 4.
 #ifndef DD_GEMM_GM_BODY
 #define DD_GEMM_GM_BODY 4
 #endif
@@ -301,7 +301,10 @@ __global__ __launch_bounds__(64 * WGM_ * WGN_, 1) void gemm_bf16_dl_kernel(GemmA
     constexpr int DM = S::DM;
     constexpr int MB = S::MB, NB = S::NB, NA = S::ALOADS, NWL = S::WLOADS;
     constexpr bool GROUP_EPI = EPI == EPI_LSE || EPI == EPI_LSE_CDF;
-    constexpr int TILE_GM = (EPI == EPI_PLAIN || GROUP_EPI) ? 8 : DD_GEMM_GM_BODY;
+    // M-tiles per group of the tile order: 8 for the vocabulary projection, 2 for QKV (whose output,
+    // stored normally, shares L2 with the operand tiles: 63.3-64.0 -> 60.3-60.7 us with 2 instead of
+    // 4 at B16 L1024), 4 for the other body projections
+    constexpr int TILE_GM = (EPI == EPI_PLAIN || GROUP_EPI) ? 8 : (EPI == EPI_BIAS ? 2 : DD_GEMM_GM_BODY);
     constexpr int AROWS = DM / S::NW, WROWS = S::TBN / S::NW;   // operand rows each wave loads
     constexpr bool RING = dl_ring<EPI, S>();
     constexpr int AST = DM * BK, WST = S::TBN * BK;   // elements of one ring stage of A / W
