@@ -285,6 +285,12 @@ static dd_status run_forward(const dd_config* c, const void* params, const int32
         return launch_gemm(dt, EPI_GATE, KC_GEMM_LORA, g, s);
     };
 
+    // With vocab_rows only the listed rows get logits.  Past the last layer's attention nothing mixes
+    // rows, so the rest of that layer runs on the listed rows alone, compacted (row j is token row
+    // vocab_rows[j]): the attention-output projection gathers its rows and writes the residual rows
+    // into the q|k|v buffer, which the attention has finished with (fp32 d per row fits in bf16 3d).
+    const bool tail_rows = vocab_rows && vocab_count && r == 0 && nl > 0 && dt == DD_BF16 &&
+                           gemm_gather_supported(dt, d) && gemm_gather_supported(dt, F);
     if (c->time_cond) DD_TRY(launch_temb(temb, d, 1000.0 * (1.0 - alpha_t), s));
     const int g0 = nl > 0 ? 2 : lnf;
     DD_TRY(launch_embed_ln(dt, c->norm, z, M, L, n_tok(c), d, tp(0), tp(1), c->time_cond ? temb : nullptr,
@@ -299,6 +305,19 @@ static dd_status run_forward(const dd_config* c, const void* params, const int32
         AttnArgs aa = {qkv, 3 * d, att, dr, B, L, H, d,
                        (float)(1.4426950408889634 / sqrt((double)(d / H))), attn_mask, err};
         DD_TRY(launch_attn(dt, aa, s));
+        if (tail_rows && l + 1 == nl) {
+            float* hc = (float*)qkv;
+            g = {att, dr, tp(b + 4), dr, tp(b + 5), hc, d, (int)M, d, dr, vocab_rows, vocab_count};
+            g.c_in = h;
+            DD_TRY(launch_gemm(dt, EPI_BIAS_RESID, KC_GEMM_O, g, s));
+            DD_TRY(launch_ln(dt, c->norm, hc, M, d, tp(b + 6), tp(b + 7), c->norm_eps, xln, dr, s, vocab_count));
+            g = {xln, dr, tp(b + 8), dr, tp(b + 9), mlp, Fr, (int)M, F, dr, nullptr, vocab_count};
+            DD_TRY(launch_gemm(dt, EPI_BIAS_GELU, KC_GEMM_MLP1, g, s));
+            g = {mlp, Fr, tp(b + 10), Fr, tp(b + 11), hc, d, (int)M, d, Fr, nullptr, vocab_count};
+            DD_TRY(launch_gemm(dt, EPI_BIAS_RESID, KC_GEMM_MLP2, g, s));
+            DD_TRY(launch_ln(dt, c->norm, hc, M, d, tp(lnf), tp(lnf + 1), c->norm_eps, xln, dr, s, vocab_count));
+            break;
+        }
         if (r > 0) DD_TRY(lora_down(att, dr, d, a0 + 1));
         g = {att, dr, tp(b + 4), dr, tp(b + 5), h, d, (int)M, d, dr, nullptr, nullptr};
         DD_TRY(launch_gemm(dt, EPI_BIAS_RESID, KC_GEMM_O, g, s));
@@ -312,8 +331,11 @@ static dd_status run_forward(const dd_config* c, const void* params, const int32
         const int gn = (l + 1 < nl) ? b + 12 : lnf;
         DD_TRY(launch_ln(dt, c->norm, h, M, d, tp(gn), tp(gn + 1), c->norm_eps, xln, dr, s));
     }
-    // with vocab_rows only the listed rows (count on the device) get logits, compacted
-    GemmArgs g = {xln, dr, tp(lnf + 2), d, nullptr, logits, ld, (int)M, V, d, vocab_rows, vocab_count};
+    // with vocab_rows only the listed rows (count on the device) get logits, compacted; after the
+    // compacted last layer the normalised rows are already in list order
+    GemmArgs g = {xln, dr, tp(lnf + 2), d, nullptr, logits, ld, (int)M, V, d,
+                  tail_rows ? nullptr : vocab_rows, vocab_count};
+    g.row_ids = tail_rows ? vocab_rows : nullptr;
     g.lse = vocab_lse;
     g.lse_ld = lse_ld;
     g.cand = vocab_cand;

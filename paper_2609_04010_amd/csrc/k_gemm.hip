@@ -711,7 +711,7 @@ __global__ __launch_bounds__(64 * WGM_ * WGN_, 1) void gemm_bf16_dl_kernel(GemmA
                         // in class order give the crossing wave, a scan of that wave's 16 chunk
                         // sums the crossing chunk and the remaining target in the wave's reference
                         const int m = tm0 + tid;
-                        const uint32_t grow = g.row0 + (uint32_t)(g.a_rows ? g.a_rows[m] : m);
+                        const uint32_t grow = g.row0 + (uint32_t)(g.row_ids ? g.row_ids[m] : g.a_rows ? g.a_rows[m] : m);
                         const uint32_t word = counter_word(g.seed, STREAM_GROUP_U, g.step, grow, (uint32_t)grp);
                         const float t = (float)(((double)word + 0.5) * 0x1p-32 * (double)sum);
                         const float* crow = chk + tid * CHK_LD;
@@ -815,8 +815,21 @@ __global__ __launch_bounds__(64 * WGM_ * WGN_, 1) void gemm_bf16_dl_kernel(GemmA
         const int cskew = skew;
         if constexpr (EPI == EPI_BIAS_RESID) {
             // residual epilogue: start from h (this lane's MFMA output positions), fetched together
-            // with the tile's first K-tile instead of after the K loop
+            // with the tile's first K-tile instead of after the K loop.  h is C itself, or (not in
+            // the ring form) the rows of c_in that the output rows gather
             const float* C = (const float*)g.C;
+            int64_t hrow[MB];
+#pragma unroll
+            for (int j = 0; j < MB; ++j) {
+                const int m = m0 + wm * S::WM + j * 32 + (lane & 31);
+                hrow[j] = m;
+                if constexpr (!RING) {
+                    if (g.c_in && g.a_rows && m < M) hrow[j] = g.a_rows[m];
+                }
+            }
+            if constexpr (!RING) {
+                if (g.c_in) C = g.c_in;
+            }
 #pragma unroll
             for (int i = 0; i < NB; ++i)
 #pragma unroll
@@ -827,11 +840,11 @@ __global__ __launch_bounds__(64 * WGM_ * WGN_, 1) void gemm_bf16_dl_kernel(GemmA
                         const int n = n0 + wn * S::WN + i * 32 + 8 * j4 + 4 * (lane >> 5);
                         float4 h = make_float4(0.f, 0.f, 0.f, 0.f);
                         if (m < M && n + 3 < g.N) {
-                            h = *(const float4*)(C + (int64_t)m * g.ldc + n);
+                            h = *(const float4*)(C + hrow[j] * g.ldc + n);
                         } else if (m < M) {
                             float t[4] = {0.f, 0.f, 0.f, 0.f};
                             for (int e = 0; e < 4; ++e)
-                                if (n + e < g.N) t[e] = C[(int64_t)m * g.ldc + n + e];
+                                if (n + e < g.N) t[e] = C[hrow[j] * g.ldc + n + e];
                             h = make_float4(t[0], t[1], t[2], t[3]);
                         }
                         acc[i][j][4 * j4] = h.x;
@@ -992,8 +1005,9 @@ static int pick_tile(const GemmArgs& g) {
     const char* e = getenv("DD_GEMM_TILE");
     const int forced = e ? atoi(e) : -1;
     if (((forced >= 4 && forced <= 7) || forced >= 9) && g.K % (2 * BK) != 0) return 0;
-    if (forced >= 0 && forced <= 10 && !(g.a_rows && (forced < 4 || forced == 8))) return forced;
-    if (g.N <= 128) return g.K % (2 * BK) == 0 ? 10 : (g.a_rows ? 0 : 8);
+    const bool gathered = g.a_rows || g.m_count || g.c_in;   // only the direct-to-LDS kernels
+    if (forced >= 0 && forced <= 10 && !(gathered && (forced < 4 || forced == 8))) return forced;
+    if (g.N <= 128) return g.K % (2 * BK) == 0 ? 10 : (gathered ? 0 : 8);
     if (g.K % (2 * BK) != 0) return 0;
     const int64_t ncu = num_cus();
     const int64_t tm = (g.M + DM - 1) / DM;
@@ -1024,8 +1038,9 @@ template <int EPI, int ROLE>
 static void launch_epi(int dtype, const GemmArgs& g, hipStream_t s) {
     if (dtype == DD_BF16) {
         int tile = pick_tile(g);
-        // the ring instance of the 256 x 192 tile takes no gathered rows: the four-wavefront form
-        if (tile == 7 && g.a_rows && dl_ring<EPI, DLShape<192, 4, 2>>()) tile = 5;
+        // the ring instance of the 256 x 192 tile takes no gathered rows and no separate residual
+        // input: the four-wavefront form
+        if (tile == 7 && (g.a_rows || g.c_in) && dl_ring<EPI, DLShape<192, 4, 2>>()) tile = 5;
         switch (tile) {
             case 7: launch_dl<EPI, ROLE, 192, 4, 2>(g, s); break;
             case 6: launch_dl<EPI, ROLE, 256, 2, 4>(g, s); break;
@@ -1054,9 +1069,13 @@ dd_status launch_gemm(int dtype, int epi, int cls, const GemmArgs& g, hipStream_
         set_error("GEMM with K = %d", g.K);
         return DD_E_ARG;
     }
-    if (g.a_rows && !gemm_gather_supported(dtype, g.K)) {
+    if ((g.a_rows || g.m_count || g.c_in || g.row_ids) && !gemm_gather_supported(dtype, g.K)) {
         set_error("row-gathered GEMM needs the bf16 path and K %% 128 == 0");
         return DD_E_UNSUPPORTED;
+    }
+    if (g.c_in && epi != EPI_BIAS_RESID) {
+        set_error("a separate residual input needs the residual epilogue");
+        return DD_E_ARG;
     }
     if ((epi == EPI_LSE || epi == EPI_LSE_CDF) &&
         (!gemm_lse_supported(dtype, g.K) || !g.lse || g.lse_ld < (g.N + 255) / 256)) {

@@ -87,9 +87,11 @@ __global__ __launch_bounds__(256) void embed_ln_kernel(const int32_t* z, int64_t
 
 template <typename W, int NPL, bool RMS>
 __global__ __launch_bounds__(256) void ln_kernel(const float* h, int64_t rows, const W* g,
-                                                 const W* b, float eps, W* out, int64_t ldo) {
+                                                 const W* b, float eps, W* out, int64_t ldo,
+                                                 const int32_t* m_count) {
     const int64_t row = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
     const int lane = threadIdx.x & 63;
+    if (m_count) rows = min(rows, (int64_t)*m_count);
     if (row >= rows) return;
     constexpr int d = NPL * 64;
     float x[NPL];
@@ -157,9 +159,11 @@ constexpr int LN_RPW = 2;
 template <int NV, bool RMS>
 __global__ __launch_bounds__(256) void ln_bf16_v4_kernel(const float* h, int64_t rows,
                                                          const bf16_t* g, const bf16_t* b,
-                                                         float eps, bf16_t* out, int64_t ldo) {
+                                                         float eps, bf16_t* out, int64_t ldo,
+                                                         const int32_t* m_count) {
     const int64_t row0 = ((int64_t)blockIdx.x * 4 + (threadIdx.x >> 6)) * LN_RPW;
     const int lane = threadIdx.x & 63;
+    if (m_count) rows = min(rows, (int64_t)*m_count);
     if (row0 >= rows) return;
     constexpr int d = NV * 256;
     float4 x[LN_RPW][NV];
@@ -278,13 +282,13 @@ dd_status launch_embed_ln(int dtype, int norm, const int32_t* z, int64_t rows, i
 
 template <typename W, bool RMS>
 dd_status launch_ln_t(const float* h, int64_t rows, int d, const void* g, const void* b, float eps,
-                      void* out, int64_t ldo, hipStream_t s) {
+                      void* out, int64_t ldo, hipStream_t s, const int32_t* m_count) {
     const dim3 grid((unsigned)ceil_div(rows, 4)), blk(256);
     switch (d / 64) {
 #define X(n)                                                                                     \
     case n:                                                                                      \
         launch_k((ln_kernel<W, n, RMS>), grid, blk, 0, s, h, rows, (const W*)g,       \
-                           (const W*)b, eps, (W*)out, ldo);                                      \
+                           (const W*)b, eps, (W*)out, ldo, m_count);                             \
         break;
         DD_NPL_CASES(X)
 #undef X
@@ -295,15 +299,15 @@ dd_status launch_ln_t(const float* h, int64_t rows, int d, const void* g, const 
 
 template <bool RMS>
 void launch_ln_v4(int d, dim3 grid, const float* h, int64_t rows, const bf16_t* g, const bf16_t* b,
-                  float eps, bf16_t* o, int64_t ldo, hipStream_t s) {
+                  float eps, bf16_t* o, int64_t ldo, hipStream_t s, const int32_t* mc) {
     const dim3 blk(256);
-    if (d == 768) launch_k((ln_bf16_v4_kernel<3, RMS>), grid, blk, 0, s, h, rows, g, b, eps, o, ldo);
-    else if (d == 1024) launch_k((ln_bf16_v4_kernel<4, RMS>), grid, blk, 0, s, h, rows, g, b, eps, o, ldo);
-    else launch_k((ln_bf16_v4_kernel<8, RMS>), grid, blk, 0, s, h, rows, g, b, eps, o, ldo);
+    if (d == 768) launch_k((ln_bf16_v4_kernel<3, RMS>), grid, blk, 0, s, h, rows, g, b, eps, o, ldo, mc);
+    else if (d == 1024) launch_k((ln_bf16_v4_kernel<4, RMS>), grid, blk, 0, s, h, rows, g, b, eps, o, ldo, mc);
+    else launch_k((ln_bf16_v4_kernel<8, RMS>), grid, blk, 0, s, h, rows, g, b, eps, o, ldo, mc);
 }
 
 dd_status launch_ln(int dtype, int norm, const float* h, int64_t rows, int d, const void* g, const void* b,
-                    float eps, void* out, int64_t ldo, hipStream_t s) {
+                    float eps, void* out, int64_t ldo, hipStream_t s, const int32_t* m_count) {
     const bool rms = norm == DD_NORM_RMS;
     ProfScope ps(KC_LN, s);
     if (dtype == DD_BF16 && (d == 768 || d == 1024 || d == 2048) && ldo % 4 == 0) {
@@ -311,15 +315,15 @@ dd_status launch_ln(int dtype, int norm, const float* h, int64_t rows, int d, co
         const bf16_t* gg = (const bf16_t*)g;
         const bf16_t* bb = (const bf16_t*)b;
         bf16_t* o = (bf16_t*)out;
-        if (rms) launch_ln_v4<true>(d, grid, h, rows, gg, bb, eps, o, ldo, s);
-        else launch_ln_v4<false>(d, grid, h, rows, gg, bb, eps, o, ldo, s);
+        if (rms) launch_ln_v4<true>(d, grid, h, rows, gg, bb, eps, o, ldo, s, m_count);
+        else launch_ln_v4<false>(d, grid, h, rows, gg, bb, eps, o, ldo, s, m_count);
         return launch_status("layernorm");
     }
     if (dtype == DD_BF16)
-        return rms ? launch_ln_t<bf16_t, true>(h, rows, d, g, b, eps, out, ldo, s)
-                   : launch_ln_t<bf16_t, false>(h, rows, d, g, b, eps, out, ldo, s);
-    return rms ? launch_ln_t<float, true>(h, rows, d, g, b, eps, out, ldo, s)
-               : launch_ln_t<float, false>(h, rows, d, g, b, eps, out, ldo, s);
+        return rms ? launch_ln_t<bf16_t, true>(h, rows, d, g, b, eps, out, ldo, s, m_count)
+                   : launch_ln_t<bf16_t, false>(h, rows, d, g, b, eps, out, ldo, s, m_count);
+    return rms ? launch_ln_t<float, true>(h, rows, d, g, b, eps, out, ldo, s, m_count)
+               : launch_ln_t<float, false>(h, rows, d, g, b, eps, out, ldo, s, m_count);
 }
 
 bool ln_supported(int d) {

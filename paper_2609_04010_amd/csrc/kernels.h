@@ -79,6 +79,12 @@ struct GemmArgs {
     int64_t cand_ld;
     uint64_t seed;
     uint32_t step, row0;
+    // EPI_BIAS_RESID, bf16 path: the residual input when it is not C itself.  Output row m of C
+    // then adds row a_rows[m] of c_in (row m without a_rows); both have row stride ldc.
+    const float* c_in;
+    // EPI_LSE_CDF: token row of output row m when A is already compacted (takes precedence over
+    // a_rows for the noise counters)
+    const int32_t* row_ids;
 };
 
 struct AttnArgs {
@@ -132,8 +138,9 @@ dd_status launch_embed_ln(int dtype, int norm, const int32_t* z, int64_t rows, i
                           const void* b, float eps, float* h, void* xln, int64_t ldo, int32_t* err,
                           hipStream_t s);
 // out rows have stride ldo (elements) >= d
+// m_count (device, nullable): only rows < *m_count are normalised (rows bounds the grid)
 dd_status launch_ln(int dtype, int norm, const float* h, int64_t rows, int d, const void* g, const void* b,
-                    float eps, void* out, int64_t ldo, hipStream_t s);
+                    float eps, void* out, int64_t ldo, hipStream_t s, const int32_t* m_count = nullptr);
 bool ln_supported(int d);
 dd_status launch_gemm(int dtype, int epi, int cls, const GemmArgs& g, hipStream_t s);
 dd_status launch_attn(int dtype, const AttnArgs& a, hipStream_t s);
