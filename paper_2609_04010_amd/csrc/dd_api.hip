@@ -203,7 +203,7 @@ static bool is_gain(const dd_config* c, int id) {
 }
 
 struct WsLayout {
-    size_t err, temb, h, xln, qkv, att, mlp, logits, rows, count, glse, row_lse, total_fwd, total_loop;
+    size_t err, temb, h, xln, qkv, att, mlp, logits, rows, count, seq, glse, row_lse, total_fwd, total_loop;
     int64_t glse_ld;   // per-group log-sum-exps per logits row (a multiple of 4 floats)
 };
 
@@ -227,6 +227,7 @@ static WsLayout ws_layout(const dd_config* c, int64_t M) {
     off = align256(off + (size_t)(M * ld) * es);
     w.rows = off; off = align256(off + (size_t)M * 4);
     w.count = off; off = align256(off + 4);
+    w.seq = off; off = align256(off + (size_t)(M + 1) * 4);   // per-sequence list starts (B + 1 <= M + 1)
     w.glse_ld = ((c->vocab + DD_GUMBEL_GROUP - 1) / DD_GUMBEL_GROUP + 3) / 4 * 4;
     w.glse = off; off = align256(off + (size_t)(M * w.glse_ld) * 4);
     w.row_lse = off; off = align256(off + (size_t)M * 4);
@@ -257,7 +258,7 @@ static dd_status run_forward(const dd_config* c, const void* params, const int32
                              const int32_t* attn_mask = nullptr, const int32_t* lora_gate = nullptr,
                              float* vocab_lse = nullptr, int64_t lse_ld = 0,
                              int32_t* vocab_cand = nullptr, uint64_t cand_seed = 0,
-                             uint32_t cand_step = 0) {
+                             uint32_t cand_step = 0, const int32_t* vocab_seq = nullptr) {
     const std::vector<Tensor> T = tensor_list(c);
     const WsLayout w = ws_layout(c, (int64_t)B * L);
     const char* P = (const char*)params;
@@ -285,12 +286,14 @@ static dd_status run_forward(const dd_config* c, const void* params, const int32
         return launch_gemm(dt, EPI_GATE, KC_GEMM_LORA, g, s);
     };
 
-    // With vocab_rows only the listed rows get logits.  Past the last layer's attention nothing mixes
-    // rows, so the rest of that layer runs on the listed rows alone, compacted (row j is token row
-    // vocab_rows[j]): the attention-output projection gathers its rows and writes the residual rows
-    // into the q|k|v buffer, which the attention has finished with (fp32 d per row fits in bf16 3d).
-    const bool tail_rows = vocab_rows && vocab_count && r == 0 && nl > 0 && dt == DD_BF16 &&
-                           gemm_gather_supported(dt, d) && gemm_gather_supported(dt, F);
+    // With vocab_rows only the listed rows get logits.  In the last layer only the attention's keys
+    // and values mix rows, so from its queries on that layer runs on the listed rows alone,
+    // compacted (row j is token row vocab_rows[j]; vocab_seq gives each sequence's first list
+    // index): the attention takes the listed queries, and the attention-output projection adds the
+    // listed residual rows and writes them into the q|k|v buffer, which the attention has finished
+    // with (fp32 d per row fits in bf16 3d).
+    const bool tail_rows = vocab_rows && vocab_count && vocab_seq && r == 0 && nl > 0 && dt == DD_BF16 &&
+                           !attn_mask && gemm_gather_supported(dt, d) && gemm_gather_supported(dt, F);
     if (c->time_cond) DD_TRY(launch_temb(temb, d, 1000.0 * (1.0 - alpha_t), s));
     const int g0 = nl > 0 ? 2 : lnf;
     DD_TRY(launch_embed_ln(dt, c->norm, z, M, L, n_tok(c), d, tp(0), tp(1), c->time_cond ? temb : nullptr,
@@ -304,11 +307,17 @@ static dd_status run_forward(const dd_config* c, const void* params, const int32
         DD_TRY(launch_gemm(dt, EPI_BIAS, KC_GEMM_QKV, g, s));
         AttnArgs aa = {qkv, 3 * d, att, dr, B, L, H, d,
                        (float)(1.4426950408889634 / sqrt((double)(d / H))), attn_mask, err};
+        const bool tail = tail_rows && l + 1 == nl;
+        if (tail) {
+            aa.qrows = vocab_rows;
+            aa.qseq = vocab_seq;
+        }
         DD_TRY(launch_attn(dt, aa, s));
-        if (tail_rows && l + 1 == nl) {
+        if (tail) {
             float* hc = (float*)qkv;
-            g = {att, dr, tp(b + 4), dr, tp(b + 5), hc, d, (int)M, d, dr, vocab_rows, vocab_count};
+            g = {att, dr, tp(b + 4), dr, tp(b + 5), hc, d, (int)M, d, dr, nullptr, vocab_count};
             g.c_in = h;
+            g.c_rows = vocab_rows;
             DD_TRY(launch_gemm(dt, EPI_BIAS_RESID, KC_GEMM_O, g, s));
             DD_TRY(launch_ln(dt, c->norm, hc, M, d, tp(b + 6), tp(b + 7), c->norm_eps, xln, dr, s, vocab_count));
             g = {xln, dr, tp(b + 8), dr, tp(b + 9), mlp, Fr, (int)M, F, dr, nullptr, vocab_count};
@@ -673,6 +682,7 @@ dd_status dd_psi_sample_loop(const dd_config* cfg, const void* params, int32_t B
     const bool compact = cfg->prior == DD_PRIOR_MASK && gemm_gather_supported(cfg->dtype, cfg->d_model);
     int32_t* rows = (int32_t*)(wsc + w.rows);
     int32_t* count = (int32_t*)(wsc + w.count);
+    int32_t* seq = (int32_t*)(wsc + w.seq);
     float* row_lse = (float*)(wsc + w.row_lse);
     // bf16 path: the vocabulary projection also emits each row's per-group log-sum-exps, so the
     // draw reads one group of logits per row instead of the whole row.  DD_LOOP_POSTERIOR_PASS keeps
@@ -687,10 +697,10 @@ dd_status dd_psi_sample_loop(const dd_config* cfg, const void* params, int32_t B
     }
     DD_TRY(trace_copy(0));
     for (int k = T; k >= 1; --k) {
-        if (compact) DD_TRY(launch_compact(z, M, cfg->mask_id, rows, count, s));
+        if (compact) DD_TRY(launch_compact(z, M, cfg->mask_id, rows, count, s, L, seq));
         DD_TRY(run_forward(cfg, params, z, B, L, alphas[k], logits, ld, wsc, s,
                            compact ? rows : nullptr, compact ? count : nullptr, nullptr, nullptr,
-                           glse, w.glse_ld, cand, noise_seed, (uint32_t)k));
+                           glse, w.glse_ld, cand, noise_seed, (uint32_t)k, compact ? seq : nullptr));
         const uint32_t* nw = noise_words ? noise_words + (int64_t)(k - 1) * M * nu : nullptr;
         PostArgs a = make_post(cfg->prior, logits, ld, (int32_t)M, cfg->vocab, z, alphas[k],
                                alphas[k - 1], kappas ? kappas[k] : 1.0, nw, noise_seed, (uint32_t)k,

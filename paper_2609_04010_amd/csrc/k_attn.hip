@@ -93,7 +93,7 @@ DD_DEV void query_window(const AttnArgs& a, int qi, int& pre, int& lo, int& hi) 
     }
 }
 
-template <bool MASKED>
+template <bool MASKED, bool LISTED = false>
 __global__ __launch_bounds__(256, MASKED ? 3 : 4) void attn_bf16_kernel(AttnArgs a) {
     __shared__ __attribute__((aligned(1024))) bf16_t Ks[2][AK * KROW];
     __shared__ __attribute__((aligned(1024))) bf16_t Vs[2][AK * KROW];
@@ -124,8 +124,15 @@ __global__ __launch_bounds__(256, MASKED ? 3 : 4) void attn_bf16_kernel(AttnArgs
     const int L = a.L, d = a.d;
     const bf16_t* base = (const bf16_t*)a.qkv + (int64_t)b * L * a.ld;
     const int q0 = qb * AQ + wave * 32;
-    const int qi = q0 + (lane & 31);
+    int qi = q0 + (lane & 31);
     const int grp = lane >> 5;
+    if constexpr (LISTED) {
+        // query block qb of sequence b's listed rows; qi becomes the position of this lane's query
+        // (L: none).  The test is the same for the whole workgroup, so it leaves before any barrier.
+        const int s0 = a.qseq[b], s1 = a.qseq[b + 1];
+        if (s0 + qb * AQ >= s1) return;
+        qi = s0 + qi < s1 ? a.qrows[s0 + qi] - b * L : L;
+    }
 
     bf16x8 qf[4];
 #pragma unroll
@@ -345,7 +352,9 @@ __global__ __launch_bounds__(256, MASKED ? 3 : 4) void attn_bf16_kernel(AttnArgs
     const float l = lpart + __shfl_xor(lpart, 32, 64);
     const float inv = 1.0f / l;
     if (qi < L) {
-        bf16_t* out = (bf16_t*)a.out + ((int64_t)b * L + qi) * a.ldo + h * DH;
+        // listed queries are written in list order
+        const int64_t orow = LISTED ? (int64_t)a.qseq[b] + q0 + (lane & 31) : (int64_t)b * L + qi;
+        bf16_t* out = (bf16_t*)a.out + orow * a.ldo + h * DH;
 #pragma unroll
         for (int blk = 0; blk < 2; ++blk)
 #pragma unroll
@@ -418,9 +427,14 @@ dd_status launch_attn(int dtype, const AttnArgs& a0, hipStream_t s) {
     // the query blocks of hgroup (batch, head) pairs
     const int nqb = ceil_div(a.L, AQ);
     a.hgroup = std::max(1, (num_cus_attn() / 8) * 3 / nqb);
+    if (a.qrows && (dtype != DD_BF16 || a.mask || !a.qseq)) {
+        set_error("listed queries need the bf16 path, no pattern and the sequence starts");
+        return DD_E_UNSUPPORTED;
+    }
     if (dtype == DD_BF16) {
         const dim3 grid((unsigned)(nqb * a.H * a.B));
         if (a.mask) launch_k(attn_bf16_kernel<true>, grid, dim3(256), 0, s, a);
+        else if (a.qrows) launch_k((attn_bf16_kernel<false, true>), grid, dim3(256), 0, s, a);
         else launch_k(attn_bf16_kernel<false>, grid, dim3(256), 0, s, a);
     } else {
         const int64_t n = (int64_t)a.B * a.H * a.L;

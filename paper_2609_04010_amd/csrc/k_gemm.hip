@@ -816,7 +816,7 @@ __global__ __launch_bounds__(64 * WGM_ * WGN_, 1) void gemm_bf16_dl_kernel(GemmA
         if constexpr (EPI == EPI_BIAS_RESID) {
             // residual epilogue: start from h (this lane's MFMA output positions), fetched together
             // with the tile's first K-tile instead of after the K loop.  h is C itself, or (not in
-            // the ring form) the rows of c_in that the output rows gather
+            // the ring form) the rows of c_in that c_rows lists
             const float* C = (const float*)g.C;
             int64_t hrow[MB];
 #pragma unroll
@@ -824,7 +824,7 @@ __global__ __launch_bounds__(64 * WGM_ * WGN_, 1) void gemm_bf16_dl_kernel(GemmA
                 const int m = m0 + wm * S::WM + j * 32 + (lane & 31);
                 hrow[j] = m;
                 if constexpr (!RING) {
-                    if (g.c_in && g.a_rows && m < M) hrow[j] = g.a_rows[m];
+                    if (g.c_in && g.c_rows && m < M) hrow[j] = g.c_rows[m];
                 }
             }
             if constexpr (!RING) {
@@ -1069,12 +1069,12 @@ dd_status launch_gemm(int dtype, int epi, int cls, const GemmArgs& g, hipStream_
         set_error("GEMM with K = %d", g.K);
         return DD_E_ARG;
     }
-    if ((g.a_rows || g.m_count || g.c_in || g.row_ids) && !gemm_gather_supported(dtype, g.K)) {
+    if ((g.a_rows || g.m_count || g.c_in || g.c_rows || g.row_ids) && !gemm_gather_supported(dtype, g.K)) {
         set_error("row-gathered GEMM needs the bf16 path and K %% 128 == 0");
         return DD_E_UNSUPPORTED;
     }
-    if (g.c_in && epi != EPI_BIAS_RESID) {
-        set_error("a separate residual input needs the residual epilogue");
+    if ((g.c_in && epi != EPI_BIAS_RESID) || (g.c_rows && !g.c_in)) {
+        set_error("a separate residual input (and its row list) needs the residual epilogue");
         return DD_E_ARG;
     }
     if ((epi == EPI_LSE || epi == EPI_LSE_CDF) &&

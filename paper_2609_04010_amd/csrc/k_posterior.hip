@@ -445,11 +445,12 @@ constexpr int CT = 1024;
 
 __global__ __launch_bounds__(CT) void compact_masked_kernel(const int32_t* z, int64_t M,
                                                             int32_t mask_id, int32_t* idx,
-                                                            int32_t* count) {
+                                                            int32_t* count, int L, int32_t* seq) {
     __shared__ int wsum[CT / 64];
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const bool vec = ((uintptr_t)z & 15) == 0;
     int base = 0;   // rows listed by earlier blocks (the same in every thread)
+    const float inv_l = seq ? 1.0f / (float)L : 0.f;
     for (int64_t b0 = 0; b0 < M; b0 += 4 * CT) {
         const int64_t i0 = b0 + 4 * (int64_t)tid;
         int f[4];
@@ -477,19 +478,43 @@ __global__ __launch_bounds__(CT) void compact_masked_kernel(const int32_t* z, in
             total += v;
         }
         int pos = base + before + incl - c;
+        if (seq) {
+            // a sequence that starts at one of this thread's rows starts at list index pos + (rows
+            // listed before it among the four); nb = the first multiple of L at or after i0 (a
+            // float quotient, corrected to the exact one)
+            int q = (int)((float)i0 * inv_l);
+            while (q > 0 && (int64_t)(q - 1) * L >= i0) --q;
+            while ((int64_t)q * L < i0) ++q;
+            int nb = q * L, p = pos;
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                if ((int)i0 + e == nb && nb < M) {
+                    seq[nb / L] = p;
+                    nb += L;
+                }
+                p += f[e];
+            }
+        }
 #pragma unroll
         for (int e = 0; e < 4; ++e)
             if (f[e]) idx[pos++] = (int32_t)(i0 + e);
         base += total;
         __syncthreads();   // wsum is rewritten by the next block
     }
-    if (tid == 0) *count = base;
+    if (tid == 0) {
+        *count = base;
+        if (seq) seq[M / L] = base;
+    }
 }
 
 dd_status launch_compact(const int32_t* z, int64_t M, int32_t mask_id, int32_t* idx, int32_t* count,
-                         hipStream_t s) {
+                         hipStream_t s, int L, int32_t* seq) {
+    if (seq && (L <= 0 || M % L != 0)) {
+        set_error("sequence starts need rows of L > 0 tokens (M = %lld, L = %d)", (long long)M, L);
+        return DD_E_ARG;
+    }
     ProfScope ps(KC_COMPACT, s);
-    launch_k(compact_masked_kernel, dim3(1), dim3(CT), 0, s, z, M, mask_id, idx, count);
+    launch_k(compact_masked_kernel, dim3(1), dim3(CT), 0, s, z, M, mask_id, idx, count, L, seq);
     return launch_status("compact_masked");
 }
 

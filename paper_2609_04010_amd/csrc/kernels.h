@@ -80,8 +80,9 @@ struct GemmArgs {
     uint64_t seed;
     uint32_t step, row0;
     // EPI_BIAS_RESID, bf16 path: the residual input when it is not C itself.  Output row m of C
-    // then adds row a_rows[m] of c_in (row m without a_rows); both have row stride ldc.
+    // then adds row c_rows[m] of c_in (row m when c_rows is NULL); both have row stride ldc.
     const float* c_in;
+    const int32_t* c_rows;
     // EPI_LSE_CDF: token row of output row m when A is already compacted (takes precedence over
     // a_rows for the noise counters)
     const int32_t* row_ids;
@@ -100,6 +101,11 @@ struct AttnArgs {
     const int32_t* mask;
     int32_t* err;
     int hgroup;   // set by launch_attn: (batch, head) pairs per dispatch group of the pattern kernel
+    // listed queries only (bf16, no pattern; nullable): qrows is a row list sorted by row, qseq[b]
+    // the index in it of sequence b's first row (qseq[B] = its length).  Output row j is the query
+    // at token row qrows[j]; every key of its sequence is still visible.
+    const int32_t* qrows;
+    const int32_t* qseq;
 };
 
 dd_status launch_posterior(const PostArgs& a, int logits_dtype, hipStream_t s);
@@ -145,8 +151,9 @@ bool ln_supported(int d);
 dd_status launch_gemm(int dtype, int epi, int cls, const GemmArgs& g, hipStream_t s);
 dd_status launch_attn(int dtype, const AttnArgs& a, hipStream_t s);
 bool attn_supported(int dtype, int dh);
+// seq (device, nullable): seq[b] = listed rows before row b L for b = 0..M/L (rows of L tokens)
 dd_status launch_compact(const int32_t* z, int64_t M, int32_t mask_id, int32_t* idx, int32_t* count,
-                         hipStream_t s);
+                         hipStream_t s, int L = 0, int32_t* seq = nullptr);
 bool gemm_gather_supported(int dtype, int K);
 // the EPI_LSE epilogue (group log-sum-exps beside the logits) runs for this dtype and K
 bool gemm_lse_supported(int dtype, int K);

@@ -278,18 +278,34 @@ def test_forward_parity_every_gemm_tile(tile, monkeypatch):
     assert err <= LOGIT_TOL["bf16"]
 
 
-@pytest.mark.parametrize("c,over,B,L,T", [(2, dict(n_layers=2), 2, 300, 6), (5, dict(n_layers=1), 1, 520, 4)])
-def test_compacted_loop_equals_full_path_loop(c, over, B, L, T):
-    """dd_sample_loop (vocabulary projection and draw on the still-masked rows only) must give the
-    same trajectory as dd_denoise_forward + dd_posterior_sample applied to every row.  (The loop's
-    group log-sum-exps come from the projection's epilogue, the entry point's from its own pass:
+def _mixed_start(B, L, V, seed):
+    """Sequence 0 fully decoded (no listed row), sequence 1 masked at a random third of its
+    positions, the others all masked."""
+    rng = np.random.default_rng(seed)
+    z1 = rng.integers(0, V, size=(B, L)).astype(np.int32)
+    if B > 1:
+        z1[1, rng.random(L) < 1 / 3] = V
+    z1[2:] = V
+    return z1
+
+
+@pytest.mark.parametrize("c,over,B,L,T,start", [
+    (2, dict(n_layers=2), 2, 300, 6, "all_mask"),
+    (5, dict(n_layers=1), 1, 520, 4, "all_mask"),
+    (2, dict(n_layers=1, vocab=1000), 3, 200, 4, "mixed"),   # a sequence with no listed row
+])
+def test_compacted_loop_equals_full_path_loop(c, over, B, L, T, start):
+    """dd_sample_loop (vocabulary projection and draw on the still-masked rows only, and the last
+    layer from its attention queries on as well) must give the same trajectory as
+    dd_denoise_forward + dd_posterior_sample applied to every row.  (The loop's group
+    log-sum-exps come from the projection's epilogue, the entry point's from its own pass:
     summation order only, which no draw at these seeds is close enough to feel.)"""
     torch = torch_or_skip()
-    say("compacted loop", c, over, B, L, T)
+    say("compacted loop", c, over, B, L, T, start)
     cfg = workloads.model_cfg(c, **over)
     V = cfg["vocab"]
     _, buf = _params_seeded(torch, cfg, 41)
-    z1 = workloads.all_mask(B, L, V)
+    z1 = workloads.all_mask(B, L, V) if start == "all_mask" else _mixed_start(B, L, V, 7)
     al = osched.alphas(T)
     _, trace = _loop_gpu(torch, cfg, buf, z1, T, al, seed=77)
     M = B * L
