@@ -453,6 +453,16 @@ __global__ __launch_bounds__(CT) void compact_masked_kernel(const int32_t* z, in
     const float inv_l = seq ? 1.0f / (float)L : 0.f;
     for (int64_t b0 = 0; b0 < M; b0 += 4 * CT) {
         const int64_t i0 = b0 + 4 * (int64_t)tid;
+        // the first sequence start at or after row i0: row nb of sequence sq (a float quotient, at
+        // most two below ceil(i0 / L), then raised to it; independent of the load below)
+        int64_t nb = 0;
+        int sq = 0;
+        if (seq) {
+            sq = max((int)((float)i0 * inv_l) - 1, 0);
+#pragma unroll
+            for (int k = 0; k < 3; ++k) sq += (int64_t)sq * L < i0;
+            nb = (int64_t)sq * L;
+        }
         int f[4];
         if (vec && i0 + 3 < M) {
             const int4 v = *(const int4*)(z + i0);
@@ -480,16 +490,12 @@ __global__ __launch_bounds__(CT) void compact_masked_kernel(const int32_t* z, in
         int pos = base + before + incl - c;
         if (seq) {
             // a sequence that starts at one of this thread's rows starts at list index pos + (rows
-            // listed before it among the four); nb = the first multiple of L at or after i0 (a
-            // float quotient, corrected to the exact one)
-            int q = (int)((float)i0 * inv_l);
-            while (q > 0 && (int64_t)(q - 1) * L >= i0) --q;
-            while ((int64_t)q * L < i0) ++q;
-            int nb = q * L, p = pos;
+            // listed before it among the four)
+            int p = pos;
 #pragma unroll
             for (int e = 0; e < 4; ++e) {
-                if ((int)i0 + e == nb && nb < M) {
-                    seq[nb / L] = p;
+                if (i0 + e == nb && nb < M) {
+                    seq[sq++] = p;
                     nb += L;
                 }
                 p += f[e];
