@@ -41,22 +41,43 @@ def log(*a):
     print(*a, file=sys.stderr, flush=True)
 
 
-def algorithmic_units(cls, cfg, B, L, vocab_rows=None):
-    """(algorithmic amount per launch, unit, bound) of a kernel class: 2 M N K flops per GEMM,
-    4 B L^2 d flops per attention launch.  vocab_rows: average rows per vocabulary projection when
-    the loop projects only the still-masked rows (default: all B L rows)."""
-    M, d, F, V, H = B * L, cfg["d_model"], cfg["d_mlp"], cfg["vocab"], cfg["n_heads"]
+TRIMMED = ("attention", "gemm_attn_out", "gemm_mlp_up", "gemm_mlp_down")
+
+
+def algorithmic_units(cls, cfg, B, L, rows=None):
+    """(algorithmic amount per launch, unit, bound) of a kernel class: 2 rows N K flops per GEMM,
+    4 rows L d flops per attention launch (rows queries, each against the L keys of its sequence).
+    rows: average rows per launch (default: all B L rows)."""
+    M, d, F, V = B * L, cfg["d_model"], cfg["d_mlp"], cfg["vocab"]
+    R = M if rows is None else rows
     flops = {
-        "gemm_qkv": 2.0 * M * d * 3 * d,
-        "gemm_attn_out": 2.0 * M * d * d,
-        "gemm_mlp_up": 2.0 * M * d * F,
-        "gemm_mlp_down": 2.0 * M * F * d,
-        "gemm_vocab": 2.0 * (M if vocab_rows is None else vocab_rows) * d * V,
-        "attention": 4.0 * B * L * L * d,
+        "gemm_qkv": 2.0 * R * d * 3 * d,
+        "gemm_attn_out": 2.0 * R * d * d,
+        "gemm_mlp_up": 2.0 * R * d * F,
+        "gemm_mlp_down": 2.0 * R * F * d,
+        "gemm_vocab": 2.0 * R * d * V,
+        "attention": 4.0 * R * L * d,
     }
     if cls in flops:
         return flops[cls], "TFLOP/s", "mfma"
     return None, None, None
+
+
+def launch_rows(cls, cfg, B, L, T, n, masked, trimmed):
+    """Average rows of the first n launches of a class in back-to-back sampling loops.  masked[s]:
+    rows still masked before the loop's step T - s (None: the loop does not compact).  The
+    vocabulary projection runs on those rows only; with `trimmed` so do the last layer's attention
+    queries, attention output, MLP up and MLP down (every other launch takes all B L rows)."""
+    M, nl = B * L, cfg["n_layers"]
+    if masked is None or n <= 0:
+        return M
+    per_step = 1 if cls == "gemm_vocab" else nl
+    total = 0
+    for i in range(n):
+        s = (i // per_step) % T
+        listed = cls == "gemm_vocab" or (trimmed and cls in TRIMMED and i % per_step == per_step - 1)
+        total += masked[s] if listed else M
+    return total / n
 
 
 def cpu_model():
@@ -364,8 +385,10 @@ def main():
     # so the first warm-up pass keeps the trajectory (the same in every pass: same inputs and noise)
     # to count them.
     compacted = cfg["prior"] == "mask" and cfg["dtype"] == "bf16" and cfg["d_model"] % 128 == 0
+    # ... and then the last layer, from its attention queries on, runs on those rows as well
+    trimmed = compacted and cfg["d_mlp"] % 128 == 0 and cfg.get("lora_rank", 0) == 0 and cfg["n_layers"] > 0
     trace = torch.empty(((T + 1) * M,), dtype=torch.int32, device=dev) if compacted else None
-    vocab_rows = None
+    masked = None
 
     # warm-up; the first pass also times every kernel class to find the dominant one
     per_job_launches = T * (8 * cfg["n_layers"] + 8) + 8 + (T + 1)   # + the trace copies
@@ -379,11 +402,10 @@ def main():
             dd.profile_end()
             prof = dd.profile_read()
             if compacted:   # rows still masked before steps T .. 1 = trace slots 0 .. T-1
-                masked = (trace.view(T + 1, M)[:T] == V).sum().item()
-                vocab_rows = masked / T
+                masked = (trace.view(T + 1, M)[:T] == V).sum(dim=1).tolist()
             ranked = sorted(prof.items(), key=lambda kv: -kv[1][1])
             log("warm-up kernel classes (launches, ms):", {k: (v[0], round(v[1], 2)) for k, v in ranked})
-            dominant = next(k for k, _ in ranked if algorithmic_units(k, cfg, B, L, vocab_rows)[0] is not None)
+            dominant = next(k for k, _ in ranked if algorithmic_units(k, cfg, B, L)[0] is not None)
     assert dd.read_device_error(ws[:4].view(torch.int32)) == 0
 
     # The dominant class is timed live with HIP events on the library's stream (recorded by the
@@ -400,7 +422,8 @@ def main():
     prof = dd.profile_read()
     elapsed = t1 - t0
     n_l, ms_l = prof[dominant]
-    per_launch, unit, bound = algorithmic_units(dominant, cfg, B, L, vocab_rows)
+    rows = launch_rows(dominant, cfg, B, L, T, n_l, masked, trimmed)
+    per_launch, unit, bound = algorithmic_units(dominant, cfg, B, L, rows)
     achieved = per_launch / (ms_l / n_l * 1e-3) / 1e12
     peak = PEAK_BF16_TFLOPS if cfg["dtype"] == "bf16" else PEAK_FP32_TFLOPS
     if cfg["dtype"] != "bf16":   # the fp32 validation build multiplies with vector FMAs, not MFMA

@@ -23,8 +23,27 @@ def test_algorithmic_flops_of_the_gpt2s_workload():
     assert bench.algorithmic_units("attention", cfg, B, L)[0] == 4.0 * B * L * L * 768
     # the vocabulary projection counts the rows it actually projects
     assert bench.algorithmic_units("gemm_vocab", cfg, B, L)[0] == 2.0 * M * 768 * 50257
-    assert bench.algorithmic_units("gemm_vocab", cfg, B, L, vocab_rows=8192.5)[0] == 2.0 * 8192.5 * 768 * 50257
+    assert bench.algorithmic_units("gemm_vocab", cfg, B, L, rows=8192.5)[0] == 2.0 * 8192.5 * 768 * 50257
+    assert bench.algorithmic_units("attention", cfg, B, L, rows=100)[0] == 4.0 * 100 * L * 768
     assert bench.algorithmic_units("layernorm", cfg, B, L) == (None, None, None)
+
+
+def test_launch_rows_follow_the_compacted_loop():
+    """Rows of the timed launches: every launch takes all B L rows, except the vocabulary
+    projection (the still-masked rows of its step) and, in a trimmed loop, the last layer's
+    attention, attention output and MLPs (the same rows)."""
+    cfg = workloads.model_cfg(2, n_layers=3)
+    B, L, T = 2, 8, 4
+    M = B * L
+    masked = [16, 12, 7, 3]                       # before steps 4, 3, 2, 1
+    assert bench.launch_rows("gemm_mlp_up", cfg, B, L, T, 5, None, True) == M
+    # vocabulary: one launch per step, wrapping into the next loop after T launches
+    assert bench.launch_rows("gemm_vocab", cfg, B, L, T, 6, masked, False) == (16 + 12 + 7 + 3 + 16 + 12) / 6
+    # three layers per step: launches 0, 1 take all rows, launch 2 (last layer) the listed ones
+    assert bench.launch_rows("gemm_mlp_down", cfg, B, L, T, 6, masked, True) == (4 * M + 16 + 12) / 6
+    assert bench.launch_rows("gemm_mlp_down", cfg, B, L, T, 6, masked, False) == M
+    assert bench.launch_rows("gemm_qkv", cfg, B, L, T, 6, masked, True) == M
+    assert bench.launch_rows("attention", cfg, B, L, T, 3, masked, True) == (2 * M + 16) / 3
 
 
 def _record(tmp_path, sha, cls="gemm_mlp_down"):
