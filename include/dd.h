@@ -145,8 +145,8 @@ size_t dd_param_bytes(const dd_config* cfg);
  * first int32).  0 if the configuration is invalid. */
 size_t dd_workspace_bytes(const dd_config* cfg, int32_t B, int32_t L);
 /* Workspace for dd_sample_loop: the forward workspace plus one logit matrix,
- * the compacted row list, the per-group log-sum-exps of every logit row and one
- * row log-sum-exp per token row. */
+ * the compacted row list with each sequence's first index in it, the per-group
+ * log-sum-exps of every logit row and one row log-sum-exp per token row. */
 size_t dd_loop_workspace_bytes(const dd_config* cfg, int32_t B, int32_t L);
 
 /*
@@ -338,7 +338,10 @@ dd_status dd_psi_posterior_sample(int32_t prior, const void* logits, int32_t log
  *                each step.
  *   ws           device workspace >= dd_loop_workspace_bytes(cfg, B, L).
  * Masked prior (bf16): each step lists the still-masked rows and runs the vocabulary projection
- * and the draw on those rows only; carried-over rows need no logits.  bf16 with d_model % 128
+ * and the draw on those rows only; carried-over rows need no logits.  With d_model and d_mlp
+ * multiples of 128 and no adapters, the last layer also runs on those rows alone from its
+ * attention queries on (keys and values still cover every row), since past that point a row's
+ * values reach only its own logits; the listed rows' logits are unchanged.  bf16 with d_model % 128
  * == 0: the vocabulary projection also writes, beside each logit row, the log-sum-exp of each
  * group of DD_GUMBEL_GROUP classes (from the rounded logits it stores), and the draw reads those
  * and one group of logits per row instead of the whole row.  The result equals calling
