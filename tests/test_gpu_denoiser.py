@@ -293,6 +293,8 @@ def _mixed_start(B, L, V, seed):
     (2, dict(n_layers=2), 2, 300, 6, "all_mask"),
     (5, dict(n_layers=1), 1, 520, 4, "all_mask"),
     (2, dict(n_layers=1, vocab=1000), 3, 200, 4, "mixed"),   # a sequence with no listed row
+    (2, dict(n_layers=1, vocab=1000), 3, 203, 4, "mixed"),   # sequence starts inside a 4-row group
+    (2, dict(n_layers=1, vocab=300), 6, 3, 3, "mixed"),      # several starts in one 4-row group
 ])
 def test_compacted_loop_equals_full_path_loop(c, over, B, L, T, start):
     """dd_sample_loop (vocabulary projection and draw on the still-masked rows only, and the last
