@@ -65,9 +65,10 @@ def algorithmic_units(cls, cfg, B, L, rows=None):
 
 def launch_rows(cls, cfg, B, L, T, n, masked, trimmed):
     """Average rows of the first n launches of a class in back-to-back sampling loops.  masked[s]:
-    rows still masked before the loop's step T - s (None: the loop does not compact).  The
-    vocabulary projection runs on those rows only; with `trimmed` so do the last layer's attention
-    queries, attention output, MLP up and MLP down (every other launch takes all B L rows)."""
+    the rows the loop lists at its step T - s, i.e. the masked rows that step unmasks (None: the
+    loop does not compact).  The vocabulary projection runs on those rows only; with `trimmed` so
+    do the last layer's attention queries, attention output, MLP up and MLP down (every other
+    launch takes all B L rows)."""
     M, nl = B * L, cfg["n_layers"]
     if masked is None or n <= 0:
         return M
@@ -401,8 +402,9 @@ def main():
         if i == 0:
             dd.profile_end()
             prof = dd.profile_read()
-            if compacted:   # rows still masked before steps T .. 1 = trace slots 0 .. T-1
-                masked = (trace.view(T + 1, M)[:T] == V).sum(dim=1).tolist()
+            if compacted:   # rows that step T - s unmasks: masked in trace slot s, not in slot s + 1
+                tr = trace.view(T + 1, M)
+                masked = ((tr[:T] == V) & (tr[1:] != V)).sum(dim=1).tolist()
             ranked = sorted(prof.items(), key=lambda kv: -kv[1][1])
             log("warm-up kernel classes (launches, ms):", {k: (v[0], round(v[1], 2)) for k, v in ranked})
             dominant = next(k for k, _ in ranked if algorithmic_units(k, cfg, B, L)[0] is not None)

@@ -7,10 +7,15 @@ made.  The reading adopted here is a two-level Gumbel-max draw, exact for any
 partition of the classes into groups:
 
   groups     real classes in contiguous groups of GROUP = 256
-             ([0,256), [256,512), ..., [.., V)); for the masked prior the
-             mask class V is one more, singleton group (the last one).
-  level 1    g* = argmax_g  log M_g + G_g,   M_g = sum_{j in g} p_j,
-             G_g = Gumbel of word (STREAM_TOP, step, row, g).
+             ([0,256), [256,512), ..., [.., V)).
+  stage 0    masked prior only: the mask class V is taken iff u < p_V, with
+             u = uniform of word (STREAM_TOP, step, row, n_groups) (the word
+             after the real groups' level-1 words).  Under App. A.1 eq.
+             (mdm-posterior) and App. A.4 eq. (psi-mdm) p_V does not depend on
+             x_theta, so this decision needs no logits; otherwise the draw goes
+             on over the real classes, whose probabilities sum to 1 - p_V.
+  level 1    g* = argmax_g  log M_g + G_g over the real groups,
+             M_g = sum_{j in g} p_j, G_g = Gumbel of word (STREAM_TOP, step, row, g).
   level 2    z_s = argmax_{j in g*}  log p_j + G_j,
              G_j = Gumbel of word (STREAM_CLASS, step, row, j).
   ties       the lowest index wins at both levels; log 0 = -inf.
@@ -28,11 +33,12 @@ Level 1 is the same in both readings (same words, same group).  Level 2' picks
 j with probability p_j / M_g because u is uniform on (0, 1) and independent of
 the level-1 noise, so the pair is again an exact draw from p.
 
-Exactness: the maximum over a group of log p_j + G_j is distributed as
-log M_g plus a standard Gumbel and is independent of the group's argmax, so
-level 1 picks group g with probability M_g and level 2 picks j with
-probability p_j / M_g (the Gumbel-max property; Maddison, Tarlow, Minka,
-"A* sampling", NeurIPS 2014, sec. 3).
+Exactness: stage 0 takes the mask with probability p_V.  The maximum over a
+group of log p_j + G_j is distributed as log M_g plus a standard Gumbel and is
+independent of the group's argmax, so level 1 picks group g with probability
+M_g / sum of the real M's and level 2 picks j with probability p_j / M_g (the
+Gumbel-max property; Maddison, Tarlow, Minka, "A* sampling", NeurIPS 2014,
+sec. 3).  Together, class j is drawn with probability (1 - p_V) p_j / (1 - p_V).
 
 Explicit-noise layout per row: NU = n_top + V words, the n_top level-1
 words first, then one level-2 word per real class.
@@ -43,7 +49,7 @@ closed forms eqs. (psi-mdm) and (psi-usdm)) with correction strength kappa in
 unmasked position's x_theta is the one-hot of its token (the carry-over
 parameterisation that makes kappa = 1 keep it), so under eq. (psi-mdm) the
 token is kept with probability a_s + kappa (1 - a_s) and remasked with
-probability (1 - kappa)(1 - a_s); its logits are never read.
+probability (1 - kappa)(1 - a_s) (stage 0 decides); its logits are never read.
 
 Pinned by chi-square tests of many draws against the enumerated posterior and
 against the flat (one Gumbel per class) Gumbel-max draw; psi_sample by equality
@@ -117,19 +123,32 @@ def _first_argmax_and_gap(scores):
     return i, float(scores[i] - second) if np.isfinite(second) else np.inf
 
 
+def mask_first(p, row, noise, V):
+    """Masked prior, stage 0: the mask class is taken iff u < p_mask, with u the uniform of the
+    mask group's level-1 word.  Returns (taken, gap) with gap = |u - p_mask|."""
+    u = float(_nz.uniform(noise.top(row, n_top("mask", V))[n_groups_real(V)]))
+    pm = float(p[V])
+    return u < pm, abs(u - pm)
+
+
 def sample_from_probs(prior, p, row, noise):
-    """Two-level Gumbel-max draw from probabilities p over K classes.
+    """Two-level Gumbel-max draw from probabilities p over K classes (masked prior: stage 0
+    first, then the two levels over the real classes).
 
     Returns (class id, level-1 gap, level-2 gap)."""
     V = p.shape[0] - (1 if prior == "mask" else 0)
-    bounds = group_bounds(prior, V)
+    bounds = group_bounds("uniform", V)
+    gap0 = np.inf
+    if prior == "mask":
+        taken, gap0 = mask_first(p, row, noise, V)
+        if taken:
+            return V, gap0, np.inf
     with np.errstate(divide="ignore"):
         logM = np.log(np.array([p[a:b].sum() for a, b in bounds]))
         G = _nz.gumbel(noise.top(row, len(bounds)))
         g, gap1 = _first_argmax_and_gap(logM + G)
+        gap1 = min(gap1, gap0)
         a, b = bounds[g]
-        if prior == "mask" and a == V:
-            return V, gap1, np.inf
         idx = np.arange(a, b)
         s = np.log(p[a:b]) + _nz.gumbel(noise.cls(row, idx))
     j, gap2 = _first_argmax_and_gap(s)
@@ -159,14 +178,18 @@ def sample_from_probs_cdf(prior, p, row, noise):
 
     Returns (class id, level-1 gap, level-2 gap); the level-2 gap is relative mass (inverse_cdf)."""
     V = p.shape[0] - (1 if prior == "mask" else 0)
-    bounds = group_bounds(prior, V)
+    bounds = group_bounds("uniform", V)
+    gap0 = np.inf
+    if prior == "mask":
+        taken, gap0 = mask_first(p, row, noise, V)
+        if taken:
+            return V, gap0, np.inf
     with np.errstate(divide="ignore"):
         logM = np.log(np.array([p[a:b].sum() for a, b in bounds]))
         G = _nz.gumbel(noise.top(row, len(bounds)))
     g, gap1 = _first_argmax_and_gap(logM + G)
+    gap1 = min(gap1, gap0)
     a, b = bounds[g]
-    if prior == "mask" and a == V:
-        return V, gap1, np.inf
     j, gap2 = inverse_cdf(p[a:b], noise.group_u(row, g))
     return a + j, gap1, gap2
 

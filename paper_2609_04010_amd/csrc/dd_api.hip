@@ -697,14 +697,16 @@ dd_status dd_psi_sample_loop(const dd_config* cfg, const void* params, int32_t B
     }
     DD_TRY(trace_copy(0));
     for (int k = T; k >= 1; --k) {
-        if (compact) DD_TRY(launch_compact(z, M, cfg->mask_id, rows, count, s, L, seq));
-        DD_TRY(run_forward(cfg, params, z, B, L, alphas[k], logits, ld, wsc, s,
-                           compact ? rows : nullptr, compact ? count : nullptr, nullptr, nullptr,
-                           glse, w.glse_ld, cand, noise_seed, (uint32_t)k, compact ? seq : nullptr));
         const uint32_t* nw = noise_words ? noise_words + (int64_t)(k - 1) * M * nu : nullptr;
         PostArgs a = make_post(cfg->prior, logits, ld, (int32_t)M, cfg->vocab, z, alphas[k],
                                alphas[k - 1], kappas ? kappas[k] : 1.0, nw, noise_seed, (uint32_t)k,
                                0u, z, row_lse, nullptr, (int32_t*)(wsc + w.err));
+        // the list holds the masked rows that stage 0 of the draw unmasks: the others stay masked
+        // whatever their logits
+        if (compact) DD_TRY(launch_compact(z, M, cfg->mask_id, rows, count, s, L, seq, &a));
+        DD_TRY(run_forward(cfg, params, z, B, L, alphas[k], logits, ld, wsc, s,
+                           compact ? rows : nullptr, compact ? count : nullptr, nullptr, nullptr,
+                           glse, w.glse_ld, cand, noise_seed, (uint32_t)k, compact ? seq : nullptr));
         if (compact) {
             // kappa < 1: the rows unmasked before this step keep or remask first (they read no
             // logits and are not in the compacted list, which was taken before the step)

@@ -74,24 +74,23 @@ DD_DEV int wave_argmax(float s, int i) {
     return i;
 }
 
-// Keep-or-remask draw of an unmasked row (masked prior, kappa < 1): the two-level draw over a
-// distribution whose only classes are the token (in group zt / GROUP) and the mask (its own group,
-// index ngroups), so level 1 decides; ties go to the token's (lower) group.
+// Stage 0 of the masked prior's draw: the uniform u(w) = (w + 1/2) 2^-32 of the mask group's
+// level-1 word (index ngroups of the row's level-1 words), exact in double.  The mask class is
+// taken iff u < its probability, which does not depend on the logits (App. A.1: the mask weight
+// (1 - a_s)/(1 - a_t), or the Psi form, App. A.4), so the decision can be made before them.
+DD_DEV double mask_word_uniform(const uint32_t* noise, int nu, int V, uint64_t seed, uint32_t step,
+                                uint32_t grow, int row) {
+    const int ngroups = (V + DD_GUMBEL_GROUP - 1) / DD_GUMBEL_GROUP;
+    const uint32_t w = noise ? noise[(int64_t)row * nu + ngroups]
+                             : counter_word(seed, STREAM_TOP, step, grow, (uint32_t)ngroups);
+    return ((double)w + 0.5) * 0x1p-32;
+}
+
+// Keep-or-remask draw of an unmasked row (masked prior, kappa < 1): its distribution has only the
+// token and the mask, so stage 0 decides.
 DD_DEV int32_t keep_or_remask(const PostArgs& a, int row, int zt) {
-    const int ngroups = (a.V + DD_GUMBEL_GROUP - 1) / DD_GUMBEL_GROUP;
-    const int gr = zt / DD_GUMBEL_GROUP;
-    uint32_t wr, wm;
-    if (a.noise) {
-        wr = a.noise[(int64_t)row * a.nu + gr];
-        wm = a.noise[(int64_t)row * a.nu + ngroups];
-    } else {
-        const uint32_t grow = a.row0 + (uint32_t)row;
-        wr = counter_word(a.seed, STREAM_TOP, a.step, grow, (uint32_t)gr);
-        wm = counter_word(a.seed, STREAM_TOP, a.step, grow, (uint32_t)ngroups);
-    }
-    const float sr = (float)a.log_keep + word_gumbel_f(wr);
-    const float sm = (float)a.log_rmask + word_gumbel_f(wm);
-    return sm > sr ? a.V : zt;
+    return mask_word_uniform(a.noise, a.nu, a.V, a.seed, a.step, a.row0 + (uint32_t)row, row) < a.rmask
+               ? a.V : zt;
 }
 
 // Level-1 and level-2 draws of one masked (or uniform-prior) row, by one wavefront, from the row's
@@ -123,22 +122,32 @@ DD_DEV void draw_row(const PostArgs& a, int row, int zt, const char* rowp, const
         Dn = (float)a.Ka_t * xr + (float)a.one_m_at;
         c_u = (float)a.c_u + (float)a.u1 * Dn;
     }
-    const float log_wx = (float)a.log_wx, log_wm = (float)a.log_wm;
+    const float log_wx = (float)a.log_wx;
     const float c_x = (float)a.c_x, log_dn = logf(Dn);
     const uint32_t k0 = (uint32_t)a.seed, k1 = (uint32_t)(a.seed >> 32);
 
-    // level 1: group g has log mass log w_x + lse_g - lse (mask prior; the mask class is group
-    // `ngroups`) or log((c_x X_g + n_g c_u + [r in g] c_r) / D) (uniform prior)
+    // stage 0 (mask prior): the mask class is taken iff the mask word's uniform is below w_m (a row
+    // without a finite log-sum-exp goes on to be reported below)
+    if (mask_prior && isfinite(lse) && mask_word_uniform(a.noise, a.nu, V, a.seed, a.step, grow, row) < a.wm) {
+        if (lane == 0) {
+            a.z_s[row] = V;
+            if (a.row_lse) a.row_lse[row] = lse;
+        }
+        return;
+    }
+
+    // level 1 over the real groups: group g has log mass log w_x + lse_g - lse (mask prior) or
+    // log((c_x X_g + n_g c_u + [r in g] c_r) / D) (uniform prior)
     float best = -INFINITY;
     int bi = 0x7FFFFFFF;
-    for (int gb = 0; gb < a.ntop; gb += 256) {
+    for (int gb = 0; gb < ngroups; gb += 256) {
         const int base = gb + 4 * lane;
-        if (base >= a.ntop) break;
+        if (base >= ngroups) break;
         uint32_t wd[4];
         if (a.noise) {
 #pragma unroll
             for (int i = 0; i < 4; ++i)
-                wd[i] = (base + i < a.ntop) ? a.noise[(int64_t)row * a.nu + base + i] : 0u;
+                wd[i] = (base + i < ngroups) ? a.noise[(int64_t)row * a.nu + base + i] : 0u;
         } else {
             const Words4 W = philox4x32_10((uint32_t)(base >> 2), grow, a.step, STREAM_TOP, k0, k1);
 #pragma unroll
@@ -147,10 +156,10 @@ DD_DEV void draw_row(const PostArgs& a, int row, int zt, const char* rowp, const
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
             const int g = base + i;
-            if (g >= a.ntop) continue;
+            if (g >= ngroups) continue;
             float logm;
             if (mask_prior) {
-                logm = (g < ngroups) ? log_wx + (glse[g] - lse) : log_wm;
+                logm = log_wx + (glse[g] - lse);
             } else {
                 const int lo = g * DD_GUMBEL_GROUP;
                 const int n = min(DD_GUMBEL_GROUP, V - lo);
@@ -166,14 +175,14 @@ DD_DEV void draw_row(const PostArgs& a, int row, int zt, const char* rowp, const
     const int gstar = wave_argmax(best, bi);
 
     int result = V;
-    if (gstar >= a.ntop || !isfinite(lse)) {
+    if (gstar >= ngroups || !isfinite(lse)) {
         // no group had a valid score (NaN or +inf logits, or no finite logit): the row keeps
         // its token and the caller is told; gstar must not index anything
         result = -1;
-    } else if (cand && !(mask_prior && gstar == ngroups)) {   // level 2 by the group's candidate
+    } else if (cand) {   // level 2 by the group's candidate
         const int c = cand[gstar], lo = gstar * DD_GUMBEL_GROUP;
         result = (c >= lo && c < min(V, lo + DD_GUMBEL_GROUP)) ? c : -1;
-    } else if (!(mask_prior && gstar == ngroups)) {   // level 2 inside the chosen group
+    } else {   // level 2 inside the chosen group
         best = -INFINITY;
         bi = 0x7FFFFFFF;
         const int base = gstar * DD_GUMBEL_GROUP + 4 * lane;
@@ -443,9 +452,19 @@ dd_status launch_remask(const PostArgs& a, hipStream_t s) {
 // through LDS, and every thread writes its rows after the rows of earlier threads and blocks.
 constexpr int CT = 1024;
 
+// stage 0 of the masked prior's draw taken ahead of the logits (see mask_word_uniform)
+struct PreDraw {
+    const uint32_t* noise;
+    int nu, V, on;
+    uint64_t seed;
+    uint32_t step, row0;
+    double wm;
+};
+
 __global__ __launch_bounds__(CT) void compact_masked_kernel(const int32_t* z, int64_t M,
                                                             int32_t mask_id, int32_t* idx,
-                                                            int32_t* count, int L, int32_t* seq) {
+                                                            int32_t* count, int L, int32_t* seq,
+                                                            PreDraw pd) {
     __shared__ int wsum[CT / 64];
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const bool vec = ((uintptr_t)z & 15) == 0;
@@ -470,6 +489,16 @@ __global__ __launch_bounds__(CT) void compact_masked_kernel(const int32_t* z, in
         } else {
 #pragma unroll
             for (int e = 0; e < 4; ++e) f[e] = (i0 + e < M) && z[i0 + e] == mask_id;
+        }
+        if (pd.on) {
+            // a masked row that stage 0 keeps masked needs no logits: it is not listed
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+                if (f[e]) {
+                    const int r = (int)i0 + e;
+                    f[e] = !(mask_word_uniform(pd.noise, pd.nu, pd.V, pd.seed, pd.step, pd.row0 + (uint32_t)r, r) <
+                             pd.wm);
+                }
         }
         const int c = f[0] + f[1] + f[2] + f[3];
         int incl = c;
@@ -514,13 +543,21 @@ __global__ __launch_bounds__(CT) void compact_masked_kernel(const int32_t* z, in
 }
 
 dd_status launch_compact(const int32_t* z, int64_t M, int32_t mask_id, int32_t* idx, int32_t* count,
-                         hipStream_t s, int L, int32_t* seq) {
+                         hipStream_t s, int L, int32_t* seq, const PostArgs* pre) {
     if (seq && (L <= 0 || M % L != 0)) {
         set_error("sequence starts need rows of L > 0 tokens (M = %lld, L = %d)", (long long)M, L);
         return DD_E_ARG;
     }
     ProfScope ps(KC_COMPACT, s);
-    launch_k(compact_masked_kernel, dim3(1), dim3(CT), 0, s, z, M, mask_id, idx, count, L, seq);
+    PreDraw pd = {};
+    if (pre) {
+        if (pre->prior != DD_PRIOR_MASK || mask_id != pre->V) {
+            set_error("the stage-0 pre-draw needs the masked prior with the mask id V");
+            return DD_E_ARG;
+        }
+        pd = {pre->noise, pre->nu, pre->V, 1, pre->seed, pre->step, pre->row0, pre->wm};
+    }
+    launch_k(compact_masked_kernel, dim3(1), dim3(CT), 0, s, z, M, mask_id, idx, count, L, seq, pd);
     return launch_status("compact_masked");
 }
 

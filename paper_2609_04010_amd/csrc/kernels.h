@@ -151,9 +151,11 @@ bool ln_supported(int d);
 dd_status launch_gemm(int dtype, int epi, int cls, const GemmArgs& g, hipStream_t s);
 dd_status launch_attn(int dtype, const AttnArgs& a, hipStream_t s);
 bool attn_supported(int dtype, int dh);
-// seq (device, nullable): seq[b] = listed rows before row b L for b = 0..M/L (rows of L tokens)
+// seq (device, nullable): seq[b] = listed rows before row b L for b = 0..M/L (rows of L tokens).
+// pre (host, nullable; masked prior): list only the masked rows that stage 0 of the draw described
+// by *pre unmasks (the others stay masked and need no logits)
 dd_status launch_compact(const int32_t* z, int64_t M, int32_t mask_id, int32_t* idx, int32_t* count,
-                         hipStream_t s, int L = 0, int32_t* seq = nullptr);
+                         hipStream_t s, int L = 0, int32_t* seq = nullptr, const PostArgs* pre = nullptr);
 bool gemm_gather_supported(int dtype, int K);
 // the EPI_LSE epilogue (group log-sum-exps beside the logits) runs for this dtype and K
 bool gemm_lse_supported(int dtype, int K);

@@ -63,7 +63,7 @@ def _one_step(torch, cfg, buf, B, L, z0, at, as_, seed, kappa, store_free, check
     return z.cpu().numpy(), count, rows, logits, glse, cand
 
 
-def _check(torch, cfg, B, L, frac, at, as_, kappa, seed, cand_rows=None, id_rows=None):
+def _check(torch, cfg, B, L, frac, at, as_, kappa, seed, cand_rows=None, ids_last_seq=False):
     V = cfg["vocab"]
     buf = _params(torch, cfg, seed)
     z0 = workloads.masked_state(seed + 1, B, L, V, frac).reshape(-1)
@@ -86,9 +86,9 @@ def _check(torch, cfg, B, L, frac, at, as_, kappa, seed, cand_rows=None, id_rows
         assert bad.size == 0, f"row {j} (token {rb[j]}): candidates {cand[j][bad]} vs {ref[bad]} in groups {bad}"
         mism += int((cand[j] != ref).sum())
     say(f"  candidates: {sel.size} rows x {cand.shape[1]} groups, {clear} clear, {mism} differ (all near a boundary)")
-    # the ids: the oracle's inverse-CDF two-level draw on the same logits and counters (on the
-    # logits rows id_rows only, if given)
-    js = np.arange(cb) if id_rows is None else id_rows
+    # the ids: the oracle's inverse-CDF two-level draw on the same logits and counters (with
+    # ids_last_seq on the logits rows of the last sequence only: the end of the list)
+    js = np.nonzero(rb >= (B - 1) * L)[0] if ids_last_seq else np.arange(cb)
     tok = rb[js]
     if kappa is None:
         zs, gaps = osampler.posterior_sample("mask", G[js], z0[tok], at, as_, nz, rows=tok, level2="cdf")
@@ -151,11 +151,7 @@ def test_store_free_step_full_size_workload4():
     B, L = w["B"], w["L"]
     say("store-free step, workload 4 full size")
     seed = workloads.seeds(4)["param"]
-    z0 = workloads.masked_state(seed + 1, B, L, cfg["vocab"], 0.25).reshape(-1)
-    last = np.nonzero(z0[(B - 1) * L:] == cfg["vocab"])[0].size
-    count = int((z0 == cfg["vocab"]).sum())
-    _check(torch, cfg, B, L, 0.25, 0.7, 0.75, None, seed, cand_rows=256,
-           id_rows=np.arange(count - last, count))
+    _check(torch, cfg, B, L, 0.25, 0.7, 0.75, None, seed, cand_rows=256, ids_last_seq=True)
 
 
 def test_store_free_loop_bookkeeping_and_determinism():
