@@ -159,7 +159,10 @@ size_t dd_loop_workspace_bytes(const dd_config* cfg, int32_t B, int32_t L);
  *               logits row j < *count belongs to token row rows[j]; otherwise
  *               logits row m belongs to token row m.
  *   rows, count int32 [B*L] and int32: the compacted list of the token rows that
- *               were masked before the step (ascending) and its length; count is
+ *               were masked before the step and that the step unmasks (stage 0 of
+ *               the masked prior's draw: the mask is kept iff the uniform of the
+ *               mask's level-1 word is below its probability, which needs no
+ *               logits), ascending, and its length; count is
  *               -1 when the loop does not compact.
  *   glse        fp32 [rows][glse_ld]: per-group log-sum-exps of each logits row
  *               (groups of DD_GUMBEL_GROUP classes) when the vocabulary
@@ -337,11 +340,13 @@ dd_status dd_psi_posterior_sample(int32_t prior, const void* logits, int32_t log
  *   z_trace      NULL or device int32 [T + 1][B*L]: z_1 then the state after
  *                each step.
  *   ws           device workspace >= dd_loop_workspace_bytes(cfg, B, L).
- * Masked prior (bf16): each step lists the still-masked rows and runs the vocabulary projection
- * and the draw on those rows only; carried-over rows need no logits.  With d_model and d_mlp
- * multiples of 128 and no adapters, the last layer also runs on those rows alone from its
- * attention queries on (keys and values still cover every row), since past that point a row's
- * values reach only its own logits; the listed rows' logits are unchanged.  bf16 with d_model % 128
+ * Masked prior (bf16): each step lists the masked rows that it unmasks (stage 0 of the draw:
+ * the mask's probability (1 - a_s)/(1 - a_t), App. A.1, does not depend on the logits) and runs
+ * the vocabulary projection and the rest of the draw on those rows only; rows that stay masked
+ * and carried-over rows need no logits.  With d_model and d_mlp multiples of 128 and no
+ * adapters, the last layer also runs on those rows alone from its attention queries on (keys and
+ * values still cover every row), since past that point a row's values reach only its own logits;
+ * the listed rows' logits are unchanged.  bf16 with d_model % 128
  * == 0: the vocabulary projection also writes, beside each logit row, the log-sum-exp of each
  * group of DD_GUMBEL_GROUP classes (from the rounded logits it stores), and the draw reads those
  * and one group of logits per row instead of the whole row.  The result equals calling
@@ -385,8 +390,8 @@ dd_status dd_sample_loop(const dd_config* cfg, const void* params, int32_t B, in
  * positions (inference-time scaling, Sec. 4); a step with alpha_s = 1 (the
  * last one) still unmasks every position.  Masked prior (bf16): the rows
  * unmasked before a step first keep or remask (no logits), then the
- * still-masked rows run the vocabulary projection and the draw as in
- * dd_sample_loop; the result equals dd_denoise_forward followed by
+ * masked rows that the step unmasks run the vocabulary projection and the draw
+ * as in dd_sample_loop; the result equals dd_denoise_forward followed by
  * dd_psi_posterior_sample on every row.
  */
 dd_status dd_psi_sample_loop(const dd_config* cfg, const void* params, int32_t B, int32_t L,
