@@ -188,6 +188,30 @@ def test_psi_sample_at_kappa_one_is_the_ancestral_step(prior):
     assert np.array_equal(a, b)
 
 
+def test_mask_first_reads_the_mask_word_and_compares_below():
+    """Stage 0 of the masked draw: the mask is taken iff the uniform of level-1 word n_groups is
+    below p_V (words chosen just below and just above the threshold; every other word fixed).
+    Pins the word index, the direction of the comparison and that the other words are not read."""
+    V = 600
+    ng = sampler.n_groups_real(V)
+    p = np.zeros(V + 1)
+    p[:V] = 0.7 / V
+    p[V] = 0.3
+    thr = int(0.3 * 2.0 ** 32)                # u(w) = (w + 1/2) 2^-32
+    for w, expect_mask in ((thr - 1, True), (thr + 1, False)):
+        for other in (0, 2 ** 32 - 1):
+            words = np.full((1, sampler.noise_width("mask", V)), other, dtype=np.uint32)
+            words[0, ng] = w
+            nz = sampler.ExplicitNoise(words, sampler.n_top("mask", V))
+            # (level 2' reads Philox uniforms, which explicit words do not carry: the inverse-CDF
+            # draw is checked where stage 0 ends it)
+            draws = (sampler.sample_from_probs,) + ((sampler.sample_from_probs_cdf,) if expect_mask else ())
+            for draw in draws:
+                z, g0, _ = draw("mask", p, 0, nz)
+                assert (z == V) == expect_mask, (draw.__name__, w, other, z)
+                assert g0 < 1e-8          # the reported gap covers the near-tie with p_V
+
+
 def test_psi_unmasked_token_keep_or_remask_chi2():
     """Masked prior, unmasked z_t: eq. (psi-mdm) with x_theta = one-hot(z_t) keeps the token with
     probability a_s + kappa (1 - a_s) and remasks otherwise; the logits are never read."""
