@@ -314,16 +314,29 @@ static dd_status run_forward(const dd_config* c, const void* params, const int32
         }
         DD_TRY(launch_attn(dt, aa, s));
         if (tail) {
+            // The listed rows are few in most steps (about M / T from an all-mask start), where the
+            // 256-row tiles leave most CUs idle through a whole K loop.  Each of these GEMMs is
+            // launched twice, gated on the device-side count: the shape's usual tiles above
+            // TAIL_ROWS rows, 64 x 128 tiles (four wavefronts) up to it.
+            constexpr int TAIL_ROWS = 2048;
+            auto gated = [&](GemmArgs ga, int epi, int cls) -> dd_status {
+                ga.m_gate = TAIL_ROWS;
+                ga.m_side = 0;
+                DD_TRY(launch_gemm(dt, epi, cls, ga, s));
+                ga.m_side = 1;
+                ga.tile_hint = 9 + 1;
+                return launch_gemm(dt, epi, cls, ga, s);
+            };
             float* hc = (float*)qkv;
             g = {att, dr, tp(b + 4), dr, tp(b + 5), hc, d, (int)M, d, dr, nullptr, vocab_count};
             g.c_in = h;
             g.c_rows = vocab_rows;
-            DD_TRY(launch_gemm(dt, EPI_BIAS_RESID, KC_GEMM_O, g, s));
+            DD_TRY(gated(g, EPI_BIAS_RESID, KC_GEMM_O));
             DD_TRY(launch_ln(dt, c->norm, hc, M, d, tp(b + 6), tp(b + 7), c->norm_eps, xln, dr, s, vocab_count));
             g = {xln, dr, tp(b + 8), dr, tp(b + 9), mlp, Fr, (int)M, F, dr, nullptr, vocab_count};
-            DD_TRY(launch_gemm(dt, EPI_BIAS_GELU, KC_GEMM_MLP1, g, s));
+            DD_TRY(gated(g, EPI_BIAS_GELU, KC_GEMM_MLP1));
             g = {mlp, Fr, tp(b + 10), Fr, tp(b + 11), hc, d, (int)M, d, Fr, nullptr, vocab_count};
-            DD_TRY(launch_gemm(dt, EPI_BIAS_RESID, KC_GEMM_MLP2, g, s));
+            DD_TRY(gated(g, EPI_BIAS_RESID, KC_GEMM_MLP2));
             DD_TRY(launch_ln(dt, c->norm, hc, M, d, tp(lnf), tp(lnf + 1), c->norm_eps, xln, dr, s, vocab_count));
             break;
         }

@@ -325,6 +325,7 @@ __global__ __launch_bounds__(64 * WGM_ * WGN_, 1) void gemm_bf16_dl_kernel(GemmA
     if (g.m_count) {
         M = *g.m_count;
         tiles_m = (M + DM - 1) / DM;
+        if (g.m_gate > 0 && ((M > g.m_gate) == (g.m_side != 0))) return;   // the other launch's rows
     }
     const int nblocks = tiles_m * tiles_n;
     int L = blockIdx.x;
@@ -1042,7 +1043,7 @@ static void launch_dl(const GemmArgs& g, hipStream_t s) {
 template <int EPI, int ROLE>
 static void launch_epi(int dtype, const GemmArgs& g, hipStream_t s) {
     if (dtype == DD_BF16) {
-        int tile = pick_tile(g);
+        int tile = g.tile_hint > 0 ? g.tile_hint - 1 : pick_tile(g);
         // the ring instance of the 256 x 192 tile takes no gathered rows and no separate residual
         // input: the four-wavefront form
         if (tile == 7 && (g.a_rows || g.c_in) && dl_ring<EPI, DLShape<192, 4, 2>>()) tile = 5;
@@ -1077,6 +1078,10 @@ dd_status launch_gemm(int dtype, int epi, int cls, const GemmArgs& g, hipStream_
     if ((g.a_rows || g.m_count || g.c_in || g.c_rows || g.row_ids) && !gemm_gather_supported(dtype, g.K)) {
         set_error("row-gathered GEMM needs the bf16 path and K %% 128 == 0");
         return DD_E_UNSUPPORTED;
+    }
+    if (g.m_gate > 0 && !g.m_count) {
+        set_error("a row-count gate needs the device-side row count");
+        return DD_E_ARG;
     }
     if ((g.c_in && epi != EPI_BIAS_RESID) || (g.c_rows && !g.c_in)) {
         set_error("a separate residual input (and its row list) needs the residual epilogue");

@@ -86,6 +86,12 @@ struct GemmArgs {
     // EPI_LSE_CDF: token row of output row m when A is already compacted (takes precedence over
     // a_rows for the noise counters)
     const int32_t* row_ids;
+    // tile_hint k > 0: use tile shape k - 1 of the launcher's table (0: chosen from the shape)
+    int tile_hint;
+    // m_gate > 0 (with m_count): the launch does its work only if *m_count > m_gate (m_side 0)
+    // or *m_count <= m_gate (m_side 1); two launches with the two sides pick a tile shape by the
+    // device-side row count
+    int m_gate, m_side;
 };
 
 struct AttnArgs {
