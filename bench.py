@@ -42,6 +42,10 @@ def log(*a):
 
 
 TRIMMED = ("attention", "gemm_attn_out", "gemm_mlp_up", "gemm_mlp_down")
+# the trimmed last layer launches each of its GEMMs twice, gated on the listed-row count: the
+# shape's usual tiles above TAIL_ROWS rows, 64-row tiles up to it (the library's threshold)
+GATED = ("gemm_attn_out", "gemm_mlp_up", "gemm_mlp_down")
+TAIL_ROWS = 2048
 
 
 def algorithmic_units(cls, cfg, B, L, rows=None):
@@ -72,12 +76,20 @@ def launch_rows(cls, cfg, B, L, T, n, masked, trimmed):
     M, nl = B * L, cfg["n_layers"]
     if masked is None or n <= 0:
         return M
-    per_step = 1 if cls == "gemm_vocab" else nl
+    gated = trimmed and cls in GATED
+    per_step = 1 if cls == "gemm_vocab" else nl + (1 if gated else 0)
     total = 0
     for i in range(n):
-        s = (i // per_step) % T
-        listed = cls == "gemm_vocab" or (trimmed and cls in TRIMMED and i % per_step == per_step - 1)
-        total += masked[s] if listed else M
+        s, j = (i // per_step) % T, i % per_step
+        if cls == "gemm_vocab":
+            total += masked[s]
+        elif gated and j >= nl - 1:    # the pair of gated launches: one of them does the rows
+            small = masked[s] <= TAIL_ROWS
+            total += masked[s] if (j == nl) == small else 0
+        elif trimmed and cls in TRIMMED and j == nl - 1:
+            total += masked[s]
+        else:
+            total += M
     return total / n
 
 

@@ -39,11 +39,16 @@ def test_launch_rows_follow_the_compacted_loop():
     assert bench.launch_rows("gemm_mlp_up", cfg, B, L, T, 5, None, True) == M
     # vocabulary: one launch per step, wrapping into the next loop after T launches
     assert bench.launch_rows("gemm_vocab", cfg, B, L, T, 6, masked, False) == (16 + 12 + 7 + 3 + 16 + 12) / 6
-    # three layers per step: launches 0, 1 take all rows, launch 2 (last layer) the listed ones
-    assert bench.launch_rows("gemm_mlp_down", cfg, B, L, T, 6, masked, True) == (4 * M + 16 + 12) / 6
+    # three layers per step: launches 0, 1 take all rows; the last layer's GEMMs are a gated pair
+    # (usual tiles, then 64-row tiles), of which the small-tile launch does the listed rows here
+    assert bench.launch_rows("gemm_mlp_down", cfg, B, L, T, 8, masked, True) == (4 * M + 0 + 16 + 0 + 12) / 8
     assert bench.launch_rows("gemm_mlp_down", cfg, B, L, T, 6, masked, False) == M
     assert bench.launch_rows("gemm_qkv", cfg, B, L, T, 6, masked, True) == M
+    # the attention has one listed-query launch per step
     assert bench.launch_rows("attention", cfg, B, L, T, 3, masked, True) == (2 * M + 16) / 3
+    # above the gate the usual tiles do the rows
+    big = [5000, 4000, 3000, 2000]
+    assert bench.launch_rows("gemm_mlp_up", cfg, B, L, T, 4, big, True) == (2 * M + 5000 + 0) / 4
 
 
 def _record(tmp_path, sha, cls="gemm_mlp_down"):
