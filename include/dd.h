@@ -184,7 +184,8 @@ dd_status dd_loop_workspace_layout(const dd_config* cfg, int32_t B, int32_t L, d
 /* Recommended logit row stride (elements): V rounded up to a multiple of 64. */
 int64_t dd_logits_ld(int32_t V);
 /* Explicit-noise words per row: level-1 words (one per group, plus one for the
- * mask class under the masked prior) followed by one word per real class. */
+ * mask class under the masked prior: the word of stage 0) followed by one word
+ * per real class. */
 int32_t dd_noise_width(int32_t prior, int32_t V);
 
 const char* dd_status_str(dd_status s);
@@ -293,10 +294,13 @@ dd_status dd_denoise_forward_ex(const dd_config* cfg, const void* params,
  *                probabilities (debug; a separate float64 kernel; slow).
  *   dev_err      NULL or device int32 error word (DD_DEVERR_TOKEN and
  *                DD_DEVERR_LOGITS are or-ed in).
- * Draw: level 1 picks group g by argmax of log M_g + Gumbel (M_g = posterior
- * mass of the group of DD_GUMBEL_GROUP consecutive classes; the mask class is a
- * group of its own), level 2 picks the class in g by argmax of log p_j + Gumbel;
- * the lowest index wins ties.  Masked prior: rows with z_t != mask are copied.
+ * Draw: masked prior, stage 0: the mask class is taken iff u < p_mask, with u =
+ * (w + 1/2) 2^-32 of the mask's level-1 word w (compared in double; p_mask =
+ * (1 - a_s)/(1 - a_t) needs no logits, App. A.1).  Then, over the real classes,
+ * level 1 picks group g by argmax of log M_g + Gumbel (M_g = posterior mass of
+ * the group of DD_GUMBEL_GROUP consecutive classes) and level 2 picks the class in
+ * g by argmax of log p_j + Gumbel; the lowest index wins ties.  Masked prior: rows
+ * with z_t != mask are copied.
  * Arithmetic: log-sum-exp, group masses and Gumbel scores in fp32 (so a draw
  * can differ from an exact one only where two scores lie within ~1e-5); the
  * debug probabilities in float64.
@@ -316,8 +320,8 @@ dd_status dd_posterior_sample(int32_t prior, const void* logits, int32_t logits_
  *                exactly dd_posterior_sample.
  * Masked prior, z_t != mask: x_theta is taken as the one-hot of z_t (the
  * carry-over parameterisation), so the token is kept with probability
- * a_s + kappa (1 - a_s) and remasked otherwise, by the level-1 Gumbel scores of
- * its own group and of the mask group; its logits are never read.  Uniform
+ * a_s + kappa (1 - a_s) and remasked otherwise, by stage 0 (remask iff the mask
+ * word's uniform is below (1 - kappa)(1 - a_s)); its logits are never read.  Uniform
  * prior: every class keeps non-zero probability for kappa < 1.
  */
 dd_status dd_psi_posterior_sample(int32_t prior, const void* logits, int32_t logits_dtype,
