@@ -317,14 +317,15 @@ static dd_status run_forward(const dd_config* c, const void* params, const int32
             // The listed rows are few in most steps (about M / T from an all-mask start), where the
             // 256-row tiles leave most CUs idle through a whole K loop.  Each of these GEMMs is
             // launched twice, gated on the device-side count: the shape's usual tiles above
-            // TAIL_ROWS rows, 64 x 128 tiles (four wavefronts) up to it.
+            // TAIL_ROWS rows, 64 x 32 tiles of one wavefront up to it (several workgroups per CU;
+            // 4.172 -> 4.159 ms per reverse step against 64 x 128 tiles of four wavefronts).
             constexpr int TAIL_ROWS = 2048;
             auto gated = [&](GemmArgs ga, int epi, int cls) -> dd_status {
                 ga.m_gate = TAIL_ROWS;
                 ga.m_side = 0;
                 DD_TRY(launch_gemm(dt, epi, cls, ga, s));
                 ga.m_side = 1;
-                ga.tile_hint = 9 + 1;
+                ga.tile_hint = 10 + 1;
                 return launch_gemm(dt, epi, cls, ga, s);
             };
             float* hc = (float*)qkv;
