@@ -400,13 +400,10 @@ static PostArgs make_post(int prior, const void* logits, int64_t ld, int32_t row
         a.wx = (as - at) / (1.0 - at) + corr;
         a.wm = (1.0 - as) / (1.0 - at) - corr;
         a.log_wx = log(a.wx);
-        a.log_wm = a.wm > 0.0 ? log(a.wm) : -INFINITY;
         // unmasked rows (x_theta = one-hot of the token): keep a_s + k (1 - a_s), remask the rest
         a.rmask = omk * (1.0 - as);
         a.keep = 1.0 - a.rmask;
         a.remask = a.rmask > 0.0;
-        a.log_keep = log(a.keep);
-        a.log_rmask = a.rmask > 0.0 ? log(a.rmask) : -INFINITY;
     } else {
         const double K = (double)V, ats = at / as;
         const double cu1 = (1.0 - ats) * (1.0 - as) / K;

@@ -11,11 +11,11 @@ struct PostArgs {
     int32_t rows, V, prior;
     const int32_t* z_t;
     int32_t* z_s;
-    // masked prior, masked rows: p_v = w_x x_v, p_mask = w_m (and their logs)
-    double log_wx, log_wm, wx, wm;
+    // masked prior, masked rows: p_v = w_x x_v, p_mask = w_m (stage 0 of the draw), log w_x
+    double log_wx, wx, wm;
     // masked prior, unmasked rows under a Psi transition with kappa < 1: keep the token with
     // probability keep, remask with probability rmask (remask != 0 when rmask > 0)
-    double keep, rmask, log_keep, log_rmask;
+    double keep, rmask;
     int32_t remask;
     // uniform prior: p_j = (c_x x_j + c_u + u1 D + [j == r](Ka_r x_r + c_z)) / D,
     // D = Ka_t x_r + one_m_at
